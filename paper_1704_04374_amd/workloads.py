@@ -1,0 +1,105 @@
+"""Seeded synthetic workloads for the transposition of Eq. (1).
+
+This module only describes problems and draws their input values; it holds
+none of the transposition's arithmetic, so both the GPU path and the CPU
+oracle may use it.  The five named workloads stand in for the paper's
+benchmark of 57 transpositions of 2-D to 6-D tensors of about 200 MB each
+(Section 4), whose case list the paper does not print: they span 2-D to 6-D,
+fp32 and fp64, beta = 0 and beta != 0, and stride-1 moved and kept.
+
+Values are uniform in [-1, 1): ``torch.rand`` in the tensor dtype, times 2,
+minus 1, which is exact in that dtype (fp32 draws are multiples of 2^-24,
+fp64 draws multiples of 2^-53), so no value is subnormal.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from math import prod
+
+import numpy as np
+import torch
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    dtype: str              # "f32" or "f64"
+    size_a: tuple           # extents of A, Fortran order (first index fastest)
+    perm: tuple             # perm[k] = A index at position k of B (0-based)
+    alpha: float
+    beta: float
+    seed_a: int
+    seed_b: int | None      # prior B contents (only when beta != 0)
+
+    @property
+    def numel(self) -> int:
+        return prod(self.size_a)
+
+    @property
+    def elem_bytes(self) -> int:
+        return 4 if self.dtype == "f32" else 8
+
+    @property
+    def size_b(self) -> tuple:
+        return tuple(self.size_a[p] for p in self.perm)
+
+    @property
+    def tensor_bytes(self) -> int:
+        """S of Eq. (2): bytes of one tensor."""
+        return self.numel * self.elem_bytes
+
+    @property
+    def lam(self) -> int:
+        """lambda of Eq. (2): 2 when B is only written, 3 when it is updated."""
+        return 2 if self.beta == 0 else 3
+
+    @property
+    def moved_bytes(self) -> int:
+        """lambda * S: bytes an ideal implementation moves through memory."""
+        return self.lam * self.tensor_bytes
+
+    def describe(self) -> str:
+        return (f"{self.name}: {self.dtype} A{self.size_a} perm{list(self.perm)} -> "
+                f"B{self.size_b}, alpha={self.alpha}, beta={self.beta}")
+
+
+WORKLOADS = [
+    Workload("transpose3d_48x40x32_f32", "f32", (48, 40, 32), (2, 0, 1), 1.0, 0.0, 0, None),
+    Workload("transpose2d_8192x8192_f32", "f32", (8192, 8192), (1, 0), 1.0, 0.0, 1, None),
+    Workload("transpose6d_24x20x16x24x18x20_f32", "f32", (24, 20, 16, 24, 18, 20),
+             (5, 2, 0, 4, 1, 3), 1.5, 0.0, 2, None),
+    Workload("transpose4d_96x96x96x96_keep1_f64", "f64", (96, 96, 96, 96), (0, 3, 2, 1),
+             2.0, 0.5, 3, 4),
+    Workload("transpose5d_3x2x640x480x96_f32", "f32", (3, 2, 640, 480, 96), (4, 2, 0, 3, 1),
+             1.0, 1.0, 5, 6),
+]
+
+BY_NAME = {w.name: w for w in WORKLOADS}
+
+TORCH_DTYPE = {"f32": torch.float32, "f64": torch.float64}
+NUMPY_DTYPE = {"f32": np.float32, "f64": np.float64}
+
+
+def uniform(numel: int, dtype: str, seed: int) -> torch.Tensor:
+    """``numel`` values uniform in [-1, 1) on the CPU, from a seeded generator."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    return torch.rand(numel, dtype=TORCH_DTYPE[dtype], generator=g) * 2 - 1
+
+
+def inputs(w: Workload):
+    """Host tensors (A, B_prior) of a workload; B_prior is None when beta == 0."""
+    A = uniform(w.numel, w.dtype, w.seed_a)
+    B = uniform(w.numel, w.dtype, w.seed_b) if w.seed_b is not None else None
+    return A, B
+
+
+def random_problem(rng: np.random.Generator, max_dims: int = 6,
+                   extents=(1, 2, 3, 5, 7, 17, 33, 64, 65), max_numel: int = 1 << 20):
+    """A random (size_a, perm) pair for sweeps, with at most ``max_numel`` elements."""
+    while True:
+        n = int(rng.integers(1, max_dims + 1))
+        size_a = tuple(int(rng.choice(extents)) for _ in range(n))
+        if prod(size_a) <= max_numel:
+            perm = tuple(int(p) for p in rng.permutation(n))
+            return size_a, perm
