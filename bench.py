@@ -1,0 +1,335 @@
+"""Benchmark of the MI355X transposition library (Eq. 1 of the HPTT paper).
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+One step is one execution of the plan (all of the hot path: the plan is
+built once, then each step launches the kernel the plan chose) on inputs
+already resident in HBM.  The headline workload is the 8192 x 8192 fp32
+matrix transpose; the other named workloads are reported in ``per_workload``.
+
+Bandwidth follows Eq. (2) of the paper: lambda * S bytes per transposition
+(S = bytes of one tensor, lambda = 2 when beta = 0, 3 otherwise), reported in
+GB/s (1e9 B/s).  Context printed on the same line:
+  - roofline: the dominant kernel's achieved GB/s over MI355X's 8 TB/s HBM
+    peak, from HIP events around every timed launch, plus the HBM bytes
+    rocprofv3 counted for it when a matching counter summary is committed;
+  - yardsticks: a same-run 16-byte-per-lane copy kernel (2S) and, for
+    beta != 0, an axpby kernel (3S) -- the SAXPY yardstick of Table 2 --
+    and hipMemcpyAsync device-to-device;
+  - flushed: the paper's protocol (Section 4), best and median of single
+    launches with the caches cleared in between;
+  - cpu_baseline: the CPU oracle on this machine's host, single-threaded.
+"""
+from __future__ import annotations
+
+import argparse
+import glob
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD published peak
+HEADLINE = "transpose2d_8192x8192_f32"
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+FLUSH_BYTES = 1 << 30           # > 256 MB last-level cache + 8 x 4 MB L2
+
+
+def kernel_source_hash() -> str:
+    """Hash of the sources that decide what the transposition kernels do."""
+    h = hashlib.sha256()
+    for f in ("kernel_body.h", "kernels.hip", "plan.cpp", "hptt_args.h"):
+        with open(os.path.join(ROOT, "paper_1704_04374_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload: str):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, or
+    None when there is none or the kernels changed since it was taken."""
+    path = os.path.join(PROFILE_DIR, f"pmc_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def _events(torch, n):
+    return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+
+
+def time_launches(torch, fn, steps: int, warmup: int):
+    """Run fn() warmup times, then `steps` times back to back with HIP events
+    around each launch on the current stream.  Returns (wall_s, [ms])."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    starts, ends = _events(torch, steps), _events(torch, steps)
+    t0 = time.perf_counter()
+    for i in range(steps):
+        starts[i].record()
+        fn()
+        ends[i].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return wall, [s.elapsed_time(e) for s, e in zip(starts, ends)]
+
+
+def time_flushed(torch, hptt, fn, flush_buf, reps: int):
+    """Single launches with the caches cleared before each (Section 4)."""
+    ms = []
+    for i in range(reps):
+        hptt.yardstick_fill(flush_buf, flush_buf.numel() * 4, i)
+        s, e = _events(torch, 2)
+        s.record()
+        fn()
+        e.record()
+        torch.cuda.synchronize()
+        ms.append(s.elapsed_time(e))
+    return ms
+
+
+def measure_workload(torch, hptt, w, steps, warmup, reps, flush_buf, full: bool):
+    """Time one workload: the transposition and its same-run yardsticks."""
+    tdt = torch.float32 if w.dtype == "f32" else torch.float64
+    gen = torch.Generator(device="cuda").manual_seed(w.seed_a)
+    A = torch.rand(w.numel, dtype=tdt, device="cuda", generator=gen) * 2 - 1
+    B = torch.rand(w.numel, dtype=tdt, device="cuda", generator=gen) * 2 - 1
+    t0 = time.perf_counter()
+    plan = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype)
+    plan_us = (time.perf_counter() - t0) * 1e6
+    moved = w.moved_bytes
+    S = w.tensor_bytes
+    out = {"workload": w.name, "plan": plan.describe(), "plan_create_us": round(plan_us, 1),
+           "bytes_per_launch": moved}
+
+    wall, ms = time_launches(torch, lambda: plan.exec(A, B), steps, warmup)
+    avg_ms = sum(ms) / len(ms)
+    out["ms_per_step"] = wall * 1e3 / steps
+    out["gbs"] = moved * steps / wall / 1e9
+    out["kernel_avg_ms"] = avg_ms
+    out["kernel_gbs"] = moved / (avg_ms * 1e-3) / 1e9
+
+    # same-run copy yardstick: read S, write S
+    C = torch.empty_like(A)
+    _, cms = time_launches(torch, lambda: hptt.yardstick_copy(A, C, S), steps, warmup)
+    out["copy_gbs"] = 2 * S / (sum(cms) / len(cms) * 1e-3) / 1e9
+    _, mms = time_launches(torch, lambda: C.copy_(A), steps, warmup)
+    out["hipmemcpy_d2d_gbs"] = 2 * S / (sum(mms) / len(mms) * 1e-3) / 1e9
+    if w.beta != 0:
+        _, ams = time_launches(torch, lambda: hptt.yardstick_axpby(w.dtype, w.alpha, A, w.beta, C,
+                                                                   w.numel), steps, warmup)
+        out["axpby_gbs"] = 3 * S / (sum(ams) / len(ams) * 1e-3) / 1e9
+        out["pct_of_axpby"] = 100 * out["kernel_gbs"] / out["axpby_gbs"]
+    out["pct_of_copy"] = 100 * out["kernel_gbs"] / out["copy_gbs"]
+    out["pct_of_hbm_peak"] = 100 * out["kernel_gbs"] / HBM_PEAK_GBS
+    if full and flush_buf is not None:
+        fms = time_flushed(torch, hptt, lambda: plan.exec(A, B), flush_buf, reps)
+        cfs = time_flushed(torch, hptt, lambda: hptt.yardstick_copy(A, C, S), flush_buf, reps)
+        out["flushed"] = {
+            "reps": reps,
+            "median_gbs": moved / (statistics.median(fms) * 1e-3) / 1e9,
+            "best_gbs": moved / (min(fms) * 1e-3) / 1e9,
+            "best_gibs_eq2": moved / (min(fms) * 1e-3) / 2 ** 30,
+            "copy_median_gbs": 2 * S / (statistics.median(cfs) * 1e-3) / 1e9,
+        }
+        out["flushed"]["median_pct_of_copy"] = (100 * out["flushed"]["median_gbs"]
+                                                / out["flushed"]["copy_median_gbs"])
+    del A, B, C
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_baseline(w, budget_s: float = 12.0):
+    """The oracle, as it stands, on this host: repeated whole transpositions
+    of the headline workload until about budget_s seconds have passed."""
+    from oracle import oracle
+    from paper_1704_04374_amd.workloads import inputs
+    A, B0 = inputs(w)
+    a = A.numpy()
+    b = None if B0 is None else B0.numpy()
+    runs, t0 = 0, time.perf_counter()
+    while True:
+        oracle.transpose(a, w.size_a, w.perm, w.alpha, w.beta, b)
+        runs += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or runs >= 50:
+            break
+    return {"value": round(w.moved_bytes * runs / el / 1e9, 3), "unit": "GB/s",
+            "cores": 1, "kind": "oracle",
+            "sample": f"{runs} whole transpositions of {w.name} "
+                      f"({w.numel} elements each, {el:.1f} s, single thread)"}
+
+
+def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, command: str, out_path: str):
+    """Turn two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) into the
+    committed summary that load_traffic() reads.  Counters are KiB per
+    dispatch; both are scaled by what they read for the copy yardstick of
+    known size in the same runs."""
+    import csv
+
+    from paper_1704_04374_amd.workloads import BY_NAME
+
+    def per_kernel(d, counter):
+        rows = []
+        for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(path) as f:
+                rows += [r for r in csv.DictReader(f) if r.get("Counter_Name") == counter]
+        acc = {}
+        for r in rows:
+            acc.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return acc
+
+    w = BY_NAME[workload]
+    fetch = per_kernel(fetch_dir, "FETCH_SIZE")
+    write = per_kernel(write_dir, "WRITE_SIZE")
+
+    def pick(acc, key):
+        names = [n for n in acc if key in n]
+        if not names:
+            raise SystemExit(f"no dispatch of a kernel matching {key!r} in the counter files")
+        vals = acc[names[0]]
+        return names[0], statistics.median(vals)
+
+    tk, tf = pick(fetch, "tile_kernel" if "keep1" not in workload else "stream_kernel")
+    _, tw = pick(write, tk.split("(")[0])
+    _, cf = pick(fetch, "copy_kernel")
+    _, cw = pick(write, "copy_kernel")
+    S = w.tensor_bytes
+    f_scale = S / (cf * 1024)    # copy kernel reads exactly S bytes
+    w_scale = S / (cw * 1024)    # and writes exactly S bytes
+    fetch_b = tf * 1024 * f_scale
+    write_b = tw * 1024 * w_scale
+    lines = [
+        f"# rocprofv3 counter summary: {tk}",
+        f"# workload: {w.describe()}",
+        f"# command (FETCH_SIZE pass): {command} --pmc FETCH_SIZE",
+        f"# command (WRITE_SIZE pass): {command} --pmc WRITE_SIZE",
+        "# FETCH_SIZE and WRITE_SIZE are KiB per dispatch (median over dispatches); each is",
+        "# scaled by (known bytes / counter) of the copy yardstick kernel in the same run.",
+        f"kernel: {tk}",
+        f"fetch_kib_per_dispatch: {tf:.1f}",
+        f"write_kib_per_dispatch: {tw:.1f}",
+        f"copy_fetch_kib_per_dispatch: {cf:.1f}",
+        f"copy_write_kib_per_dispatch: {cw:.1f}",
+        f"copy_bytes_each_way: {S}",
+        f"fetch_scale: {f_scale:.4f}",
+        f"write_scale: {w_scale:.4f}",
+        f"hbm_fetch_bytes_per_launch: {fetch_b:.0f}",
+        f"hbm_write_bytes_per_launch: {write_b:.0f}",
+        f"hbm_bytes_per_launch: {fetch_b + write_b:.0f}",
+        f"algorithmic_bytes_per_launch: {w.moved_bytes}",
+        f"traffic_over_algorithmic: {(fetch_b + write_b) / w.moved_bytes:.4f}",
+        f"kernel_source_hash: {kernel_source_hash()}",
+    ]
+    with open(out_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=HEADLINE)
+    ap.add_argument("--reps", type=int, default=20, help="flushed single launches per workload")
+    ap.add_argument("--only-headline", action="store_true",
+                    help="time only the headline workload (for profiler runs)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--pmc-command", default="")
+    ap.add_argument("--pmc-out", default="")
+    args = ap.parse_args()
+
+    if args.summarize_pmc:
+        out = args.pmc_out or os.path.join(PROFILE_DIR, f"pmc_{args.workload}.txt")
+        summarize_pmc(*args.summarize_pmc, args.workload, args.pmc_command, out)
+        return 0
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this transposition library has no multi-GPU "
+              "path (use --gpus 1)", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_1704_04374_amd import hptt
+    from paper_1704_04374_amd.workloads import BY_NAME, WORKLOADS
+
+    if not os.path.exists(hptt.LIB_PATH):
+        from paper_1704_04374_amd import build
+        build.build()
+    torch.cuda.set_device(0)
+    head = BY_NAME[args.workload]
+    flush_buf = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
+    print(f"[bench] device {torch.cuda.get_device_name(0)}; headline {head.describe()}",
+          file=sys.stderr, flush=True)
+
+    headline = measure_workload(torch, hptt, head, args.steps, args.warmup, args.reps, flush_buf,
+                                full=not args.only_headline)
+    print(f"[bench] {head.name}: {headline['gbs']:.0f} GB/s, {headline['pct_of_copy']:.1f}% "
+          f"of copy", file=sys.stderr, flush=True)
+    per = {}
+    if not args.only_headline:
+        for w in WORKLOADS:
+            r = headline if w.name == head.name else measure_workload(
+                torch, hptt, w, args.steps, args.warmup, args.reps, flush_buf, full=True)
+            per[w.name] = {k: (round(v, 2) if isinstance(v, float) else v) for k, v in r.items()}
+            print(f"[bench] {w.name}: kernel {r['kernel_gbs']:.0f} GB/s, "
+                  f"{r['pct_of_copy']:.1f}% of copy, {r['pct_of_hbm_peak']:.1f}% of peak",
+                  file=sys.stderr, flush=True)
+
+    traffic = load_traffic(head.name)
+    achieved = headline["kernel_gbs"]
+    line = {
+        "metric": "effective GB/s per transpose (Eq. 2 bytes) and % of HBM peak / same-run copy",
+        "value": round(headline["gbs"], 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(headline["ms_per_step"], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": head.dtype,
+        "data": "synthetic: seeded uniform [-1,1) tensors resident in HBM",
+        "config": {"workload": head.name, "dtype": head.dtype, "size_a": list(head.size_a),
+                   "perm": list(head.perm), "alpha": head.alpha, "beta": head.beta,
+                   "bytes_per_step": head.moved_bytes},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic},
+        "pct_of_copy": round(headline["pct_of_copy"], 2),
+        "copy_gbs": round(headline["copy_gbs"], 1),
+        "hipmemcpy_d2d_gbs": round(headline["hipmemcpy_d2d_gbs"], 1),
+        "flushed": headline.get("flushed"),
+        "plan": headline["plan"],
+        "plan_create_us": headline["plan_create_us"],
+        "kernel_source_hash": kernel_source_hash(),
+        "per_workload": per or None,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(head)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

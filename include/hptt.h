@@ -1,0 +1,172 @@
+/*
+ * hptt.h -- C ABI of an MI355X (gfx950) library for the out-of-place tensor
+ * transposition of Eq. (1) of the HPTT paper (Springer, Su, Bientinesi,
+ * Section 1):
+ *
+ *     B_{Pi(i_1 .. i_N)}  <-  alpha * A_{i_1 .. i_N}  +  beta * B_{Pi(i_1 .. i_N)}
+ *
+ * A and B are dense N-dimensional tensors in the Fortran layout of Section 1
+ * (the first index has stride 1), Pi is any permutation of the N indices and
+ * alpha, beta are scalars.
+ *
+ * Usage follows the plan/execute split of Section 3.1 and Fig. 3b: a plan is
+ * built once on the host from the permutation, the extents, the scalars and
+ * the element type, and is then executed any number of times on device
+ * pointers and a HIP stream.  A plan holds no pointers to tensor data.
+ *
+ * Conventions shared by every call:
+ *  - perm is 0-based and perm[k] is the index of A that sits at position k of
+ *    B, so the compact extents of B are sizeB[k] = sizeA[perm[k]] (Fig. 3b
+ *    passes a zero-based permutation; Table 1 names B's indices in this order).
+ *  - A and B are compact (no outer sizes), hold numel = prod(sizeA) elements
+ *    each, and must not overlap (the operation is out-of-place, Section 3).
+ *  - Every function returns a status and never aborts or throws.
+ *  - Ownership: a plan owns only host memory.  The caller owns A, B and the
+ *    stream and keeps them alive until the work queued on the stream is done.
+ */
+#ifndef HPTT_HIP_H
+#define HPTT_HIP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HPTT_MAX_DIMS 16
+
+typedef struct hptt_plan_s *hptt_plan_t;
+
+/* Element type of A, B, alpha and beta.  The paper's kernels are written for
+ * single precision (Fig. 5) and its contraction study runs in double (Fig. 9). */
+typedef enum {
+    HPTT_FLOAT32 = 0,
+    HPTT_FLOAT64 = 1
+} hptt_dtype_t;
+
+typedef enum {
+    HPTT_SUCCESS = 0,
+    HPTT_ERROR_INVALID_ARGUMENT = 1, /* bad perm, rank, extent, null pointer, misaligned element */
+    HPTT_ERROR_UNSUPPORTED = 2,      /* a forced option the plan cannot honour */
+    HPTT_ERROR_OVERLAP = 3,          /* A and B share memory */
+    HPTT_ERROR_OUT_OF_MEMORY = 4,    /* host allocation of the plan failed */
+    HPTT_ERROR_HIP = 5               /* the kernel launch failed */
+} hptt_status_t;
+
+/* Kernel classes a plan can execute with. */
+typedef enum {
+    HPTT_KERNEL_AUTO = 0,    /* options only: let the plan builder choose */
+    HPTT_KERNEL_NONE = 1,    /* an extent is 0: execute launches nothing */
+    HPTT_KERNEL_AXPBY = 2,   /* the fused permutation is the identity: B <- alpha*A + beta*B */
+    HPTT_KERNEL_STREAM = 3,  /* A's stride-1 index is also B's: rows streamed in B order */
+    HPTT_KERNEL_TILE = 4,    /* stride-1 index moves: 2-D tiles staged through LDS */
+    HPTT_KERNEL_GENERIC = 5  /* one element per thread in B order; any shape */
+} hptt_kernel_t;
+
+/* Optional knobs of hptt_create_plan_ex.  Zero-initialise and set what you
+ * need; zero means "choose".  They exist to measure each design choice. */
+typedef struct {
+    hptt_kernel_t kernel;  /* force a kernel class; TILE and STREAM fail with
+                              HPTT_ERROR_UNSUPPORTED where they do not apply */
+    int32_t run_a;         /* TILE: target length, in elements, of the contiguous
+                              A run of a tile (its columns) */
+    int32_t run_b;         /* TILE: target length of the contiguous B run (rows) */
+    int32_t max_vec;       /* cap on the vector width in elements (1 = scalar) */
+    int32_t nontemporal;   /* 1: non-temporal B stores when beta = 0; 2: never */
+    int32_t rows_per_block;/* STREAM: rows of the kept index per workgroup */
+    int32_t lds_pad;       /* TILE: LDS row padding in elements, 0 = default, -1 = none */
+    int32_t max_blocks;    /* cap on the grid; workgroups loop over tiles beyond it */
+} hptt_options_t;
+
+/* What the plan builder decided; for inspection and tests. */
+typedef struct {
+    int32_t ndim;                      /* rank after dropping extent-1 indices and fusing */
+    int64_t size[HPTT_MAX_DIMS];       /* fused extents of A */
+    int32_t perm[HPTT_MAX_DIMS];       /* fused permutation, same convention as perm */
+    hptt_kernel_t kernel;
+    int64_t numel;
+    int32_t elem_bytes;
+    int64_t run_a;                     /* TILE: A-run (columns) of a tile, elements */
+    int64_t run_b;                     /* TILE: B-run (rows); STREAM: row length */
+    int32_t dims_a;                    /* TILE: fused A indices inside the A run */
+    int32_t dims_b;                    /* TILE: fused B positions inside the B run */
+    int32_t vec_a;                     /* vector width of A accesses for 16-byte aligned bases */
+    int32_t vec_b;                     /* vector width of B accesses */
+    int32_t lds_pitch;                 /* TILE: LDS row pitch in elements */
+    int32_t lds_bytes;                 /* LDS per workgroup */
+    int64_t tiles;                     /* TILE: tiles; STREAM: row groups; others: work items */
+    int64_t grid;                      /* workgroups launched */
+    int32_t block;                     /* threads per workgroup */
+    int32_t nontemporal;               /* 1 when B is written with non-temporal stores */
+    int32_t mode;                      /* 0 raw copy, 1 scale (beta = 0), 2 alpha*A + beta*B */
+} hptt_plan_info_t;
+
+/*
+ * Build a plan for Eq. (1) (Section 1) with the quick path of Section 3.1:
+ * indices that are consecutive in both A and B are merged into superindices
+ * (Section 3.1, footnote 4), extent-1 indices are dropped, and one kernel and
+ * tile shape is chosen from the fused shape without any search.
+ *
+ *   plan   out: the new plan; set to NULL on any error.
+ *   perm   N entries, a permutation of 0..N-1 (see the conventions above).
+ *   N      rank, 1 <= N <= HPTT_MAX_DIMS.
+ *   sizeA  N extents of A, each >= 0 (any 0 makes the plan a no-op).
+ *   alpha, beta  scalars, rounded once to dtype here.  beta == 0 means B is
+ *          never read (Eq. 2 counts B once); alpha == 1 with beta == 0 is a
+ *          bit-exact copy; alpha == 0 is not short-cut (A is still read).
+ *   dtype  element type of A and B.
+ * Makes no HIP call.  Errors: HPTT_ERROR_INVALID_ARGUMENT, HPTT_ERROR_OUT_OF_MEMORY.
+ */
+hptt_status_t hptt_create_plan(hptt_plan_t *plan, const int32_t *perm, int32_t N,
+                               const int64_t *sizeA, double alpha, double beta,
+                               hptt_dtype_t dtype);
+
+/* As hptt_create_plan, with optional knobs (options may be NULL).  A forced
+ * kernel class or tile that cannot serve the problem gives
+ * HPTT_ERROR_UNSUPPORTED. */
+hptt_status_t hptt_create_plan_ex(hptt_plan_t *plan, const int32_t *perm, int32_t N,
+                                  const int64_t *sizeA, double alpha, double beta,
+                                  hptt_dtype_t dtype, const hptt_options_t *options);
+
+/*
+ * Execute a plan (Fig. 3b's plan->exec()): queue the transposition of A into B
+ * on `stream` and return without waiting.
+ *
+ *   A  device pointer to numel elements of dtype (read only).
+ *   B  device pointer to numel elements of dtype; read only when beta != 0.
+ *   stream  HIP stream (0 = the null stream).
+ * A and B must be aligned to the element size.  Pointers aligned to 16 bytes
+ * get 16-byte vector accesses; others get narrower ones (still correct).
+ * The plan is not modified, so one plan may execute concurrently on several
+ * streams.  numel == 0 returns HPTT_SUCCESS without a launch.
+ * Errors: HPTT_ERROR_INVALID_ARGUMENT (null plan; null or misaligned A or B),
+ * HPTT_ERROR_OVERLAP (the byte ranges of A and B intersect), HPTT_ERROR_HIP
+ * (the launch failed; see hptt_last_hip_error).
+ */
+hptt_status_t hptt_exec(hptt_plan_t plan, const void *A, void *B, hipStream_t stream);
+
+/* Free a plan (NULL is accepted).  The plan must not be used afterwards; work
+ * already queued by hptt_exec does not depend on it. */
+hptt_status_t hptt_destroy_plan(hptt_plan_t plan);
+
+/* Copy the plan builder's decisions into *info. */
+hptt_status_t hptt_plan_info(hptt_plan_t plan, hptt_plan_info_t *info);
+
+/* Write a one-line, NUL-terminated human-readable summary of the plan into
+ * buf (at most len bytes, truncated if needed). */
+hptt_status_t hptt_describe_plan(hptt_plan_t plan, char *buf, size_t len);
+
+/* Static English name of a status code. */
+const char *hptt_status_string(hptt_status_t status);
+
+/* The hipError_t of the last failed launch on this thread (hipSuccess if none). */
+int32_t hptt_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HPTT_HIP_H */

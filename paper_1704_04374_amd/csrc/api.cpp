@@ -1,0 +1,61 @@
+// Host half of the C ABI: plan creation, inspection and destruction.  None of
+// these functions makes a HIP call; hptt_exec lives in kernels.hip.
+#include <new>
+#include <string.h>
+
+#include "plan.h"
+
+extern "C" {
+
+hptt_status_t hptt_create_plan_ex(hptt_plan_t* plan, const int32_t* perm, int32_t N,
+                                  const int64_t* sizeA, double alpha, double beta,
+                                  hptt_dtype_t dtype, const hptt_options_t* options) {
+    if (!plan) return HPTT_ERROR_INVALID_ARGUMENT;
+    *plan = nullptr;
+    hptt_plan_s* p = new (std::nothrow) hptt_plan_s;
+    if (!p) return HPTT_ERROR_OUT_OF_MEMORY;
+    hptt_status_t st = hptt::build_plan(perm, N, sizeA, alpha, beta, dtype, options, p);
+    if (st != HPTT_SUCCESS) {
+        delete p;
+        return st;
+    }
+    *plan = p;
+    return HPTT_SUCCESS;
+}
+
+hptt_status_t hptt_create_plan(hptt_plan_t* plan, const int32_t* perm, int32_t N,
+                               const int64_t* sizeA, double alpha, double beta,
+                               hptt_dtype_t dtype) {
+    return hptt_create_plan_ex(plan, perm, N, sizeA, alpha, beta, dtype, nullptr);
+}
+
+hptt_status_t hptt_destroy_plan(hptt_plan_t plan) {
+    delete plan;
+    return HPTT_SUCCESS;
+}
+
+hptt_status_t hptt_plan_info(hptt_plan_t plan, hptt_plan_info_t* info) {
+    if (!plan || !info) return HPTT_ERROR_INVALID_ARGUMENT;
+    *info = plan->info;
+    return HPTT_SUCCESS;
+}
+
+hptt_status_t hptt_describe_plan(hptt_plan_t plan, char* buf, size_t len) {
+    if (!plan || !buf || len == 0) return HPTT_ERROR_INVALID_ARGUMENT;
+    hptt::describe_plan(plan, buf, len);
+    return HPTT_SUCCESS;
+}
+
+const char* hptt_status_string(hptt_status_t status) {
+    switch (status) {
+        case HPTT_SUCCESS: return "success";
+        case HPTT_ERROR_INVALID_ARGUMENT: return "invalid argument";
+        case HPTT_ERROR_UNSUPPORTED: return "unsupported option for this problem";
+        case HPTT_ERROR_OVERLAP: return "A and B overlap";
+        case HPTT_ERROR_OUT_OF_MEMORY: return "out of host memory";
+        case HPTT_ERROR_HIP: return "HIP launch failed";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,96 @@
+// Kernel argument blocks of the transposition library.  The plan builder
+// (plan.cpp) fills them once per plan; hptt_exec passes them by value to the
+// kernels (kernels.hip), whose bodies live in kernel_body.h.
+#pragma once
+
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+namespace hptt {
+
+constexpr int kMaxDims = 16;  // = HPTT_MAX_DIMS
+constexpr int kBlock = 256;   // threads per workgroup: 4 waves of 64
+
+// Unsigned division of n < 2^32 by a divisor 1 <= d < 2^32 fixed at plan
+// time, with one 32x32->64 multiply and a shift (Granlund and Montgomery,
+// "Division by invariant integers using multiplication", PLDI 1994, the
+// unsigned round-up method): l = ceil(log2 d),
+// m = floor(2^32 * (2^l - d) / d) + 1, and n / d = (mulhi(n, m) + n) >> l.
+struct FastDiv {
+    uint32_t d;
+    uint32_t m;
+    uint32_t l;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+    FastDiv f;
+    f.d = d;
+    uint32_t l = 0;
+    while (l < 32 && (uint64_t(1) << l) < d) ++l;
+    f.l = l;
+    f.m = uint32_t((((uint64_t(1) << l) - d) << 32) / d + 1);
+    return f;
+}
+
+__host__ __device__ __forceinline__ uint32_t fast_div(uint32_t n, const FastDiv& f) {
+    uint32_t t = uint32_t((uint64_t(n) * f.m) >> 32);
+    return uint32_t((uint64_t(t) + n) >> f.l);
+}
+
+// How B is updated (Eq. 1): a raw bit copy (alpha = 1, beta = 0), a scaled
+// copy (beta = 0, B not read) or the full update alpha*A + beta*B.
+enum Mode : int { kCopy = 0, kScale = 1, kAxpby = 2 };
+
+// Kernel T: the transposition is cut into independent 2-D tiles (the
+// macro-tiles of Section 3.2).  A tile's columns form a contiguous run of A
+// (fused A indices 0..nC-1, the last one possibly cut into chunks) and its
+// rows a contiguous run of B (fused B positions 0..nR-1, the last one
+// possibly chunked); every other index, and the chunk counters, span the grid.
+struct TileArgs {
+    int64_t runA;        // columns per tile = length of each A run (elements)
+    int64_t runB;        // rows per tile = length of each B run
+    int32_t pitch;       // LDS row pitch in elements (runA plus padding)
+    int32_t nC;          // fused A indices inside the A run (A order)
+    int32_t nR;          // fused B positions inside the B run (B order)
+    int32_t nG;          // grid digits (fastest first)
+    uint32_t numTiles;
+    int32_t gChunkC;     // grid digit that counts chunks of the last A-run index, or -1
+    int32_t gChunkR;     // grid digit that counts chunks of the last B-run index, or -1
+    int32_t pad_;
+    int64_t cInner, cChunk, cLast;  // valid columns = cInner * min(cChunk, cLast - j*cChunk)
+    int64_t rInner, rChunk, rLast;  // valid rows    = rInner * min(rChunk, rLast - j*rChunk)
+    FastDiv cExt[kMaxDims];         // tile extents of the A-run indices
+    int64_t cStrideB[kMaxDims];     // their strides in B
+    FastDiv rExt[kMaxDims];         // tile extents of the B-run indices
+    int64_t rStrideA[kMaxDims];     // their strides in A
+    FastDiv gExt[kMaxDims];         // grid digit extents
+    int64_t gStrideA[kMaxDims];     // grid digit strides in A
+    int64_t gStrideB[kMaxDims];     // grid digit strides in B
+};
+
+// Kernel S: A's stride-1 index is also B's.  Each "row" is one full run of
+// that index, contiguous in both tensors; rows are visited in B order, so B
+// is one sequential stream and A a gather of rows.
+struct StreamArgs {
+    int64_t rowLen;       // extent of the kept stride-1 index
+    int64_t numRows;      // numel / rowLen
+    int32_t rowsPerBlock; // rows handled by one workgroup per step
+    int32_t nO;           // outer B positions 1..N'-1
+    uint32_t numGroups;   // ceil(numRows / rowsPerBlock)
+    int32_t pad_;
+    FastDiv oExt[kMaxDims];     // extents of B positions 1.. (B order)
+    int64_t oStrideA[kMaxDims]; // A strides of the indices at those positions
+};
+
+// Fallback: one element per thread in B order, any shape.
+struct GenericArgs {
+    int64_t numel;
+    int32_t n;                  // fused rank
+    int32_t pad_;
+    FastDiv bExt[kMaxDims];     // extents of B positions (used when numel < 2^32)
+    int64_t bExt64[kMaxDims];   // the same extents as 64-bit values
+    int64_t bStrideA[kMaxDims]; // A stride of the index at each B position
+};
+
+}  // namespace hptt

@@ -1,0 +1,334 @@
+// Work of each kernel, split at its workgroup barriers into per-thread phase
+// functions.  The __global__ wrappers in kernels.hip call the phases with a
+// barrier between them; every global and LDS access goes through the memory
+// policy `Mem`, which on the device is a plain load or store.
+//
+// Index arithmetic is hoisted out of the per-element path: each workgroup
+// builds its tile's offset tables once, and the per-thread sweeps step their
+// (row, column) position incrementally instead of dividing per element.
+#pragma once
+
+#include "hptt_args.h"
+
+namespace hptt {
+
+template <typename T, int V>
+struct alignas(sizeof(T) * V) Vec {
+    T v[V];
+};
+
+// One element of Eq. (1).  alpha*a and beta*b are rounded separately and then
+// added; contraction into a fused multiply-add is switched off so the result
+// is the same on every device.
+template <int MODE, typename T>
+__host__ __device__ __forceinline__ T update(T a, T b, T alpha, T beta) {
+#pragma clang fp contract(off)
+    if (MODE == kCopy) return a;
+    if (MODE == kScale) return alpha * a;
+    T x = alpha * a;
+    T y = beta * b;
+    return x + y;
+}
+
+template <typename I>
+__host__ __device__ __forceinline__ I imin(I a, I b) { return a < b ? a : b; }
+
+// ---------------------------------------------------------------------------
+// Kernel T: 2-D tile staged through LDS
+// ---------------------------------------------------------------------------
+
+struct TileBase {
+    int64_t a;          // offset of the tile's first element in A
+    int64_t b;          // offset of the tile's first element in B
+    int64_t validCols;  // columns (A-run elements) inside the tensor
+    int64_t validRows;  // rows (B-run elements) inside the tensor
+};
+
+// Split the tile number into grid digits (fastest first).
+__host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
+    TileBase tb;
+    tb.a = 0;
+    tb.b = 0;
+    tb.validCols = g.runA;
+    tb.validRows = g.runB;
+    for (int k = 0; k < g.nG; ++k) {
+        uint32_t q = fast_div(t, g.gExt[k]);
+        int64_t j = int64_t(t - q * g.gExt[k].d);
+        t = q;
+        tb.a += j * g.gStrideA[k];
+        tb.b += j * g.gStrideB[k];
+        if (k == g.gChunkC) tb.validCols = g.cInner * imin(g.cChunk, g.cLast - j * g.cChunk);
+        if (k == g.gChunkR) tb.validRows = g.rInner * imin(g.rChunk, g.rLast - j * g.rChunk);
+    }
+    return tb;
+}
+
+// Offset tables shared by every tile of the launch: rowOffA[r] is the A
+// offset of row r (a B-run position) and colOffB[c] the B offset of column c
+// (an A-run position), both relative to the tile origin.
+template <class Mem>
+__host__ __device__ inline void tile_tables(const TileArgs& g, int tid, int64_t* rowOffA,
+                                            int64_t* colOffB) {
+    for (int64_t r = tid; r < g.runB; r += kBlock) {
+        uint32_t x = uint32_t(r);
+        int64_t off = 0;
+        for (int k = 0; k < g.nR; ++k) {
+            uint32_t q = fast_div(x, g.rExt[k]);
+            off += int64_t(x - q * g.rExt[k].d) * g.rStrideA[k];
+            x = q;
+        }
+        Mem::template lds_st<int64_t>(rowOffA, r, off);
+    }
+    for (int64_t c = tid; c < g.runA; c += kBlock) {
+        uint32_t x = uint32_t(c);
+        int64_t off = 0;
+        for (int k = 0; k < g.nC; ++k) {
+            uint32_t q = fast_div(x, g.cExt[k]);
+            off += int64_t(x - q * g.cExt[k].d) * g.cStrideB[k];
+            x = q;
+        }
+        Mem::template lds_st<int64_t>(colOffB, c, off);
+    }
+}
+
+// Number of items a thread takes per batch: loads of a batch are all issued
+// before the first of them is consumed.
+constexpr int kBatch = 8;
+
+// Load phase: the tile's rows are contiguous runs of A.  Thread tid takes the
+// vectors tid, tid + kBlock, ... of the (row, vector) space, vector fastest,
+// so a wave reads whole runs.  The vectors land in LDS at [row][column].
+template <class Mem, typename T, int VA>
+__host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb, int tid,
+                                          const T* A, T* lds, const int64_t* rowOffA) {
+    const int64_t W = (g.runA + VA - 1) / VA;  // vectors per row
+    int64_t r = tid / W, c = tid % W;
+    const int64_t dr = kBlock / W, dc = kBlock % W;
+    while (r < g.runB) {
+        Vec<T, VA> v[kBatch];
+        int64_t rr[kBatch], cc[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            rr[u] = r;
+            cc[u] = c * VA;
+            if (r < tb.validRows && cc[u] < tb.validCols) {
+                const int64_t off = tb.a + Mem::template lds_ld<int64_t>(rowOffA, r) + cc[u];
+                if (cc[u] + VA <= tb.validCols) {
+                    v[u] = Mem::template ld<T, VA>(A, off);
+                } else {
+                    for (int e = 0; e < VA; ++e)
+                        if (cc[u] + e < tb.validCols) v[u].v[e] = Mem::template ld1<T>(A, off + e);
+                }
+            }
+            c += dc;
+            r += dr;
+            if (c >= W) {
+                c -= W;
+                r += 1;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            if (rr[u] < tb.validRows && cc[u] < tb.validCols) {
+                const int64_t base = rr[u] * g.pitch + cc[u];
+#pragma unroll
+                for (int e = 0; e < VA; ++e)
+                    if (cc[u] + e < tb.validCols) Mem::template lds_st<T>(lds, base + e, v[u].v[e]);
+            }
+        }
+    }
+}
+
+// Store phase: the tile's columns are contiguous runs of B.  Thread tid takes
+// the vectors tid, tid + kBlock, ... of the (column, vector) space, vector
+// fastest, gathers each vector's VB elements from consecutive LDS rows, and
+// writes it to B (reading B first when beta != 0).
+template <class Mem, typename T, int VB, int MODE, bool NT>
+__host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb, int tid, T* B,
+                                           const T* lds, const int64_t* colOffB, T alpha,
+                                           T beta) {
+    const int64_t W = (g.runB + VB - 1) / VB;  // vectors per column
+    int64_t q = tid / W, s = tid % W;
+    const int64_t dq = kBlock / W, ds = kBlock % W;
+    while (q < g.runA) {
+        Vec<T, VB> x[kBatch], y[kBatch];
+        int64_t qq[kBatch], ss[kBatch], off[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            qq[u] = q;
+            ss[u] = s * VB;
+            off[u] = 0;
+            if (q < tb.validCols && ss[u] < tb.validRows) {
+                off[u] = tb.b + Mem::template lds_ld<int64_t>(colOffB, q) + ss[u];
+#pragma unroll
+                for (int e = 0; e < VB; ++e)
+                    if (ss[u] + e < tb.validRows)
+                        x[u].v[e] = Mem::template lds_ld<T>(lds, (ss[u] + e) * g.pitch + q);
+                if (MODE == kAxpby) {
+                    if (ss[u] + VB <= tb.validRows) {
+                        y[u] = Mem::template ld<T, VB>(B, off[u]);
+                    } else {
+                        for (int e = 0; e < VB; ++e)
+                            if (ss[u] + e < tb.validRows) y[u].v[e] = Mem::template ld1<T>(B, off[u] + e);
+                    }
+                }
+            }
+            s += ds;
+            q += dq;
+            if (s >= W) {
+                s -= W;
+                q += 1;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            if (qq[u] < tb.validCols && ss[u] < tb.validRows) {
+                Vec<T, VB> z;
+#pragma unroll
+                for (int e = 0; e < VB; ++e)
+                    z.v[e] = update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
+                if (ss[u] + VB <= tb.validRows) {
+                    Mem::template st<NT, T, VB>(B, off[u], z);
+                } else {
+                    for (int e = 0; e < VB; ++e)
+                        if (ss[u] + e < tb.validRows) Mem::template st1<NT, T>(B, off[u] + e, z.v[e]);
+                }
+            }
+        }
+    }
+}
+
+// LDS layout of kernel T: rowOffA[runB], colOffB[runA], then the tile.
+__host__ __device__ inline int64_t tile_lds_bytes(const TileArgs& g, int elem) {
+    return (g.runA + g.runB) * int64_t(sizeof(int64_t)) + g.runB * g.pitch * int64_t(elem);
+}
+
+// ---------------------------------------------------------------------------
+// Kernel S: the stride-1 index is kept
+// ---------------------------------------------------------------------------
+
+// A offsets of the rows of group `grp` (rows are numbered in B order).
+template <class Mem>
+__host__ __device__ inline void stream_rows(const StreamArgs& g, uint32_t grp, int tid,
+                                            int64_t* rowOffA) {
+    const int64_t first = int64_t(grp) * g.rowsPerBlock;
+    for (int64_t i = tid; i < g.rowsPerBlock && first + i < g.numRows; i += kBlock) {
+        uint32_t x = uint32_t(first + i);
+        int64_t off = 0;
+        for (int k = 0; k < g.nO; ++k) {
+            uint32_t q = fast_div(x, g.oExt[k]);
+            off += int64_t(x - q * g.oExt[k].d) * g.oStrideA[k];
+            x = q;
+        }
+        Mem::template lds_st<int64_t>(rowOffA, i, off);
+    }
+}
+
+// Copy the rows of group `grp`: B is written as one contiguous stream, A is
+// read row by row from the gathered offsets.
+template <class Mem, typename T, int V, int MODE, bool NT>
+__host__ __device__ inline void stream_copy(const StreamArgs& g, uint32_t grp, int tid,
+                                            const T* A, T* B, const int64_t* rowOffA, T alpha,
+                                            T beta) {
+    const int64_t first = int64_t(grp) * g.rowsPerBlock;
+    const int64_t rows = imin(int64_t(g.rowsPerBlock), g.numRows - first);
+    const int64_t W = (g.rowLen + V - 1) / V;  // vectors per row
+    int64_t r = tid / W, c = tid % W;
+    const int64_t dr = kBlock / W, dc = kBlock % W;
+    while (r < rows) {
+        Vec<T, V> x[kBatch], y[kBatch];
+        int64_t offB[kBatch], cc[kBatch];
+        bool ok[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            ok[u] = r < rows;
+            cc[u] = c * V;
+            offB[u] = (first + r) * g.rowLen + cc[u];
+            if (ok[u]) {
+                const int64_t offA = Mem::template lds_ld<int64_t>(rowOffA, r) + cc[u];
+                if (cc[u] + V <= g.rowLen) {
+                    x[u] = Mem::template ld<T, V>(A, offA);
+                    if (MODE == kAxpby) y[u] = Mem::template ld<T, V>(B, offB[u]);
+                } else {
+                    for (int e = 0; e < V; ++e)
+                        if (cc[u] + e < g.rowLen) {
+                            x[u].v[e] = Mem::template ld1<T>(A, offA + e);
+                            if (MODE == kAxpby) y[u].v[e] = Mem::template ld1<T>(B, offB[u] + e);
+                        }
+                }
+            }
+            c += dc;
+            r += dr;
+            if (c >= W) {
+                c -= W;
+                r += 1;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            if (!ok[u]) continue;
+            Vec<T, V> z;
+#pragma unroll
+            for (int e = 0; e < V; ++e)
+                z.v[e] = update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
+            if (cc[u] + V <= g.rowLen) {
+                Mem::template st<NT, T, V>(B, offB[u], z);
+            } else {
+                for (int e = 0; e < V; ++e)
+                    if (cc[u] + e < g.rowLen) Mem::template st1<NT, T>(B, offB[u] + e, z.v[e]);
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Identity after fusion: B <- alpha*A + beta*B over a flat range
+// ---------------------------------------------------------------------------
+
+// Vector i covers elements [i*V, i*V + V); the last vector may be partial.
+template <class Mem, typename T, int V, int MODE, bool NT>
+__host__ __device__ inline void axpby_vec(int64_t numel, int64_t i, const T* A, T* B, T alpha,
+                                          T beta) {
+    const int64_t off = i * V;
+    if (off + V <= numel) {
+        Vec<T, V> x = Mem::template ld<T, V>(A, off), y, z;
+        if (MODE == kAxpby) y = Mem::template ld<T, V>(B, off);
+#pragma unroll
+        for (int e = 0; e < V; ++e)
+            z.v[e] = update<MODE>(x.v[e], MODE == kAxpby ? y.v[e] : T(0), alpha, beta);
+        Mem::template st<NT, T, V>(B, off, z);
+    } else {
+        for (int64_t e = off; e < numel; ++e) {
+            T b = MODE == kAxpby ? Mem::template ld1<T>(B, e) : T(0);
+            Mem::template st1<NT, T>(B, e, update<MODE>(Mem::template ld1<T>(A, e), b, alpha, beta));
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Fallback: one B element per thread, any shape
+// ---------------------------------------------------------------------------
+
+template <class Mem, typename T, int MODE, bool NT, bool BIG>
+__host__ __device__ inline void generic_elem(const GenericArgs& g, int64_t e, const T* A, T* B,
+                                             T alpha, T beta) {
+    int64_t offA = 0;
+    if (BIG) {
+        int64_t x = e;
+        for (int k = 0; k < g.n; ++k) {
+            offA += (x % g.bExt64[k]) * g.bStrideA[k];
+            x /= g.bExt64[k];
+        }
+    } else {
+        uint32_t x = uint32_t(e);
+        for (int k = 0; k < g.n; ++k) {
+            uint32_t q = fast_div(x, g.bExt[k]);
+            offA += int64_t(x - q * g.bExt[k].d) * g.bStrideA[k];
+            x = q;
+        }
+    }
+    T b = MODE == kAxpby ? Mem::template ld1<T>(B, e) : T(0);
+    Mem::template st1<NT, T>(B, e, update<MODE>(Mem::template ld1<T>(A, offA), b, alpha, beta));
+}
+
+}  // namespace hptt

@@ -1,0 +1,420 @@
+// Plan builder: the quick path of plan creation (Section 3.1).  It validates
+// the problem, drops extent-1 indices, merges indices that are consecutive in
+// both A and B into superindices (Section 3.1, footnote 4), classifies the
+// fused problem, and picks one kernel, tile and vector width without any
+// search.  Host code only; it makes no HIP call.
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "plan.h"
+
+namespace hptt {
+
+int64_t tile_lds_bytes_host(const TileArgs& t, int elem) {
+    return (t.runA + t.runB) * int64_t(sizeof(int64_t)) + t.runB * int64_t(t.pitch) * elem;
+}
+
+namespace {
+
+constexpr int64_t kLdsBudget = 64 * 1024;  // bytes of LDS per workgroup for kernel T
+constexpr int64_t kLine = 128;             // L2 cache line of gfx950
+constexpr int64_t kVecBytes = 16;          // widest global access per lane (dwordx4)
+
+int64_t gcd64(int64_t a, int64_t b) {
+    if (a < 0) a = -a;
+    if (b < 0) b = -b;
+    while (b) {
+        int64_t t = a % b;
+        a = b;
+        b = t;
+    }
+    return a;
+}
+
+// Largest power-of-two vector width (in elements, at most 16 bytes and at
+// most `cap`) that divides `gran`; gran == 0 means every offset is 0.
+int32_t vec_width(int64_t gran, int elem, int32_t cap) {
+    int32_t v = int32_t(kVecBytes / elem);
+    while (cap > 0 && v > cap) v /= 2;
+    while (v > 1 && gran % v != 0) v /= 2;
+    return v;
+}
+
+// The fused problem: M indices of A with extents n, B position k holding
+// fused A index p[k], and the compact strides of every A index in A and B.
+struct Fused {
+    int M;
+    int64_t n[kMaxDims];
+    int32_t p[kMaxDims];
+    int64_t sA[kMaxDims];  // stride in A of A index d
+    int64_t sB[kMaxDims];  // stride in B of A index d
+};
+
+// Drop extent-1 indices, then merge maximal groups of B positions whose A
+// indices are consecutive and increasing: such a group is contiguous in both
+// tensors and behaves as one index (Section 3.1, footnote 4).
+void fuse(const int32_t* perm, int32_t N, const int64_t* sizeA, Fused& f) {
+    int32_t newIdx[kMaxDims];
+    int kept = 0;
+    for (int d = 0; d < N; ++d) newIdx[d] = sizeA[d] > 1 ? kept++ : -1;
+    int64_t n[kMaxDims];
+    int32_t p[kMaxDims];
+    int m = 0;
+    for (int d = 0; d < N; ++d)
+        if (sizeA[d] > 1) n[newIdx[d]] = sizeA[d];
+    for (int k = 0; k < N; ++k)
+        if (newIdx[perm[k]] >= 0) p[m++] = newIdx[perm[k]];
+    if (m == 0) {  // every extent is 1
+        f.M = 1;
+        f.n[0] = 1;
+        f.p[0] = 0;
+    } else {
+        // groups in B order: first A index and extent
+        int32_t first[kMaxDims];
+        int64_t ext[kMaxDims];
+        int G = 0;
+        for (int k = 0; k < m; ++k) {
+            if (k > 0 && p[k] == p[k - 1] + 1) {
+                ext[G - 1] *= n[p[k]];
+            } else {
+                first[G] = p[k];
+                ext[G] = n[p[k]];
+                ++G;
+            }
+        }
+        // fused A index of a group = rank of its first A index
+        for (int g = 0; g < G; ++g) {
+            int rank = 0;
+            for (int h = 0; h < G; ++h) rank += first[h] < first[g];
+            f.p[g] = rank;
+            f.n[rank] = ext[g];
+        }
+        f.M = G;
+    }
+    int64_t s = 1;
+    for (int d = 0; d < f.M; ++d) {
+        f.sA[d] = s;
+        s *= f.n[d];
+    }
+    s = 1;
+    for (int k = 0; k < f.M; ++k) {
+        f.sB[f.p[k]] = s;
+        s *= f.n[f.p[k]];
+    }
+}
+
+// Chunk of an index of extent n that extends a run whose inner part has
+// `inner` elements, aiming at a run of `target` elements.  Preference order:
+// every run starts and ends on a 128-byte line (no line is shared between
+// workgroups), no partial edge tile, then the run length closest to target.
+int64_t choose_chunk(int64_t inner, int64_t n, int64_t target, int elem) {
+    int64_t best = 1;
+    double bestScore = 1e30;
+    for (int64_t k = 1; k <= n && (k == 1 || inner * k <= 4 * target); ++k) {
+        const int64_t run = inner * k;
+        const int64_t gran = inner * gcd64(k, n);
+        const bool aligned = (gran * elem) % kLine == 0 && (run * elem) % kLine == 0;
+        const bool edge = n % k != 0;
+        const double score = (aligned ? 0.0 : 4.0) + (edge ? 2.0 : 0.0) +
+                             fabs(log2(double(run) / double(target)));
+        if (score < bestScore) {
+            bestScore = score;
+            best = k;
+        }
+    }
+    return best;
+}
+
+void set_div(FastDiv& f, int64_t d) { f = make_fastdiv(uint32_t(d)); }
+
+// Kernel T set-up for targets tA (A-run) and tB (B-run).  Returns false if the
+// tile does not fit the LDS budget or the grid is too large.
+bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_options_t& opt,
+                TileArgs& t, hptt_plan_info_t& info) {
+    memset(&t, 0, sizeof(t));
+    const int M = f.M;
+    const int p0 = f.p[0];  // A index that is B's stride-1 index (never 0 here)
+    // A run: A indices 0, 1, ... (never reaching p0), the last possibly chunked.
+    int64_t inner = 1;
+    int d = 0;
+    while (d < p0 - 1 && inner * f.n[d] <= tA) inner *= f.n[d++];
+    int64_t cChunk = f.n[d];
+    if (inner * f.n[d] > tA) cChunk = choose_chunk(inner, f.n[d], tA, elem);
+    const int nC = d + 1;
+    t.nC = nC;
+    t.cInner = inner;
+    t.cChunk = cChunk;
+    t.cLast = f.n[d];
+    for (int k = 0; k < nC; ++k) {
+        set_div(t.cExt[k], k == nC - 1 ? cChunk : f.n[k]);
+        t.cStrideB[k] = f.sB[k];
+    }
+    // B run: B positions 0, 1, ... up to (not into) an index of the A run.
+    inner = 1;
+    int k = 0;
+    while (k + 1 < M && f.p[k + 1] >= nC && inner * f.n[f.p[k]] <= tB) inner *= f.n[f.p[k++]];
+    int64_t rChunk = f.n[f.p[k]];
+    if (inner * rChunk > tB) rChunk = choose_chunk(inner, f.n[f.p[k]], tB, elem);
+    const int nR = k + 1;
+    t.nR = nR;
+    t.rInner = inner;
+    t.rChunk = rChunk;
+    t.rLast = f.n[f.p[k]];
+    for (int j = 0; j < nR; ++j) {
+        set_div(t.rExt[j], j == nR - 1 ? rChunk : f.n[f.p[j]]);
+        t.rStrideA[j] = f.sA[f.p[j]];
+    }
+    t.runA = t.cInner * t.cChunk;
+    t.runB = t.rInner * t.rChunk;
+    // Grid digits: chunk counters first, then the remaining indices in A order.
+    bool inRun[kMaxDims] = {false};
+    for (int j = 0; j < nC; ++j) inRun[j] = true;
+    for (int j = 0; j < nR; ++j) inRun[f.p[j]] = true;
+    int g = 0;
+    uint64_t tiles = 1;
+    int64_t ext[kMaxDims];
+    t.gChunkC = t.gChunkR = -1;
+    if (t.cChunk < t.cLast) {
+        ext[g] = (t.cLast + t.cChunk - 1) / t.cChunk;
+        t.gStrideA[g] = t.cChunk * f.sA[nC - 1];
+        t.gStrideB[g] = t.cChunk * f.sB[nC - 1];
+        t.gChunkC = g++;
+    }
+    if (t.rChunk < t.rLast) {
+        const int a = f.p[nR - 1];
+        ext[g] = (t.rLast + t.rChunk - 1) / t.rChunk;
+        t.gStrideA[g] = t.rChunk * f.sA[a];
+        t.gStrideB[g] = t.rChunk * f.sB[a];
+        t.gChunkR = g++;
+    }
+    for (int a = 0; a < M; ++a) {
+        if (inRun[a]) continue;
+        ext[g] = f.n[a];
+        t.gStrideA[g] = f.sA[a];
+        t.gStrideB[g] = f.sB[a];
+        ++g;
+    }
+    t.nG = g;
+    for (int j = 0; j < g; ++j) {
+        if (ext[j] >= (int64_t(1) << 32)) return false;
+        set_div(t.gExt[j], ext[j]);
+        tiles *= uint64_t(ext[j]);
+        if (tiles >= (uint64_t(1) << 32)) return false;
+    }
+    t.numTiles = uint32_t(tiles);
+    // LDS pitch: an odd number of elements by default, so the column-wise
+    // reads of the store phase spread over the LDS banks.
+    int64_t pad = t.runA % 2 == 0 ? 1 : 0;
+    if (opt.lds_pad > 0) pad = opt.lds_pad;
+    if (opt.lds_pad < 0) pad = 0;
+    t.pitch = int32_t(t.runA + pad);
+    const int64_t lds = tile_lds_bytes_host(t, elem);
+    if (lds > kLdsBudget) return false;
+    // Vector widths: every A run must start on a multiple of vec_a elements,
+    // every B run on a multiple of vec_b.
+    int64_t granA = 0, granB = 0;
+    for (int j = 0; j < g; ++j)
+        if (ext[j] > 1) {
+            granA = gcd64(granA, t.gStrideA[j]);
+            granB = gcd64(granB, t.gStrideB[j]);
+        }
+    for (int j = 0; j < nR; ++j)
+        if (t.rExt[j].d > 1) granA = gcd64(granA, t.rStrideA[j]);
+    for (int j = 0; j < nC; ++j)
+        if (t.cExt[j].d > 1) granB = gcd64(granB, t.cStrideB[j]);
+    info.vec_a = vec_width(granA, elem, opt.max_vec);
+    info.vec_b = vec_width(granB, elem, opt.max_vec);
+    info.run_a = t.runA;
+    info.run_b = t.runB;
+    info.dims_a = nC;
+    info.dims_b = nR;
+    info.lds_pitch = t.pitch;
+    info.lds_bytes = int32_t(lds);
+    info.tiles = t.numTiles;
+    return true;
+}
+
+bool setup_stream(const Fused& f, int elem, const hptt_options_t& opt, StreamArgs& s,
+                  hptt_plan_info_t& info) {
+    memset(&s, 0, sizeof(s));
+    s.rowLen = f.n[0];
+    int64_t rows = 1;
+    for (int d = 1; d < f.M; ++d) rows *= f.n[d];
+    if (rows >= (int64_t(1) << 32)) return false;
+    s.numRows = rows;
+    s.nO = f.M - 1;
+    for (int k = 1; k < f.M; ++k) {
+        set_div(s.oExt[k - 1], f.n[f.p[k]]);
+        s.oStrideA[k - 1] = f.sA[f.p[k]];
+    }
+    int64_t rpb = opt.rows_per_block;
+    if (rpb <= 0) rpb = (16 * 1024) / (s.rowLen * elem);
+    if (rpb < 1) rpb = 1;
+    if (rpb > 4096) rpb = 4096;
+    if (rpb > rows) rpb = rows;
+    s.rowsPerBlock = int32_t(rpb);
+    s.numGroups = uint32_t((rows + rpb - 1) / rpb);
+    info.vec_a = info.vec_b = vec_width(s.rowLen, elem, opt.max_vec);
+    info.run_b = s.rowLen;
+    info.lds_bytes = int32_t(rpb * sizeof(int64_t));
+    info.tiles = s.numGroups;
+    return true;
+}
+
+void setup_generic(const Fused& f, int64_t numel, GenericArgs& g) {
+    memset(&g, 0, sizeof(g));
+    g.numel = numel;
+    g.n = f.M;
+    for (int k = 0; k < f.M; ++k) {
+        const int64_t e = f.n[f.p[k]];
+        g.bExt64[k] = e;
+        if (e < (int64_t(1) << 32)) set_div(g.bExt[k], e);
+        g.bStrideA[k] = f.sA[f.p[k]];
+    }
+}
+
+}  // namespace
+
+hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, double alpha,
+                         double beta, hptt_dtype_t dtype, const hptt_options_t* options,
+                         hptt_plan_s* plan) {
+    if (!perm || !sizeA || !plan) return HPTT_ERROR_INVALID_ARGUMENT;
+    if (N < 1 || N > kMaxDims) return HPTT_ERROR_INVALID_ARGUMENT;
+    if (dtype != HPTT_FLOAT32 && dtype != HPTT_FLOAT64) return HPTT_ERROR_INVALID_ARGUMENT;
+    bool seen[kMaxDims] = {false};
+    for (int k = 0; k < N; ++k) {
+        if (perm[k] < 0 || perm[k] >= N || seen[perm[k]]) return HPTT_ERROR_INVALID_ARGUMENT;
+        seen[perm[k]] = true;
+        if (sizeA[k] < 0) return HPTT_ERROR_INVALID_ARGUMENT;
+    }
+    hptt_options_t opt;
+    memset(&opt, 0, sizeof(opt));
+    if (options) opt = *options;
+    if (opt.kernel < HPTT_KERNEL_AUTO || opt.kernel > HPTT_KERNEL_GENERIC ||
+        opt.kernel == HPTT_KERNEL_NONE || opt.run_a < 0 || opt.run_b < 0 || opt.max_vec < 0 ||
+        opt.nontemporal < 0 || opt.nontemporal > 2 || opt.rows_per_block < 0 ||
+        opt.lds_pad < -1 || opt.lds_pad > 64 || opt.max_blocks < 0)
+        return HPTT_ERROR_INVALID_ARGUMENT;
+
+    const int elem = dtype == HPTT_FLOAT32 ? 4 : 8;
+    memset(plan, 0, sizeof(*plan));
+    plan->dtype = dtype;
+    plan->alpha = dtype == HPTT_FLOAT32 ? double(float(alpha)) : alpha;
+    plan->beta = dtype == HPTT_FLOAT32 ? double(float(beta)) : beta;
+    hptt_plan_info_t& info = plan->info;
+    info.elem_bytes = elem;
+    info.block = kBlock;
+    info.mode = plan->beta != 0.0 ? kAxpby : (plan->alpha == 1.0 ? kCopy : kScale);
+    info.nontemporal = (opt.nontemporal == 1 && info.mode != kAxpby) ? 1 : 0;
+
+    int64_t numel = 1;
+    bool empty = false;
+    for (int d = 0; d < N; ++d) {
+        if (sizeA[d] == 0) empty = true;
+        else if (numel > (int64_t(1) << 60) / sizeA[d]) return HPTT_ERROR_INVALID_ARGUMENT;
+        else numel *= sizeA[d];
+    }
+    if (empty) numel = 0;
+    info.numel = numel;
+
+    Fused f;
+    if (empty) {
+        f.M = N;
+        for (int d = 0; d < N; ++d) {
+            f.n[d] = sizeA[d];
+            f.p[d] = perm[d];
+        }
+    } else {
+        fuse(perm, N, sizeA, f);
+    }
+    info.ndim = f.M;
+    for (int d = 0; d < f.M; ++d) {
+        info.size[d] = f.n[d];
+        info.perm[d] = f.p[d];
+    }
+    if (empty) {
+        info.kernel = HPTT_KERNEL_NONE;
+        return HPTT_SUCCESS;
+    }
+
+    const bool identity = f.M == 1;
+    const bool kept = f.p[0] == 0;
+    hptt_kernel_t k = opt.kernel;
+    if (k == HPTT_KERNEL_AXPBY && !identity) return HPTT_ERROR_UNSUPPORTED;
+    if (k == HPTT_KERNEL_STREAM && (!kept || identity)) return HPTT_ERROR_UNSUPPORTED;
+    if (k == HPTT_KERNEL_TILE && kept) return HPTT_ERROR_UNSUPPORTED;
+    if (k == HPTT_KERNEL_AUTO) {
+        if (identity) k = HPTT_KERNEL_AXPBY;
+        else if (kept) k = f.n[0] * elem >= 64 ? HPTT_KERNEL_STREAM : HPTT_KERNEL_GENERIC;
+        else k = HPTT_KERNEL_TILE;
+    }
+    const int64_t maxBlocks = opt.max_blocks > 0 ? opt.max_blocks : (int64_t(1) << 31) - 1;
+
+    if (k == HPTT_KERNEL_TILE) {
+        int64_t tA = opt.run_a > 0 ? opt.run_a : 256 / elem;
+        int64_t tB = opt.run_b > 0 ? opt.run_b : 256 / elem;
+        bool ok = false;
+        for (int attempt = 0; attempt < 24 && !ok; ++attempt) {
+            ok = setup_tile(f, elem, tA, tB, opt, plan->tile, info);
+            if (!ok) {
+                if (tA >= tB && tA > 1) tA /= 2;
+                else if (tB > 1) tB /= 2;
+                else break;
+            }
+        }
+        if (!ok) {
+            if (opt.kernel == HPTT_KERNEL_TILE) return HPTT_ERROR_UNSUPPORTED;
+            k = HPTT_KERNEL_GENERIC;
+        } else {
+            info.grid = plan->tile.numTiles < maxBlocks ? plan->tile.numTiles : maxBlocks;
+        }
+    }
+    if (k == HPTT_KERNEL_STREAM) {
+        if (!setup_stream(f, elem, opt, plan->stream, info)) {
+            if (opt.kernel == HPTT_KERNEL_STREAM) return HPTT_ERROR_UNSUPPORTED;
+            k = HPTT_KERNEL_GENERIC;
+        } else {
+            info.grid = plan->stream.numGroups < maxBlocks ? plan->stream.numGroups : maxBlocks;
+        }
+    }
+    if (k == HPTT_KERNEL_AXPBY) {
+        info.vec_a = info.vec_b = vec_width(0, elem, opt.max_vec);
+        const int64_t vecs = (numel + info.vec_a - 1) / info.vec_a;
+        info.tiles = vecs;
+        int64_t grid = (vecs + kBlock * 4 - 1) / (kBlock * 4);
+        if (grid > 65536) grid = 65536;
+        info.grid = grid < maxBlocks ? grid : maxBlocks;
+    }
+    if (k == HPTT_KERNEL_GENERIC) {
+        setup_generic(f, numel, plan->generic);
+        info.vec_a = info.vec_b = 1;
+        info.tiles = numel;
+        int64_t grid = (numel + kBlock - 1) / kBlock;
+        if (grid > 65536) grid = 65536;
+        info.grid = grid < maxBlocks ? grid : maxBlocks;
+    }
+    info.kernel = k;
+    return HPTT_SUCCESS;
+}
+
+void describe_plan(const hptt_plan_s* p, char* buf, size_t len) {
+    static const char* kKernel[] = {"auto", "none", "axpby", "stream", "tile", "generic"};
+    static const char* kMode[] = {"copy", "scale", "axpby"};
+    const hptt_plan_info_t& in = p->info;
+    char shape[256] = "", perm[256] = "";
+    size_t a = 0, b = 0;
+    for (int d = 0; d < in.ndim; ++d) {
+        a += snprintf(shape + a, sizeof(shape) - a, "%s%lld", d ? "," : "", (long long)in.size[d]);
+        b += snprintf(perm + b, sizeof(perm) - b, "%s%d", d ? "," : "", in.perm[d]);
+    }
+    snprintf(buf, len,
+             "kernel=%s dtype=%s mode=%s fused=(%s) perm=(%s) run_a=%lld run_b=%lld "
+             "dims_a=%d dims_b=%d vec=%d/%d pitch=%d lds=%d tiles=%lld grid=%lld block=%d nt=%d",
+             kKernel[in.kernel], p->dtype == HPTT_FLOAT32 ? "f32" : "f64", kMode[in.mode], shape,
+             perm, (long long)in.run_a, (long long)in.run_b, in.dims_a, in.dims_b, in.vec_a,
+             in.vec_b, in.lds_pitch, in.lds_bytes, (long long)in.tiles, (long long)in.grid,
+             in.block, in.nontemporal);
+}
+
+}  // namespace hptt

@@ -1,0 +1,267 @@
+"""Python binding of the C ABI in ``include/hptt.h``.
+
+Argument marshalling only: every step of the transposition runs in the HIP
+library ``libhptt.so`` built from ``csrc/``; PyTorch provides device memory
+and streams.  There is no fallback: without the built library every call
+raises ``HpttError``.
+
+    plan = create_plan(perm=(1, 0), size_a=(8192, 8192), alpha=1.0, beta=0.0, dtype="f32")
+    plan.exec(A, B)                       # A, B: flat CUDA tensors of numel elements
+    B = transpose(A, (8192, 8192), (1, 0))
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libhptt.so")
+MAX_DIMS = 16
+
+DTYPES = {"f32": 0, "f64": 1}
+KERNELS = {0: "auto", 1: "none", 2: "axpby", 3: "stream", 4: "tile", 5: "generic"}
+KERNEL_IDS = {v: k for k, v in KERNELS.items()}
+MODES = {0: "copy", 1: "scale", 2: "axpby"}
+
+SUCCESS = 0
+STATUS = {0: "HPTT_SUCCESS", 1: "HPTT_ERROR_INVALID_ARGUMENT", 2: "HPTT_ERROR_UNSUPPORTED",
+          3: "HPTT_ERROR_OVERLAP", 4: "HPTT_ERROR_OUT_OF_MEMORY", 5: "HPTT_ERROR_HIP"}
+
+
+class HpttError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {STATUS.get(status, status)}")
+        self.status = status
+
+
+class Options(ctypes.Structure):
+    """hptt_options_t"""
+    _fields_ = [("kernel", ctypes.c_int), ("run_a", ctypes.c_int32), ("run_b", ctypes.c_int32),
+                ("max_vec", ctypes.c_int32), ("nontemporal", ctypes.c_int32),
+                ("rows_per_block", ctypes.c_int32), ("lds_pad", ctypes.c_int32),
+                ("max_blocks", ctypes.c_int32)]
+
+
+class PlanInfo(ctypes.Structure):
+    """hptt_plan_info_t"""
+    _fields_ = [("ndim", ctypes.c_int32), ("size", ctypes.c_int64 * MAX_DIMS),
+                ("perm", ctypes.c_int32 * MAX_DIMS), ("kernel", ctypes.c_int),
+                ("numel", ctypes.c_int64), ("elem_bytes", ctypes.c_int32),
+                ("run_a", ctypes.c_int64), ("run_b", ctypes.c_int64),
+                ("dims_a", ctypes.c_int32), ("dims_b", ctypes.c_int32),
+                ("vec_a", ctypes.c_int32), ("vec_b", ctypes.c_int32),
+                ("lds_pitch", ctypes.c_int32), ("lds_bytes", ctypes.c_int32),
+                ("tiles", ctypes.c_int64), ("grid", ctypes.c_int64), ("block", ctypes.c_int32),
+                ("nontemporal", ctypes.c_int32), ("mode", ctypes.c_int32)]
+
+    def as_dict(self) -> dict:
+        n = self.ndim
+        return {"ndim": n, "size": tuple(self.size[:n]), "perm": tuple(self.perm[:n]),
+                "kernel": KERNELS[self.kernel], "numel": self.numel,
+                "elem_bytes": self.elem_bytes, "run_a": self.run_a, "run_b": self.run_b,
+                "dims_a": self.dims_a, "dims_b": self.dims_b, "vec_a": self.vec_a,
+                "vec_b": self.vec_b, "lds_pitch": self.lds_pitch, "lds_bytes": self.lds_bytes,
+                "tiles": self.tiles, "grid": self.grid, "block": self.block,
+                "nontemporal": self.nontemporal, "mode": MODES[self.mode]}
+
+
+# Every entry point declared in include/hptt.h and include/hptt_yardstick.h.
+EXPORTS = ("hptt_create_plan", "hptt_create_plan_ex", "hptt_exec", "hptt_destroy_plan",
+           "hptt_plan_info", "hptt_describe_plan", "hptt_status_string",
+           "hptt_last_hip_error", "hptt_yardstick_copy", "hptt_yardstick_axpby",
+           "hptt_yardstick_fill")
+
+
+def _declare(lib: ctypes.CDLL, gpu: bool) -> ctypes.CDLL:
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    vp = ctypes.c_void_p
+    st = ctypes.c_int
+    lib.hptt_create_plan.argtypes = [ctypes.POINTER(vp), i32p, ctypes.c_int32, i64p,
+                                     ctypes.c_double, ctypes.c_double, ctypes.c_int]
+    lib.hptt_create_plan_ex.argtypes = lib.hptt_create_plan.argtypes + [ctypes.POINTER(Options)]
+    lib.hptt_destroy_plan.argtypes = [vp]
+    lib.hptt_plan_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]
+    lib.hptt_describe_plan.argtypes = [vp, ctypes.c_char_p, ctypes.c_size_t]
+    lib.hptt_status_string.argtypes = [ctypes.c_int]
+    lib.hptt_status_string.restype = ctypes.c_char_p
+    for f in ("hptt_create_plan", "hptt_create_plan_ex", "hptt_destroy_plan", "hptt_plan_info",
+              "hptt_describe_plan"):
+        getattr(lib, f).restype = st
+    if gpu:
+        lib.hptt_exec.argtypes = [vp, vp, vp, vp]
+        lib.hptt_exec.restype = st
+        lib.hptt_last_hip_error.restype = ctypes.c_int32
+        lib.hptt_yardstick_copy.argtypes = [vp, vp, ctypes.c_size_t, vp]
+        lib.hptt_yardstick_axpby.argtypes = [ctypes.c_int, ctypes.c_double, vp, ctypes.c_double,
+                                             vp, ctypes.c_size_t, vp]
+        lib.hptt_yardstick_fill.argtypes = [vp, ctypes.c_size_t, ctypes.c_uint32, vp]
+        for f in ("hptt_yardstick_copy", "hptt_yardstick_axpby", "hptt_yardstick_fill"):
+            getattr(lib, f).restype = st
+    return lib
+
+
+_lib = None
+
+
+def library() -> ctypes.CDLL:
+    """The loaded ``libhptt.so``; raises HpttError if it was not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise HpttError(-1, f"{LIB_PATH} is missing; run paper_1704_04374_amd.build")
+        _lib = _declare(ctypes.CDLL(LIB_PATH), gpu=True)
+    return _lib
+
+
+def load_plan_api(path: str) -> ctypes.CDLL:
+    """Load another library that exports the plan half of the ABI (for tests)."""
+    return _declare(ctypes.CDLL(path), gpu=False)
+
+
+def _dtype_id(dtype) -> int:
+    if isinstance(dtype, str):
+        return DTYPES[dtype]
+    import torch
+    if dtype == torch.float32:
+        return 0
+    if dtype == torch.float64:
+        return 1
+    raise TypeError(f"unsupported dtype {dtype}")
+
+
+def _check(status: int, what: str):
+    if status != SUCCESS:
+        raise HpttError(status, what)
+
+
+class Plan:
+    """A plan for Eq. (1): perm[k] is the A index at position k of B (0-based),
+    tensors are compact and Fortran-ordered (first index fastest)."""
+
+    def __init__(self, perm, size_a, alpha: float = 1.0, beta: float = 0.0, dtype="f32",
+                 options: Options | None = None, lib: ctypes.CDLL | None = None, **knobs):
+        self._lib = lib if lib is not None else library()
+        self._handle = None
+        n = len(perm)
+        if len(size_a) != n:
+            raise ValueError("perm and size_a differ in length")
+        self.perm = tuple(int(p) for p in perm)
+        self.size_a = tuple(int(s) for s in size_a)
+        self.alpha, self.beta = float(alpha), float(beta)
+        self.dtype = dtype if isinstance(dtype, str) else {0: "f32", 1: "f64"}[_dtype_id(dtype)]
+        pm = (ctypes.c_int32 * max(n, 1))(*self.perm)
+        sz = (ctypes.c_int64 * max(n, 1))(*self.size_a)
+        handle = ctypes.c_void_p()
+        if knobs:
+            options = options or Options()
+            for k, v in knobs.items():
+                setattr(options, k, KERNEL_IDS[v] if k == "kernel" and isinstance(v, str) else v)
+        if options is None:
+            st = self._lib.hptt_create_plan(ctypes.byref(handle), pm, n, sz, self.alpha,
+                                            self.beta, DTYPES[self.dtype])
+        else:
+            st = self._lib.hptt_create_plan_ex(ctypes.byref(handle), pm, n, sz, self.alpha,
+                                               self.beta, DTYPES[self.dtype], ctypes.byref(options))
+        _check(st, "hptt_create_plan")
+        self._handle = handle
+
+    @property
+    def handle(self) -> ctypes.c_void_p:
+        return self._handle
+
+    @property
+    def info(self) -> dict:
+        out = PlanInfo()
+        _check(self._lib.hptt_plan_info(self._handle, ctypes.byref(out)), "hptt_plan_info")
+        return out.as_dict()
+
+    def describe(self) -> str:
+        buf = ctypes.create_string_buffer(512)
+        _check(self._lib.hptt_describe_plan(self._handle, buf, len(buf)), "hptt_describe_plan")
+        return buf.value.decode()
+
+    @property
+    def numel(self) -> int:
+        n = 1
+        for s in self.size_a:
+            n *= s
+        return n
+
+    @property
+    def size_b(self) -> tuple:
+        return tuple(self.size_a[p] for p in self.perm)
+
+    def exec(self, A, B, stream=None):
+        """Queue B <- alpha*A + beta*B (permuted) on `stream` (default: torch's
+        current stream).  A and B are CUDA tensors (or raw device pointers)."""
+        a = A if isinstance(A, int) else A.data_ptr()
+        b = B if isinstance(B, int) else B.data_ptr()
+        if not isinstance(A, int):
+            self._check_tensor(A, "A")
+            self._check_tensor(B, "B")
+        if stream is None:
+            import torch
+            stream = torch.cuda.current_stream().cuda_stream
+        elif not isinstance(stream, int):
+            stream = stream.cuda_stream
+        st = self._lib.hptt_exec(self._handle, ctypes.c_void_p(a), ctypes.c_void_p(b),
+                                 ctypes.c_void_p(stream))
+        if st == 5:
+            raise HpttError(st, f"hptt_exec (hipError {self._lib.hptt_last_hip_error()})")
+        _check(st, "hptt_exec")
+
+    def _check_tensor(self, t, name):
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a device tensor")
+        if t.numel() != self.numel or not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous with {self.numel} elements")
+        if _dtype_id(t.dtype) != DTYPES[self.dtype]:
+            raise ValueError(f"{name} has dtype {t.dtype}, plan is {self.dtype}")
+
+    def __del__(self):
+        if getattr(self, "_handle", None) is not None and self._handle.value:
+            self._lib.hptt_destroy_plan(self._handle)
+            self._handle = None
+
+
+def create_plan(perm, size_a, alpha=1.0, beta=0.0, dtype="f32", **knobs) -> Plan:
+    return Plan(perm, size_a, alpha, beta, dtype, **knobs)
+
+
+def transpose(A, size_a, perm, alpha=1.0, beta=0.0, B=None, **knobs):
+    """Return B with B_{perm} = alpha*A + beta*B for a flat CUDA tensor A
+    holding a Fortran-ordered tensor of extents size_a."""
+    import torch
+    plan = Plan(perm, size_a, alpha, beta, A.dtype, **knobs)
+    if B is None:
+        if beta != 0:
+            raise ValueError("beta != 0 needs B")
+        B = torch.empty_like(A)
+    plan.exec(A, B)
+    return B
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return stream if isinstance(stream, int) else stream.cuda_stream
+
+
+def yardstick_copy(src, dst, nbytes: int, stream=None):
+    _check(library().hptt_yardstick_copy(ctypes.c_void_p(src.data_ptr()),
+                                         ctypes.c_void_p(dst.data_ptr()), nbytes,
+                                         ctypes.c_void_p(_stream(stream))), "hptt_yardstick_copy")
+
+
+def yardstick_axpby(dtype, alpha, x, beta, y, n: int, stream=None):
+    _check(library().hptt_yardstick_axpby(_dtype_id(dtype), float(alpha),
+                                          ctypes.c_void_p(x.data_ptr()), float(beta),
+                                          ctypes.c_void_p(y.data_ptr()), n,
+                                          ctypes.c_void_p(_stream(stream))), "hptt_yardstick_axpby")
+
+
+def yardstick_fill(buf, nbytes: int, value: int = 0, stream=None):
+    _check(library().hptt_yardstick_fill(ctypes.c_void_p(buf.data_ptr()), nbytes, value,
+                                         ctypes.c_void_p(_stream(stream))), "hptt_yardstick_fill")

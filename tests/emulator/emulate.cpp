@@ -1,0 +1,277 @@
+// Host emulation of the library's kernels, for CPU tests only.
+//
+// It runs the same phase functions (kernel_body.h) that the gfx950 kernels
+// run, one workgroup at a time and one thread after another between the
+// points where the device kernels place a barrier, with a memory policy that
+// checks every access:
+//   - every global offset lies inside its tensor and every vector access is
+//     aligned to its width (relative to a 16-byte aligned base);
+//   - B is read only when the plan's mode reads it (beta != 0);
+//   - every LDS access stays inside the workgroup's LDS, and never reads a
+//     word that was not written earlier in the same tile (a missing barrier or
+//     a load/store phase mismatch would read stale LDS on the device);
+//   - optionally, how many times each B element is written.
+// With A and B NULL it only checks offsets ("dry run"), so the launch
+// geometry of full-size problems can be verified without their data.
+//
+// This file is never linked into libhptt.so: it is built into its own test
+// library together with the plan builder, and hptt_exec never reaches it.
+#include <stdio.h>
+#include <string.h>
+
+#include <vector>
+
+#include "kernel_body.h"
+#include "plan.h"
+
+namespace {
+
+struct EmuState {
+    int64_t numel = 0;
+    const void* A = nullptr;
+    void* B = nullptr;
+    bool readsB = false;
+    uint8_t* counts = nullptr;
+    std::vector<uint8_t> lds;       // emulated LDS bytes
+    std::vector<uint8_t> written;   // 1 where the current tile wrote LDS
+    const uint8_t* ldsBase = nullptr;
+    int64_t errors = 0;
+    char msg[512] = {0};
+    bool dry = false;
+};
+
+EmuState* S = nullptr;
+const void* kDryA = reinterpret_cast<const void*>(uintptr_t(0x1000000));
+void* kDryB = reinterpret_cast<void*>(uintptr_t(0x80000000000));
+
+void fail(const char* what, long long a, long long b) {
+    if (S->errors++ == 0) snprintf(S->msg, sizeof(S->msg), "%s (%lld, %lld)", what, a, b);
+}
+
+template <typename T>
+bool check_global(const T* p, int64_t off, int V, bool isStore) {
+    const bool isA = static_cast<const void*>(p) == S->A;
+    const bool isB = static_cast<const void*>(p) == S->B;
+    if (!isA && !isB) { fail("access to an unknown buffer", off, V); return false; }
+    if (isA && isStore) { fail("store into A", off, V); return false; }
+    if (isB && !isStore && !S->readsB) { fail("B read although beta == 0", off, V); return false; }
+    if (off < 0 || off + V > S->numel) { fail(isA ? "A offset out of bounds" : "B offset out of bounds", off, V); return false; }
+    if (off % V != 0) { fail("misaligned vector access", off, V); return false; }
+    return true;
+}
+
+void check_lds(const void* p, int64_t bytes, bool isStore) {
+    const int64_t at = static_cast<const uint8_t*>(p) - S->lds.data();
+    if (at < 0 || at + bytes > int64_t(S->lds.size())) { fail("LDS access out of bounds", at, bytes); return; }
+    for (int64_t i = 0; i < bytes; ++i) {
+        if (isStore) S->written[at + i] = 1;
+        else if (!S->written[at + i]) { fail("LDS read of a word not written in this tile", at, bytes); return; }
+    }
+}
+
+struct HostMem {
+    template <typename T, int V>
+    static hptt::Vec<T, V> ld(const T* p, int64_t off) {
+        hptt::Vec<T, V> r;
+        memset(&r, 0, sizeof(r));
+        if (check_global(p, off, V, false) && !S->dry) memcpy(&r, p + off, sizeof(r));
+        return r;
+    }
+    template <typename T>
+    static T ld1(const T* p, int64_t off) {
+        T r = T(0);
+        if (check_global(p, off, 1, false) && !S->dry) r = p[off];
+        return r;
+    }
+    template <bool NT, typename T, int V>
+    static void st(T* p, int64_t off, const hptt::Vec<T, V>& v) {
+        if (!check_global(p, off, V, true)) return;
+        if (!S->dry) memcpy(p + off, &v, sizeof(v));
+        if (S->counts)
+            for (int e = 0; e < V; ++e)
+                if (S->counts[off + e] < 255) ++S->counts[off + e];
+    }
+    template <bool NT, typename T>
+    static void st1(T* p, int64_t off, T v) {
+        if (!check_global(p, off, 1, true)) return;
+        if (!S->dry) p[off] = v;
+        if (S->counts && S->counts[off] < 255) ++S->counts[off];
+    }
+    template <typename T>
+    static T lds_ld(const T* l, int64_t i) {
+        check_lds(l + i, sizeof(T), false);
+        T r;
+        memcpy(&r, l + i, sizeof(T));
+        return r;
+    }
+    template <typename T>
+    static void lds_st(T* l, int64_t i, T v) {
+        check_lds(l + i, sizeof(T), true);
+        if (S->errors == 0) memcpy(l + i, &v, sizeof(T));
+    }
+};
+
+void clear_written(int64_t from, int64_t to) {
+    memset(S->written.data() + from, 0, size_t(to - from));
+}
+
+// Mirrors tile_kernel in kernels.hip.
+template <typename T, int VA, int VB, int MODE, bool NT>
+void emu_tile(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
+    using namespace hptt;
+    const TileArgs& g = p->tile;
+    const T alpha = T(p->alpha), beta = T(p->beta);
+    const int64_t ldsBytes = p->info.lds_bytes;
+    const int64_t tableBytes = (g.runA + g.runB) * int64_t(sizeof(int64_t));
+    S->lds.assign(size_t(ldsBytes), 0);
+    S->written.assign(size_t(ldsBytes), 0);
+    int64_t* rowOffA = reinterpret_cast<int64_t*>(S->lds.data());
+    int64_t* colOffB = rowOffA + g.runB;
+    T* lds = reinterpret_cast<T*>(colOffB + g.runA);
+    const int64_t grid = p->info.grid;
+    for (int64_t blk = 0; blk < grid && S->errors == 0; blk += blockStride) {
+        clear_written(0, ldsBytes);
+        for (int tid = 0; tid < kBlock; ++tid) tile_tables<HostMem>(g, tid, rowOffA, colOffB);
+        for (int64_t t = blk; t < g.numTiles && S->errors == 0; t += grid) {
+            clear_written(tableBytes, ldsBytes);
+            const TileBase tb = tile_base(g, uint32_t(t));
+            for (int tid = 0; tid < kBlock; ++tid) tile_load<HostMem, T, VA>(g, tb, tid, A, lds, rowOffA);
+            for (int tid = 0; tid < kBlock; ++tid)
+                tile_store<HostMem, T, VB, MODE, NT>(g, tb, tid, B, lds, colOffB, alpha, beta);
+        }
+    }
+}
+
+// Mirrors stream_kernel in kernels.hip.
+template <typename T, int V, int MODE, bool NT>
+void emu_stream(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
+    using namespace hptt;
+    const StreamArgs& g = p->stream;
+    const T alpha = T(p->alpha), beta = T(p->beta);
+    S->lds.assign(size_t(p->info.lds_bytes), 0);
+    S->written.assign(size_t(p->info.lds_bytes), 0);
+    int64_t* rows = reinterpret_cast<int64_t*>(S->lds.data());
+    const int64_t grid = p->info.grid;
+    for (int64_t blk = 0; blk < grid && S->errors == 0; blk += blockStride) {
+        for (int64_t grp = blk; grp < g.numGroups && S->errors == 0; grp += grid) {
+            clear_written(0, int64_t(S->lds.size()));
+            for (int tid = 0; tid < kBlock; ++tid) stream_rows<HostMem>(g, uint32_t(grp), tid, rows);
+            for (int tid = 0; tid < kBlock; ++tid)
+                stream_copy<HostMem, T, V, MODE, NT>(g, uint32_t(grp), tid, A, B, rows, alpha, beta);
+        }
+    }
+}
+
+// Mirrors axpby_kernel and generic_kernel in kernels.hip.
+template <typename T, int V, int MODE, bool NT>
+void emu_axpby(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
+    using namespace hptt;
+    const int64_t numel = p->info.numel, vecs = (numel + V - 1) / V;
+    const int64_t grid = p->info.grid, stride = grid * kBlock;
+    for (int64_t blk = 0; blk < grid && S->errors == 0; blk += blockStride)
+        for (int tid = 0; tid < kBlock; ++tid)
+            for (int64_t i = blk * kBlock + tid; i < vecs; i += stride)
+                axpby_vec<HostMem, T, V, MODE, NT>(numel, i, A, B, T(p->alpha), T(p->beta));
+}
+
+template <typename T, int MODE, bool NT>
+void emu_generic(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
+    using namespace hptt;
+    const GenericArgs& g = p->generic;
+    const int64_t grid = p->info.grid, stride = grid * kBlock;
+    const bool big = g.numel >= (int64_t(1) << 32);
+    for (int64_t blk = 0; blk < grid && S->errors == 0; blk += blockStride)
+        for (int tid = 0; tid < kBlock; ++tid)
+            for (int64_t e = blk * kBlock + tid; e < g.numel; e += stride) {
+                if (big) generic_elem<HostMem, T, MODE, NT, true>(g, e, A, B, T(p->alpha), T(p->beta));
+                else generic_elem<HostMem, T, MODE, NT, false>(g, e, A, B, T(p->alpha), T(p->beta));
+            }
+}
+
+template <typename T, int MODE, bool NT, int VA, int VB>
+void run_widths(const hptt_plan_s* p, const T* A, T* B, int64_t bs) {
+    switch (p->info.kernel) {
+        case HPTT_KERNEL_TILE: emu_tile<T, VA, VB, MODE, NT>(p, A, B, bs); break;
+        case HPTT_KERNEL_STREAM: emu_stream<T, (VA < VB ? VA : VB), MODE, NT>(p, A, B, bs); break;
+        case HPTT_KERNEL_AXPBY: emu_axpby<T, (VA < VB ? VA : VB), MODE, NT>(p, A, B, bs); break;
+        case HPTT_KERNEL_GENERIC: emu_generic<T, MODE, NT>(p, A, B, bs); break;
+        default: break;
+    }
+}
+
+template <typename T, int MODE, bool NT, int VA>
+void run_vb(const hptt_plan_s* p, const T* A, T* B, int vb, int64_t bs) {
+    if (vb == 1) run_widths<T, MODE, NT, VA, 1>(p, A, B, bs);
+    else if (vb == 2) run_widths<T, MODE, NT, VA, 2>(p, A, B, bs);
+    else if constexpr (sizeof(T) == 4) run_widths<T, MODE, NT, VA, 4>(p, A, B, bs);
+}
+
+template <typename T, int MODE, bool NT>
+void run_va(const hptt_plan_s* p, const T* A, T* B, int va, int vb, int64_t bs) {
+    if (va == 1) run_vb<T, MODE, NT, 1>(p, A, B, vb, bs);
+    else if (va == 2) run_vb<T, MODE, NT, 2>(p, A, B, vb, bs);
+    else if constexpr (sizeof(T) == 4) run_vb<T, MODE, NT, 4>(p, A, B, vb, bs);
+}
+
+template <typename T>
+void run(const hptt_plan_s* p, const T* A, T* B, int va, int vb, int64_t bs) {
+    const bool nt = p->info.nontemporal != 0;
+    switch (p->info.mode) {
+        case hptt::kCopy:
+            if (nt) run_va<T, hptt::kCopy, true>(p, A, B, va, vb, bs);
+            else run_va<T, hptt::kCopy, false>(p, A, B, va, vb, bs);
+            break;
+        case hptt::kScale:
+            if (nt) run_va<T, hptt::kScale, true>(p, A, B, va, vb, bs);
+            else run_va<T, hptt::kScale, false>(p, A, B, va, vb, bs);
+            break;
+        default: run_va<T, hptt::kAxpby, false>(p, A, B, va, vb, bs);
+    }
+}
+
+}  // namespace
+
+extern "C" {
+
+// Emulate hptt_exec of `plan` on host buffers A and B (or, with both NULL,
+// only the offsets).  va/vb = 0 use the plan's vector widths, others force
+// narrower ones as hptt_exec does for less aligned pointers.  counts (numel
+// bytes, or NULL) is incremented at every B element written.  Only
+// workgroups 0, block_stride, 2*block_stride, ... are run.  Returns the
+// number of violations; the first is described in msg.
+int64_t hptt_emulate_exec(hptt_plan_t plan, const void* A, void* B, int32_t va, int32_t vb,
+                          uint8_t* counts, int64_t block_stride, char* msg, size_t msglen) {
+    if (!plan) return -1;
+    EmuState st;
+    S = &st;
+    st.numel = plan->info.numel;
+    st.dry = (A == nullptr && B == nullptr);
+    st.A = st.dry ? kDryA : A;
+    st.B = st.dry ? kDryB : B;
+    st.readsB = plan->info.mode == hptt::kAxpby;
+    st.counts = counts;
+    if (va <= 0) va = plan->info.vec_a;
+    if (vb <= 0) vb = plan->info.vec_b;
+    if (block_stride < 1) block_stride = 1;
+    if (plan->info.kernel != HPTT_KERNEL_NONE && st.numel > 0) {
+        if (plan->dtype == HPTT_FLOAT32)
+            run<float>(plan, static_cast<const float*>(st.A), static_cast<float*>(st.B), va, vb, block_stride);
+        else
+            run<double>(plan, static_cast<const double*>(st.A), static_cast<double*>(st.B), va, vb, block_stride);
+    }
+    if (msg && msglen) snprintf(msg, msglen, "%s", st.msg);
+    S = nullptr;
+    return st.errors;
+}
+
+// Exhaustive check of the fast division used by every kernel: n / d for the
+// given divisor and every dividend in [lo, hi).  Returns the first dividend
+// that divides wrongly, or -1.
+int64_t hptt_emulate_check_fastdiv(uint32_t d, uint64_t lo, uint64_t hi) {
+    const hptt::FastDiv f = hptt::make_fastdiv(d);
+    for (uint64_t n = lo; n < hi; ++n)
+        if (hptt::fast_div(uint32_t(n), f) != uint32_t(n) / d) return int64_t(n);
+    return -1;
+}
+
+}  // extern "C"

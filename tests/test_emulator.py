@@ -1,0 +1,119 @@
+"""The kernels' index arithmetic, run on the CPU by the host emulator and
+compared with the oracle (bit for bit), with every global and LDS access
+bounds-checked and every B element counted.  Catches out-of-bounds and
+coverage bugs before any kernel runs on a GPU."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from oracle import oracle as orc
+from paper_1704_04374_amd.workloads import WORKLOADS, random_problem
+from emulator import emu
+
+CASES = [(1.0, 0.0), (1.5, 0.0), (-0.3, 1.25), (2.0, 0.5), (0.0, 1.0)]
+
+
+def _rand(rng, n, dtype):
+    return (rng.integers(-(1 << 20), 1 << 20, size=n) / float(1 << 20)).astype(dtype)
+
+
+def _check(p, size_a, perm, alpha, beta, dtype, rng, **run_kw):
+    npd = np.float32 if dtype == "f32" else np.float64
+    A = _rand(rng, p.numel, npd)
+    B0 = _rand(rng, p.numel, npd) if beta != 0 else np.full(p.numel, np.nan, npd)
+    want = orc.transpose(A, size_a, perm, alpha, beta, B0 if beta != 0 else None)
+    B = B0.copy()
+    err, msg, cnt = emu.run(p, A, B, counts=True, **run_kw)
+    assert err == 0, f"{p.describe()}: {msg}"
+    assert np.all(cnt == 1), f"{p.describe()}: B elements written {np.unique(cnt)} times"
+    assert np.array_equal(B, want), p.describe()
+
+
+@pytest.mark.parametrize("d", [1, 2, 3, 5, 7, 24, 96, 97, 640, 1000, 65536, 65537, 3840,
+                               (1 << 31) - 1, 1 << 31, (1 << 31) + 1, (1 << 32) - 1])
+def test_fast_division(d):
+    lib = emu.library()
+    top = 1 << 32
+    for lo, hi in [(0, 1 << 16), (top - (1 << 16), top), (d * 977 % top, d * 977 % top + 4096)]:
+        hi = min(hi, top)
+        assert lib.hptt_emulate_check_fastdiv(d, lo, hi) == -1, (d, lo)
+
+
+def test_fast_division_random_divisors():
+    lib = emu.library()
+    rng = np.random.default_rng(7)
+    for d in rng.integers(1, 1 << 32, size=200):
+        start = int(rng.integers(0, (1 << 32) - 2048))
+        assert lib.hptt_emulate_check_fastdiv(int(d), start, start + 2048) == -1, d
+        assert lib.hptt_emulate_check_fastdiv(int(d), (1 << 32) - 512, 1 << 32) == -1, d
+
+
+def test_random_problems_match_oracle():
+    """Seeded sweep of small odd shapes over every kernel class, with tails."""
+    rng = np.random.default_rng(2017)
+    for it in range(120):
+        size_a, perm = random_problem(rng, max_dims=6, max_numel=40000)
+        dtype = "f32" if it % 2 == 0 else "f64"
+        alpha, beta = CASES[it % len(CASES)]
+        p = emu.plan(perm, size_a, alpha, beta, dtype)
+        _check(p, size_a, perm, alpha, beta, dtype, rng)
+
+
+@pytest.mark.parametrize("knobs", [
+    dict(kernel="generic"),
+    dict(run_a=4, run_b=4),
+    dict(run_a=3, run_b=5),
+    dict(run_a=1, run_b=1),
+    dict(max_blocks=3),
+    dict(lds_pad=-1),
+    dict(lds_pad=4),
+    dict(max_vec=1),
+    dict(max_vec=2),
+    dict(nontemporal=1),
+])
+def test_knobs_match_oracle(knobs):
+    rng = np.random.default_rng(11)
+    for it in range(40):
+        size_a, perm = random_problem(rng, max_dims=5, max_numel=20000)
+        dtype = "f32" if it % 3 else "f64"
+        alpha, beta = CASES[it % len(CASES)]
+        p = emu.plan(perm, size_a, alpha, beta, dtype, **knobs)
+        _check(p, size_a, perm, alpha, beta, dtype, rng)
+
+
+@pytest.mark.parametrize("va,vb", [(1, 1), (1, 4), (4, 1), (2, 2), (2, 4)])
+def test_narrow_vectors_as_for_misaligned_pointers(va, vb):
+    """hptt_exec narrows the vector widths for less aligned pointers."""
+    rng = np.random.default_rng(13)
+    for size_a, perm in [((64, 33), (1, 0)), ((24, 20, 16, 5), (3, 2, 0, 1)),
+                         ((3, 2, 64, 7, 32), (4, 2, 0, 3, 1)), ((96, 7, 9), (0, 2, 1))]:
+        p = emu.plan(perm, size_a, 1.5, 0.5, "f32")
+        _check(p, size_a, perm, 1.5, 0.5, "f32", rng, va=min(va, p.info["vec_a"]),
+               vb=min(vb, p.info["vec_b"]))
+
+
+def test_edge_tiles_and_tails():
+    rng = np.random.default_rng(17)
+    for size_a, perm in [((65, 65), (1, 0)), ((33, 17, 5), (2, 0, 1)), ((7, 130, 3), (1, 2, 0)),
+                         ((5, 3, 65, 9), (3, 2, 0, 1)), ((129, 3), (1, 0)), ((17, 1, 33), (2, 1, 0))]:
+        for dtype in ("f32", "f64"):
+            p = emu.plan(perm, size_a, 1.0, 0.0, dtype)
+            _check(p, size_a, perm, 1.0, 0.0, dtype, rng)
+
+
+@pytest.mark.parametrize("w", WORKLOADS[:1], ids=lambda w: w.name)
+def test_small_workload_matches_oracle(w):
+    rng = np.random.default_rng(w.seed_a)
+    p = emu.plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype)
+    _check(p, w.size_a, w.perm, w.alpha, w.beta, w.dtype, rng)
+
+
+@pytest.mark.parametrize("w", WORKLOADS, ids=lambda w: w.name)
+def test_full_size_geometry(w):
+    """Dry run of every workgroup of each full-size workload: every offset in
+    bounds and aligned, every B element written exactly once."""
+    p = emu.plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype)
+    err, msg, cnt = emu.run(p, counts=True)
+    assert err == 0, msg
+    assert cnt.min() == 1 and cnt.max() == 1

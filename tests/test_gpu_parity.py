@@ -1,0 +1,225 @@
+"""Parity of the HIP path with the CPU oracle, element by element, on an
+MI355X.  Every call goes through the C ABI (paper_1704_04374_amd.hptt).
+
+Bar: bit-exact.  The kernels and the oracle both compute
+fl(fl(alpha*a) + fl(beta*b)) in the tensor dtype with no fused multiply-add
+(and a raw copy for alpha = 1, beta = 0), so no rounding difference is
+expected; the relative-error bound 2^-22 (fp32) / 2^-51 (fp64) is what the
+results must meet at the very least, and is reported on failure.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as orc
+from paper_1704_04374_amd import hptt
+from paper_1704_04374_amd.workloads import WORKLOADS, NUMPY_DTYPE, inputs, random_problem
+
+pytestmark = pytest.mark.gpu
+
+REL_BOUND = {"f32": 2.0 ** -22, "f64": 2.0 ** -51}
+TORCH = {"f32": torch.float32, "f64": torch.float64}
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _assert_parity(got: np.ndarray, want: np.ndarray, dtype: str, what: str):
+    if np.array_equal(got, want, equal_nan=True):
+        return
+    bad = np.flatnonzero(~((got == want) | (np.isnan(got) & np.isnan(want))))
+    with np.errstate(all="ignore"):
+        rel = np.abs(got[bad].astype(np.float64) - want[bad]) / np.maximum(
+            np.abs(want[bad].astype(np.float64)), np.finfo(np.float64).tiny)
+    raise AssertionError(f"{what}: {bad.size} elements differ, first at {bad[0]} "
+                         f"(got {got[bad[0]]!r}, want {want[bad[0]]!r}), max rel err "
+                         f"{rel.max():.3e} (bound {REL_BOUND[dtype]:.3e})")
+
+
+def _rand(rng, n, dtype):
+    return (rng.integers(-(1 << 20), 1 << 20, size=n) / float(1 << 20)).astype(NUMPY_DTYPE[dtype])
+
+
+def _run_case(size_a, perm, alpha, beta, dtype, rng, **knobs):
+    p = hptt.create_plan(perm, size_a, alpha, beta, dtype, **knobs)
+    n = p.numel
+    A = _rand(rng, n, dtype)
+    B0 = _rand(rng, n, dtype) if beta != 0 else np.full(n, np.nan, NUMPY_DTYPE[dtype])
+    want = orc.transpose(A, size_a, perm, alpha, beta, B0 if beta != 0 else None)
+    dA = torch.from_numpy(A).cuda()
+    dB = torch.from_numpy(B0).cuda()
+    p.exec(dA, dB)
+    torch.cuda.synchronize()
+    _assert_parity(dB.cpu().numpy(), want, dtype, p.describe())
+    return p
+
+
+@pytest.mark.parametrize("w", WORKLOADS, ids=lambda w: w.name)
+def test_workload_full_size(w):
+    """Each named workload at its full size, in the launch configuration the
+    benchmark times, against the whole oracle result."""
+    _say(f"[parity] {w.describe()}")
+    A, B0 = inputs(w)
+    if B0 is None:
+        B0 = torch.full_like(A, float("nan"))   # beta = 0: B must be fully overwritten
+    want = orc.transpose(A.numpy(), w.size_a, w.perm, w.alpha, w.beta,
+                         B0.numpy() if w.beta != 0 else None)
+    p = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype)
+    dA, dB = A.cuda(), B0.cuda()
+    p.exec(dA, dB)
+    torch.cuda.synchronize()
+    got = dB.cpu().numpy()
+    _assert_parity(got, want, w.dtype, p.describe())
+    # one-by-one samples from the oracle agree too (first, last, random)
+    rng = np.random.default_rng(w.seed_a)
+    offs = np.concatenate([[0, w.numel - 1], rng.integers(0, w.numel, 2000)])
+    samp = orc.sample(A.numpy(), w.size_a, w.perm, w.alpha, w.beta,
+                      B0.numpy() if w.beta != 0 else None, offs)
+    _assert_parity(got[offs], samp, w.dtype, "sampled " + p.describe())
+
+
+def test_random_sweep():
+    """Seeded sweep of small odd shapes: rank 1..6, extents with tails, both
+    dtypes, several alpha and beta, every kernel class."""
+    rng = np.random.default_rng(4374)
+    seen = set()
+    alphas, betas = (1.0, 1.5, -0.3), (0.0, 1.0, 0.5, -1.25)
+    for it in range(160):
+        size_a, perm = random_problem(rng, max_dims=6, max_numel=1 << 18)
+        dtype = ("f32", "f64")[it % 2]
+        alpha, beta = alphas[it % 3], betas[(it // 3) % 4]
+        p = _run_case(size_a, perm, alpha, beta, dtype, rng)
+        seen.add(p.info["kernel"])
+    assert {"tile", "axpby", "generic", "stream"} <= seen
+
+
+@pytest.mark.parametrize("knobs", [dict(kernel="generic"), dict(run_a=8, run_b=8),
+                                   dict(run_a=3, run_b=5), dict(max_blocks=7),
+                                   dict(max_vec=1), dict(nontemporal=1), dict(lds_pad=-1)],
+                         ids=lambda k: ",".join(f"{a}={b}" for a, b in k.items()))
+def test_forced_variants(knobs):
+    rng = np.random.default_rng(99)
+    for size_a, perm in [((65, 65), (1, 0)), ((33, 17, 5), (2, 0, 1)),
+                         ((24, 20, 16, 5, 3), (4, 2, 0, 3, 1)), ((3, 2, 64, 9, 32), (4, 2, 0, 3, 1))]:
+        for dtype, (alpha, beta) in (("f32", (1.0, 0.0)), ("f64", (1.5, -0.5))):
+            _run_case(size_a, perm, alpha, beta, dtype, rng, **knobs)
+
+
+def test_stream_kernel_variants():
+    rng = np.random.default_rng(5)
+    for size_a, perm in [((96, 7, 9, 5), (0, 3, 2, 1)), ((33, 8, 8), (0, 2, 1)),
+                         ((16, 5, 6), (0, 2, 1))]:
+        for rpb in (0, 1, 3):
+            _run_case(size_a, perm, 2.0, 0.5, "f64", rng, kernel="stream", rows_per_block=rpb)
+            _run_case(size_a, perm, 1.0, 0.0, "f32", rng, kernel="stream", rows_per_block=rpb)
+
+
+def test_misaligned_pointers_fall_back():
+    """Tensors starting one element past a 16-byte boundary take narrower
+    vector accesses and stay correct."""
+    rng = np.random.default_rng(3)
+    for size_a, perm, dtype in [((64, 64), (1, 0), "f32"), ((3, 2, 64, 8, 32), (4, 2, 0, 3, 1), "f32"),
+                                ((96, 6, 7), (0, 2, 1), "f64"), ((1000,), (0,), "f32")]:
+        p = hptt.create_plan(perm, size_a, 1.5, 0.5, dtype)
+        n = p.numel
+        A = _rand(rng, n, dtype)
+        B0 = _rand(rng, n, dtype)
+        want = orc.transpose(A, size_a, perm, 1.5, 0.5, B0)
+        bufA = torch.zeros(n + 1, dtype=TORCH[dtype], device="cuda")
+        bufB = torch.zeros(n + 3, dtype=TORCH[dtype], device="cuda")
+        dA, dB = bufA[1:], bufB[3:3 + n]
+        dA.copy_(torch.from_numpy(A))
+        dB.copy_(torch.from_numpy(B0))
+        p.exec(dA, dB)
+        torch.cuda.synchronize()
+        _assert_parity(dB.cpu().numpy(), want, dtype, "misaligned " + p.describe())
+        assert bufB[:3].abs().sum().item() == 0      # nothing written before B
+
+
+def test_overlap_rejected_and_nothing_written():
+    p = hptt.create_plan((1, 0), (64, 64))
+    buf = torch.zeros(64 * 64 + 64, device="cuda")
+    with pytest.raises(hptt.HpttError) as e:
+        p.exec(buf[:4096].data_ptr(), buf[64:].data_ptr())
+    assert e.value.status == 3
+    torch.cuda.synchronize()
+    assert buf.abs().sum().item() == 0
+
+
+def test_zero_size_is_noop():
+    p = hptt.create_plan((2, 1, 0), (4, 0, 3))
+    assert p.info["kernel"] == "none"
+    p.exec(0, 0)
+    torch.cuda.synchronize()
+
+
+def test_alpha_zero_beta_one_keeps_b():
+    """The non-destructive autotuning setting of Section 3.1: alpha = 0,
+    beta = 1 rewrites B with its own value (A finite, footnote 5)."""
+    rng = np.random.default_rng(8)
+    for size_a, perm in [((128, 96), (1, 0)), ((24, 20, 16), (2, 0, 1))]:
+        A = torch.from_numpy(_rand(rng, int(np.prod(size_a)), "f32")).cuda()
+        B0 = torch.from_numpy(_rand(rng, A.numel(), "f32") + np.float32(0.5)).cuda()
+        B = B0.clone()
+        hptt.create_plan(perm, size_a, 0.0, 1.0).exec(A, B)
+        torch.cuda.synchronize()
+        assert torch.equal(B, B0)
+
+
+def test_streams_and_plan_reuse():
+    """One plan executed on two streams and repeatedly; results independent."""
+    rng = np.random.default_rng(21)
+    size_a, perm = (256, 96, 8), (1, 2, 0)
+    p = hptt.create_plan(perm, size_a, 1.0, 0.0)
+    n = p.numel
+    As = [_rand(rng, n, "f32") for _ in range(2)]
+    wants = [orc.transpose(a, size_a, perm) for a in As]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    dA = [torch.from_numpy(a).cuda() for a in As]
+    dB = [torch.empty_like(x) for x in dA]
+    torch.cuda.synchronize()
+    for _ in range(3):
+        with torch.cuda.stream(s1):
+            p.exec(dA[0], dB[0])
+        with torch.cuda.stream(s2):
+            p.exec(dA[1], dB[1])
+    torch.cuda.synchronize()
+    for b, w in zip(dB, wants):
+        _assert_parity(b.cpu().numpy(), w, "f32", p.describe())
+
+
+def test_inverse_round_trip_on_gpu():
+    """Pi then Pi^-1 returns A bit for bit on the device."""
+    rng = np.random.default_rng(31)
+    for size_a, perm in [((24, 20, 16, 24, 3), (4, 2, 0, 3, 1)), ((130, 70), (1, 0))]:
+        inv = [0] * len(perm)
+        for k, q in enumerate(perm):
+            inv[q] = k
+        size_b = tuple(size_a[q] for q in perm)
+        A = torch.from_numpy(_rand(rng, int(np.prod(size_a)), "f64")).cuda()
+        B = torch.empty_like(A)
+        C = torch.empty_like(A)
+        hptt.create_plan(perm, size_a, dtype="f64").exec(A, B)
+        hptt.create_plan(inv, size_b, dtype="f64").exec(B, C)
+        torch.cuda.synchronize()
+        assert torch.equal(A, C)
+
+
+def test_yardsticks():
+    n = 1 << 20
+    x = torch.rand(n, device="cuda")
+    y = torch.rand(n, device="cuda")
+    z = torch.empty_like(x)
+    hptt.yardstick_copy(x, z, n * 4)
+    torch.cuda.synchronize()
+    assert torch.equal(x, z)
+    y0 = y.clone()
+    hptt.yardstick_axpby("f32", 2.0, x, 0.5, y, n)
+    torch.cuda.synchronize()
+    assert torch.equal(y.cpu(), 2.0 * x.cpu() + 0.5 * y0.cpu())
+    hptt.yardstick_fill(z, n * 4, 0)
+    torch.cuda.synchronize()
+    assert z.abs().sum().item() == 0

@@ -1,0 +1,213 @@
+"""The C ABI and the plan builder, on the CPU (hptt_create_plan makes no HIP
+call; hptt_exec's argument checks run before any launch)."""
+from __future__ import annotations
+
+import ctypes
+import glob
+import os
+import re
+
+import pytest
+
+from conftest import ROOT, golden
+from paper_1704_04374_amd import hptt
+from paper_1704_04374_amd.workloads import WORKLOADS, BY_NAME
+
+
+def _declared_functions():
+    names = set()
+    for path in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = open(path).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        names.update(re.findall(r"\b(hptt_[a-z0-9_]+)\s*\(", text))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(hptt.LIB_PATH)
+    declared = _declared_functions()
+    assert declared, "no declarations found"
+    for name in sorted(declared):
+        assert hasattr(lib, name), f"{name} declared but not exported"
+    assert declared == set(hptt.EXPORTS)
+
+
+def test_status_strings():
+    lib = hptt.library()
+    for code in range(6):
+        assert lib.hptt_status_string(code)
+    assert lib.hptt_status_string(99) == b"unknown status"
+
+
+def test_fig1_plan():
+    """Fig. 1: B_{i2 i1} <- A_{i1 i2}, A 6x4: a 2-D transpose, nothing to fuse."""
+    rows = {r[0]: r[1:] for r in golden("fig1_plan.txt")}
+    size_a = tuple(int(x) for x in rows["sizeA"])
+    perm = tuple(int(x) for x in rows["perm"])
+    info = hptt.create_plan(perm, size_a).info
+    assert info["size"] == size_a and info["perm"] == perm
+    assert info["kernel"] == "tile" and info["dims_a"] == 1 and info["dims_b"] == 1
+
+
+def test_fn4_fusion():
+    """Footnote 4: B_{i2 i3 i1} <- A_{i1 i2 i3} becomes a 2-D problem."""
+    rows = {r[0]: r[1:] for r in golden("fn4_fusion.txt")}
+    perm = tuple(int(x) for x in rows["perm"])
+    fused = tuple(int(x) for x in rows["fused_perm"])
+    info = hptt.create_plan(perm, (6, 7, 8)).info
+    assert info["ndim"] == 2 and info["size"] == (6, 56) and info["perm"] == fused
+
+
+@pytest.mark.parametrize("perm,size,fsize,fperm", [
+    ((2, 1, 0), (5, 1, 7), (5, 7), (1, 0)),            # extent-1 index dropped
+    ((0, 1, 2), (3, 4, 5), (60,), (0,)),               # identity fuses to one index
+    ((1, 0), (1, 1), (1,), (0,)),                      # all extents 1
+    ((0, 2, 1, 3), (4, 5, 6, 7), (4, 5, 6, 7), (0, 2, 1, 3)),
+    ((2, 3, 0, 1), (2, 3, 4, 5), (6, 20), (1, 0)),     # two superindices
+    ((3, 0, 1, 2), (2, 3, 4, 5), (24, 5), (1, 0)),
+    ((1, 2, 3, 0), (2, 1, 4, 5), (2, 20), (1, 0)),     # extent 1 inside a group
+])
+def test_fusion_cases(perm, size, fsize, fperm):
+    info = hptt.create_plan(perm, size).info
+    assert info["size"] == fsize and info["perm"] == fperm
+
+
+def test_kernel_classes():
+    assert hptt.create_plan((0, 1), (5, 7)).info["kernel"] == "axpby"
+    assert hptt.create_plan((0, 2, 1), (64, 5, 7)).info["kernel"] == "stream"
+    assert hptt.create_plan((0, 2, 1), (3, 5, 7)).info["kernel"] == "generic"   # 12-byte rows
+    assert hptt.create_plan((1, 0), (5, 7)).info["kernel"] == "tile"
+    assert hptt.create_plan((1, 0), (0, 7)).info["kernel"] == "none"
+
+
+# What the plan builder must decide for each named workload.
+EXPECTED = {
+    "transpose3d_48x40x32_f32": dict(kernel="tile", size=(1920, 32), perm=(1, 0), run_a=64,
+                                     run_b=32, tiles=30),
+    "transpose2d_8192x8192_f32": dict(kernel="tile", size=(8192, 8192), perm=(1, 0), run_a=64,
+                                      run_b=64, tiles=16384),
+    "transpose6d_24x20x16x24x18x20_f32": dict(kernel="tile", size=(24, 20, 16, 24, 18, 20),
+                                              perm=(5, 2, 0, 4, 1, 3), run_a=96, run_b=160,
+                                              dims_a=2, dims_b=2, tiles=4320),
+    "transpose4d_96x96x96x96_keep1_f64": dict(kernel="stream", size=(96, 96, 96, 96),
+                                              perm=(0, 3, 2, 1), run_b=96, vec_a=2, vec_b=2),
+    "transpose5d_3x2x640x480x96_f32": dict(kernel="tile", size=(3, 2, 640, 480, 96),
+                                           perm=(4, 2, 0, 3, 1), run_a=96, run_b=96, dims_a=3,
+                                           dims_b=1, tiles=19200),
+}
+
+
+@pytest.mark.parametrize("name", sorted(EXPECTED))
+def test_workload_plans(name):
+    w = BY_NAME[name]
+    info = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype).info
+    for k, v in EXPECTED[name].items():
+        assert info[k] == v, (k, info[k], v)
+    assert info["mode"] == ("copy" if (w.alpha, w.beta) == (1.0, 0.0)
+                            else "scale" if w.beta == 0 else "axpby")
+    assert info["numel"] == w.numel
+    if info["kernel"] == "tile":
+        assert info["vec_a"] == info["vec_b"] == 16 // w.elem_bytes
+        assert info["lds_bytes"] <= 65536
+        # runs of whole 128-byte lines on both sides
+        assert (info["run_a"] * w.elem_bytes) % 128 == 0
+        assert (info["run_b"] * w.elem_bytes) % 128 == 0
+        assert info["lds_pitch"] % 2 == 1
+
+
+def test_alpha_beta_rounded_to_dtype():
+    p = hptt.create_plan((1, 0), (4, 4), alpha=0.1, beta=0.0, dtype="f32")
+    assert p.info["mode"] == "scale"
+    # 1 + 2^-30 rounds to 1.0 in float: a copy
+    assert hptt.create_plan((1, 0), (4, 4), alpha=1 + 2 ** -30, dtype="f32").info["mode"] == "copy"
+    assert hptt.create_plan((1, 0), (4, 4), alpha=1 + 2 ** -30, dtype="f64").info["mode"] == "scale"
+
+
+def _raw_create(perm, size, dtype=0, options=None, n=None):
+    lib = hptt.library()
+    n = len(perm) if n is None else n
+    pm = (ctypes.c_int32 * max(len(perm), 1))(*perm)
+    sz = (ctypes.c_int64 * max(len(size), 1))(*size)
+    h = ctypes.c_void_p(12345)
+    if options is None:
+        st = lib.hptt_create_plan(ctypes.byref(h), pm, n, sz, 1.0, 0.0, dtype)
+    else:
+        st = lib.hptt_create_plan_ex(ctypes.byref(h), pm, n, sz, 1.0, 0.0, dtype,
+                                     ctypes.byref(options))
+    return st, h
+
+
+@pytest.mark.parametrize("perm,size,dtype,n", [
+    ((0, 0), (2, 3), 0, None),       # not a permutation
+    ((0, 2), (2, 3), 0, None),       # index out of range
+    ((1, 0), (2, -1), 0, None),      # negative extent
+    ((1, 0), (2, 3), 7, None),       # unknown dtype
+    ((0,), (2,), 0, 0),              # N = 0
+    (tuple(range(17)), (1,) * 17, 0, None),  # N above 16
+])
+def test_invalid_problems(perm, size, dtype, n):
+    st, h = _raw_create(perm, size, dtype, n=n)
+    assert st == 1 and not h.value
+
+
+def test_null_arguments():
+    lib = hptt.library()
+    pm = (ctypes.c_int32 * 2)(1, 0)
+    sz = (ctypes.c_int64 * 2)(2, 3)
+    assert lib.hptt_create_plan(None, pm, 2, sz, 1.0, 0.0, 0) == 1
+    h = ctypes.c_void_p()
+    assert lib.hptt_create_plan(ctypes.byref(h), None, 2, sz, 1.0, 0.0, 0) == 1
+    assert lib.hptt_create_plan(ctypes.byref(h), pm, 2, None, 1.0, 0.0, 0) == 1
+    assert lib.hptt_plan_info(None, None) == 1
+    assert lib.hptt_describe_plan(None, None, 0) == 1
+    assert lib.hptt_destroy_plan(None) == 0
+
+
+@pytest.mark.parametrize("field,value", [("kernel", 9), ("kernel", 1), ("run_a", -1),
+                                         ("nontemporal", 3), ("lds_pad", 65), ("max_blocks", -2)])
+def test_invalid_options(field, value):
+    opt = hptt.Options()
+    setattr(opt, field, value)
+    st, h = _raw_create((1, 0), (4, 4), options=opt)
+    assert st == 1 and not h.value
+
+
+def test_forced_kernel_that_does_not_apply():
+    with pytest.raises(hptt.HpttError) as e:
+        hptt.create_plan((0, 2, 1), (64, 5, 7), kernel="tile")
+    assert e.value.status == 2
+    with pytest.raises(hptt.HpttError):
+        hptt.create_plan((1, 0), (64, 5), kernel="stream")
+    with pytest.raises(hptt.HpttError):
+        hptt.create_plan((1, 0), (64, 5), kernel="axpby")
+    assert hptt.create_plan((1, 0), (64, 5), kernel="generic").info["kernel"] == "generic"
+    assert hptt.create_plan((0, 2, 1), (2, 5, 7), kernel="stream").info["kernel"] == "stream"
+
+
+def test_exec_argument_checks_before_launch():
+    """hptt_exec rejects bad arguments before touching the GPU."""
+    lib = hptt.library()
+    vp = ctypes.c_void_p
+    assert lib.hptt_exec(None, vp(4096), vp(8192), None) == 1
+    empty = hptt.create_plan((1, 0), (0, 5))
+    assert lib.hptt_exec(empty.handle, None, None, None) == 0       # nothing to do
+    p = hptt.create_plan((1, 0), (4, 4))
+    assert lib.hptt_exec(p.handle, None, vp(1 << 20), None) == 1     # null A
+    assert lib.hptt_exec(p.handle, vp(1 << 20), None, None) == 1     # null B
+    assert lib.hptt_exec(p.handle, vp((1 << 20) + 2), vp(1 << 21), None) == 1   # misaligned
+    assert lib.hptt_exec(p.handle, vp(1 << 20), vp((1 << 20) + 60), None) == 3  # overlap
+    assert lib.hptt_exec(p.handle, vp(1 << 20), vp(1 << 20), None) == 3          # in place
+
+
+def test_describe():
+    d = hptt.create_plan((1, 0), (8192, 8192)).describe()
+    assert "kernel=tile" in d and "fused=(8192,8192)" in d
+
+
+def test_workload_bytes_follow_eq2():
+    """Eq. (2): lambda = 2 when beta = 0 and 3 otherwise."""
+    table = {float(b): int(l) for b, l in golden("eq2_lambda.txt")}
+    for w in WORKLOADS:
+        assert w.lam == table.get(w.beta, 3 if w.beta else 2)
+        assert w.moved_bytes == w.lam * w.numel * w.elem_bytes
