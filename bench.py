@@ -4,7 +4,8 @@
 
 One step is one execution of the plan (all of the hot path: the plan is
 built once, then each step launches the kernel the plan chose) on inputs
-already resident in HBM.  The headline workload is the 8192 x 8192 fp32
+already resident in HBM.  Steps cycle through enough buffer sets that no
+launch finds its tensors in the 256 MB last-level cache.  The headline workload is the 8192 x 8192 fp32
 matrix transpose; the other named workloads are reported in ``per_workload``.
 
 Bandwidth follows Eq. (2) of the paper: lambda * S bytes per transposition
@@ -16,7 +17,7 @@ GB/s (1e9 B/s).  Context printed on the same line:
   - yardsticks: a same-run 16-byte-per-lane copy kernel (2S) and, for
     beta != 0, an axpby kernel (3S) -- the SAXPY yardstick of Table 2 --
     and hipMemcpyAsync device-to-device;
-  - flushed: the paper's protocol (Section 4), best and median of single
+  - cold: the paper's protocol (Section 4), best and median of single
     launches with the caches cleared in between;
   - cpu_baseline: the CPU oracle on this machine's host, single-threaded.
 """
@@ -38,6 +39,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD published peak
 HEADLINE = "transpose2d_8192x8192_f32"
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 FLUSH_BYTES = 1 << 30           # > 256 MB last-level cache + 8 x 4 MB L2
+ROTATE_BYTES = 2 << 30          # traffic between two uses of one buffer set
 
 
 def kernel_source_hash() -> str:
@@ -74,83 +76,102 @@ def _events(torch, n):
 
 
 def time_launches(torch, fn, steps: int, warmup: int):
-    """Run fn() warmup times, then `steps` times back to back with HIP events
-    around each launch on the current stream.  Returns (wall_s, [ms])."""
-    for _ in range(warmup):
-        fn()
+    """Run fn(i) for i < warmup, then for `steps` more i back to back with HIP
+    events around each launch on the current stream.  Returns (wall_s, [ms])."""
+    for i in range(warmup):
+        fn(i)
     torch.cuda.synchronize()
     starts, ends = _events(torch, steps), _events(torch, steps)
     t0 = time.perf_counter()
     for i in range(steps):
         starts[i].record()
-        fn()
+        fn(warmup + i)
         ends[i].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     return wall, [s.elapsed_time(e) for s, e in zip(starts, ends)]
 
 
-def time_flushed(torch, hptt, fn, flush_buf, reps: int):
-    """Single launches with the caches cleared before each (Section 4)."""
+def time_cold(torch, hptt, fn, flush_buf, sink, reps: int):
+    """Single launches, each after a read-only sweep of 1 GiB that leaves the
+    caches holding only clean, unrelated lines ("caches are cleared in between
+    runs", Section 4)."""
     ms = []
     for i in range(reps):
-        hptt.yardstick_fill(flush_buf, flush_buf.numel() * 4, i)
+        hptt.yardstick_read(flush_buf, flush_buf.numel() * 4, sink)
         s, e = _events(torch, 2)
         s.record()
-        fn()
+        fn(i)
         e.record()
         torch.cuda.synchronize()
         ms.append(s.elapsed_time(e))
     return ms
 
 
-def measure_workload(torch, hptt, w, steps, warmup, reps, flush_buf, full: bool):
-    """Time one workload: the transposition and its same-run yardsticks."""
+def rotation(w) -> int:
+    """Buffer sets cycled through by back-to-back steps, so that at least
+    ROTATE_BYTES of other traffic separate two uses of the same tensors and no
+    launch finds its inputs in the 256 MB last-level cache."""
+    per_set = 2 * w.tensor_bytes
+    return max(2, min(8, -(-ROTATE_BYTES // per_set)))
+
+
+def measure_workload(torch, hptt, w, steps, warmup, reps, flush_buf, sink, full: bool):
+    """Time one workload: the transposition and its same-run yardsticks, all
+    over the same rotating buffer sets."""
     tdt = torch.float32 if w.dtype == "f32" else torch.float64
     gen = torch.Generator(device="cuda").manual_seed(w.seed_a)
-    A = torch.rand(w.numel, dtype=tdt, device="cuda", generator=gen) * 2 - 1
-    B = torch.rand(w.numel, dtype=tdt, device="cuda", generator=gen) * 2 - 1
+    k = rotation(w)
+    As = [torch.rand(w.numel, dtype=tdt, device="cuda", generator=gen) * 2 - 1 for _ in range(k)]
+    Bs = [torch.rand(w.numel, dtype=tdt, device="cuda", generator=gen) * 2 - 1 for _ in range(k)]
     t0 = time.perf_counter()
     plan = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype)
     plan_us = (time.perf_counter() - t0) * 1e6
     moved = w.moved_bytes
     S = w.tensor_bytes
     out = {"workload": w.name, "plan": plan.describe(), "plan_create_us": round(plan_us, 1),
-           "bytes_per_launch": moved}
+           "bytes_per_launch": moved, "buffer_sets": k}
 
-    wall, ms = time_launches(torch, lambda: plan.exec(A, B), steps, warmup)
-    avg_ms = sum(ms) / len(ms)
+    def transpose(i):
+        plan.exec(As[i % k], Bs[i % k])
+
+    def copy(i):
+        hptt.yardstick_copy(As[i % k], Bs[i % k], S)
+
+    def memcpy(i):
+        Bs[i % k].copy_(As[i % k])
+
+    def axpby(i):
+        hptt.yardstick_axpby(w.dtype, w.alpha, As[i % k], w.beta, Bs[i % k], w.numel)
+
+    def gbs(nbytes, ms):
+        return nbytes / (sum(ms) / len(ms) * 1e-3) / 1e9
+
+    wall, ms = time_launches(torch, transpose, steps, warmup)
     out["ms_per_step"] = wall * 1e3 / steps
     out["gbs"] = moved * steps / wall / 1e9
-    out["kernel_avg_ms"] = avg_ms
-    out["kernel_gbs"] = moved / (avg_ms * 1e-3) / 1e9
-
-    # same-run copy yardstick: read S, write S
-    C = torch.empty_like(A)
-    _, cms = time_launches(torch, lambda: hptt.yardstick_copy(A, C, S), steps, warmup)
-    out["copy_gbs"] = 2 * S / (sum(cms) / len(cms) * 1e-3) / 1e9
-    _, mms = time_launches(torch, lambda: C.copy_(A), steps, warmup)
-    out["hipmemcpy_d2d_gbs"] = 2 * S / (sum(mms) / len(mms) * 1e-3) / 1e9
+    out["kernel_avg_ms"] = sum(ms) / len(ms)
+    out["kernel_gbs"] = gbs(moved, ms)
+    out["copy_gbs"] = gbs(2 * S, time_launches(torch, copy, steps, warmup)[1])
+    out["hipmemcpy_d2d_gbs"] = gbs(2 * S, time_launches(torch, memcpy, steps, warmup)[1])
     if w.beta != 0:
-        _, ams = time_launches(torch, lambda: hptt.yardstick_axpby(w.dtype, w.alpha, A, w.beta, C,
-                                                                   w.numel), steps, warmup)
-        out["axpby_gbs"] = 3 * S / (sum(ams) / len(ams) * 1e-3) / 1e9
+        out["axpby_gbs"] = gbs(3 * S, time_launches(torch, axpby, steps, warmup)[1])
         out["pct_of_axpby"] = 100 * out["kernel_gbs"] / out["axpby_gbs"]
     out["pct_of_copy"] = 100 * out["kernel_gbs"] / out["copy_gbs"]
     out["pct_of_hbm_peak"] = 100 * out["kernel_gbs"] / HBM_PEAK_GBS
-    if full and flush_buf is not None:
-        fms = time_flushed(torch, hptt, lambda: plan.exec(A, B), flush_buf, reps)
-        cfs = time_flushed(torch, hptt, lambda: hptt.yardstick_copy(A, C, S), flush_buf, reps)
-        out["flushed"] = {
+    if full:
+        fms = time_cold(torch, hptt, transpose, flush_buf, sink, reps)
+        cfs = time_cold(torch, hptt, copy, flush_buf, sink, reps)
+        out["cold"] = {
             "reps": reps,
             "median_gbs": moved / (statistics.median(fms) * 1e-3) / 1e9,
             "best_gbs": moved / (min(fms) * 1e-3) / 1e9,
             "best_gibs_eq2": moved / (min(fms) * 1e-3) / 2 ** 30,
             "copy_median_gbs": 2 * S / (statistics.median(cfs) * 1e-3) / 1e9,
         }
-        out["flushed"]["median_pct_of_copy"] = (100 * out["flushed"]["median_gbs"]
-                                                / out["flushed"]["copy_median_gbs"])
-    del A, B, C
+        out["cold"]["median_pct_of_copy"] = (100 * out["cold"]["median_gbs"]
+                                             / out["cold"]["copy_median_gbs"])
+    del As, Bs
     torch.cuda.empty_cache()
     return out
 
@@ -276,19 +297,20 @@ def main():
         build.build()
     torch.cuda.set_device(0)
     head = BY_NAME[args.workload]
-    flush_buf = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
+    flush_buf = torch.zeros(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
+    sink = torch.zeros(4096, dtype=torch.int32, device="cuda")
     print(f"[bench] device {torch.cuda.get_device_name(0)}; headline {head.describe()}",
           file=sys.stderr, flush=True)
 
     headline = measure_workload(torch, hptt, head, args.steps, args.warmup, args.reps, flush_buf,
-                                full=not args.only_headline)
+                                sink, full=not args.only_headline)
     print(f"[bench] {head.name}: {headline['gbs']:.0f} GB/s, {headline['pct_of_copy']:.1f}% "
           f"of copy", file=sys.stderr, flush=True)
     per = {}
     if not args.only_headline:
         for w in WORKLOADS:
             r = headline if w.name == head.name else measure_workload(
-                torch, hptt, w, args.steps, args.warmup, args.reps, flush_buf, full=True)
+                torch, hptt, w, args.steps, args.warmup, args.reps, flush_buf, sink, full=True)
             per[w.name] = {k: (round(v, 2) if isinstance(v, float) else v) for k, v in r.items()}
             print(f"[bench] {w.name}: kernel {r['kernel_gbs']:.0f} GB/s, "
                   f"{r['pct_of_copy']:.1f}% of copy, {r['pct_of_hbm_peak']:.1f}% of peak",
@@ -318,7 +340,8 @@ def main():
         "pct_of_copy": round(headline["pct_of_copy"], 2),
         "copy_gbs": round(headline["copy_gbs"], 1),
         "hipmemcpy_d2d_gbs": round(headline["hipmemcpy_d2d_gbs"], 1),
-        "flushed": headline.get("flushed"),
+        "buffer_sets": headline["buffer_sets"],
+        "cold": headline.get("cold"),
         "plan": headline["plan"],
         "plan_create_us": headline["plan_create_us"],
         "kernel_source_hash": kernel_source_hash(),

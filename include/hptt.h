@@ -76,9 +76,13 @@ typedef struct {
     int32_t run_b;         /* TILE: target length of the contiguous B run (rows) */
     int32_t max_vec;       /* cap on the vector width in elements (1 = scalar) */
     int32_t nontemporal;   /* 1: non-temporal B stores when beta = 0; 2: never */
-    int32_t rows_per_block;/* STREAM: rows of the kept index per workgroup */
     int32_t lds_pad;       /* TILE: LDS row padding in elements, 0 = default, -1 = none */
     int32_t max_blocks;    /* cap on the grid; workgroups loop over tiles beyond it */
+    int32_t tile_order;    /* TILE: 1 = tiles in grid-digit order, 2 = diagonal
+                              (second grid digit rotated by the first) */
+    int32_t pipeline;      /* TILE: 1 = one tile per workgroup, 2 = persistent
+                              workgroups that fetch the next tile while writing
+                              the current one */
 } hptt_options_t;
 
 /* What the plan builder decided; for inspection and tests. */
@@ -90,18 +94,22 @@ typedef struct {
     int64_t numel;
     int32_t elem_bytes;
     int64_t run_a;                     /* TILE: A-run (columns) of a tile, elements */
-    int64_t run_b;                     /* TILE: B-run (rows); STREAM: row length */
+    int64_t run_b;                     /* TILE: B-run (rows); STREAM: kept row length */
     int32_t dims_a;                    /* TILE: fused A indices inside the A run */
     int32_t dims_b;                    /* TILE: fused B positions inside the B run */
     int32_t vec_a;                     /* vector width of A accesses for 16-byte aligned bases */
     int32_t vec_b;                     /* vector width of B accesses */
     int32_t lds_pitch;                 /* TILE: LDS row pitch in elements */
     int32_t lds_bytes;                 /* LDS per workgroup */
-    int64_t tiles;                     /* TILE: tiles; STREAM: row groups; others: work items */
+    int64_t tiles;                     /* TILE: tiles; STREAM, AXPBY: 16-byte vectors;
+                                          GENERIC: elements */
     int64_t grid;                      /* workgroups launched */
     int32_t block;                     /* threads per workgroup */
     int32_t nontemporal;               /* 1 when B is written with non-temporal stores */
     int32_t mode;                      /* 0 raw copy, 1 scale (beta = 0), 2 alpha*A + beta*B */
+    int32_t tile_order;                /* TILE: 1 grid-digit order, 2 diagonal */
+    int32_t pipeline;                  /* TILE: A vectors per thread held across tiles
+                                          by the persistent kernel, 0 = not used */
 } hptt_plan_info_t;
 
 /*

@@ -37,6 +37,12 @@ hptt_status_t hptt_yardstick_axpby(hptt_dtype_t dtype, double alpha, const void 
  * Section 4). */
 hptt_status_t hptt_yardstick_fill(void *buf, size_t bytes, uint32_t value, hipStream_t stream);
 
+/* Read `bytes` bytes of buf (16-byte aligned, a multiple of 16) and write
+ * one 32-bit checksum per workgroup into sink (at least 4096 bytes).  Reading
+ * more than the last-level cache leaves it holding only clean lines of buf,
+ * so the next kernel starts cold and owes no write-back of earlier data. */
+hptt_status_t hptt_yardstick_read(const void *buf, size_t bytes, void *sink, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -11,6 +11,7 @@ namespace hptt {
 
 constexpr int kMaxDims = 16;  // = HPTT_MAX_DIMS
 constexpr int kBlock = 256;   // threads per workgroup: 4 waves of 64
+constexpr int kItems = 4;     // vectors per lane of the streaming kernels
 
 // Unsigned division of n < 2^32 by a divisor 1 <= d < 2^32 fixed at plan
 // time, with one 32x32->64 multiply and a shift (Granlund and Montgomery,
@@ -57,7 +58,8 @@ struct TileArgs {
     uint32_t numTiles;
     int32_t gChunkC;     // grid digit that counts chunks of the last A-run index, or -1
     int32_t gChunkR;     // grid digit that counts chunks of the last B-run index, or -1
-    int32_t pad_;
+    int32_t skew;        // 1: grid digit 1 is shifted by digit 0 (diagonal tile order)
+    int32_t ipt;         // pipelined kernel: A vectors per thread per tile (4, 8 or 16), 0 = off
     int64_t cInner, cChunk, cLast;  // valid columns = cInner * min(cChunk, cLast - j*cChunk)
     int64_t rInner, rChunk, rLast;  // valid rows    = rInner * min(rChunk, rLast - j*rChunk)
     FastDiv cExt[kMaxDims];         // tile extents of the A-run indices
@@ -70,18 +72,22 @@ struct TileArgs {
 };
 
 // Kernel S: A's stride-1 index is also B's.  Each "row" is one full run of
-// that index, contiguous in both tensors; rows are visited in B order, so B
-// is one sequential stream and A a gather of rows.
+// that index, contiguous in both tensors.  Work item i = r*W + c is vector c
+// of row r (rows in B order, W vectors per row), so consecutive lanes write
+// consecutive B vectors and read whole rows of A.
+// hptt_exec may narrow the vector width V for less aligned pointers, so the
+// plan keeps W and the item count for each width: entry log2(V).
 struct StreamArgs {
-    int64_t rowLen;       // extent of the kept stride-1 index
-    int64_t numRows;      // numel / rowLen
-    int32_t rowsPerBlock; // rows handled by one workgroup per step
-    int32_t nO;           // outer B positions 1..N'-1
-    uint32_t numGroups;   // ceil(numRows / rowsPerBlock)
-    int32_t pad_;
+    int64_t rowLen;             // extent of the kept stride-1 index
+    int64_t numRows;            // numel / rowLen
+    uint32_t numItems[3];       // numRows * W for V = 1, 2, 4
+    int32_t nO;                 // outer B positions 1..N'-1
+    FastDiv W[3];               // vectors per row for V = 1, 2, 4
     FastDiv oExt[kMaxDims];     // extents of B positions 1.. (B order)
     int64_t oStrideA[kMaxDims]; // A strides of the indices at those positions
 };
+
+constexpr int log2_width(int v) { return v >= 4 ? 2 : v >= 2 ? 1 : 0; }
 
 // Fallback: one element per thread in B order, any shape.
 struct GenericArgs {

@@ -3,9 +3,10 @@
 // barrier between them; every global and LDS access goes through the memory
 // policy `Mem`, which on the device is a plain load or store.
 //
-// Index arithmetic is hoisted out of the per-element path: each workgroup
-// builds its tile's offset tables once, and the per-thread sweeps step their
-// (row, column) position incrementally instead of dividing per element.
+// Index arithmetic is hoisted out of the per-element path: each tile
+// workgroup builds its offset tables once and its sweeps step their (row,
+// column) position incrementally; the streaming kernels split a lane's item
+// number with plan-time magic-number division, once per 16-byte vector.
 #pragma once
 
 #include "hptt_args.h"
@@ -44,17 +45,29 @@ struct TileBase {
     int64_t validRows;  // rows (B-run elements) inside the tensor
 };
 
-// Split the tile number into grid digits (fastest first).
+// Split the tile number into grid digits (fastest first).  With g.skew the
+// second digit is rotated by the first (j1 <- (j1 + j0) mod n1), a bijection
+// of the tiles: workgroups that run at the same time then start their B runs
+// (and A runs) at many different offsets modulo a power-of-two stride instead
+// of one, which spreads their traffic over the HBM channels.
 __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
     TileBase tb;
     tb.a = 0;
     tb.b = 0;
     tb.validCols = g.runA;
     tb.validRows = g.runB;
+    uint32_t j0 = 0;
     for (int k = 0; k < g.nG; ++k) {
         uint32_t q = fast_div(t, g.gExt[k]);
-        int64_t j = int64_t(t - q * g.gExt[k].d);
+        uint32_t jj = t - q * g.gExt[k].d;
         t = q;
+        if (k == 0) j0 = jj;
+        if (k == 1 && g.skew) {
+            const uint32_t r = j0 - fast_div(j0, g.gExt[1]) * g.gExt[1].d;  // j0 mod n1
+            jj += r;
+            if (jj >= g.gExt[1].d) jj -= g.gExt[1].d;
+        }
+        const int64_t j = int64_t(jj);
         tb.a += j * g.gStrideA[k];
         tb.b += j * g.gStrideB[k];
         if (k == g.gChunkC) tb.validCols = g.cInner * imin(g.cChunk, g.cLast - j * g.cChunk);
@@ -139,6 +152,62 @@ __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb,
     }
 }
 
+// Pipelined variant of the load phase, in two halves so that the loads of the
+// next tile can stay in flight (in registers) while the current tile is being
+// written out.  Thread tid owns items tid + k*kBlock, k < IPT, of the
+// (row, vector) space; the plan guarantees runB * W <= IPT * kBlock.
+template <class Mem, typename T, int VA, int IPT>
+__host__ __device__ inline void tile_fetch(const TileArgs& g, const TileBase& tb, int tid,
+                                           const T* A, const int64_t* rowOffA,
+                                           Vec<T, VA> (&v)[IPT]) {
+    const int64_t W = (g.runA + VA - 1) / VA;
+    int64_t r = tid / W, c = tid % W;
+    const int64_t dr = kBlock / W, dc = kBlock % W;
+#pragma unroll
+    for (int u = 0; u < IPT; ++u) {
+        const int64_t cc = c * VA;
+        if (r < tb.validRows && cc < tb.validCols) {
+            const int64_t off = tb.a + Mem::template lds_ld<int64_t>(rowOffA, r) + cc;
+            if (cc + VA <= tb.validCols) {
+                v[u] = Mem::template ld<T, VA>(A, off);
+            } else {
+                for (int e = 0; e < VA; ++e)
+                    if (cc + e < tb.validCols) v[u].v[e] = Mem::template ld1<T>(A, off + e);
+            }
+        }
+        c += dc;
+        r += dr;
+        if (c >= W) {
+            c -= W;
+            r += 1;
+        }
+    }
+}
+
+template <class Mem, typename T, int VA, int IPT>
+__host__ __device__ inline void tile_park(const TileArgs& g, const TileBase& tb, int tid,
+                                          const Vec<T, VA> (&v)[IPT], T* lds) {
+    const int64_t W = (g.runA + VA - 1) / VA;
+    int64_t r = tid / W, c = tid % W;
+    const int64_t dr = kBlock / W, dc = kBlock % W;
+#pragma unroll
+    for (int u = 0; u < IPT; ++u) {
+        const int64_t cc = c * VA;
+        if (r < tb.validRows && cc < tb.validCols) {
+            const int64_t base = r * g.pitch + cc;
+#pragma unroll
+            for (int e = 0; e < VA; ++e)
+                if (cc + e < tb.validCols) Mem::template lds_st<T>(lds, base + e, v[u].v[e]);
+        }
+        c += dc;
+        r += dr;
+        if (c >= W) {
+            c -= W;
+            r += 1;
+        }
+    }
+}
+
 // Store phase: the tile's columns are contiguous runs of B.  Thread tid takes
 // the vectors tid, tid + kBlock, ... of the (column, vector) space, vector
 // fastest, gathers each vector's VB elements from consecutive LDS rows, and
@@ -207,76 +276,58 @@ __host__ __device__ inline int64_t tile_lds_bytes(const TileArgs& g, int elem) {
 // Kernel S: the stride-1 index is kept
 // ---------------------------------------------------------------------------
 
-// A offsets of the rows of group `grp` (rows are numbered in B order).
-template <class Mem>
-__host__ __device__ inline void stream_rows(const StreamArgs& g, uint32_t grp, int tid,
-                                            int64_t* rowOffA) {
-    const int64_t first = int64_t(grp) * g.rowsPerBlock;
-    for (int64_t i = tid; i < g.rowsPerBlock && first + i < g.numRows; i += kBlock) {
-        uint32_t x = uint32_t(first + i);
-        int64_t off = 0;
-        for (int k = 0; k < g.nO; ++k) {
-            uint32_t q = fast_div(x, g.oExt[k]);
-            off += int64_t(x - q * g.oExt[k].d) * g.oStrideA[k];
-            x = q;
-        }
-        Mem::template lds_st<int64_t>(rowOffA, i, off);
-    }
-}
 
-// Copy the rows of group `grp`: B is written as one contiguous stream, A is
-// read row by row from the gathered offsets.
+// Block `blk` handles items [blk*kBlock*kItems, (blk+1)*kBlock*kItems); lane
+// tid takes items first + u*kBlock + tid, so each wave covers consecutive B
+// vectors.  All loads of a lane are issued before its first store.
 template <class Mem, typename T, int V, int MODE, bool NT>
-__host__ __device__ inline void stream_copy(const StreamArgs& g, uint32_t grp, int tid,
-                                            const T* A, T* B, const int64_t* rowOffA, T alpha,
-                                            T beta) {
-    const int64_t first = int64_t(grp) * g.rowsPerBlock;
-    const int64_t rows = imin(int64_t(g.rowsPerBlock), g.numRows - first);
-    const int64_t W = (g.rowLen + V - 1) / V;  // vectors per row
-    int64_t r = tid / W, c = tid % W;
-    const int64_t dr = kBlock / W, dc = kBlock % W;
-    while (r < rows) {
-        Vec<T, V> x[kBatch], y[kBatch];
-        int64_t offB[kBatch], cc[kBatch];
-        bool ok[kBatch];
+__host__ __device__ inline void stream_items(const StreamArgs& g, uint32_t first, int tid,
+                                             const T* A, T* B, T alpha, T beta) {
+    const FastDiv& W = g.W[log2_width(V)];
+    const uint32_t numItems = g.numItems[log2_width(V)];
+    Vec<T, V> x[kItems], y[kItems];
+    int64_t offA[kItems], offB[kItems], col[kItems];
+    bool ok[kItems];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            ok[u] = r < rows;
-            cc[u] = c * V;
-            offB[u] = (first + r) * g.rowLen + cc[u];
-            if (ok[u]) {
-                const int64_t offA = Mem::template lds_ld<int64_t>(rowOffA, r) + cc[u];
-                if (cc[u] + V <= g.rowLen) {
-                    x[u] = Mem::template ld<T, V>(A, offA);
-                    if (MODE == kAxpby) y[u] = Mem::template ld<T, V>(B, offB[u]);
-                } else {
-                    for (int e = 0; e < V; ++e)
-                        if (cc[u] + e < g.rowLen) {
-                            x[u].v[e] = Mem::template ld1<T>(A, offA + e);
-                            if (MODE == kAxpby) y[u].v[e] = Mem::template ld1<T>(B, offB[u] + e);
-                        }
-                }
+    for (int u = 0; u < kItems; ++u) {
+        const uint64_t item = uint64_t(first) + uint64_t(u) * kBlock + uint64_t(tid);
+        ok[u] = item < numItems;
+        offA[u] = offB[u] = col[u] = 0;
+        if (ok[u]) {
+            uint32_t r = fast_div(uint32_t(item), W);
+            col[u] = int64_t(uint32_t(item) - r * W.d) * V;
+            offB[u] = int64_t(r) * g.rowLen + col[u];
+            int64_t a = 0;
+            for (int k = 0; k < g.nO; ++k) {
+                uint32_t q = fast_div(r, g.oExt[k]);
+                a += int64_t(r - q * g.oExt[k].d) * g.oStrideA[k];
+                r = q;
             }
-            c += dc;
-            r += dr;
-            if (c >= W) {
-                c -= W;
-                r += 1;
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            if (!ok[u]) continue;
-            Vec<T, V> z;
-#pragma unroll
-            for (int e = 0; e < V; ++e)
-                z.v[e] = update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
-            if (cc[u] + V <= g.rowLen) {
-                Mem::template st<NT, T, V>(B, offB[u], z);
+            offA[u] = a + col[u];
+            if (col[u] + V <= g.rowLen) {
+                x[u] = Mem::template ld<T, V>(A, offA[u]);
+                if (MODE == kAxpby) y[u] = Mem::template ld<T, V>(B, offB[u]);
             } else {
                 for (int e = 0; e < V; ++e)
-                    if (cc[u] + e < g.rowLen) Mem::template st1<NT, T>(B, offB[u] + e, z.v[e]);
+                    if (col[u] + e < g.rowLen) {
+                        x[u].v[e] = Mem::template ld1<T>(A, offA[u] + e);
+                        if (MODE == kAxpby) y[u].v[e] = Mem::template ld1<T>(B, offB[u] + e);
+                    }
             }
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kItems; ++u) {
+        if (!ok[u]) continue;
+        Vec<T, V> z;
+#pragma unroll
+        for (int e = 0; e < V; ++e)
+            z.v[e] = update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
+        if (col[u] + V <= g.rowLen) {
+            Mem::template st<NT, T, V>(B, offB[u], z);
+        } else {
+            for (int e = 0; e < V; ++e)
+                if (col[u] + e < g.rowLen) Mem::template st1<NT, T>(B, offB[u] + e, z.v[e]);
         }
     }
 }
@@ -285,22 +336,35 @@ __host__ __device__ inline void stream_copy(const StreamArgs& g, uint32_t grp, i
 // Identity after fusion: B <- alpha*A + beta*B over a flat range
 // ---------------------------------------------------------------------------
 
-// Vector i covers elements [i*V, i*V + V); the last vector may be partial.
+// Lane tid of the block starting at vector `first` takes vectors
+// first + u*kBlock + tid; vector i covers elements [i*V, i*V + V), the last
+// one possibly partial.
 template <class Mem, typename T, int V, int MODE, bool NT>
-__host__ __device__ inline void axpby_vec(int64_t numel, int64_t i, const T* A, T* B, T alpha,
-                                          T beta) {
-    const int64_t off = i * V;
-    if (off + V <= numel) {
-        Vec<T, V> x = Mem::template ld<T, V>(A, off), y, z;
-        if (MODE == kAxpby) y = Mem::template ld<T, V>(B, off);
+__host__ __device__ inline void axpby_items(int64_t numel, int64_t first, int tid, const T* A,
+                                            T* B, T alpha, T beta) {
+    Vec<T, V> x[kItems], y[kItems];
 #pragma unroll
-        for (int e = 0; e < V; ++e)
-            z.v[e] = update<MODE>(x.v[e], MODE == kAxpby ? y.v[e] : T(0), alpha, beta);
-        Mem::template st<NT, T, V>(B, off, z);
-    } else {
-        for (int64_t e = off; e < numel; ++e) {
-            T b = MODE == kAxpby ? Mem::template ld1<T>(B, e) : T(0);
-            Mem::template st1<NT, T>(B, e, update<MODE>(Mem::template ld1<T>(A, e), b, alpha, beta));
+    for (int u = 0; u < kItems; ++u) {
+        const int64_t off = (first + int64_t(u) * kBlock + tid) * V;
+        if (off + V <= numel) {
+            x[u] = Mem::template ld<T, V>(A, off);
+            if (MODE == kAxpby) y[u] = Mem::template ld<T, V>(B, off);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kItems; ++u) {
+        const int64_t off = (first + int64_t(u) * kBlock + tid) * V;
+        if (off + V <= numel) {
+            Vec<T, V> z;
+#pragma unroll
+            for (int e = 0; e < V; ++e)
+                z.v[e] = update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
+            Mem::template st<NT, T, V>(B, off, z);
+        } else {
+            for (int64_t e = off; e < numel; ++e) {
+                T b = MODE == kAxpby ? Mem::template ld1<T>(B, e) : T(0);
+                Mem::template st1<NT, T>(B, e, update<MODE>(Mem::template ld1<T>(A, e), b, alpha, beta));
+            }
         }
     }
 }

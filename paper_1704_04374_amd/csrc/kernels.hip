@@ -81,18 +81,52 @@ __global__ __launch_bounds__(kBlock) void tile_kernel(const T* __restrict__ A, T
     }
 }
 
+// Persistent, software-pipelined kernel T: a workgroup walks tiles
+// blockIdx.x, blockIdx.x + gridDim.x, ...; the A vectors of the next tile are
+// fetched into registers right after the current tile is parked in LDS, so
+// they are in flight while the current tile is written to B.
+template <typename T, int VA, int VB, int MODE, bool NT, int IPT>
+__global__ __launch_bounds__(kBlock) void tile_pipe_kernel(const T* __restrict__ A,
+                                                           T* __restrict__ B, const TileArgs g,
+                                                           T alpha, T beta) {
+    extern __shared__ int64_t smem[];
+    int64_t* rowOffA = smem;
+    int64_t* colOffB = smem + g.runB;
+    T* lds = reinterpret_cast<T*>(colOffB + g.runA);
+    const int tid = int(threadIdx.x);
+    tile_tables<DeviceMem>(g, tid, rowOffA, colOffB);
+    __syncthreads();
+    uint32_t t = blockIdx.x;
+    if (t >= g.numTiles) return;
+    Vec<T, VA> v[IPT];
+    TileBase tb = tile_base(g, t);
+    tile_fetch<DeviceMem, T, VA, IPT>(g, tb, tid, A, rowOffA, v);
+    while (true) {
+        tile_park<DeviceMem, T, VA, IPT>(g, tb, tid, v, lds);
+        __syncthreads();
+        const uint32_t next = t + gridDim.x;
+        const bool more = next < g.numTiles && next > t;
+        TileBase tn = tb;
+        if (more) {
+            tn = tile_base(g, next);
+            tile_fetch<DeviceMem, T, VA, IPT>(g, tn, tid, A, rowOffA, v);
+        }
+        tile_store<DeviceMem, T, VB, MODE, NT>(g, tb, tid, B, lds, colOffB, alpha, beta);
+        if (!more) break;
+        __syncthreads();  // the LDS tile is read out before the next one is parked
+        t = next;
+        tb = tn;
+    }
+}
+
 template <typename T, int V, int MODE, bool NT>
 __global__ __launch_bounds__(kBlock) void stream_kernel(const T* __restrict__ A,
                                                         T* __restrict__ B, const StreamArgs g,
                                                         T alpha, T beta) {
-    extern __shared__ int64_t smem[];
-    const int tid = int(threadIdx.x);
-    for (uint32_t grp = blockIdx.x; grp < g.numGroups; grp += gridDim.x) {
-        if (grp != blockIdx.x) __syncthreads();
-        stream_rows<DeviceMem>(g, grp, tid, smem);
-        __syncthreads();
-        stream_copy<DeviceMem, T, V, MODE, NT>(g, grp, tid, A, B, smem, alpha, beta);
-    }
+    const uint64_t step = uint64_t(gridDim.x) * kBlock * kItems;
+    const uint64_t items = g.numItems[log2_width(V)];
+    for (uint64_t first = uint64_t(blockIdx.x) * kBlock * kItems; first < items; first += step)
+        stream_items<DeviceMem, T, V, MODE, NT>(g, uint32_t(first), int(threadIdx.x), A, B, alpha, beta);
 }
 
 template <typename T, int V, int MODE, bool NT>
@@ -100,9 +134,9 @@ __global__ __launch_bounds__(kBlock) void axpby_kernel(const T* __restrict__ A,
                                                        T* __restrict__ B, const int64_t numel,
                                                        T alpha, T beta) {
     const int64_t vecs = (numel + V - 1) / V;
-    const int64_t stride = int64_t(gridDim.x) * kBlock;
-    for (int64_t i = int64_t(blockIdx.x) * kBlock + threadIdx.x; i < vecs; i += stride)
-        axpby_vec<DeviceMem, T, V, MODE, NT>(numel, i, A, B, alpha, beta);
+    const int64_t step = int64_t(gridDim.x) * kBlock * kItems;
+    for (int64_t first = int64_t(blockIdx.x) * kBlock * kItems; first < vecs; first += step)
+        axpby_items<DeviceMem, T, V, MODE, NT>(numel, first, int(threadIdx.x), A, B, alpha, beta);
 }
 
 template <typename T, int MODE, bool NT, bool BIG>
@@ -121,26 +155,44 @@ __global__ __launch_bounds__(kBlock) void generic_kernel(const T* __restrict__ A
 template <typename T>
 constexpr int kMaxVec = int(16 / sizeof(T));
 
+template <typename T, int VA, int VB, int MODE, bool NT>
+const void* tile_fn_ipt(int ipt) {
+    switch (ipt) {
+        case 0: return reinterpret_cast<const void*>(&tile_kernel<T, VA, VB, MODE, NT>);
+        case 4: return reinterpret_cast<const void*>(&tile_pipe_kernel<T, VA, VB, MODE, NT, 4>);
+        case 8: return reinterpret_cast<const void*>(&tile_pipe_kernel<T, VA, VB, MODE, NT, 8>);
+        case 16: return reinterpret_cast<const void*>(&tile_pipe_kernel<T, VA, VB, MODE, NT, 16>);
+    }
+    return nullptr;
+}
+
 template <typename T, int MODE, bool NT, int VA>
-const void* tile_fn_vb(int vb) {
+const void* tile_fn_vb(int vb, int ipt) {
     switch (vb) {
-        case 1: return reinterpret_cast<const void*>(&tile_kernel<T, VA, 1, MODE, NT>);
-        case 2: return reinterpret_cast<const void*>(&tile_kernel<T, VA, 2, MODE, NT>);
+        case 1: return tile_fn_ipt<T, VA, 1, MODE, NT>(ipt);
+        case 2: return tile_fn_ipt<T, VA, 2, MODE, NT>(ipt);
         case 4:
-            if constexpr (kMaxVec<T> >= 4)
-                return reinterpret_cast<const void*>(&tile_kernel<T, VA, 4, MODE, NT>);
+            if constexpr (kMaxVec<T> >= 4) return tile_fn_ipt<T, VA, 4, MODE, NT>(ipt);
             return nullptr;
     }
     return nullptr;
 }
 
+// The pipelined kernel needs the tile's A vectors to fit IPT per thread; a
+// narrower VA (less aligned A) multiplies them, so it may fall back to the
+// plain kernel.
 template <typename T, int MODE, bool NT>
-const void* tile_fn(int va, int vb) {
+const void* tile_fn(const TileArgs& g, int va, int vb) {
+    int ipt = g.ipt;
+    if (ipt) {
+        const int64_t items = g.runB * ((g.runA + va - 1) / va);
+        ipt = items <= 4 * kBlock ? 4 : items <= 8 * kBlock ? 8 : items <= 16 * kBlock ? 16 : 0;
+    }
     switch (va) {
-        case 1: return tile_fn_vb<T, MODE, NT, 1>(vb);
-        case 2: return tile_fn_vb<T, MODE, NT, 2>(vb);
+        case 1: return tile_fn_vb<T, MODE, NT, 1>(vb, ipt);
+        case 2: return tile_fn_vb<T, MODE, NT, 2>(vb, ipt);
         case 4:
-            if constexpr (kMaxVec<T> >= 4) return tile_fn_vb<T, MODE, NT, 4>(vb);
+            if constexpr (kMaxVec<T> >= 4) return tile_fn_vb<T, MODE, NT, 4>(vb, ipt);
             return nullptr;
     }
     return nullptr;
@@ -182,7 +234,7 @@ const void* generic_fn(bool big) {
 template <typename T, int MODE, bool NT>
 const void* select(const hptt_plan_s* p, int va, int vb) {
     switch (p->info.kernel) {
-        case HPTT_KERNEL_TILE: return tile_fn<T, MODE, NT>(va, vb);
+        case HPTT_KERNEL_TILE: return tile_fn<T, MODE, NT>(p->tile, va, vb);
         case HPTT_KERNEL_STREAM: return stream_fn<T, MODE, NT>(va < vb ? va : vb);
         case HPTT_KERNEL_AXPBY: return axpby_fn<T, MODE, NT>(va < vb ? va : vb);
         case HPTT_KERNEL_GENERIC:

@@ -20,6 +20,7 @@ namespace {
 constexpr int64_t kLdsBudget = 64 * 1024;  // bytes of LDS per workgroup for kernel T
 constexpr int64_t kLine = 128;             // L2 cache line of gfx950
 constexpr int64_t kVecBytes = 16;          // widest global access per lane (dwordx4)
+constexpr int64_t kComputeUnits = 256;     // MI355X
 
 int64_t gcd64(int64_t a, int64_t b) {
     if (a < 0) a = -a;
@@ -196,6 +197,8 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
         ++g;
     }
     t.nG = g;
+    t.skew = (g >= 2 && opt.tile_order != 1) ? 1 : 0;
+    info.tile_order = t.skew ? 2 : 1;
     for (int j = 0; j < g; ++j) {
         if (ext[j] >= (int64_t(1) << 32)) return false;
         set_div(t.gExt[j], ext[j]);
@@ -241,24 +244,23 @@ bool setup_stream(const Fused& f, int elem, const hptt_options_t& opt, StreamArg
     s.rowLen = f.n[0];
     int64_t rows = 1;
     for (int d = 1; d < f.M; ++d) rows *= f.n[d];
-    if (rows >= (int64_t(1) << 32)) return false;
     s.numRows = rows;
     s.nO = f.M - 1;
     for (int k = 1; k < f.M; ++k) {
         set_div(s.oExt[k - 1], f.n[f.p[k]]);
         s.oStrideA[k - 1] = f.sA[f.p[k]];
     }
-    int64_t rpb = opt.rows_per_block;
-    if (rpb <= 0) rpb = (16 * 1024) / (s.rowLen * elem);
-    if (rpb < 1) rpb = 1;
-    if (rpb > 4096) rpb = 4096;
-    if (rpb > rows) rpb = rows;
-    s.rowsPerBlock = int32_t(rpb);
-    s.numGroups = uint32_t((rows + rpb - 1) / rpb);
-    info.vec_a = info.vec_b = vec_width(s.rowLen, elem, opt.max_vec);
+    const int32_t v = vec_width(s.rowLen, elem, opt.max_vec);
+    for (int w = 0; w < 3; ++w) {  // every width hptt_exec may launch with
+        const int64_t W = (s.rowLen + (1 << w) - 1) >> w;
+        const int64_t items = rows * W;
+        if (items >= (int64_t(1) << 32) - int64_t(kBlock) * kItems) return false;
+        set_div(s.W[w], W);
+        s.numItems[w] = uint32_t(items);
+    }
+    info.vec_a = info.vec_b = v;
     info.run_b = s.rowLen;
-    info.lds_bytes = int32_t(rpb * sizeof(int64_t));
-    info.tiles = s.numGroups;
+    info.tiles = s.numItems[v >= 4 ? 2 : v >= 2 ? 1 : 0];
     return true;
 }
 
@@ -293,8 +295,9 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, d
     if (options) opt = *options;
     if (opt.kernel < HPTT_KERNEL_AUTO || opt.kernel > HPTT_KERNEL_GENERIC ||
         opt.kernel == HPTT_KERNEL_NONE || opt.run_a < 0 || opt.run_b < 0 || opt.max_vec < 0 ||
-        opt.nontemporal < 0 || opt.nontemporal > 2 || opt.rows_per_block < 0 ||
-        opt.lds_pad < -1 || opt.lds_pad > 64 || opt.max_blocks < 0)
+        opt.nontemporal < 0 || opt.nontemporal > 2 ||
+        opt.lds_pad < -1 || opt.lds_pad > 64 || opt.max_blocks < 0 || opt.tile_order < 0 ||
+        opt.tile_order > 2 || opt.pipeline < 0 || opt.pipeline > 2)
         return HPTT_ERROR_INVALID_ARGUMENT;
 
     const int elem = dtype == HPTT_FLOAT32 ? 4 : 8;
@@ -352,7 +355,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, d
     const int64_t maxBlocks = opt.max_blocks > 0 ? opt.max_blocks : (int64_t(1) << 31) - 1;
 
     if (k == HPTT_KERNEL_TILE) {
-        int64_t tA = opt.run_a > 0 ? opt.run_a : 256 / elem;
+        int64_t tA = opt.run_a > 0 ? opt.run_a : 512 / elem;
         int64_t tB = opt.run_b > 0 ? opt.run_b : 256 / elem;
         bool ok = false;
         for (int attempt = 0; attempt < 24 && !ok; ++attempt) {
@@ -363,11 +366,39 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, d
                 else break;
             }
         }
+        // Small problems: shorter runs (down to one 128-byte line) for more
+        // tiles, so that more CUs take part.
+        while (ok && opt.run_a == 0 && opt.run_b == 0 && plan->tile.numTiles < 512 &&
+               (tA * elem > kLine || tB * elem > kLine)) {
+            TileArgs keep = plan->tile;
+            hptt_plan_info_t keepInfo = info;
+            if (tA >= tB) tA /= 2;
+            else tB /= 2;
+            if (!setup_tile(f, elem, tA, tB, opt, plan->tile, info) ||
+                plan->tile.numTiles <= keep.numTiles) {
+                plan->tile = keep;
+                info = keepInfo;
+                break;
+            }
+        }
         if (!ok) {
             if (opt.kernel == HPTT_KERNEL_TILE) return HPTT_ERROR_UNSUPPORTED;
             k = HPTT_KERNEL_GENERIC;
         } else {
-            info.grid = plan->tile.numTiles < maxBlocks ? plan->tile.numTiles : maxBlocks;
+            TileArgs& t = plan->tile;
+            int64_t grid = t.numTiles;
+            // Persistent pipelined kernel: the tile's A vectors must fit 16 per
+            // thread; the grid is what the LDS lets stay resident on 256 CUs.
+            const int64_t items = t.runB * ((t.runA + info.vec_a - 1) / info.vec_a);
+            t.ipt = 0;
+            if (opt.pipeline == 2 && items <= 16 * kBlock) {
+                t.ipt = items <= 4 * kBlock ? 4 : items <= 8 * kBlock ? 8 : 16;
+                int64_t perCU = (160 * 1024) / info.lds_bytes;
+                perCU = perCU < 1 ? 1 : perCU > 8 ? 8 : perCU;
+                if (grid > kComputeUnits * perCU) grid = kComputeUnits * perCU;
+            }
+            info.pipeline = t.ipt;
+            info.grid = grid < maxBlocks ? grid : maxBlocks;
         }
     }
     if (k == HPTT_KERNEL_STREAM) {
@@ -375,15 +406,18 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, d
             if (opt.kernel == HPTT_KERNEL_STREAM) return HPTT_ERROR_UNSUPPORTED;
             k = HPTT_KERNEL_GENERIC;
         } else {
-            info.grid = plan->stream.numGroups < maxBlocks ? plan->stream.numGroups : maxBlocks;
+            const int64_t per = int64_t(kBlock) * kItems;
+            const int64_t grid = (info.tiles + per - 1) / per;
+            info.grid = grid < maxBlocks ? grid : maxBlocks;
         }
     }
     if (k == HPTT_KERNEL_AXPBY) {
         info.vec_a = info.vec_b = vec_width(0, elem, opt.max_vec);
         const int64_t vecs = (numel + info.vec_a - 1) / info.vec_a;
+        const int64_t per = int64_t(kBlock) * kItems;
         info.tiles = vecs;
-        int64_t grid = (vecs + kBlock * 4 - 1) / (kBlock * 4);
-        if (grid > 65536) grid = 65536;
+        int64_t grid = (vecs + per - 1) / per;
+        if (grid > (int64_t(1) << 30)) grid = int64_t(1) << 30;
         info.grid = grid < maxBlocks ? grid : maxBlocks;
     }
     if (k == HPTT_KERNEL_GENERIC) {
@@ -410,11 +444,12 @@ void describe_plan(const hptt_plan_s* p, char* buf, size_t len) {
     }
     snprintf(buf, len,
              "kernel=%s dtype=%s mode=%s fused=(%s) perm=(%s) run_a=%lld run_b=%lld "
-             "dims_a=%d dims_b=%d vec=%d/%d pitch=%d lds=%d tiles=%lld grid=%lld block=%d nt=%d",
+             "dims_a=%d dims_b=%d vec=%d/%d pitch=%d lds=%d tiles=%lld grid=%lld block=%d nt=%d "
+             "order=%d pipe=%d",
              kKernel[in.kernel], p->dtype == HPTT_FLOAT32 ? "f32" : "f64", kMode[in.mode], shape,
              perm, (long long)in.run_a, (long long)in.run_b, in.dims_a, in.dims_b, in.vec_a,
              in.vec_b, in.lds_pitch, in.lds_bytes, (long long)in.tiles, (long long)in.grid,
-             in.block, in.nontemporal);
+             in.block, in.nontemporal, in.tile_order, in.pipeline);
 }
 
 }  // namespace hptt

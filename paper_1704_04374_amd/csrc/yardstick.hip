@@ -1,6 +1,6 @@
-// Measurement kernels: a 16-byte-per-lane streaming copy, an axpby and a
-// fill.  Each block moves kUnroll vectors per thread with all loads issued
-// before the stores, the usual shape of a bandwidth-bound gfx950 kernel.
+// Measurement kernels: a 16-byte-per-lane streaming copy, an axpby, a fill
+// and a read-only sweep.  The fill and axpby blocks move kUnroll vectors per
+// lane with all loads issued before the stores.
 #include <hip/hip_runtime.h>
 
 #include "hptt_yardstick.h"
@@ -8,22 +8,37 @@
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kUnroll = 4;
+constexpr int kUnroll = 4;      // vectors per lane of the fill and axpby kernels
+constexpr int kReadBlocks = 1024;
 
 struct alignas(16) V16 {
     uint32_t w[4];
 };
 
+// One 16-byte vector per lane and a grid that covers the buffer once: the
+// fastest plain copy among the unroll depths and grid shapes tried on MI355X.
 __global__ __launch_bounds__(kThreads) void copy_kernel(const V16* __restrict__ src,
                                                         V16* __restrict__ dst, size_t n) {
-    const size_t i = size_t(blockIdx.x) * (kThreads * kUnroll) + threadIdx.x;
-    V16 v[kUnroll];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u)
-        if (i + size_t(u) * kThreads < n) v[u] = src[i + size_t(u) * kThreads];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u)
-        if (i + size_t(u) * kThreads < n) dst[i + size_t(u) * kThreads] = v[u];
+    const size_t i = size_t(blockIdx.x) * kThreads + threadIdx.x;
+    if (i < n) dst[i] = src[i];
+}
+
+__global__ __launch_bounds__(kThreads) void read_kernel(const V16* __restrict__ src, size_t n,
+                                                        uint32_t* __restrict__ sink) {
+    __shared__ uint32_t part[kThreads];
+    uint32_t acc = 0;
+    for (size_t i = size_t(blockIdx.x) * kThreads + threadIdx.x; i < n;
+         i += size_t(gridDim.x) * kThreads) {
+        const V16 v = src[i];
+        acc ^= v.w[0] ^ v.w[1] ^ v.w[2] ^ v.w[3];
+    }
+    part[threadIdx.x] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t x = 0;
+        for (int t = 0; t < kThreads; ++t) x ^= part[t];
+        sink[blockIdx.x] = x;
+    }
 }
 
 __global__ __launch_bounds__(kThreads) void fill_kernel(V16* __restrict__ dst, size_t n,
@@ -85,8 +100,19 @@ hptt_status_t hptt_yardstick_copy(const void* src, void* dst, size_t bytes, hipS
         return HPTT_ERROR_INVALID_ARGUMENT;
     const size_t n = bytes / 16;
     if (n == 0) return HPTT_SUCCESS;
-    hipLaunchKernelGGL(copy_kernel, dim3(uint32_t(blocks_for(n))), dim3(kThreads), 0, stream,
-                       static_cast<const V16*>(src), static_cast<V16*>(dst), n);
+    hipLaunchKernelGGL(copy_kernel, dim3(uint32_t((n + kThreads - 1) / kThreads)), dim3(kThreads),
+                       0, stream, static_cast<const V16*>(src), static_cast<V16*>(dst), n);
+    return check_launch();
+}
+
+hptt_status_t hptt_yardstick_read(const void* buf, size_t bytes, void* sink, hipStream_t stream) {
+    if (!buf || !sink || bytes % 16 || reinterpret_cast<uintptr_t>(buf) % 16 ||
+        reinterpret_cast<uintptr_t>(sink) % 4)
+        return HPTT_ERROR_INVALID_ARGUMENT;
+    const size_t n = bytes / 16;
+    if (n == 0) return HPTT_SUCCESS;
+    hipLaunchKernelGGL(read_kernel, dim3(kReadBlocks), dim3(kThreads), 0, stream,
+                       static_cast<const V16*>(buf), n, static_cast<uint32_t*>(sink));
     return check_launch();
 }
 

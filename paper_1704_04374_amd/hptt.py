@@ -38,8 +38,9 @@ class Options(ctypes.Structure):
     """hptt_options_t"""
     _fields_ = [("kernel", ctypes.c_int), ("run_a", ctypes.c_int32), ("run_b", ctypes.c_int32),
                 ("max_vec", ctypes.c_int32), ("nontemporal", ctypes.c_int32),
-                ("rows_per_block", ctypes.c_int32), ("lds_pad", ctypes.c_int32),
-                ("max_blocks", ctypes.c_int32)]
+                ("lds_pad", ctypes.c_int32),
+                ("max_blocks", ctypes.c_int32), ("tile_order", ctypes.c_int32),
+                ("pipeline", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -52,7 +53,8 @@ class PlanInfo(ctypes.Structure):
                 ("vec_a", ctypes.c_int32), ("vec_b", ctypes.c_int32),
                 ("lds_pitch", ctypes.c_int32), ("lds_bytes", ctypes.c_int32),
                 ("tiles", ctypes.c_int64), ("grid", ctypes.c_int64), ("block", ctypes.c_int32),
-                ("nontemporal", ctypes.c_int32), ("mode", ctypes.c_int32)]
+                ("nontemporal", ctypes.c_int32), ("mode", ctypes.c_int32),
+                ("tile_order", ctypes.c_int32), ("pipeline", ctypes.c_int32)]
 
     def as_dict(self) -> dict:
         n = self.ndim
@@ -62,14 +64,15 @@ class PlanInfo(ctypes.Structure):
                 "dims_a": self.dims_a, "dims_b": self.dims_b, "vec_a": self.vec_a,
                 "vec_b": self.vec_b, "lds_pitch": self.lds_pitch, "lds_bytes": self.lds_bytes,
                 "tiles": self.tiles, "grid": self.grid, "block": self.block,
-                "nontemporal": self.nontemporal, "mode": MODES[self.mode]}
+                "nontemporal": self.nontemporal, "mode": MODES[self.mode],
+                "tile_order": self.tile_order, "pipeline": self.pipeline}
 
 
 # Every entry point declared in include/hptt.h and include/hptt_yardstick.h.
 EXPORTS = ("hptt_create_plan", "hptt_create_plan_ex", "hptt_exec", "hptt_destroy_plan",
            "hptt_plan_info", "hptt_describe_plan", "hptt_status_string",
            "hptt_last_hip_error", "hptt_yardstick_copy", "hptt_yardstick_axpby",
-           "hptt_yardstick_fill")
+           "hptt_yardstick_fill", "hptt_yardstick_read")
 
 
 def _declare(lib: ctypes.CDLL, gpu: bool) -> ctypes.CDLL:
@@ -96,7 +99,9 @@ def _declare(lib: ctypes.CDLL, gpu: bool) -> ctypes.CDLL:
         lib.hptt_yardstick_axpby.argtypes = [ctypes.c_int, ctypes.c_double, vp, ctypes.c_double,
                                              vp, ctypes.c_size_t, vp]
         lib.hptt_yardstick_fill.argtypes = [vp, ctypes.c_size_t, ctypes.c_uint32, vp]
-        for f in ("hptt_yardstick_copy", "hptt_yardstick_axpby", "hptt_yardstick_fill"):
+        lib.hptt_yardstick_read.argtypes = [vp, ctypes.c_size_t, vp, vp]
+        for f in ("hptt_yardstick_copy", "hptt_yardstick_axpby", "hptt_yardstick_fill",
+                  "hptt_yardstick_read"):
             getattr(lib, f).restype = st
     return lib
 
@@ -265,3 +270,9 @@ def yardstick_axpby(dtype, alpha, x, beta, y, n: int, stream=None):
 def yardstick_fill(buf, nbytes: int, value: int = 0, stream=None):
     _check(library().hptt_yardstick_fill(ctypes.c_void_p(buf.data_ptr()), nbytes, value,
                                          ctypes.c_void_p(_stream(stream))), "hptt_yardstick_fill")
+
+
+def yardstick_read(buf, nbytes: int, sink, stream=None):
+    _check(library().hptt_yardstick_read(ctypes.c_void_p(buf.data_ptr()), nbytes,
+                                         ctypes.c_void_p(sink.data_ptr()),
+                                         ctypes.c_void_p(_stream(stream))), "hptt_yardstick_read")

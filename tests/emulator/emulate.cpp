@@ -142,24 +142,63 @@ void emu_tile(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     }
 }
 
+// Mirrors tile_pipe_kernel in kernels.hip; each thread keeps its fetched
+// vectors in its own register file between the phases.
+template <typename T, int VA, int VB, int MODE, bool NT, int IPT>
+void emu_tile_pipe(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
+    using namespace hptt;
+    const TileArgs& g = p->tile;
+    const T alpha = T(p->alpha), beta = T(p->beta);
+    const int64_t ldsBytes = p->info.lds_bytes;
+    const int64_t tableBytes = (g.runA + g.runB) * int64_t(sizeof(int64_t));
+    S->lds.assign(size_t(ldsBytes), 0);
+    S->written.assign(size_t(ldsBytes), 0);
+    int64_t* rowOffA = reinterpret_cast<int64_t*>(S->lds.data());
+    int64_t* colOffB = rowOffA + g.runB;
+    T* lds = reinterpret_cast<T*>(colOffB + g.runA);
+    const int64_t grid = p->info.grid;
+    std::vector<Vec<T, VA>> regs(size_t(kBlock) * IPT);
+    auto reg = [&](int tid) -> Vec<T, VA>(&)[IPT] {
+        return *reinterpret_cast<Vec<T, VA>(*)[IPT]>(&regs[size_t(tid) * IPT]);
+    };
+    for (int64_t blk = 0; blk < grid && S->errors == 0; blk += blockStride) {
+        if (blk >= g.numTiles) continue;
+        clear_written(0, ldsBytes);
+        for (int tid = 0; tid < kBlock; ++tid) tile_tables<HostMem>(g, tid, rowOffA, colOffB);
+        int64_t t = blk;
+        TileBase tb = tile_base(g, uint32_t(t));
+        for (int tid = 0; tid < kBlock; ++tid) tile_fetch<HostMem, T, VA, IPT>(g, tb, tid, A, rowOffA, reg(tid));
+        while (S->errors == 0) {
+            clear_written(tableBytes, ldsBytes);
+            for (int tid = 0; tid < kBlock; ++tid) tile_park<HostMem, T, VA, IPT>(g, tb, tid, reg(tid), lds);
+            const int64_t next = t + grid;
+            const bool more = next < g.numTiles;
+            TileBase tn = tb;
+            if (more) {
+                tn = tile_base(g, uint32_t(next));
+                for (int tid = 0; tid < kBlock; ++tid) tile_fetch<HostMem, T, VA, IPT>(g, tn, tid, A, rowOffA, reg(tid));
+            }
+            for (int tid = 0; tid < kBlock; ++tid)
+                tile_store<HostMem, T, VB, MODE, NT>(g, tb, tid, B, lds, colOffB, alpha, beta);
+            if (!more) break;
+            t = next;
+            tb = tn;
+        }
+    }
+}
+
 // Mirrors stream_kernel in kernels.hip.
 template <typename T, int V, int MODE, bool NT>
 void emu_stream(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     using namespace hptt;
     const StreamArgs& g = p->stream;
     const T alpha = T(p->alpha), beta = T(p->beta);
-    S->lds.assign(size_t(p->info.lds_bytes), 0);
-    S->written.assign(size_t(p->info.lds_bytes), 0);
-    int64_t* rows = reinterpret_cast<int64_t*>(S->lds.data());
-    const int64_t grid = p->info.grid;
-    for (int64_t blk = 0; blk < grid && S->errors == 0; blk += blockStride) {
-        for (int64_t grp = blk; grp < g.numGroups && S->errors == 0; grp += grid) {
-            clear_written(0, int64_t(S->lds.size()));
-            for (int tid = 0; tid < kBlock; ++tid) stream_rows<HostMem>(g, uint32_t(grp), tid, rows);
+    const uint64_t grid = uint64_t(p->info.grid), step = grid * kBlock * kItems;
+    for (uint64_t blk = 0; blk < grid && S->errors == 0; blk += uint64_t(blockStride))
+        for (uint64_t first = blk * kBlock * kItems;
+             first < g.numItems[log2_width(V)] && S->errors == 0; first += step)
             for (int tid = 0; tid < kBlock; ++tid)
-                stream_copy<HostMem, T, V, MODE, NT>(g, uint32_t(grp), tid, A, B, rows, alpha, beta);
-        }
-    }
+                stream_items<HostMem, T, V, MODE, NT>(g, uint32_t(first), tid, A, B, alpha, beta);
 }
 
 // Mirrors axpby_kernel and generic_kernel in kernels.hip.
@@ -167,11 +206,11 @@ template <typename T, int V, int MODE, bool NT>
 void emu_axpby(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     using namespace hptt;
     const int64_t numel = p->info.numel, vecs = (numel + V - 1) / V;
-    const int64_t grid = p->info.grid, stride = grid * kBlock;
+    const int64_t grid = p->info.grid, step = grid * kBlock * kItems;
     for (int64_t blk = 0; blk < grid && S->errors == 0; blk += blockStride)
-        for (int tid = 0; tid < kBlock; ++tid)
-            for (int64_t i = blk * kBlock + tid; i < vecs; i += stride)
-                axpby_vec<HostMem, T, V, MODE, NT>(numel, i, A, B, T(p->alpha), T(p->beta));
+        for (int64_t first = blk * kBlock * kItems; first < vecs; first += step)
+            for (int tid = 0; tid < kBlock; ++tid)
+                axpby_items<HostMem, T, V, MODE, NT>(numel, first, tid, A, B, T(p->alpha), T(p->beta));
 }
 
 template <typename T, int MODE, bool NT>
@@ -191,7 +230,20 @@ void emu_generic(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
 template <typename T, int MODE, bool NT, int VA, int VB>
 void run_widths(const hptt_plan_s* p, const T* A, T* B, int64_t bs) {
     switch (p->info.kernel) {
-        case HPTT_KERNEL_TILE: emu_tile<T, VA, VB, MODE, NT>(p, A, B, bs); break;
+        case HPTT_KERNEL_TILE: {
+            // same choice as tile_fn in kernels.hip
+            int ipt = p->tile.ipt;
+            if (ipt) {
+                const int64_t items = p->tile.runB * ((p->tile.runA + VA - 1) / VA);
+                ipt = items <= 4 * hptt::kBlock ? 4 : items <= 8 * hptt::kBlock ? 8
+                      : items <= 16 * hptt::kBlock ? 16 : 0;
+            }
+            if (ipt == 4) emu_tile_pipe<T, VA, VB, MODE, NT, 4>(p, A, B, bs);
+            else if (ipt == 8) emu_tile_pipe<T, VA, VB, MODE, NT, 8>(p, A, B, bs);
+            else if (ipt == 16) emu_tile_pipe<T, VA, VB, MODE, NT, 16>(p, A, B, bs);
+            else emu_tile<T, VA, VB, MODE, NT>(p, A, B, bs);
+            break;
+        }
         case HPTT_KERNEL_STREAM: emu_stream<T, (VA < VB ? VA : VB), MODE, NT>(p, A, B, bs); break;
         case HPTT_KERNEL_AXPBY: emu_axpby<T, (VA < VB ? VA : VB), MODE, NT>(p, A, B, bs); break;
         case HPTT_KERNEL_GENERIC: emu_generic<T, MODE, NT>(p, A, B, bs); break;

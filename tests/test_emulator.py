@@ -71,6 +71,11 @@ def test_random_problems_match_oracle():
     dict(max_vec=1),
     dict(max_vec=2),
     dict(nontemporal=1),
+    dict(tile_order=1),
+    dict(pipeline=2),
+    dict(pipeline=2, max_blocks=3),
+    dict(pipeline=2, run_a=4, run_b=4),
+    dict(pipeline=2, max_vec=1),
 ])
 def test_knobs_match_oracle(knobs):
     rng = np.random.default_rng(11)
@@ -83,12 +88,13 @@ def test_knobs_match_oracle(knobs):
 
 
 @pytest.mark.parametrize("va,vb", [(1, 1), (1, 4), (4, 1), (2, 2), (2, 4)])
-def test_narrow_vectors_as_for_misaligned_pointers(va, vb):
+@pytest.mark.parametrize("pipeline", [1, 2])
+def test_narrow_vectors_as_for_misaligned_pointers(va, vb, pipeline):
     """hptt_exec narrows the vector widths for less aligned pointers."""
     rng = np.random.default_rng(13)
     for size_a, perm in [((64, 33), (1, 0)), ((24, 20, 16, 5), (3, 2, 0, 1)),
                          ((3, 2, 64, 7, 32), (4, 2, 0, 3, 1)), ((96, 7, 9), (0, 2, 1))]:
-        p = emu.plan(perm, size_a, 1.5, 0.5, "f32")
+        p = emu.plan(perm, size_a, 1.5, 0.5, "f32", pipeline=pipeline)
         _check(p, size_a, perm, 1.5, 0.5, "f32", rng, va=min(va, p.info["vec_a"]),
                vb=min(vb, p.info["vec_b"]))
 
@@ -109,11 +115,12 @@ def test_small_workload_matches_oracle(w):
     _check(p, w.size_a, w.perm, w.alpha, w.beta, w.dtype, rng)
 
 
+@pytest.mark.parametrize("knobs", [dict(), dict(pipeline=2)], ids=["default", "pipelined"])
 @pytest.mark.parametrize("w", WORKLOADS, ids=lambda w: w.name)
-def test_full_size_geometry(w):
+def test_full_size_geometry(w, knobs):
     """Dry run of every workgroup of each full-size workload: every offset in
     bounds and aligned, every B element written exactly once."""
-    p = emu.plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype)
+    p = emu.plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype, **knobs)
     err, msg, cnt = emu.run(p, counts=True)
     assert err == 0, msg
     assert cnt.min() == 1 and cnt.max() == 1

@@ -9,6 +9,8 @@ results must meet at the very least, and is reported on failure.
 """
 from __future__ import annotations
 
+import itertools
+
 import numpy as np
 import pytest
 import torch
@@ -98,7 +100,9 @@ def test_random_sweep():
 
 @pytest.mark.parametrize("knobs", [dict(kernel="generic"), dict(run_a=8, run_b=8),
                                    dict(run_a=3, run_b=5), dict(max_blocks=7),
-                                   dict(max_vec=1), dict(nontemporal=1), dict(lds_pad=-1)],
+                                   dict(max_vec=1), dict(nontemporal=1), dict(lds_pad=-1),
+                                   dict(tile_order=1), dict(pipeline=2),
+                                   dict(pipeline=2, max_blocks=3), dict(pipeline=2, max_vec=1)],
                          ids=lambda k: ",".join(f"{a}={b}" for a, b in k.items()))
 def test_forced_variants(knobs):
     rng = np.random.default_rng(99)
@@ -112,18 +116,19 @@ def test_stream_kernel_variants():
     rng = np.random.default_rng(5)
     for size_a, perm in [((96, 7, 9, 5), (0, 3, 2, 1)), ((33, 8, 8), (0, 2, 1)),
                          ((16, 5, 6), (0, 2, 1))]:
-        for rpb in (0, 1, 3):
-            _run_case(size_a, perm, 2.0, 0.5, "f64", rng, kernel="stream", rows_per_block=rpb)
-            _run_case(size_a, perm, 1.0, 0.0, "f32", rng, kernel="stream", rows_per_block=rpb)
+        for knobs in (dict(), dict(max_vec=1), dict(max_blocks=3)):
+            _run_case(size_a, perm, 2.0, 0.5, "f64", rng, kernel="stream", **knobs)
+            _run_case(size_a, perm, 1.0, 0.0, "f32", rng, kernel="stream", **knobs)
 
 
 def test_misaligned_pointers_fall_back():
     """Tensors starting one element past a 16-byte boundary take narrower
     vector accesses and stay correct."""
     rng = np.random.default_rng(3)
-    for size_a, perm, dtype in [((64, 64), (1, 0), "f32"), ((3, 2, 64, 8, 32), (4, 2, 0, 3, 1), "f32"),
-                                ((96, 6, 7), (0, 2, 1), "f64"), ((1000,), (0,), "f32")]:
-        p = hptt.create_plan(perm, size_a, 1.5, 0.5, dtype)
+    for (size_a, perm, dtype), pipe in itertools.product(
+            [((64, 64), (1, 0), "f32"), ((3, 2, 64, 8, 32), (4, 2, 0, 3, 1), "f32"),
+             ((96, 6, 7), (0, 2, 1), "f64"), ((1000,), (0,), "f32")], (1, 2)):
+        p = hptt.create_plan(perm, size_a, 1.5, 0.5, dtype, pipeline=pipe)
         n = p.numel
         A = _rand(rng, n, dtype)
         B0 = _rand(rng, n, dtype)

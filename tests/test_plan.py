@@ -83,10 +83,10 @@ def test_kernel_classes():
 
 # What the plan builder must decide for each named workload.
 EXPECTED = {
-    "transpose3d_48x40x32_f32": dict(kernel="tile", size=(1920, 32), perm=(1, 0), run_a=64,
-                                     run_b=32, tiles=30),
-    "transpose2d_8192x8192_f32": dict(kernel="tile", size=(8192, 8192), perm=(1, 0), run_a=64,
-                                      run_b=64, tiles=16384),
+    "transpose3d_48x40x32_f32": dict(kernel="tile", size=(1920, 32), perm=(1, 0), run_a=32,
+                                     run_b=32, tiles=60),
+    "transpose2d_8192x8192_f32": dict(kernel="tile", size=(8192, 8192), perm=(1, 0), run_a=128,
+                                      run_b=64, tiles=8192, tile_order=2),
     "transpose6d_24x20x16x24x18x20_f32": dict(kernel="tile", size=(24, 20, 16, 24, 18, 20),
                                               perm=(5, 2, 0, 4, 1, 3), run_a=96, run_b=160,
                                               dims_a=2, dims_b=2, tiles=4320),
