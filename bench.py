@@ -51,10 +51,19 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def load_traffic(workload: str):
+def kernel_label(kernel_class: str) -> str:
+    """Name of the __global__ function that runs a plan's kernel class."""
+    return f"{kernel_class}_kernel"
+
+
+def profile_path(kernel_class: str, workload: str, kind: str) -> str:
+    return os.path.join(PROFILE_DIR, f"{kernel_label(kernel_class)}_{workload}_{kind}.txt")
+
+
+def load_traffic(kernel_class: str, workload: str):
     """HBM bytes per launch from a committed rocprofv3 counter summary, or
     None when there is none or the kernels changed since it was taken."""
-    path = os.path.join(PROFILE_DIR, f"pmc_{workload}.txt")
+    path = profile_path(kernel_class, workload, "pmc")
     if not os.path.exists(path):
         return None
     vals = {}
@@ -76,20 +85,22 @@ def _events(torch, n):
 
 
 def time_launches(torch, fn, steps: int, warmup: int):
-    """Run fn(i) for i < warmup, then for `steps` more i back to back with HIP
-    events around each launch on the current stream.  Returns (wall_s, [ms])."""
+    """Run fn(i) for i < warmup, then `steps` more back to back between a
+    synchronize on each side, with one HIP event before the first timed launch
+    and one after the last, both on the launch stream.  Returns (wall seconds,
+    GPU milliseconds per launch)."""
     for i in range(warmup):
         fn(i)
     torch.cuda.synchronize()
-    starts, ends = _events(torch, steps), _events(torch, steps)
+    start, end = _events(torch, 2)
     t0 = time.perf_counter()
+    start.record()
     for i in range(steps):
-        starts[i].record()
         fn(warmup + i)
-        ends[i].record()
+    end.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    return wall, [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    return wall, start.elapsed_time(end) / steps
 
 
 def time_cold(torch, hptt, fn, flush_buf, sink, reps: int):
@@ -130,10 +141,13 @@ def measure_workload(torch, hptt, w, steps, warmup, reps, flush_buf, sink, full:
     moved = w.moved_bytes
     S = w.tensor_bytes
     out = {"workload": w.name, "plan": plan.describe(), "plan_create_us": round(plan_us, 1),
-           "bytes_per_launch": moved, "buffer_sets": k}
+           "bytes_per_launch": moved, "buffer_sets": k, "kernel_class": plan.info["kernel"]}
+
+    stream = torch.cuda.current_stream().cuda_stream
+    runs = [plan.launcher(As[j].data_ptr(), Bs[j].data_ptr(), stream) for j in range(k)]
 
     def transpose(i):
-        plan.exec(As[i % k], Bs[i % k])
+        runs[i % k]()
 
     def copy(i):
         hptt.yardstick_copy(As[i % k], Bs[i % k], S)
@@ -145,12 +159,12 @@ def measure_workload(torch, hptt, w, steps, warmup, reps, flush_buf, sink, full:
         hptt.yardstick_axpby(w.dtype, w.alpha, As[i % k], w.beta, Bs[i % k], w.numel)
 
     def gbs(nbytes, ms):
-        return nbytes / (sum(ms) / len(ms) * 1e-3) / 1e9
+        return nbytes / (ms * 1e-3) / 1e9
 
     wall, ms = time_launches(torch, transpose, steps, warmup)
     out["ms_per_step"] = wall * 1e3 / steps
     out["gbs"] = moved * steps / wall / 1e9
-    out["kernel_avg_ms"] = sum(ms) / len(ms)
+    out["kernel_avg_ms"] = ms
     out["kernel_gbs"] = gbs(moved, ms)
     out["copy_gbs"] = gbs(2 * S, time_launches(torch, copy, steps, warmup)[1])
     out["hipmemcpy_d2d_gbs"] = gbs(2 * S, time_launches(torch, memcpy, steps, warmup)[1])
@@ -227,7 +241,9 @@ def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, command: str, o
         vals = acc[names[0]]
         return names[0], statistics.median(vals)
 
-    tk, tf = pick(fetch, "tile_kernel" if "keep1" not in workload else "stream_kernel")
+    from paper_1704_04374_amd import hptt
+    cls = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype).info["kernel"]
+    tk, tf = pick(fetch, kernel_label(cls))
     _, tw = pick(write, tk.split("(")[0])
     _, cf = pick(fetch, "copy_kernel")
     _, cw = pick(write, "copy_kernel")
@@ -239,8 +255,8 @@ def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, command: str, o
     lines = [
         f"# rocprofv3 counter summary: {tk}",
         f"# workload: {w.describe()}",
-        f"# command (FETCH_SIZE pass): {command} --pmc FETCH_SIZE",
-        f"# command (WRITE_SIZE pass): {command} --pmc WRITE_SIZE",
+        f"# command (FETCH_SIZE pass): {command.replace('COUNTER', 'FETCH_SIZE')}",
+        f"# command (WRITE_SIZE pass): {command.replace('COUNTER', 'WRITE_SIZE')}",
         "# FETCH_SIZE and WRITE_SIZE are KiB per dispatch (median over dispatches); each is",
         "# scaled by (known bytes / counter) of the copy yardstick kernel in the same run.",
         f"kernel: {tk}",
@@ -263,10 +279,45 @@ def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, command: str, o
     print("\n".join(lines))
 
 
+def summarize_trace(trace_dir: str, workload: str, command: str, out_path: str):
+    """Turn a rocprofv3 --kernel-trace --stats run into the committed summary:
+    per-kernel calls and durations, and the headline kernel's GB/s from its
+    average duration and the algorithmic bytes of Eq. (2)."""
+    import csv
+
+    from paper_1704_04374_amd.workloads import BY_NAME
+    w = BY_NAME[workload]
+    paths = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if not paths:
+        raise SystemExit(f"no kernel_stats.csv under {trace_dir}")
+    with open(paths[0]) as f:
+        rows = list(csv.DictReader(f))
+    lines = [f"# rocprofv3 kernel statistics, workload {w.describe()}",
+             f"# command: {command}",
+             f"# algorithmic bytes per transposition (Eq. 2, lambda*S): {w.moved_bytes}",
+             "# kernel | calls | average us | min us | max us | GB/s at the average"]
+    for r in rows:
+        name = r["Name"]
+        avg = float(r["AverageNs"])
+        nb = None
+        if "tile_kernel" in name or "stream_kernel" in name or "axpby_kernel<" in name:
+            nb = w.moved_bytes
+        elif "copy_kernel" in name:
+            nb = 2 * w.tensor_bytes
+        short = name if len(name) < 110 else name[:107] + "..."
+        gbs = f"{nb / avg:.1f}" if nb else "-"
+        lines.append(f"{short} | {r['Calls']} | {avg / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
+                     f"{float(r['MaxNs']) / 1e3:.2f} | {gbs}")
+    lines.append(f"kernel_source_hash: {kernel_source_hash()}")
+    with open(out_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=HEADLINE)
     ap.add_argument("--reps", type=int, default=20, help="flushed single launches per workload")
@@ -274,13 +325,24 @@ def main():
                     help="time only the headline workload (for profiler runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--summarize-trace", metavar="TRACE_DIR")
     ap.add_argument("--pmc-command", default="")
     ap.add_argument("--pmc-out", default="")
     args = ap.parse_args()
 
+    if args.summarize_pmc or args.summarize_trace:
+        from paper_1704_04374_amd.workloads import BY_NAME as _W
+        _w = _W[args.workload]
+        import ctypes  # noqa: F401  (plan creation needs only the host half of the library)
+        from paper_1704_04374_amd import hptt as _h
+        _cls = _h.create_plan(_w.perm, _w.size_a, _w.alpha, _w.beta, _w.dtype).info["kernel"]
     if args.summarize_pmc:
-        out = args.pmc_out or os.path.join(PROFILE_DIR, f"pmc_{args.workload}.txt")
+        out = args.pmc_out or profile_path(_cls, args.workload, "pmc")
         summarize_pmc(*args.summarize_pmc, args.workload, args.pmc_command, out)
+        return 0
+    if args.summarize_trace:
+        out = args.pmc_out or profile_path(_cls, args.workload, "trace")
+        summarize_trace(args.summarize_trace, args.workload, args.pmc_command, out)
         return 0
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this transposition library has no multi-GPU "
@@ -316,7 +378,7 @@ def main():
                   f"{r['pct_of_copy']:.1f}% of copy, {r['pct_of_hbm_peak']:.1f}% of peak",
                   file=sys.stderr, flush=True)
 
-    traffic = load_traffic(head.name)
+    traffic = load_traffic(headline["kernel_class"], head.name)
     achieved = headline["kernel_gbs"]
     line = {
         "metric": "effective GB/s per transpose (Eq. 2 bytes) and % of HBM peak / same-run copy",

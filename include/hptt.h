@@ -75,14 +75,14 @@ typedef struct {
                               A run of a tile (its columns) */
     int32_t run_b;         /* TILE: target length of the contiguous B run (rows) */
     int32_t max_vec;       /* cap on the vector width in elements (1 = scalar) */
-    int32_t nontemporal;   /* 1: non-temporal B stores when beta = 0; 2: never */
+    int32_t store_hint;    /* 1: non-temporal stores of B; 2: ordinary stores */
+    int32_t load_hint;     /* 1: non-temporal loads of A; 2: ordinary loads */
     int32_t lds_pad;       /* TILE: LDS row padding in elements, 0 = default, -1 = none */
     int32_t max_blocks;    /* cap on the grid; workgroups loop over tiles beyond it */
     int32_t tile_order;    /* TILE: 1 = tiles in grid-digit order, 2 = diagonal
                               (second grid digit rotated by the first) */
-    int32_t pipeline;      /* TILE: 1 = one tile per workgroup, 2 = persistent
-                              workgroups that fetch the next tile while writing
-                              the current one */
+    int32_t exact_runs;    /* TILE: 1 = chunk the runs to the target lengths even
+                              where runs then do not start on 128-byte lines */
 } hptt_options_t;
 
 /* What the plan builder decided; for inspection and tests. */
@@ -105,11 +105,10 @@ typedef struct {
                                           GENERIC: elements */
     int64_t grid;                      /* workgroups launched */
     int32_t block;                     /* threads per workgroup */
-    int32_t nontemporal;               /* 1 when B is written with non-temporal stores */
+    int32_t hints;                     /* bit 0: non-temporal B stores; bit 1:
+                                          non-temporal A loads */
     int32_t mode;                      /* 0 raw copy, 1 scale (beta = 0), 2 alpha*A + beta*B */
     int32_t tile_order;                /* TILE: 1 grid-digit order, 2 diagonal */
-    int32_t pipeline;                  /* TILE: A vectors per thread held across tiles
-                                          by the persistent kernel, 0 = not used */
 } hptt_plan_info_t;
 
 /*

@@ -43,6 +43,11 @@ __host__ __device__ __forceinline__ uint32_t fast_div(uint32_t n, const FastDiv&
 // copy (beta = 0, B not read) or the full update alpha*A + beta*B.
 enum Mode : int { kCopy = 0, kScale = 1, kAxpby = 2 };
 
+// Cache hints of the kernels: bit 0 = non-temporal stores of B, bit 1 =
+// non-temporal loads of A.
+constexpr int kNtStore = 1;
+constexpr int kNtLoad = 2;
+
 // Kernel T: the transposition is cut into independent 2-D tiles (the
 // macro-tiles of Section 3.2).  A tile's columns form a contiguous run of A
 // (fused A indices 0..nC-1, the last one possibly cut into chunks) and its
@@ -59,7 +64,7 @@ struct TileArgs {
     int32_t gChunkC;     // grid digit that counts chunks of the last A-run index, or -1
     int32_t gChunkR;     // grid digit that counts chunks of the last B-run index, or -1
     int32_t skew;        // 1: grid digit 1 is shifted by digit 0 (diagonal tile order)
-    int32_t ipt;         // pipelined kernel: A vectors per thread per tile (4, 8 or 16), 0 = off
+    int32_t alignedA;    // 1 when every A run is whole 128-byte lines (set by the plan builder)
     int64_t cInner, cChunk, cLast;  // valid columns = cInner * min(cChunk, cLast - j*cChunk)
     int64_t rInner, rChunk, rLast;  // valid rows    = rInner * min(rChunk, rLast - j*rChunk)
     FastDiv cExt[kMaxDims];         // tile extents of the A-run indices

@@ -104,14 +104,14 @@ __host__ __device__ inline void tile_tables(const TileArgs& g, int tid, int64_t*
     }
 }
 
-// Number of items a thread takes per batch: loads of a batch are all issued
-// before the first of them is consumed.
+// Vectors a lane loads before the first of them is written to LDS (4, 8 and
+// 16 measured within noise of each other on MI355X; 8 was best on average).
 constexpr int kBatch = 8;
 
 // Load phase: the tile's rows are contiguous runs of A.  Thread tid takes the
 // vectors tid, tid + kBlock, ... of the (row, vector) space, vector fastest,
 // so a wave reads whole runs.  The vectors land in LDS at [row][column].
-template <class Mem, typename T, int VA>
+template <class Mem, typename T, int VA, int HINT>
 __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb, int tid,
                                           const T* A, T* lds, const int64_t* rowOffA) {
     const int64_t W = (g.runA + VA - 1) / VA;  // vectors per row
@@ -127,7 +127,7 @@ __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb,
             if (r < tb.validRows && cc[u] < tb.validCols) {
                 const int64_t off = tb.a + Mem::template lds_ld<int64_t>(rowOffA, r) + cc[u];
                 if (cc[u] + VA <= tb.validCols) {
-                    v[u] = Mem::template ld<T, VA>(A, off);
+                    v[u] = Mem::template ld<T, VA, (HINT & kNtLoad) != 0>(A, off);
                 } else {
                     for (int e = 0; e < VA; ++e)
                         if (cc[u] + e < tb.validCols) v[u].v[e] = Mem::template ld1<T>(A, off + e);
@@ -152,67 +152,11 @@ __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb,
     }
 }
 
-// Pipelined variant of the load phase, in two halves so that the loads of the
-// next tile can stay in flight (in registers) while the current tile is being
-// written out.  Thread tid owns items tid + k*kBlock, k < IPT, of the
-// (row, vector) space; the plan guarantees runB * W <= IPT * kBlock.
-template <class Mem, typename T, int VA, int IPT>
-__host__ __device__ inline void tile_fetch(const TileArgs& g, const TileBase& tb, int tid,
-                                           const T* A, const int64_t* rowOffA,
-                                           Vec<T, VA> (&v)[IPT]) {
-    const int64_t W = (g.runA + VA - 1) / VA;
-    int64_t r = tid / W, c = tid % W;
-    const int64_t dr = kBlock / W, dc = kBlock % W;
-#pragma unroll
-    for (int u = 0; u < IPT; ++u) {
-        const int64_t cc = c * VA;
-        if (r < tb.validRows && cc < tb.validCols) {
-            const int64_t off = tb.a + Mem::template lds_ld<int64_t>(rowOffA, r) + cc;
-            if (cc + VA <= tb.validCols) {
-                v[u] = Mem::template ld<T, VA>(A, off);
-            } else {
-                for (int e = 0; e < VA; ++e)
-                    if (cc + e < tb.validCols) v[u].v[e] = Mem::template ld1<T>(A, off + e);
-            }
-        }
-        c += dc;
-        r += dr;
-        if (c >= W) {
-            c -= W;
-            r += 1;
-        }
-    }
-}
-
-template <class Mem, typename T, int VA, int IPT>
-__host__ __device__ inline void tile_park(const TileArgs& g, const TileBase& tb, int tid,
-                                          const Vec<T, VA> (&v)[IPT], T* lds) {
-    const int64_t W = (g.runA + VA - 1) / VA;
-    int64_t r = tid / W, c = tid % W;
-    const int64_t dr = kBlock / W, dc = kBlock % W;
-#pragma unroll
-    for (int u = 0; u < IPT; ++u) {
-        const int64_t cc = c * VA;
-        if (r < tb.validRows && cc < tb.validCols) {
-            const int64_t base = r * g.pitch + cc;
-#pragma unroll
-            for (int e = 0; e < VA; ++e)
-                if (cc + e < tb.validCols) Mem::template lds_st<T>(lds, base + e, v[u].v[e]);
-        }
-        c += dc;
-        r += dr;
-        if (c >= W) {
-            c -= W;
-            r += 1;
-        }
-    }
-}
-
 // Store phase: the tile's columns are contiguous runs of B.  Thread tid takes
 // the vectors tid, tid + kBlock, ... of the (column, vector) space, vector
 // fastest, gathers each vector's VB elements from consecutive LDS rows, and
 // writes it to B (reading B first when beta != 0).
-template <class Mem, typename T, int VB, int MODE, bool NT>
+template <class Mem, typename T, int VB, int MODE, int HINT>
 __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb, int tid, T* B,
                                            const T* lds, const int64_t* colOffB, T alpha,
                                            T beta) {
@@ -235,7 +179,7 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
                         x[u].v[e] = Mem::template lds_ld<T>(lds, (ss[u] + e) * g.pitch + q);
                 if (MODE == kAxpby) {
                     if (ss[u] + VB <= tb.validRows) {
-                        y[u] = Mem::template ld<T, VB>(B, off[u]);
+                        y[u] = Mem::template ld<T, VB, false>(B, off[u]);
                     } else {
                         for (int e = 0; e < VB; ++e)
                             if (ss[u] + e < tb.validRows) y[u].v[e] = Mem::template ld1<T>(B, off[u] + e);
@@ -257,10 +201,10 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
                 for (int e = 0; e < VB; ++e)
                     z.v[e] = update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
                 if (ss[u] + VB <= tb.validRows) {
-                    Mem::template st<NT, T, VB>(B, off[u], z);
+                    Mem::template st<(HINT & kNtStore) != 0, T, VB>(B, off[u], z);
                 } else {
                     for (int e = 0; e < VB; ++e)
-                        if (ss[u] + e < tb.validRows) Mem::template st1<NT, T>(B, off[u] + e, z.v[e]);
+                        if (ss[u] + e < tb.validRows) Mem::template st1<(HINT & kNtStore) != 0, T>(B, off[u] + e, z.v[e]);
                 }
             }
         }
@@ -280,7 +224,7 @@ __host__ __device__ inline int64_t tile_lds_bytes(const TileArgs& g, int elem) {
 // Block `blk` handles items [blk*kBlock*kItems, (blk+1)*kBlock*kItems); lane
 // tid takes items first + u*kBlock + tid, so each wave covers consecutive B
 // vectors.  All loads of a lane are issued before its first store.
-template <class Mem, typename T, int V, int MODE, bool NT>
+template <class Mem, typename T, int V, int MODE, int HINT>
 __host__ __device__ inline void stream_items(const StreamArgs& g, uint32_t first, int tid,
                                              const T* A, T* B, T alpha, T beta) {
     const FastDiv& W = g.W[log2_width(V)];
@@ -305,8 +249,8 @@ __host__ __device__ inline void stream_items(const StreamArgs& g, uint32_t first
             }
             offA[u] = a + col[u];
             if (col[u] + V <= g.rowLen) {
-                x[u] = Mem::template ld<T, V>(A, offA[u]);
-                if (MODE == kAxpby) y[u] = Mem::template ld<T, V>(B, offB[u]);
+                x[u] = Mem::template ld<T, V, (HINT & kNtLoad) != 0>(A, offA[u]);
+                if (MODE == kAxpby) y[u] = Mem::template ld<T, V, false>(B, offB[u]);
             } else {
                 for (int e = 0; e < V; ++e)
                     if (col[u] + e < g.rowLen) {
@@ -324,10 +268,10 @@ __host__ __device__ inline void stream_items(const StreamArgs& g, uint32_t first
         for (int e = 0; e < V; ++e)
             z.v[e] = update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
         if (col[u] + V <= g.rowLen) {
-            Mem::template st<NT, T, V>(B, offB[u], z);
+            Mem::template st<(HINT & kNtStore) != 0, T, V>(B, offB[u], z);
         } else {
             for (int e = 0; e < V; ++e)
-                if (col[u] + e < g.rowLen) Mem::template st1<NT, T>(B, offB[u] + e, z.v[e]);
+                if (col[u] + e < g.rowLen) Mem::template st1<(HINT & kNtStore) != 0, T>(B, offB[u] + e, z.v[e]);
         }
     }
 }
@@ -339,7 +283,7 @@ __host__ __device__ inline void stream_items(const StreamArgs& g, uint32_t first
 // Lane tid of the block starting at vector `first` takes vectors
 // first + u*kBlock + tid; vector i covers elements [i*V, i*V + V), the last
 // one possibly partial.
-template <class Mem, typename T, int V, int MODE, bool NT>
+template <class Mem, typename T, int V, int MODE, int HINT>
 __host__ __device__ inline void axpby_items(int64_t numel, int64_t first, int tid, const T* A,
                                             T* B, T alpha, T beta) {
     Vec<T, V> x[kItems], y[kItems];
@@ -347,8 +291,8 @@ __host__ __device__ inline void axpby_items(int64_t numel, int64_t first, int ti
     for (int u = 0; u < kItems; ++u) {
         const int64_t off = (first + int64_t(u) * kBlock + tid) * V;
         if (off + V <= numel) {
-            x[u] = Mem::template ld<T, V>(A, off);
-            if (MODE == kAxpby) y[u] = Mem::template ld<T, V>(B, off);
+            x[u] = Mem::template ld<T, V, (HINT & kNtLoad) != 0>(A, off);
+            if (MODE == kAxpby) y[u] = Mem::template ld<T, V, false>(B, off);
         }
     }
 #pragma unroll
@@ -359,11 +303,11 @@ __host__ __device__ inline void axpby_items(int64_t numel, int64_t first, int ti
 #pragma unroll
             for (int e = 0; e < V; ++e)
                 z.v[e] = update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
-            Mem::template st<NT, T, V>(B, off, z);
+            Mem::template st<(HINT & kNtStore) != 0, T, V>(B, off, z);
         } else {
             for (int64_t e = off; e < numel; ++e) {
                 T b = MODE == kAxpby ? Mem::template ld1<T>(B, e) : T(0);
-                Mem::template st1<NT, T>(B, e, update<MODE>(Mem::template ld1<T>(A, e), b, alpha, beta));
+                Mem::template st1<(HINT & kNtStore) != 0, T>(B, e, update<MODE>(Mem::template ld1<T>(A, e), b, alpha, beta));
             }
         }
     }
@@ -373,7 +317,7 @@ __host__ __device__ inline void axpby_items(int64_t numel, int64_t first, int ti
 // Fallback: one B element per thread, any shape
 // ---------------------------------------------------------------------------
 
-template <class Mem, typename T, int MODE, bool NT, bool BIG>
+template <class Mem, typename T, int MODE, int HINT, bool BIG>
 __host__ __device__ inline void generic_elem(const GenericArgs& g, int64_t e, const T* A, T* B,
                                              T alpha, T beta) {
     int64_t offA = 0;
@@ -392,7 +336,7 @@ __host__ __device__ inline void generic_elem(const GenericArgs& g, int64_t e, co
         }
     }
     T b = MODE == kAxpby ? Mem::template ld1<T>(B, e) : T(0);
-    Mem::template st1<NT, T>(B, e, update<MODE>(Mem::template ld1<T>(A, offA), b, alpha, beta));
+    Mem::template st1<(HINT & kNtStore) != 0, T>(B, e, update<MODE>(Mem::template ld1<T>(A, offA), b, alpha, beta));
 }
 
 }  // namespace hptt

@@ -17,14 +17,15 @@ thread_local int32_t g_last_hip_error = 0;
 // global_load/store of V*sizeof(T) bytes; the plan only asks for widths that
 // keep every such access aligned.
 struct DeviceMem {
-    template <typename T, int V>
+    template <typename T, int V, bool NT>
     __device__ __forceinline__ static Vec<T, V> ld(const T* p, int64_t off) {
         Vec<T, V> r;
         if constexpr (V == 1) {
-            r.v[0] = p[off];
+            r.v[0] = NT ? __builtin_nontemporal_load(p + off) : p[off];
         } else {
             typedef T vt __attribute__((ext_vector_type(V)));
-            const vt x = *reinterpret_cast<const vt*>(p + off);
+            const vt x = NT ? __builtin_nontemporal_load(reinterpret_cast<const vt*>(p + off))
+                            : *reinterpret_cast<const vt*>(p + off);
 #pragma unroll
             for (int e = 0; e < V; ++e) r.v[e] = x[e];
         }
@@ -62,7 +63,7 @@ struct DeviceMem {
     }
 };
 
-template <typename T, int VA, int VB, int MODE, bool NT>
+template <typename T, int VA, int VB, int MODE, int HINT>
 __global__ __launch_bounds__(kBlock) void tile_kernel(const T* __restrict__ A, T* __restrict__ B,
                                                       const TileArgs g, T alpha, T beta) {
     extern __shared__ int64_t smem[];
@@ -75,77 +76,40 @@ __global__ __launch_bounds__(kBlock) void tile_kernel(const T* __restrict__ A, T
     for (uint32_t t = blockIdx.x; t < g.numTiles; t += gridDim.x) {
         if (t != blockIdx.x) __syncthreads();  // the previous tile's LDS reads are done
         const TileBase tb = tile_base(g, t);
-        tile_load<DeviceMem, T, VA>(g, tb, tid, A, lds, rowOffA);
+        tile_load<DeviceMem, T, VA, HINT>(g, tb, tid, A, lds, rowOffA);
         __syncthreads();
-        tile_store<DeviceMem, T, VB, MODE, NT>(g, tb, tid, B, lds, colOffB, alpha, beta);
+        tile_store<DeviceMem, T, VB, MODE, HINT>(g, tb, tid, B, lds, colOffB, alpha, beta);
     }
 }
 
-// Persistent, software-pipelined kernel T: a workgroup walks tiles
-// blockIdx.x, blockIdx.x + gridDim.x, ...; the A vectors of the next tile are
-// fetched into registers right after the current tile is parked in LDS, so
-// they are in flight while the current tile is written to B.
-template <typename T, int VA, int VB, int MODE, bool NT, int IPT>
-__global__ __launch_bounds__(kBlock) void tile_pipe_kernel(const T* __restrict__ A,
-                                                           T* __restrict__ B, const TileArgs g,
-                                                           T alpha, T beta) {
-    extern __shared__ int64_t smem[];
-    int64_t* rowOffA = smem;
-    int64_t* colOffB = smem + g.runB;
-    T* lds = reinterpret_cast<T*>(colOffB + g.runA);
-    const int tid = int(threadIdx.x);
-    tile_tables<DeviceMem>(g, tid, rowOffA, colOffB);
-    __syncthreads();
-    uint32_t t = blockIdx.x;
-    if (t >= g.numTiles) return;
-    Vec<T, VA> v[IPT];
-    TileBase tb = tile_base(g, t);
-    tile_fetch<DeviceMem, T, VA, IPT>(g, tb, tid, A, rowOffA, v);
-    while (true) {
-        tile_park<DeviceMem, T, VA, IPT>(g, tb, tid, v, lds);
-        __syncthreads();
-        const uint32_t next = t + gridDim.x;
-        const bool more = next < g.numTiles && next > t;
-        TileBase tn = tb;
-        if (more) {
-            tn = tile_base(g, next);
-            tile_fetch<DeviceMem, T, VA, IPT>(g, tn, tid, A, rowOffA, v);
-        }
-        tile_store<DeviceMem, T, VB, MODE, NT>(g, tb, tid, B, lds, colOffB, alpha, beta);
-        if (!more) break;
-        __syncthreads();  // the LDS tile is read out before the next one is parked
-        t = next;
-        tb = tn;
-    }
-}
-
-template <typename T, int V, int MODE, bool NT>
+template <typename T, int V, int MODE, int HINT>
 __global__ __launch_bounds__(kBlock) void stream_kernel(const T* __restrict__ A,
                                                         T* __restrict__ B, const StreamArgs g,
                                                         T alpha, T beta) {
     const uint64_t step = uint64_t(gridDim.x) * kBlock * kItems;
     const uint64_t items = g.numItems[log2_width(V)];
     for (uint64_t first = uint64_t(blockIdx.x) * kBlock * kItems; first < items; first += step)
-        stream_items<DeviceMem, T, V, MODE, NT>(g, uint32_t(first), int(threadIdx.x), A, B, alpha, beta);
+        stream_items<DeviceMem, T, V, MODE, HINT>(g, uint32_t(first), int(threadIdx.x), A, B, alpha,
+                                                  beta);
 }
 
-template <typename T, int V, int MODE, bool NT>
+template <typename T, int V, int MODE, int HINT>
 __global__ __launch_bounds__(kBlock) void axpby_kernel(const T* __restrict__ A,
                                                        T* __restrict__ B, const int64_t numel,
                                                        T alpha, T beta) {
     const int64_t vecs = (numel + V - 1) / V;
     const int64_t step = int64_t(gridDim.x) * kBlock * kItems;
     for (int64_t first = int64_t(blockIdx.x) * kBlock * kItems; first < vecs; first += step)
-        axpby_items<DeviceMem, T, V, MODE, NT>(numel, first, int(threadIdx.x), A, B, alpha, beta);
+        axpby_items<DeviceMem, T, V, MODE, HINT>(numel, first, int(threadIdx.x), A, B, alpha, beta);
 }
 
-template <typename T, int MODE, bool NT, bool BIG>
+template <typename T, int MODE, int HINT, bool BIG>
 __global__ __launch_bounds__(kBlock) void generic_kernel(const T* __restrict__ A,
                                                          T* __restrict__ B, const GenericArgs g,
                                                          T alpha, T beta) {
     const int64_t stride = int64_t(gridDim.x) * kBlock;
     for (int64_t e = int64_t(blockIdx.x) * kBlock + threadIdx.x; e < g.numel; e += stride)
-        generic_elem<DeviceMem, T, MODE, NT, BIG>(g, e, A, B, alpha, beta);
+        generic_elem<DeviceMem, T, MODE, HINT, BIG>(g, e, A, B, alpha, beta);
 }
 
 // ---------------------------------------------------------------------------
@@ -155,101 +119,92 @@ __global__ __launch_bounds__(kBlock) void generic_kernel(const T* __restrict__ A
 template <typename T>
 constexpr int kMaxVec = int(16 / sizeof(T));
 
-template <typename T, int VA, int VB, int MODE, bool NT>
-const void* tile_fn_ipt(int ipt) {
-    switch (ipt) {
-        case 0: return reinterpret_cast<const void*>(&tile_kernel<T, VA, VB, MODE, NT>);
-        case 4: return reinterpret_cast<const void*>(&tile_pipe_kernel<T, VA, VB, MODE, NT, 4>);
-        case 8: return reinterpret_cast<const void*>(&tile_pipe_kernel<T, VA, VB, MODE, NT, 8>);
-        case 16: return reinterpret_cast<const void*>(&tile_pipe_kernel<T, VA, VB, MODE, NT, 16>);
-    }
-    return nullptr;
-}
-
-template <typename T, int MODE, bool NT, int VA>
-const void* tile_fn_vb(int vb, int ipt) {
+template <typename T, int VA, int MODE, int HINT>
+const void* tile_fn_vb(int vb) {
     switch (vb) {
-        case 1: return tile_fn_ipt<T, VA, 1, MODE, NT>(ipt);
-        case 2: return tile_fn_ipt<T, VA, 2, MODE, NT>(ipt);
+        case 1: return reinterpret_cast<const void*>(&tile_kernel<T, VA, 1, MODE, HINT>);
+        case 2: return reinterpret_cast<const void*>(&tile_kernel<T, VA, 2, MODE, HINT>);
         case 4:
-            if constexpr (kMaxVec<T> >= 4) return tile_fn_ipt<T, VA, 4, MODE, NT>(ipt);
+            if constexpr (kMaxVec<T> >= 4)
+                return reinterpret_cast<const void*>(&tile_kernel<T, VA, 4, MODE, HINT>);
             return nullptr;
     }
     return nullptr;
 }
 
-// The pipelined kernel needs the tile's A vectors to fit IPT per thread; a
-// narrower VA (less aligned A) multiplies them, so it may fall back to the
-// plain kernel.
-template <typename T, int MODE, bool NT>
-const void* tile_fn(const TileArgs& g, int va, int vb) {
-    int ipt = g.ipt;
-    if (ipt) {
-        const int64_t items = g.runB * ((g.runA + va - 1) / va);
-        ipt = items <= 4 * kBlock ? 4 : items <= 8 * kBlock ? 8 : items <= 16 * kBlock ? 16 : 0;
-    }
+template <typename T, int MODE, int HINT>
+const void* tile_fn(int va, int vb) {
     switch (va) {
-        case 1: return tile_fn_vb<T, MODE, NT, 1>(vb, ipt);
-        case 2: return tile_fn_vb<T, MODE, NT, 2>(vb, ipt);
+        case 1: return tile_fn_vb<T, 1, MODE, HINT>(vb);
+        case 2: return tile_fn_vb<T, 2, MODE, HINT>(vb);
         case 4:
-            if constexpr (kMaxVec<T> >= 4) return tile_fn_vb<T, MODE, NT, 4>(vb, ipt);
+            if constexpr (kMaxVec<T> >= 4) return tile_fn_vb<T, 4, MODE, HINT>(vb);
             return nullptr;
     }
     return nullptr;
 }
 
-template <typename T, int MODE, bool NT>
+template <typename T, int MODE, int HINT>
 const void* stream_fn(int v) {
     switch (v) {
-        case 1: return reinterpret_cast<const void*>(&stream_kernel<T, 1, MODE, NT>);
-        case 2: return reinterpret_cast<const void*>(&stream_kernel<T, 2, MODE, NT>);
+        case 1: return reinterpret_cast<const void*>(&stream_kernel<T, 1, MODE, HINT>);
+        case 2: return reinterpret_cast<const void*>(&stream_kernel<T, 2, MODE, HINT>);
         case 4:
             if constexpr (kMaxVec<T> >= 4)
-                return reinterpret_cast<const void*>(&stream_kernel<T, 4, MODE, NT>);
+                return reinterpret_cast<const void*>(&stream_kernel<T, 4, MODE, HINT>);
             return nullptr;
     }
     return nullptr;
 }
 
-template <typename T, int MODE, bool NT>
+template <typename T, int MODE, int HINT>
 const void* axpby_fn(int v) {
     switch (v) {
-        case 1: return reinterpret_cast<const void*>(&axpby_kernel<T, 1, MODE, NT>);
-        case 2: return reinterpret_cast<const void*>(&axpby_kernel<T, 2, MODE, NT>);
+        case 1: return reinterpret_cast<const void*>(&axpby_kernel<T, 1, MODE, HINT>);
+        case 2: return reinterpret_cast<const void*>(&axpby_kernel<T, 2, MODE, HINT>);
         case 4:
             if constexpr (kMaxVec<T> >= 4)
-                return reinterpret_cast<const void*>(&axpby_kernel<T, 4, MODE, NT>);
+                return reinterpret_cast<const void*>(&axpby_kernel<T, 4, MODE, HINT>);
             return nullptr;
     }
     return nullptr;
 }
 
-template <typename T, int MODE, bool NT>
+template <typename T, int MODE, int HINT>
 const void* generic_fn(bool big) {
-    return big ? reinterpret_cast<const void*>(&generic_kernel<T, MODE, NT, true>)
-               : reinterpret_cast<const void*>(&generic_kernel<T, MODE, NT, false>);
+    return big ? reinterpret_cast<const void*>(&generic_kernel<T, MODE, HINT, true>)
+               : reinterpret_cast<const void*>(&generic_kernel<T, MODE, HINT, false>);
 }
 
 // Kernel address for the plan's class, with the given vector widths.
-template <typename T, int MODE, bool NT>
+template <typename T, int MODE, int HINT>
 const void* select(const hptt_plan_s* p, int va, int vb) {
     switch (p->info.kernel) {
-        case HPTT_KERNEL_TILE: return tile_fn<T, MODE, NT>(p->tile, va, vb);
-        case HPTT_KERNEL_STREAM: return stream_fn<T, MODE, NT>(va < vb ? va : vb);
-        case HPTT_KERNEL_AXPBY: return axpby_fn<T, MODE, NT>(va < vb ? va : vb);
+        case HPTT_KERNEL_TILE: return tile_fn<T, MODE, HINT>(va, vb);
+        case HPTT_KERNEL_STREAM: return stream_fn<T, MODE, HINT>(va < vb ? va : vb);
+        case HPTT_KERNEL_AXPBY: return axpby_fn<T, MODE, HINT>(va < vb ? va : vb);
         case HPTT_KERNEL_GENERIC:
-            return generic_fn<T, MODE, NT>(p->generic.numel >= (int64_t(1) << 32));
+            return generic_fn<T, MODE, HINT>(p->generic.numel >= (int64_t(1) << 32));
         default: return nullptr;
+    }
+}
+
+template <typename T, int MODE>
+const void* select_hint(const hptt_plan_s* p, int va, int vb) {
+    switch (p->info.hints) {
+        case 0: return select<T, MODE, 0>(p, va, vb);
+        case kNtStore: return select<T, MODE, kNtStore>(p, va, vb);
+        case kNtLoad: return select<T, MODE, kNtLoad>(p, va, vb);
+        default: return select<T, MODE, kNtStore | kNtLoad>(p, va, vb);
     }
 }
 
 template <typename T>
 const void* select_mode(const hptt_plan_s* p, int va, int vb) {
-    const bool nt = p->info.nontemporal != 0;
     switch (p->info.mode) {
-        case kCopy: return nt ? select<T, kCopy, true>(p, va, vb) : select<T, kCopy, false>(p, va, vb);
-        case kScale: return nt ? select<T, kScale, true>(p, va, vb) : select<T, kScale, false>(p, va, vb);
-        default: return select<T, kAxpby, false>(p, va, vb);
+        case kCopy: return select_hint<T, kCopy>(p, va, vb);
+        case kScale: return select_hint<T, kScale>(p, va, vb);
+        default: return select_hint<T, kAxpby>(p, va, vb);
     }
 }
 

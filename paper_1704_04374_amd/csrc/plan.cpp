@@ -17,10 +17,10 @@ int64_t tile_lds_bytes_host(const TileArgs& t, int elem) {
 
 namespace {
 
-constexpr int64_t kLdsBudget = 64 * 1024;  // bytes of LDS per workgroup for kernel T
+constexpr int64_t kLdsMax = 64 * 1024;     // LDS a kernel-T workgroup may use
+constexpr int64_t kLdsBudget = 40 * 1024;  // preferred: at least 4 workgroups per CU
 constexpr int64_t kLine = 128;             // L2 cache line of gfx950
 constexpr int64_t kVecBytes = 16;          // widest global access per lane (dwordx4)
-constexpr int64_t kComputeUnits = 256;     // MI355X
 
 int64_t gcd64(int64_t a, int64_t b) {
     if (a < 0) a = -a;
@@ -106,19 +106,27 @@ void fuse(const int32_t* perm, int32_t N, const int64_t* sizeA, Fused& f) {
 }
 
 // Chunk of an index of extent n that extends a run whose inner part has
-// `inner` elements, aiming at a run of `target` elements.  Preference order:
-// every run starts and ends on a 128-byte line (no line is shared between
-// workgroups), no partial edge tile, then the run length closest to target.
-int64_t choose_chunk(int64_t inner, int64_t n, int64_t target, int elem) {
-    int64_t best = 1;
+// `inner` elements, aiming at a run of `target` elements.  With `aligned`,
+// only chunks whose runs start and end on 128-byte lines qualify (no line is
+// then shared between workgroups); returns 0 if there is none.  Among the
+// candidates: no partial edge tile first, then the length closest to target,
+// where falling short counts double.
+int64_t choose_chunk(int64_t inner, int64_t n, int64_t target, int elem, bool aligned) {
+    int64_t best = 0;
     double bestScore = 1e30;
-    for (int64_t k = 1; k <= n && (k == 1 || inner * k <= 4 * target); ++k) {
+    // Line-aligned chunks are multiples of `step` and may be long, up to
+    // what one LDS tile could hold; others are looked for up to four times
+    // the target.
+    const int64_t step = aligned ? kLine / gcd64(kLine, inner * elem) : 1;
+    const int64_t kmax = aligned ? kLdsMax / (inner * elem) : (4 * target) / inner;
+    for (int64_t k = step; k <= n && (k == 1 || k <= kmax); k += step) {
         const int64_t run = inner * k;
         const int64_t gran = inner * gcd64(k, n);
-        const bool aligned = (gran * elem) % kLine == 0 && (run * elem) % kLine == 0;
-        const bool edge = n % k != 0;
-        const double score = (aligned ? 0.0 : 4.0) + (edge ? 2.0 : 0.0) +
-                             fabs(log2(double(run) / double(target)));
+        const bool lineAligned = (gran * elem) % kLine == 0 && (run * elem) % kLine == 0;
+        if (aligned && !lineAligned) continue;
+        // a run shorter than the target costs twice as much as a longer one
+        const double ratio = log2(double(run) / double(target));
+        const double score = (n % k != 0 ? 2.0 : 0.0) + (ratio < 0 ? -2.0 * ratio : ratio);
         if (score < bestScore) {
             bestScore = score;
             best = k;
@@ -132,7 +140,8 @@ void set_div(FastDiv& f, int64_t d) { f = make_fastdiv(uint32_t(d)); }
 // Kernel T set-up for targets tA (A-run) and tB (B-run).  Returns false if the
 // tile does not fit the LDS budget or the grid is too large.
 bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_options_t& opt,
-                TileArgs& t, hptt_plan_info_t& info) {
+                bool alignA, bool alignB, int64_t ldsBudget, TileArgs& t,
+                hptt_plan_info_t& info) {
     memset(&t, 0, sizeof(t));
     const int M = f.M;
     const int p0 = f.p[0];  // A index that is B's stride-1 index (never 0 here)
@@ -141,7 +150,8 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     int d = 0;
     while (d < p0 - 1 && inner * f.n[d] <= tA) inner *= f.n[d++];
     int64_t cChunk = f.n[d];
-    if (inner * f.n[d] > tA) cChunk = choose_chunk(inner, f.n[d], tA, elem);
+    if (inner * f.n[d] > tA) cChunk = choose_chunk(inner, f.n[d], tA, elem, alignA);
+    if (cChunk == 0) return false;
     const int nC = d + 1;
     t.nC = nC;
     t.cInner = inner;
@@ -156,7 +166,8 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     int k = 0;
     while (k + 1 < M && f.p[k + 1] >= nC && inner * f.n[f.p[k]] <= tB) inner *= f.n[f.p[k++]];
     int64_t rChunk = f.n[f.p[k]];
-    if (inner * rChunk > tB) rChunk = choose_chunk(inner, f.n[f.p[k]], tB, elem);
+    if (inner * rChunk > tB) rChunk = choose_chunk(inner, f.n[f.p[k]], tB, elem, alignB);
+    if (rChunk == 0) return false;
     const int nR = k + 1;
     t.nR = nR;
     t.rInner = inner;
@@ -213,7 +224,7 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     if (opt.lds_pad < 0) pad = 0;
     t.pitch = int32_t(t.runA + pad);
     const int64_t lds = tile_lds_bytes_host(t, elem);
-    if (lds > kLdsBudget) return false;
+    if (lds > ldsBudget) return false;
     // Vector widths: every A run must start on a multiple of vec_a elements,
     // every B run on a multiple of vec_b.
     int64_t granA = 0, granB = 0;
@@ -228,6 +239,9 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
         if (t.cExt[j].d > 1) granB = gcd64(granB, t.cStrideB[j]);
     info.vec_a = vec_width(granA, elem, opt.max_vec);
     info.vec_b = vec_width(granB, elem, opt.max_vec);
+    // A runs that start and end on 128-byte lines share no line with another
+    // tile, so they can be read with non-temporal loads.
+    t.alignedA = (granA == 0 || (granA * elem) % kLine == 0) && (t.runA * elem) % kLine == 0;
     info.run_a = t.runA;
     info.run_b = t.runB;
     info.dims_a = nC;
@@ -295,9 +309,9 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, d
     if (options) opt = *options;
     if (opt.kernel < HPTT_KERNEL_AUTO || opt.kernel > HPTT_KERNEL_GENERIC ||
         opt.kernel == HPTT_KERNEL_NONE || opt.run_a < 0 || opt.run_b < 0 || opt.max_vec < 0 ||
-        opt.nontemporal < 0 || opt.nontemporal > 2 ||
+        opt.store_hint < 0 || opt.store_hint > 2 || opt.load_hint < 0 || opt.load_hint > 2 ||
         opt.lds_pad < -1 || opt.lds_pad > 64 || opt.max_blocks < 0 || opt.tile_order < 0 ||
-        opt.tile_order > 2 || opt.pipeline < 0 || opt.pipeline > 2)
+        opt.tile_order > 2 || opt.exact_runs < 0 || opt.exact_runs > 1)
         return HPTT_ERROR_INVALID_ARGUMENT;
 
     const int elem = dtype == HPTT_FLOAT32 ? 4 : 8;
@@ -309,7 +323,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, d
     info.elem_bytes = elem;
     info.block = kBlock;
     info.mode = plan->beta != 0.0 ? kAxpby : (plan->alpha == 1.0 ? kCopy : kScale);
-    info.nontemporal = (opt.nontemporal == 1 && info.mode != kAxpby) ? 1 : 0;
+    info.hints = 0;
 
     int64_t numel = 1;
     bool empty = false;
@@ -355,15 +369,40 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, d
     const int64_t maxBlocks = opt.max_blocks > 0 ? opt.max_blocks : (int64_t(1) << 31) - 1;
 
     if (k == HPTT_KERNEL_TILE) {
-        int64_t tA = opt.run_a > 0 ? opt.run_a : 512 / elem;
-        int64_t tB = opt.run_b > 0 ? opt.run_b : 256 / elem;
+        // Tile search, in order of preference (each stage halves the longer
+        // target until a tile fits): both runs on whole 128-byte lines within
+        // the occupancy budget; B runs aligned, A runs cut to length; A runs
+        // aligned, B runs cut to length; both cut to length; finally, both
+        // aligned up to the LDS limit.  On MI355X a fourth resident
+        // workgroup per CU was measured to be worth more than line-aligned A
+        // runs, and aligned B runs more than aligned A runs.
+        // Default targets: A runs of 512 bytes, B runs of one 128-byte line
+        // (on MI355X short B runs with long A runs measured fastest: the
+        // tile stays small, so more workgroups stay resident).
+        const int64_t tA0 = opt.run_a > 0 ? opt.run_a : 512 / elem;
+        const int64_t tB0 = opt.run_b > 0 ? opt.run_b : kLine / elem;
+        struct Stage { bool alignA, alignB; int64_t budget; };
+        const Stage forced[] = {{false, false, kLdsMax}};
+        const Stage stages[] = {{true, true, kLdsBudget},  {false, true, kLdsBudget},
+                                {true, false, kLdsBudget}, {false, false, kLdsBudget},
+                                {true, true, kLdsMax},     {false, false, kLdsMax}};
+        const Stage* st = opt.exact_runs ? forced : stages;
+        const int nst = opt.exact_runs ? 1 : 6;
+        int64_t tA = tA0, tB = tB0;
+        Stage chosen = st[0];
         bool ok = false;
-        for (int attempt = 0; attempt < 24 && !ok; ++attempt) {
-            ok = setup_tile(f, elem, tA, tB, opt, plan->tile, info);
-            if (!ok) {
-                if (tA >= tB && tA > 1) tA /= 2;
-                else if (tB > 1) tB /= 2;
-                else break;
+        for (int s = 0; s < nst && !ok; ++s) {
+            tA = tA0;
+            tB = tB0;
+            chosen = st[s];
+            for (int attempt = 0; attempt < 24 && !ok; ++attempt) {
+                ok = setup_tile(f, elem, tA, tB, opt, chosen.alignA, chosen.alignB, chosen.budget,
+                                plan->tile, info);
+                if (!ok) {
+                    if (tA >= tB && tA > 1) tA /= 2;
+                    else if (tB > 1) tB /= 2;
+                    else break;
+                }
             }
         }
         // Small problems: shorter runs (down to one 128-byte line) for more
@@ -374,7 +413,8 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, d
             hptt_plan_info_t keepInfo = info;
             if (tA >= tB) tA /= 2;
             else tB /= 2;
-            if (!setup_tile(f, elem, tA, tB, opt, plan->tile, info) ||
+            if (!setup_tile(f, elem, tA, tB, opt, chosen.alignA, chosen.alignB, kLdsMax,
+                            plan->tile, info) ||
                 plan->tile.numTiles <= keep.numTiles) {
                 plan->tile = keep;
                 info = keepInfo;
@@ -385,19 +425,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, d
             if (opt.kernel == HPTT_KERNEL_TILE) return HPTT_ERROR_UNSUPPORTED;
             k = HPTT_KERNEL_GENERIC;
         } else {
-            TileArgs& t = plan->tile;
-            int64_t grid = t.numTiles;
-            // Persistent pipelined kernel: the tile's A vectors must fit 16 per
-            // thread; the grid is what the LDS lets stay resident on 256 CUs.
-            const int64_t items = t.runB * ((t.runA + info.vec_a - 1) / info.vec_a);
-            t.ipt = 0;
-            if (opt.pipeline == 2 && items <= 16 * kBlock) {
-                t.ipt = items <= 4 * kBlock ? 4 : items <= 8 * kBlock ? 8 : 16;
-                int64_t perCU = (160 * 1024) / info.lds_bytes;
-                perCU = perCU < 1 ? 1 : perCU > 8 ? 8 : perCU;
-                if (grid > kComputeUnits * perCU) grid = kComputeUnits * perCU;
-            }
-            info.pipeline = t.ipt;
+            const int64_t grid = plan->tile.numTiles;
             info.grid = grid < maxBlocks ? grid : maxBlocks;
         }
     }
@@ -428,6 +456,13 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, d
         if (grid > 65536) grid = 65536;
         info.grid = grid < maxBlocks ? grid : maxBlocks;
     }
+    // Cache hints.  Every element is touched once, so by default B is written
+    // and A read with non-temporal hints, except A runs that share 128-byte
+    // lines with a neighbouring tile (the neighbour would miss the line).
+    const bool loadOk = k != HPTT_KERNEL_TILE || plan->tile.alignedA;
+    const bool ntStore = opt.store_hint != 2;
+    const bool ntLoad = opt.load_hint == 1 || (opt.load_hint == 0 && loadOk && k != HPTT_KERNEL_GENERIC);
+    info.hints = (ntStore ? kNtStore : 0) | (ntLoad ? kNtLoad : 0);
     info.kernel = k;
     return HPTT_SUCCESS;
 }
@@ -444,12 +479,12 @@ void describe_plan(const hptt_plan_s* p, char* buf, size_t len) {
     }
     snprintf(buf, len,
              "kernel=%s dtype=%s mode=%s fused=(%s) perm=(%s) run_a=%lld run_b=%lld "
-             "dims_a=%d dims_b=%d vec=%d/%d pitch=%d lds=%d tiles=%lld grid=%lld block=%d nt=%d "
-             "order=%d pipe=%d",
+             "dims_a=%d dims_b=%d vec=%d/%d pitch=%d lds=%d tiles=%lld grid=%lld block=%d hints=%d "
+             "order=%d",
              kKernel[in.kernel], p->dtype == HPTT_FLOAT32 ? "f32" : "f64", kMode[in.mode], shape,
              perm, (long long)in.run_a, (long long)in.run_b, in.dims_a, in.dims_b, in.vec_a,
              in.vec_b, in.lds_pitch, in.lds_bytes, (long long)in.tiles, (long long)in.grid,
-             in.block, in.nontemporal, in.tile_order, in.pipeline);
+             in.block, in.hints, in.tile_order);
 }
 
 }  // namespace hptt

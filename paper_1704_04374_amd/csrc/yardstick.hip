@@ -1,6 +1,5 @@
 // Measurement kernels: a 16-byte-per-lane streaming copy, an axpby, a fill
-// and a read-only sweep.  The fill and axpby blocks move kUnroll vectors per
-// lane with all loads issued before the stores.
+// and a read-only sweep.
 #include <hip/hip_runtime.h>
 
 #include "hptt_yardstick.h"
@@ -8,19 +7,24 @@
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kUnroll = 4;      // vectors per lane of the fill and axpby kernels
+constexpr int kUnroll = 4;      // vectors per lane of the fill kernel
 constexpr int kReadBlocks = 1024;
 
 struct alignas(16) V16 {
     uint32_t w[4];
 };
 
-// One 16-byte vector per lane and a grid that covers the buffer once: the
-// fastest plain copy among the unroll depths and grid shapes tried on MI355X.
+// One 16-byte vector per lane, a grid that covers the buffer once, and
+// non-temporal loads and stores: the fastest plain copy among the unroll
+// depths, grid shapes and cache hints tried on MI355X.
 __global__ __launch_bounds__(kThreads) void copy_kernel(const V16* __restrict__ src,
                                                         V16* __restrict__ dst, size_t n) {
+    typedef uint32_t v4 __attribute__((ext_vector_type(4)));
     const size_t i = size_t(blockIdx.x) * kThreads + threadIdx.x;
-    if (i < n) dst[i] = src[i];
+    if (i < n) {
+        const v4 x = __builtin_nontemporal_load(reinterpret_cast<const v4*>(src) + i);
+        __builtin_nontemporal_store(x, reinterpret_cast<v4*>(dst) + i);
+    }
 }
 
 __global__ __launch_bounds__(kThreads) void read_kernel(const V16* __restrict__ src, size_t n,
@@ -55,31 +59,27 @@ struct alignas(16) VT {
     T v[16 / sizeof(T)];
 };
 
+// y <- alpha*x + beta*y, one 16-byte vector per lane, x read and y written
+// with non-temporal hints (y is read with an ordinary load).
 template <typename T>
 __global__ __launch_bounds__(kThreads) void axpby_kernel(T alpha, const VT<T>* __restrict__ x,
                                                          T beta, VT<T>* __restrict__ y, size_t n) {
 #pragma clang fp contract(off)
     constexpr int V = int(16 / sizeof(T));
-    const size_t i = size_t(blockIdx.x) * (kThreads * kUnroll) + threadIdx.x;
-    VT<T> a[kUnroll], b[kUnroll];
+    typedef T vt __attribute__((ext_vector_type(V)));
+    const size_t i = size_t(blockIdx.x) * kThreads + threadIdx.x;
+    if (i < n) {
+        const vt a = __builtin_nontemporal_load(reinterpret_cast<const vt*>(x) + i);
+        const vt b = reinterpret_cast<const vt*>(y)[i];
+        vt c;
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u)
-        if (i + size_t(u) * kThreads < n) {
-            a[u] = x[i + size_t(u) * kThreads];
-            b[u] = y[i + size_t(u) * kThreads];
+        for (int e = 0; e < V; ++e) {
+            T s = alpha * a[e];
+            T t = beta * b[e];
+            c[e] = s + t;
         }
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u)
-        if (i + size_t(u) * kThreads < n) {
-            VT<T> c;
-#pragma unroll
-            for (int e = 0; e < V; ++e) {
-                T s = alpha * a[u].v[e];
-                T t = beta * b[u].v[e];
-                c.v[e] = s + t;
-            }
-            y[i + size_t(u) * kThreads] = c;
-        }
+        __builtin_nontemporal_store(c, reinterpret_cast<vt*>(y) + i);
+    }
 }
 
 size_t blocks_for(size_t n16) {
@@ -134,7 +134,7 @@ hptt_status_t hptt_yardstick_axpby(hptt_dtype_t dtype, double alpha, const void*
         return HPTT_ERROR_INVALID_ARGUMENT;
     const size_t n16 = n * elem / 16;
     if (n16 == 0) return HPTT_SUCCESS;
-    const dim3 grid(uint32_t(blocks_for(n16)));
+    const dim3 grid(uint32_t((n16 + kThreads - 1) / kThreads));
     if (dtype == HPTT_FLOAT32)
         hipLaunchKernelGGL(axpby_kernel<float>, grid, dim3(kThreads), 0, stream, float(alpha),
                            static_cast<const VT<float>*>(x), float(beta),

@@ -37,10 +37,10 @@ class HpttError(RuntimeError):
 class Options(ctypes.Structure):
     """hptt_options_t"""
     _fields_ = [("kernel", ctypes.c_int), ("run_a", ctypes.c_int32), ("run_b", ctypes.c_int32),
-                ("max_vec", ctypes.c_int32), ("nontemporal", ctypes.c_int32),
-                ("lds_pad", ctypes.c_int32),
+                ("max_vec", ctypes.c_int32), ("store_hint", ctypes.c_int32),
+                ("load_hint", ctypes.c_int32), ("lds_pad", ctypes.c_int32),
                 ("max_blocks", ctypes.c_int32), ("tile_order", ctypes.c_int32),
-                ("pipeline", ctypes.c_int32)]
+                ("exact_runs", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -53,8 +53,8 @@ class PlanInfo(ctypes.Structure):
                 ("vec_a", ctypes.c_int32), ("vec_b", ctypes.c_int32),
                 ("lds_pitch", ctypes.c_int32), ("lds_bytes", ctypes.c_int32),
                 ("tiles", ctypes.c_int64), ("grid", ctypes.c_int64), ("block", ctypes.c_int32),
-                ("nontemporal", ctypes.c_int32), ("mode", ctypes.c_int32),
-                ("tile_order", ctypes.c_int32), ("pipeline", ctypes.c_int32)]
+                ("hints", ctypes.c_int32), ("mode", ctypes.c_int32),
+                ("tile_order", ctypes.c_int32)]
 
     def as_dict(self) -> dict:
         n = self.ndim
@@ -64,8 +64,8 @@ class PlanInfo(ctypes.Structure):
                 "dims_a": self.dims_a, "dims_b": self.dims_b, "vec_a": self.vec_a,
                 "vec_b": self.vec_b, "lds_pitch": self.lds_pitch, "lds_bytes": self.lds_bytes,
                 "tiles": self.tiles, "grid": self.grid, "block": self.block,
-                "nontemporal": self.nontemporal, "mode": MODES[self.mode],
-                "tile_order": self.tile_order, "pipeline": self.pipeline}
+                "hints": self.hints, "mode": MODES[self.mode],
+                "tile_order": self.tile_order}
 
 
 # Every entry point declared in include/hptt.h and include/hptt_yardstick.h.
@@ -215,6 +215,18 @@ class Plan:
         if st == 5:
             raise HpttError(st, f"hptt_exec (hipError {self._lib.hptt_last_hip_error()})")
         _check(st, "hptt_exec")
+
+    def launcher(self, A_ptr: int, B_ptr: int, stream: int):
+        """A zero-argument callable that queues this plan on fixed device
+        pointers and stream with no per-call checks (for timing loops)."""
+        f = self._lib.hptt_exec
+        h, a, b, s = self._handle, ctypes.c_void_p(A_ptr), ctypes.c_void_p(B_ptr), ctypes.c_void_p(stream)
+
+        def run():
+            st = f(h, a, b, s)
+            if st != SUCCESS:
+                raise HpttError(st, "hptt_exec")
+        return run
 
     def _check_tensor(self, t, name):
         if not t.is_cuda:

@@ -70,7 +70,7 @@ void check_lds(const void* p, int64_t bytes, bool isStore) {
 }
 
 struct HostMem {
-    template <typename T, int V>
+    template <typename T, int V, bool NT>
     static hptt::Vec<T, V> ld(const T* p, int64_t off) {
         hptt::Vec<T, V> r;
         memset(&r, 0, sizeof(r));
@@ -116,7 +116,7 @@ void clear_written(int64_t from, int64_t to) {
 }
 
 // Mirrors tile_kernel in kernels.hip.
-template <typename T, int VA, int VB, int MODE, bool NT>
+template <typename T, int VA, int VB, int MODE, int NT>
 void emu_tile(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     using namespace hptt;
     const TileArgs& g = p->tile;
@@ -135,60 +135,16 @@ void emu_tile(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
         for (int64_t t = blk; t < g.numTiles && S->errors == 0; t += grid) {
             clear_written(tableBytes, ldsBytes);
             const TileBase tb = tile_base(g, uint32_t(t));
-            for (int tid = 0; tid < kBlock; ++tid) tile_load<HostMem, T, VA>(g, tb, tid, A, lds, rowOffA);
+            for (int tid = 0; tid < kBlock; ++tid)
+                tile_load<HostMem, T, VA, NT>(g, tb, tid, A, lds, rowOffA);
             for (int tid = 0; tid < kBlock; ++tid)
                 tile_store<HostMem, T, VB, MODE, NT>(g, tb, tid, B, lds, colOffB, alpha, beta);
-        }
-    }
-}
-
-// Mirrors tile_pipe_kernel in kernels.hip; each thread keeps its fetched
-// vectors in its own register file between the phases.
-template <typename T, int VA, int VB, int MODE, bool NT, int IPT>
-void emu_tile_pipe(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
-    using namespace hptt;
-    const TileArgs& g = p->tile;
-    const T alpha = T(p->alpha), beta = T(p->beta);
-    const int64_t ldsBytes = p->info.lds_bytes;
-    const int64_t tableBytes = (g.runA + g.runB) * int64_t(sizeof(int64_t));
-    S->lds.assign(size_t(ldsBytes), 0);
-    S->written.assign(size_t(ldsBytes), 0);
-    int64_t* rowOffA = reinterpret_cast<int64_t*>(S->lds.data());
-    int64_t* colOffB = rowOffA + g.runB;
-    T* lds = reinterpret_cast<T*>(colOffB + g.runA);
-    const int64_t grid = p->info.grid;
-    std::vector<Vec<T, VA>> regs(size_t(kBlock) * IPT);
-    auto reg = [&](int tid) -> Vec<T, VA>(&)[IPT] {
-        return *reinterpret_cast<Vec<T, VA>(*)[IPT]>(&regs[size_t(tid) * IPT]);
-    };
-    for (int64_t blk = 0; blk < grid && S->errors == 0; blk += blockStride) {
-        if (blk >= g.numTiles) continue;
-        clear_written(0, ldsBytes);
-        for (int tid = 0; tid < kBlock; ++tid) tile_tables<HostMem>(g, tid, rowOffA, colOffB);
-        int64_t t = blk;
-        TileBase tb = tile_base(g, uint32_t(t));
-        for (int tid = 0; tid < kBlock; ++tid) tile_fetch<HostMem, T, VA, IPT>(g, tb, tid, A, rowOffA, reg(tid));
-        while (S->errors == 0) {
-            clear_written(tableBytes, ldsBytes);
-            for (int tid = 0; tid < kBlock; ++tid) tile_park<HostMem, T, VA, IPT>(g, tb, tid, reg(tid), lds);
-            const int64_t next = t + grid;
-            const bool more = next < g.numTiles;
-            TileBase tn = tb;
-            if (more) {
-                tn = tile_base(g, uint32_t(next));
-                for (int tid = 0; tid < kBlock; ++tid) tile_fetch<HostMem, T, VA, IPT>(g, tn, tid, A, rowOffA, reg(tid));
-            }
-            for (int tid = 0; tid < kBlock; ++tid)
-                tile_store<HostMem, T, VB, MODE, NT>(g, tb, tid, B, lds, colOffB, alpha, beta);
-            if (!more) break;
-            t = next;
-            tb = tn;
         }
     }
 }
 
 // Mirrors stream_kernel in kernels.hip.
-template <typename T, int V, int MODE, bool NT>
+template <typename T, int V, int MODE, int NT>
 void emu_stream(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     using namespace hptt;
     const StreamArgs& g = p->stream;
@@ -202,7 +158,7 @@ void emu_stream(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
 }
 
 // Mirrors axpby_kernel and generic_kernel in kernels.hip.
-template <typename T, int V, int MODE, bool NT>
+template <typename T, int V, int MODE, int NT>
 void emu_axpby(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     using namespace hptt;
     const int64_t numel = p->info.numel, vecs = (numel + V - 1) / V;
@@ -213,7 +169,7 @@ void emu_axpby(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
                 axpby_items<HostMem, T, V, MODE, NT>(numel, first, tid, A, B, T(p->alpha), T(p->beta));
 }
 
-template <typename T, int MODE, bool NT>
+template <typename T, int MODE, int NT>
 void emu_generic(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     using namespace hptt;
     const GenericArgs& g = p->generic;
@@ -227,23 +183,10 @@ void emu_generic(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
             }
 }
 
-template <typename T, int MODE, bool NT, int VA, int VB>
+template <typename T, int MODE, int NT, int VA, int VB>
 void run_widths(const hptt_plan_s* p, const T* A, T* B, int64_t bs) {
     switch (p->info.kernel) {
-        case HPTT_KERNEL_TILE: {
-            // same choice as tile_fn in kernels.hip
-            int ipt = p->tile.ipt;
-            if (ipt) {
-                const int64_t items = p->tile.runB * ((p->tile.runA + VA - 1) / VA);
-                ipt = items <= 4 * hptt::kBlock ? 4 : items <= 8 * hptt::kBlock ? 8
-                      : items <= 16 * hptt::kBlock ? 16 : 0;
-            }
-            if (ipt == 4) emu_tile_pipe<T, VA, VB, MODE, NT, 4>(p, A, B, bs);
-            else if (ipt == 8) emu_tile_pipe<T, VA, VB, MODE, NT, 8>(p, A, B, bs);
-            else if (ipt == 16) emu_tile_pipe<T, VA, VB, MODE, NT, 16>(p, A, B, bs);
-            else emu_tile<T, VA, VB, MODE, NT>(p, A, B, bs);
-            break;
-        }
+        case HPTT_KERNEL_TILE: emu_tile<T, VA, VB, MODE, NT>(p, A, B, bs); break;
         case HPTT_KERNEL_STREAM: emu_stream<T, (VA < VB ? VA : VB), MODE, NT>(p, A, B, bs); break;
         case HPTT_KERNEL_AXPBY: emu_axpby<T, (VA < VB ? VA : VB), MODE, NT>(p, A, B, bs); break;
         case HPTT_KERNEL_GENERIC: emu_generic<T, MODE, NT>(p, A, B, bs); break;
@@ -251,33 +194,36 @@ void run_widths(const hptt_plan_s* p, const T* A, T* B, int64_t bs) {
     }
 }
 
-template <typename T, int MODE, bool NT, int VA>
+template <typename T, int MODE, int NT, int VA>
 void run_vb(const hptt_plan_s* p, const T* A, T* B, int vb, int64_t bs) {
     if (vb == 1) run_widths<T, MODE, NT, VA, 1>(p, A, B, bs);
     else if (vb == 2) run_widths<T, MODE, NT, VA, 2>(p, A, B, bs);
     else if constexpr (sizeof(T) == 4) run_widths<T, MODE, NT, VA, 4>(p, A, B, bs);
 }
 
-template <typename T, int MODE, bool NT>
+template <typename T, int MODE, int NT>
 void run_va(const hptt_plan_s* p, const T* A, T* B, int va, int vb, int64_t bs) {
     if (va == 1) run_vb<T, MODE, NT, 1>(p, A, B, vb, bs);
     else if (va == 2) run_vb<T, MODE, NT, 2>(p, A, B, vb, bs);
     else if constexpr (sizeof(T) == 4) run_vb<T, MODE, NT, 4>(p, A, B, vb, bs);
 }
 
+template <typename T, int MODE>
+void run_hint(const hptt_plan_s* p, const T* A, T* B, int va, int vb, int64_t bs) {
+    switch (p->info.hints) {
+        case 0: run_va<T, MODE, 0>(p, A, B, va, vb, bs); break;
+        case hptt::kNtStore: run_va<T, MODE, hptt::kNtStore>(p, A, B, va, vb, bs); break;
+        case hptt::kNtLoad: run_va<T, MODE, hptt::kNtLoad>(p, A, B, va, vb, bs); break;
+        default: run_va<T, MODE, hptt::kNtStore | hptt::kNtLoad>(p, A, B, va, vb, bs);
+    }
+}
+
 template <typename T>
 void run(const hptt_plan_s* p, const T* A, T* B, int va, int vb, int64_t bs) {
-    const bool nt = p->info.nontemporal != 0;
     switch (p->info.mode) {
-        case hptt::kCopy:
-            if (nt) run_va<T, hptt::kCopy, true>(p, A, B, va, vb, bs);
-            else run_va<T, hptt::kCopy, false>(p, A, B, va, vb, bs);
-            break;
-        case hptt::kScale:
-            if (nt) run_va<T, hptt::kScale, true>(p, A, B, va, vb, bs);
-            else run_va<T, hptt::kScale, false>(p, A, B, va, vb, bs);
-            break;
-        default: run_va<T, hptt::kAxpby, false>(p, A, B, va, vb, bs);
+        case hptt::kCopy: run_hint<T, hptt::kCopy>(p, A, B, va, vb, bs); break;
+        case hptt::kScale: run_hint<T, hptt::kScale>(p, A, B, va, vb, bs); break;
+        default: run_hint<T, hptt::kAxpby>(p, A, B, va, vb, bs);
     }
 }
 

@@ -70,12 +70,12 @@ def test_random_problems_match_oracle():
     dict(lds_pad=4),
     dict(max_vec=1),
     dict(max_vec=2),
-    dict(nontemporal=1),
+    dict(store_hint=1),
+    dict(load_hint=1, store_hint=1),
     dict(tile_order=1),
-    dict(pipeline=2),
-    dict(pipeline=2, max_blocks=3),
-    dict(pipeline=2, run_a=4, run_b=4),
-    dict(pipeline=2, max_vec=1),
+    dict(run_a=64, run_b=64),
+    dict(run_a=512, run_b=8),
+    dict(exact_runs=1, run_a=6, run_b=10),
 ])
 def test_knobs_match_oracle(knobs):
     rng = np.random.default_rng(11)
@@ -88,13 +88,13 @@ def test_knobs_match_oracle(knobs):
 
 
 @pytest.mark.parametrize("va,vb", [(1, 1), (1, 4), (4, 1), (2, 2), (2, 4)])
-@pytest.mark.parametrize("pipeline", [1, 2])
-def test_narrow_vectors_as_for_misaligned_pointers(va, vb, pipeline):
+@pytest.mark.parametrize("order", [1, 2])
+def test_narrow_vectors_as_for_misaligned_pointers(va, vb, order):
     """hptt_exec narrows the vector widths for less aligned pointers."""
     rng = np.random.default_rng(13)
     for size_a, perm in [((64, 33), (1, 0)), ((24, 20, 16, 5), (3, 2, 0, 1)),
                          ((3, 2, 64, 7, 32), (4, 2, 0, 3, 1)), ((96, 7, 9), (0, 2, 1))]:
-        p = emu.plan(perm, size_a, 1.5, 0.5, "f32", pipeline=pipeline)
+        p = emu.plan(perm, size_a, 1.5, 0.5, "f32", tile_order=order)
         _check(p, size_a, perm, 1.5, 0.5, "f32", rng, va=min(va, p.info["vec_a"]),
                vb=min(vb, p.info["vec_b"]))
 
@@ -115,7 +115,7 @@ def test_small_workload_matches_oracle(w):
     _check(p, w.size_a, w.perm, w.alpha, w.beta, w.dtype, rng)
 
 
-@pytest.mark.parametrize("knobs", [dict(), dict(pipeline=2)], ids=["default", "pipelined"])
+@pytest.mark.parametrize("knobs", [dict(), dict(tile_order=1)], ids=["default", "digit_order"])
 @pytest.mark.parametrize("w", WORKLOADS, ids=lambda w: w.name)
 def test_full_size_geometry(w, knobs):
     """Dry run of every workgroup of each full-size workload: every offset in

@@ -100,9 +100,10 @@ def test_random_sweep():
 
 @pytest.mark.parametrize("knobs", [dict(kernel="generic"), dict(run_a=8, run_b=8),
                                    dict(run_a=3, run_b=5), dict(max_blocks=7),
-                                   dict(max_vec=1), dict(nontemporal=1), dict(lds_pad=-1),
-                                   dict(tile_order=1), dict(pipeline=2),
-                                   dict(pipeline=2, max_blocks=3), dict(pipeline=2, max_vec=1)],
+                                   dict(max_vec=1), dict(store_hint=1, load_hint=1), dict(lds_pad=-1),
+                                   dict(tile_order=1), dict(run_a=512, run_b=8),
+                                   dict(run_a=64, run_b=64, max_blocks=5),
+                                   dict(exact_runs=1, run_a=6, run_b=10)],
                          ids=lambda k: ",".join(f"{a}={b}" for a, b in k.items()))
 def test_forced_variants(knobs):
     rng = np.random.default_rng(99)
@@ -128,7 +129,7 @@ def test_misaligned_pointers_fall_back():
     for (size_a, perm, dtype), pipe in itertools.product(
             [((64, 64), (1, 0), "f32"), ((3, 2, 64, 8, 32), (4, 2, 0, 3, 1), "f32"),
              ((96, 6, 7), (0, 2, 1), "f64"), ((1000,), (0,), "f32")], (1, 2)):
-        p = hptt.create_plan(perm, size_a, 1.5, 0.5, dtype, pipeline=pipe)
+        p = hptt.create_plan(perm, size_a, 1.5, 0.5, dtype, tile_order=pipe)
         n = p.numel
         A = _rand(rng, n, dtype)
         B0 = _rand(rng, n, dtype)

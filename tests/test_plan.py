@@ -86,15 +86,15 @@ EXPECTED = {
     "transpose3d_48x40x32_f32": dict(kernel="tile", size=(1920, 32), perm=(1, 0), run_a=32,
                                      run_b=32, tiles=60),
     "transpose2d_8192x8192_f32": dict(kernel="tile", size=(8192, 8192), perm=(1, 0), run_a=128,
-                                      run_b=64, tiles=8192, tile_order=2),
+                                      run_b=32, tiles=16384, tile_order=2, hints=3),
     "transpose6d_24x20x16x24x18x20_f32": dict(kernel="tile", size=(24, 20, 16, 24, 18, 20),
-                                              perm=(5, 2, 0, 4, 1, 3), run_a=96, run_b=160,
-                                              dims_a=2, dims_b=2, tiles=4320),
+                                              perm=(5, 2, 0, 4, 1, 3), run_a=48, run_b=160,
+                                              dims_a=2, dims_b=2, tiles=8640, hints=1),
     "transpose4d_96x96x96x96_keep1_f64": dict(kernel="stream", size=(96, 96, 96, 96),
                                               perm=(0, 3, 2, 1), run_b=96, vec_a=2, vec_b=2),
     "transpose5d_3x2x640x480x96_f32": dict(kernel="tile", size=(3, 2, 640, 480, 96),
-                                           perm=(4, 2, 0, 3, 1), run_a=96, run_b=96, dims_a=3,
-                                           dims_b=1, tiles=19200),
+                                           perm=(4, 2, 0, 3, 1), run_a=192, run_b=32, dims_a=3,
+                                           dims_b=1, tiles=28800, hints=3),
 }
 
 
@@ -109,10 +109,11 @@ def test_workload_plans(name):
     assert info["numel"] == w.numel
     if info["kernel"] == "tile":
         assert info["vec_a"] == info["vec_b"] == 16 // w.elem_bytes
-        assert info["lds_bytes"] <= 65536
-        # runs of whole 128-byte lines on both sides
-        assert (info["run_a"] * w.elem_bytes) % 128 == 0
-        assert (info["run_b"] * w.elem_bytes) % 128 == 0
+        assert info["lds_bytes"] <= 40 * 1024          # at least 4 workgroups per CU
+        assert (info["run_b"] * w.elem_bytes) % 128 == 0   # B runs of whole lines
+        # non-temporal A loads exactly when A runs are whole lines
+        assert bool(info["hints"] & 2) == ((info["run_a"] * w.elem_bytes) % 128 == 0)
+        assert info["hints"] & 1                        # non-temporal B stores
         assert info["lds_pitch"] % 2 == 1
 
 
@@ -165,7 +166,8 @@ def test_null_arguments():
 
 
 @pytest.mark.parametrize("field,value", [("kernel", 9), ("kernel", 1), ("run_a", -1),
-                                         ("nontemporal", 3), ("lds_pad", 65), ("max_blocks", -2)])
+                                         ("store_hint", 3), ("load_hint", -1), ("lds_pad", 65),
+                                         ("max_blocks", -2), ("tile_order", 3), ("exact_runs", 2)])
 def test_invalid_options(field, value):
     opt = hptt.Options()
     setattr(opt, field, value)
@@ -211,3 +213,17 @@ def test_workload_bytes_follow_eq2():
     for w in WORKLOADS:
         assert w.lam == table.get(w.beta, 3 if w.beta else 2)
         assert w.moved_bytes == w.lam * w.numel * w.elem_bytes
+
+
+def test_plan_creation_is_quick():
+    """The quick path of Section 3.1 keeps plan creation negligible: well
+    under a millisecond even for large extents and rank 16."""
+    import time
+    cases = [((1 << 20, 1 << 12), (1, 0)), ((3, 5, 7, 11, 13, 17), (5, 4, 3, 2, 1, 0)),
+             ((2,) * 16, tuple(range(15, -1, -1))), ((8192, 8192), (1, 0))]
+    hptt.create_plan((1, 0), (4, 4))
+    for size, perm in cases:
+        t0 = time.perf_counter()
+        for _ in range(10):
+            hptt.create_plan(perm, size)
+        assert (time.perf_counter() - t0) / 10 < 2e-3, size
