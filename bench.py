@@ -86,21 +86,22 @@ def _events(torch, n):
 
 def time_launches(torch, fn, steps: int, warmup: int):
     """Run fn(i) for i < warmup, then `steps` more back to back between a
-    synchronize on each side, with one HIP event before the first timed launch
-    and one after the last, both on the launch stream.  Returns (wall seconds,
-    GPU milliseconds per launch)."""
+    synchronize on each side, with a HIP event pair around every launch on
+    the launch stream.  Returns (wall seconds of the whole timed region,
+    mean GPU milliseconds of one launch).  The wall time also contains the
+    gaps the GPU leaves between dependent launches in one stream."""
     for i in range(warmup):
         fn(i)
     torch.cuda.synchronize()
-    start, end = _events(torch, 2)
+    starts, ends = _events(torch, steps), _events(torch, steps)
     t0 = time.perf_counter()
-    start.record()
     for i in range(steps):
+        starts[i].record()
         fn(warmup + i)
-    end.record()
+        ends[i].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    return wall, start.elapsed_time(end) / steps
+    return wall, sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / steps
 
 
 def time_cold(torch, hptt, fn, flush_buf, sink, reps: int):
