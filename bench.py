@@ -101,7 +101,9 @@ def time_launches(torch, fn, steps: int, warmup: int):
         ends[i].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    return wall, sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / steps
+    ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    time_launches.last = sorted(ms)
+    return wall, sum(ms) / steps
 
 
 def time_cold(torch, hptt, fn, flush_buf, sink, reps: int):
@@ -118,6 +120,21 @@ def time_cold(torch, hptt, fn, flush_buf, sink, reps: int):
         torch.cuda.synchronize()
         ms.append(s.elapsed_time(e))
     return ms
+
+
+def preheat(torch, hptt, seconds: float = 0.3):
+    """Untimed streaming copies until the GPU has run for `seconds`: launch
+    times fall by about 10 % over the first few hundred milliseconds of work
+    as the clocks settle, which would otherwise bias the first workload."""
+    buf = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    half = buf.numel() // 2
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(10):
+            hptt.yardstick_copy(buf[:half], buf[half:], half * 4)
+        torch.cuda.synchronize()
+    del buf
+    torch.cuda.empty_cache()
 
 
 def rotation(w) -> int:
@@ -163,6 +180,10 @@ def measure_workload(torch, hptt, w, steps, warmup, reps, flush_buf, sink, full:
         return nbytes / (ms * 1e-3) / 1e9
 
     wall, ms = time_launches(torch, transpose, steps, warmup)
+    dist = time_launches.last
+    out["kernel_us"] = {"mean": round(ms * 1e3, 2), "min": round(dist[0] * 1e3, 2),
+                        "median": round(dist[len(dist) // 2] * 1e3, 2),
+                        "max": round(dist[-1] * 1e3, 2)}
     out["ms_per_step"] = wall * 1e3 / steps
     out["gbs"] = moved * steps / wall / 1e9
     out["kernel_avg_ms"] = ms
@@ -318,8 +339,8 @@ def summarize_trace(trace_dir: str, workload: str, command: str, out_path: str):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=HEADLINE)
     ap.add_argument("--reps", type=int, default=20, help="flushed single launches per workload")
     ap.add_argument("--only-headline", action="store_true",
@@ -365,6 +386,7 @@ def main():
     print(f"[bench] device {torch.cuda.get_device_name(0)}; headline {head.describe()}",
           file=sys.stderr, flush=True)
 
+    preheat(torch, hptt)
     headline = measure_workload(torch, hptt, head, args.steps, args.warmup, args.reps, flush_buf,
                                 sink, full=not args.only_headline)
     print(f"[bench] {head.name}: {headline['gbs']:.0f} GB/s, {headline['pct_of_copy']:.1f}% "
@@ -404,6 +426,7 @@ def main():
         "copy_gbs": round(headline["copy_gbs"], 1),
         "hipmemcpy_d2d_gbs": round(headline["hipmemcpy_d2d_gbs"], 1),
         "buffer_sets": headline["buffer_sets"],
+        "kernel_us": headline["kernel_us"],
         "cold": headline.get("cold"),
         "plan": headline["plan"],
         "plan_create_us": headline["plan_create_us"],
