@@ -123,15 +123,16 @@ def time_cold(torch, hptt, fn, flush_buf, sink, reps: int):
 
 
 def preheat(torch, hptt, seconds: float = 0.3):
-    """Untimed streaming copies until the GPU has run for `seconds`: launch
+    """Untimed streaming fills until the GPU has run for `seconds`: launch
     times fall by about 10 % over the first few hundred milliseconds of work
-    as the clocks settle, which would otherwise bias the first workload."""
-    buf = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
-    half = buf.numel() // 2
+    as the clocks settle, which would otherwise bias the first workload.  (A
+    fill, not the copy kernel, so that profiles of the copy kernel contain
+    only the measured copies.)"""
+    buf = torch.empty(1 << 27, dtype=torch.float32, device="cuda")
     t0 = time.perf_counter()
     while time.perf_counter() - t0 < seconds:
         for _ in range(10):
-            hptt.yardstick_copy(buf[:half], buf[half:], half * 4)
+            hptt.yardstick_fill(buf, buf.numel() * 4, 0)
         torch.cuda.synchronize()
     del buf
     torch.cuda.empty_cache()

@@ -80,9 +80,13 @@ typedef struct {
     int32_t lds_pad;       /* TILE: LDS row padding in elements, 0 = default, -1 = none */
     int32_t max_blocks;    /* cap on the grid; workgroups loop over tiles beyond it */
     int32_t tile_order;    /* TILE: 1 = tiles in grid-digit order, 2 = diagonal
-                              (second grid digit rotated by the first) */
+                              (second grid digit rotated by the first), 3 =
+                              diagonal, with each XCD given a contiguous range
+                              of tiles */
     int32_t exact_runs;    /* TILE: 1 = chunk the runs to the target lengths even
                               where runs then do not start on 128-byte lines */
+    int32_t row_passes;    /* TILE: N > 1 = stage each tile through LDS in N passes
+                              over its rows (less LDS, one more barrier per pass) */
 } hptt_options_t;
 
 /* What the plan builder decided; for inspection and tests. */
@@ -100,6 +104,7 @@ typedef struct {
     int32_t vec_a;                     /* vector width of A accesses for 16-byte aligned bases */
     int32_t vec_b;                     /* vector width of B accesses */
     int32_t lds_pitch;                 /* TILE: LDS row pitch in elements */
+    int32_t rows_per_pass;             /* TILE: tile rows staged through LDS at once */
     int32_t lds_bytes;                 /* LDS per workgroup */
     int64_t tiles;                     /* TILE: tiles; STREAM, AXPBY: 16-byte vectors;
                                           GENERIC: elements */
@@ -108,7 +113,8 @@ typedef struct {
     int32_t hints;                     /* bit 0: non-temporal B stores; bit 1:
                                           non-temporal A loads */
     int32_t mode;                      /* 0 raw copy, 1 scale (beta = 0), 2 alpha*A + beta*B */
-    int32_t tile_order;                /* TILE: 1 grid-digit order, 2 diagonal */
+    int32_t tile_order;                /* TILE: 1 grid-digit order, 2 diagonal, 3 diagonal
+                                          with contiguous tile ranges per XCD */
 } hptt_plan_info_t;
 
 /*

@@ -12,6 +12,7 @@ namespace hptt {
 constexpr int kMaxDims = 16;  // = HPTT_MAX_DIMS
 constexpr int kBlock = 256;   // threads per workgroup: 4 waves of 64
 constexpr int kItems = 4;     // vectors per lane of the streaming kernels
+constexpr int kXcds = 8;      // MI355X: workgroups are dealt to 8 XCDs round robin
 
 // Unsigned division of n < 2^32 by a divisor 1 <= d < 2^32 fixed at plan
 // time, with one 32x32->64 multiply and a shift (Granlund and Montgomery,
@@ -64,7 +65,9 @@ struct TileArgs {
     int32_t gChunkC;     // grid digit that counts chunks of the last A-run index, or -1
     int32_t gChunkR;     // grid digit that counts chunks of the last B-run index, or -1
     int32_t skew;        // 1: grid digit 1 is shifted by digit 0 (diagonal tile order)
+    int32_t xcdSplit;    // 1: tile numbers dealt so that each XCD gets a contiguous range
     int32_t alignedA;    // 1 when every A run is whole 128-byte lines (set by the plan builder)
+    int32_t subRows;     // rows staged through LDS per pass (runB, or runB / passes)
     int64_t cInner, cChunk, cLast;  // valid columns = cInner * min(cChunk, cLast - j*cChunk)
     int64_t rInner, rChunk, rLast;  // valid rows    = rInner * min(rChunk, rLast - j*rChunk)
     FastDiv cExt[kMaxDims];         // tile extents of the A-run indices

@@ -50,7 +50,16 @@ struct TileBase {
 // of the tiles: workgroups that run at the same time then start their B runs
 // (and A runs) at many different offsets modulo a power-of-two stride instead
 // of one, which spreads their traffic over the HBM channels.
+//
+// With g.xcdSplit the workgroup number is first mapped so that the workgroups
+// one XCD receives (numbers x, x + 8, x + 16, ...) take a contiguous range of
+// tile numbers: tiles that share cache lines then share an L2.
 __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
+    if (g.xcdSplit) {
+        const uint32_t x = t % kXcds, i = t / kXcds;
+        const uint32_t q = g.numTiles / kXcds, r = g.numTiles % kXcds;
+        t = x * q + (x < r ? x : r) + i;
+    }
     TileBase tb;
     tb.a = 0;
     tb.b = 0;
@@ -108,24 +117,26 @@ __host__ __device__ inline void tile_tables(const TileArgs& g, int tid, int64_t*
 // 16 measured within noise of each other on MI355X; 8 was best on average).
 constexpr int kBatch = 8;
 
-// Load phase: the tile's rows are contiguous runs of A.  Thread tid takes the
-// vectors tid, tid + kBlock, ... of the (row, vector) space, vector fastest,
-// so a wave reads whole runs.  The vectors land in LDS at [row][column].
+// Load phase of the pass over tile rows [r0, r0 + subRows): the tile's rows
+// are contiguous runs of A.  Thread tid takes the vectors tid, tid + kBlock,
+// ... of the (row, vector) space, vector fastest, so a wave reads whole runs.
+// The vectors land in LDS at [row - r0][column].
 template <class Mem, typename T, int VA, int HINT>
-__host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb, int tid,
-                                          const T* A, T* lds, const int64_t* rowOffA) {
+__host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb, int64_t r0,
+                                          int tid, const T* A, T* lds, const int64_t* rowOffA) {
     const int64_t W = (g.runA + VA - 1) / VA;  // vectors per row
+    const int64_t rows = imin(int64_t(g.subRows), tb.validRows - r0);  // rows of this pass
     int64_t r = tid / W, c = tid % W;
     const int64_t dr = kBlock / W, dc = kBlock % W;
-    while (r < g.runB) {
+    while (r < g.subRows) {
         Vec<T, VA> v[kBatch];
         int64_t rr[kBatch], cc[kBatch];
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             rr[u] = r;
             cc[u] = c * VA;
-            if (r < tb.validRows && cc[u] < tb.validCols) {
-                const int64_t off = tb.a + Mem::template lds_ld<int64_t>(rowOffA, r) + cc[u];
+            if (r < rows && cc[u] < tb.validCols) {
+                const int64_t off = tb.a + Mem::template lds_ld<int64_t>(rowOffA, r0 + r) + cc[u];
                 if (cc[u] + VA <= tb.validCols) {
                     v[u] = Mem::template ld<T, VA, (HINT & kNtLoad) != 0>(A, off);
                 } else {
@@ -142,7 +153,7 @@ __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb,
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
-            if (rr[u] < tb.validRows && cc[u] < tb.validCols) {
+            if (rr[u] < rows && cc[u] < tb.validCols) {
                 const int64_t base = rr[u] * g.pitch + cc[u];
 #pragma unroll
                 for (int e = 0; e < VA; ++e)
@@ -152,15 +163,17 @@ __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb,
     }
 }
 
-// Store phase: the tile's columns are contiguous runs of B.  Thread tid takes
-// the vectors tid, tid + kBlock, ... of the (column, vector) space, vector
+// Store phase of the same pass: the tile's columns are contiguous runs of B,
+// of which this pass writes rows [r0, r0 + subRows).  Thread tid takes the
+// vectors tid, tid + kBlock, ... of the (column, vector) space, vector
 // fastest, gathers each vector's VB elements from consecutive LDS rows, and
 // writes it to B (reading B first when beta != 0).
 template <class Mem, typename T, int VB, int MODE, int HINT>
-__host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb, int tid, T* B,
-                                           const T* lds, const int64_t* colOffB, T alpha,
-                                           T beta) {
-    const int64_t W = (g.runB + VB - 1) / VB;  // vectors per column
+__host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb, int64_t r0,
+                                           int tid, T* B, const T* lds, const int64_t* colOffB,
+                                           T alpha, T beta) {
+    const int64_t W = (g.subRows + VB - 1) / VB;  // vectors per column in this pass
+    const int64_t rows = imin(int64_t(g.subRows), tb.validRows - r0);
     int64_t q = tid / W, s = tid % W;
     const int64_t dq = kBlock / W, ds = kBlock % W;
     while (q < g.runA) {
@@ -171,18 +184,18 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
             qq[u] = q;
             ss[u] = s * VB;
             off[u] = 0;
-            if (q < tb.validCols && ss[u] < tb.validRows) {
-                off[u] = tb.b + Mem::template lds_ld<int64_t>(colOffB, q) + ss[u];
+            if (q < tb.validCols && ss[u] < rows) {
+                off[u] = tb.b + Mem::template lds_ld<int64_t>(colOffB, q) + r0 + ss[u];
 #pragma unroll
                 for (int e = 0; e < VB; ++e)
-                    if (ss[u] + e < tb.validRows)
+                    if (ss[u] + e < rows)
                         x[u].v[e] = Mem::template lds_ld<T>(lds, (ss[u] + e) * g.pitch + q);
                 if (MODE == kAxpby) {
-                    if (ss[u] + VB <= tb.validRows) {
+                    if (ss[u] + VB <= rows) {
                         y[u] = Mem::template ld<T, VB, false>(B, off[u]);
                     } else {
                         for (int e = 0; e < VB; ++e)
-                            if (ss[u] + e < tb.validRows) y[u].v[e] = Mem::template ld1<T>(B, off[u] + e);
+                            if (ss[u] + e < rows) y[u].v[e] = Mem::template ld1<T>(B, off[u] + e);
                     }
                 }
             }
@@ -195,25 +208,27 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
-            if (qq[u] < tb.validCols && ss[u] < tb.validRows) {
+            if (qq[u] < tb.validCols && ss[u] < rows) {
                 Vec<T, VB> z;
 #pragma unroll
                 for (int e = 0; e < VB; ++e)
                     z.v[e] = update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
-                if (ss[u] + VB <= tb.validRows) {
+                if (ss[u] + VB <= rows) {
                     Mem::template st<(HINT & kNtStore) != 0, T, VB>(B, off[u], z);
                 } else {
                     for (int e = 0; e < VB; ++e)
-                        if (ss[u] + e < tb.validRows) Mem::template st1<(HINT & kNtStore) != 0, T>(B, off[u] + e, z.v[e]);
+                        if (ss[u] + e < rows)
+                            Mem::template st1<(HINT & kNtStore) != 0, T>(B, off[u] + e, z.v[e]);
                 }
             }
         }
     }
 }
 
-// LDS layout of kernel T: rowOffA[runB], colOffB[runA], then the tile.
+// LDS layout of kernel T: rowOffA[runB], colOffB[runA], then subRows rows of
+// the tile.  A tile with runB > subRows is staged in passes of subRows rows.
 __host__ __device__ inline int64_t tile_lds_bytes(const TileArgs& g, int elem) {
-    return (g.runA + g.runB) * int64_t(sizeof(int64_t)) + g.runB * g.pitch * int64_t(elem);
+    return (g.runA + g.runB) * int64_t(sizeof(int64_t)) + int64_t(g.subRows) * g.pitch * elem;
 }
 
 // ---------------------------------------------------------------------------

@@ -73,12 +73,16 @@ __global__ __launch_bounds__(kBlock) void tile_kernel(const T* __restrict__ A, T
     const int tid = int(threadIdx.x);
     tile_tables<DeviceMem>(g, tid, rowOffA, colOffB);
     __syncthreads();
+    bool first = true;
     for (uint32_t t = blockIdx.x; t < g.numTiles; t += gridDim.x) {
-        if (t != blockIdx.x) __syncthreads();  // the previous tile's LDS reads are done
         const TileBase tb = tile_base(g, t);
-        tile_load<DeviceMem, T, VA, HINT>(g, tb, tid, A, lds, rowOffA);
-        __syncthreads();
-        tile_store<DeviceMem, T, VB, MODE, HINT>(g, tb, tid, B, lds, colOffB, alpha, beta);
+        for (int64_t r0 = 0; r0 < tb.validRows; r0 += g.subRows) {
+            if (!first) __syncthreads();  // the previous pass's LDS reads are done
+            first = false;
+            tile_load<DeviceMem, T, VA, HINT>(g, tb, r0, tid, A, lds, rowOffA);
+            __syncthreads();
+            tile_store<DeviceMem, T, VB, MODE, HINT>(g, tb, r0, tid, B, lds, colOffB, alpha, beta);
+        }
     }
 }
 

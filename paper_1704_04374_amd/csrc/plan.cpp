@@ -12,7 +12,7 @@
 namespace hptt {
 
 int64_t tile_lds_bytes_host(const TileArgs& t, int elem) {
-    return (t.runA + t.runB) * int64_t(sizeof(int64_t)) + t.runB * int64_t(t.pitch) * elem;
+    return (t.runA + t.runB) * int64_t(sizeof(int64_t)) + int64_t(t.subRows) * t.pitch * elem;
 }
 
 namespace {
@@ -209,7 +209,8 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     }
     t.nG = g;
     t.skew = (g >= 2 && opt.tile_order != 1) ? 1 : 0;
-    info.tile_order = t.skew ? 2 : 1;
+    t.xcdSplit = opt.tile_order == 3 ? 1 : 0;
+    info.tile_order = t.xcdSplit ? 3 : t.skew ? 2 : 1;
     for (int j = 0; j < g; ++j) {
         if (ext[j] >= (int64_t(1) << 32)) return false;
         set_div(t.gExt[j], ext[j]);
@@ -223,8 +224,6 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     if (opt.lds_pad > 0) pad = opt.lds_pad;
     if (opt.lds_pad < 0) pad = 0;
     t.pitch = int32_t(t.runA + pad);
-    const int64_t lds = tile_lds_bytes_host(t, elem);
-    if (lds > ldsBudget) return false;
     // Vector widths: every A run must start on a multiple of vec_a elements,
     // every B run on a multiple of vec_b.
     int64_t granA = 0, granB = 0;
@@ -242,11 +241,24 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     // A runs that start and end on 128-byte lines share no line with another
     // tile, so they can be read with non-temporal loads.
     t.alignedA = (granA == 0 || (granA * elem) % kLine == 0) && (t.runA * elem) % kLine == 0;
+    // Rows staged through LDS per pass: the whole tile by default.  Staging a
+    // tile in several passes keeps its run lengths with less LDS, but each
+    // pass adds a barrier round trip; on MI355X that cost more than it saved
+    // (the 6-D workload: 96x160 in two passes 4.62 TB/s, 48x160 in one
+    // 4.80), so passes are only taken on request.
+    t.subRows = int32_t(t.runB);
+    if (opt.row_passes > 1) {
+        const int64_t want = (t.runB + opt.row_passes - 1) / opt.row_passes;
+        t.subRows = int32_t((want + info.vec_b - 1) / info.vec_b * info.vec_b);
+    }
+    const int64_t lds = tile_lds_bytes_host(t, elem);
+    if (lds > ldsBudget) return false;
     info.run_a = t.runA;
     info.run_b = t.runB;
     info.dims_a = nC;
     info.dims_b = nR;
     info.lds_pitch = t.pitch;
+    info.rows_per_pass = t.subRows;
     info.lds_bytes = int32_t(lds);
     info.tiles = t.numTiles;
     return true;
@@ -311,7 +323,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, d
         opt.kernel == HPTT_KERNEL_NONE || opt.run_a < 0 || opt.run_b < 0 || opt.max_vec < 0 ||
         opt.store_hint < 0 || opt.store_hint > 2 || opt.load_hint < 0 || opt.load_hint > 2 ||
         opt.lds_pad < -1 || opt.lds_pad > 64 || opt.max_blocks < 0 || opt.tile_order < 0 ||
-        opt.tile_order > 2 || opt.exact_runs < 0 || opt.exact_runs > 1)
+        opt.tile_order > 3 || opt.row_passes < 0 || opt.row_passes > 64 || opt.exact_runs < 0 || opt.exact_runs > 1)
         return HPTT_ERROR_INVALID_ARGUMENT;
 
     const int elem = dtype == HPTT_FLOAT32 ? 4 : 8;
@@ -479,11 +491,12 @@ void describe_plan(const hptt_plan_s* p, char* buf, size_t len) {
     }
     snprintf(buf, len,
              "kernel=%s dtype=%s mode=%s fused=(%s) perm=(%s) run_a=%lld run_b=%lld "
-             "dims_a=%d dims_b=%d vec=%d/%d pitch=%d lds=%d tiles=%lld grid=%lld block=%d hints=%d "
-             "order=%d",
+             "dims_a=%d dims_b=%d vec=%d/%d pitch=%d rows=%d lds=%d tiles=%lld grid=%lld block=%d "
+             "hints=%d order=%d",
              kKernel[in.kernel], p->dtype == HPTT_FLOAT32 ? "f32" : "f64", kMode[in.mode], shape,
              perm, (long long)in.run_a, (long long)in.run_b, in.dims_a, in.dims_b, in.vec_a,
-             in.vec_b, in.lds_pitch, in.lds_bytes, (long long)in.tiles, (long long)in.grid,
+             in.vec_b, in.lds_pitch, in.rows_per_pass, in.lds_bytes, (long long)in.tiles,
+             (long long)in.grid,
              in.block, in.hints, in.tile_order);
 }
 

@@ -40,7 +40,7 @@ class Options(ctypes.Structure):
                 ("max_vec", ctypes.c_int32), ("store_hint", ctypes.c_int32),
                 ("load_hint", ctypes.c_int32), ("lds_pad", ctypes.c_int32),
                 ("max_blocks", ctypes.c_int32), ("tile_order", ctypes.c_int32),
-                ("exact_runs", ctypes.c_int32)]
+                ("exact_runs", ctypes.c_int32), ("row_passes", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -51,7 +51,8 @@ class PlanInfo(ctypes.Structure):
                 ("run_a", ctypes.c_int64), ("run_b", ctypes.c_int64),
                 ("dims_a", ctypes.c_int32), ("dims_b", ctypes.c_int32),
                 ("vec_a", ctypes.c_int32), ("vec_b", ctypes.c_int32),
-                ("lds_pitch", ctypes.c_int32), ("lds_bytes", ctypes.c_int32),
+                ("lds_pitch", ctypes.c_int32), ("rows_per_pass", ctypes.c_int32),
+                ("lds_bytes", ctypes.c_int32),
                 ("tiles", ctypes.c_int64), ("grid", ctypes.c_int64), ("block", ctypes.c_int32),
                 ("hints", ctypes.c_int32), ("mode", ctypes.c_int32),
                 ("tile_order", ctypes.c_int32)]
@@ -62,7 +63,8 @@ class PlanInfo(ctypes.Structure):
                 "kernel": KERNELS[self.kernel], "numel": self.numel,
                 "elem_bytes": self.elem_bytes, "run_a": self.run_a, "run_b": self.run_b,
                 "dims_a": self.dims_a, "dims_b": self.dims_b, "vec_a": self.vec_a,
-                "vec_b": self.vec_b, "lds_pitch": self.lds_pitch, "lds_bytes": self.lds_bytes,
+                "vec_b": self.vec_b, "lds_pitch": self.lds_pitch,
+                "rows_per_pass": self.rows_per_pass, "lds_bytes": self.lds_bytes,
                 "tiles": self.tiles, "grid": self.grid, "block": self.block,
                 "hints": self.hints, "mode": MODES[self.mode],
                 "tile_order": self.tile_order}

@@ -133,12 +133,15 @@ void emu_tile(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
         clear_written(0, ldsBytes);
         for (int tid = 0; tid < kBlock; ++tid) tile_tables<HostMem>(g, tid, rowOffA, colOffB);
         for (int64_t t = blk; t < g.numTiles && S->errors == 0; t += grid) {
-            clear_written(tableBytes, ldsBytes);
             const TileBase tb = tile_base(g, uint32_t(t));
-            for (int tid = 0; tid < kBlock; ++tid)
-                tile_load<HostMem, T, VA, NT>(g, tb, tid, A, lds, rowOffA);
-            for (int tid = 0; tid < kBlock; ++tid)
-                tile_store<HostMem, T, VB, MODE, NT>(g, tb, tid, B, lds, colOffB, alpha, beta);
+            for (int64_t r0 = 0; r0 < tb.validRows && S->errors == 0; r0 += g.subRows) {
+                clear_written(tableBytes, ldsBytes);
+                for (int tid = 0; tid < kBlock; ++tid)
+                    tile_load<HostMem, T, VA, NT>(g, tb, r0, tid, A, lds, rowOffA);
+                for (int tid = 0; tid < kBlock; ++tid)
+                    tile_store<HostMem, T, VB, MODE, NT>(g, tb, r0, tid, B, lds, colOffB, alpha,
+                                                         beta);
+            }
         }
     }
 }

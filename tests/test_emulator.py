@@ -73,6 +73,13 @@ def test_random_problems_match_oracle():
     dict(store_hint=1),
     dict(load_hint=1, store_hint=1),
     dict(tile_order=1),
+    dict(tile_order=3),
+    dict(row_passes=2),
+    dict(row_passes=3, max_blocks=7),
+    dict(row_passes=5, run_a=8, run_b=40),
+    dict(row_passes=1),
+    dict(tile_order=3, max_blocks=16),
+    dict(tile_order=3, max_blocks=5),
     dict(run_a=64, run_b=64),
     dict(run_a=512, run_b=8),
     dict(exact_runs=1, run_a=6, run_b=10),
@@ -115,7 +122,9 @@ def test_small_workload_matches_oracle(w):
     _check(p, w.size_a, w.perm, w.alpha, w.beta, w.dtype, rng)
 
 
-@pytest.mark.parametrize("knobs", [dict(), dict(tile_order=1)], ids=["default", "digit_order"])
+@pytest.mark.parametrize("knobs", [dict(), dict(tile_order=1), dict(tile_order=3),
+                                   dict(row_passes=3)],
+                         ids=["default", "digit_order", "xcd_order", "three_passes"])
 @pytest.mark.parametrize("w", WORKLOADS, ids=lambda w: w.name)
 def test_full_size_geometry(w, knobs):
     """Dry run of every workgroup of each full-size workload: every offset in

@@ -101,7 +101,8 @@ def test_random_sweep():
 @pytest.mark.parametrize("knobs", [dict(kernel="generic"), dict(run_a=8, run_b=8),
                                    dict(run_a=3, run_b=5), dict(max_blocks=7),
                                    dict(max_vec=1), dict(store_hint=1, load_hint=1), dict(lds_pad=-1),
-                                   dict(tile_order=1), dict(run_a=512, run_b=8),
+                                   dict(tile_order=1), dict(tile_order=3), dict(run_a=512, run_b=8),
+                                   dict(row_passes=3), dict(row_passes=2, max_blocks=5),
                                    dict(run_a=64, run_b=64, max_blocks=5),
                                    dict(exact_runs=1, run_a=6, run_b=10)],
                          ids=lambda k: ",".join(f"{a}={b}" for a, b in k.items()))

@@ -89,7 +89,8 @@ EXPECTED = {
                                       run_b=32, tiles=16384, tile_order=2, hints=3),
     "transpose6d_24x20x16x24x18x20_f32": dict(kernel="tile", size=(24, 20, 16, 24, 18, 20),
                                               perm=(5, 2, 0, 4, 1, 3), run_a=48, run_b=160,
-                                              dims_a=2, dims_b=2, tiles=8640, hints=1),
+                                              dims_a=2, dims_b=2, tiles=8640, hints=1,
+                                              rows_per_pass=160),
     "transpose4d_96x96x96x96_keep1_f64": dict(kernel="stream", size=(96, 96, 96, 96),
                                               perm=(0, 3, 2, 1), run_b=96, vec_a=2, vec_b=2),
     "transpose5d_3x2x640x480x96_f32": dict(kernel="tile", size=(3, 2, 640, 480, 96),
@@ -111,6 +112,7 @@ def test_workload_plans(name):
         assert info["vec_a"] == info["vec_b"] == 16 // w.elem_bytes
         assert info["lds_bytes"] <= 40 * 1024          # at least 4 workgroups per CU
         assert (info["run_b"] * w.elem_bytes) % 128 == 0   # B runs of whole lines
+        assert (info["rows_per_pass"] * w.elem_bytes) % 128 == 0  # passes of whole lines
         # non-temporal A loads exactly when A runs are whole lines
         assert bool(info["hints"] & 2) == ((info["run_a"] * w.elem_bytes) % 128 == 0)
         assert info["hints"] & 1                        # non-temporal B stores
@@ -167,7 +169,8 @@ def test_null_arguments():
 
 @pytest.mark.parametrize("field,value", [("kernel", 9), ("kernel", 1), ("run_a", -1),
                                          ("store_hint", 3), ("load_hint", -1), ("lds_pad", 65),
-                                         ("max_blocks", -2), ("tile_order", 3), ("exact_runs", 2)])
+                                         ("max_blocks", -2), ("tile_order", 4), ("exact_runs", 2),
+                                         ("row_passes", -1), ("row_passes", 65)])
 def test_invalid_options(field, value):
     opt = hptt.Options()
     setattr(opt, field, value)
