@@ -29,6 +29,13 @@
  *    rounded once, then their sum is rounded once; no fused multiply-add.
  *    Build with -ffp-contract=off.
  *  - Any extent 0 makes the operation a no-op; extent-1 indices are allowed.
+ *  - Outer sizes (Section 3.1, Fig. 3): A and B may be sub-tensors of larger
+ *    enclosing tensors, like a BLAS leading dimension.  Their strides are the
+ *    Fortran strides of the enclosing extents outerSizeA (in A's index order)
+ *    and outerSizeB (in B's index order); the pointers address the
+ *    sub-tensors' first elements; elements of B outside the sub-tensor are
+ *    neither read nor written.  Each outer extent must be >= the extent it
+ *    encloses.  NULL outer sizes mean compact tensors.
  */
 #include <stddef.h>
 #include <stdint.h>
@@ -119,18 +126,35 @@ static double update_f64(double a, double b, double alpha, double beta)
     return scaled_a + scaled_b;
 }
 
-/* The whole transposition: visit every multi-index of A once, in Fortran
- * order, and update the B element it maps to.  Returns 0 on success. */
-int oracle_transpose_f32(int N, const int64_t *sizeA, const int32_t *perm,
-                         float alpha, float beta, const float *A, float *B)
+/* Check the outer extents and derive both tensors' strides. */
+static int outer_strides(int N, const int64_t *sizeA, const int32_t *perm,
+                         const int64_t *outerSizeA, const int64_t *outerSizeB,
+                         int64_t *strideA, int64_t *strideB)
 {
-    int64_t sizeB[ORACLE_MAX_DIMS], strideA[ORACLE_MAX_DIMS], strideB[ORACLE_MAX_DIMS];
-    int64_t i[ORACLE_MAX_DIMS] = {0};
+    int64_t sizeB[ORACLE_MAX_DIMS], outerA[ORACLE_MAX_DIMS], outerB[ORACLE_MAX_DIMS];
     int err = oracle_size_b(N, sizeA, perm, sizeB);
     if (err) return err;
+    for (int d = 0; d < N; ++d) {
+        outerA[d] = outerSizeA ? outerSizeA[d] : sizeA[d];
+        outerB[d] = outerSizeB ? outerSizeB[d] : sizeB[d];
+        if (outerA[d] < sizeA[d] || outerB[d] < sizeB[d]) return 5;
+    }
+    fortran_strides(N, outerA, strideA);
+    fortran_strides(N, outerB, strideB);
+    return 0;
+}
+
+/* The whole transposition: visit every multi-index of A once, in Fortran
+ * order, and update the B element it maps to.  Returns 0 on success. */
+int oracle_transpose_outer_f32(int N, const int64_t *sizeA, const int32_t *perm,
+                               const int64_t *outerSizeA, const int64_t *outerSizeB,
+                               float alpha, float beta, const float *A, float *B)
+{
+    int64_t strideA[ORACLE_MAX_DIMS], strideB[ORACLE_MAX_DIMS];
+    int64_t i[ORACLE_MAX_DIMS] = {0};
+    int err = outer_strides(N, sizeA, perm, outerSizeA, outerSizeB, strideA, strideB);
+    if (err) return err;
     if (numel_of(N, sizeA) == 0) return 0;
-    fortran_strides(N, sizeA, strideA);
-    fortran_strides(N, sizeB, strideB);
     do {
         int64_t offA, offB;
         offsets(N, i, perm, strideA, strideB, &offA, &offB);
@@ -139,22 +163,34 @@ int oracle_transpose_f32(int N, const int64_t *sizeA, const int32_t *perm,
     return 0;
 }
 
-int oracle_transpose_f64(int N, const int64_t *sizeA, const int32_t *perm,
-                         double alpha, double beta, const double *A, double *B)
+int oracle_transpose_outer_f64(int N, const int64_t *sizeA, const int32_t *perm,
+                               const int64_t *outerSizeA, const int64_t *outerSizeB,
+                               double alpha, double beta, const double *A, double *B)
 {
-    int64_t sizeB[ORACLE_MAX_DIMS], strideA[ORACLE_MAX_DIMS], strideB[ORACLE_MAX_DIMS];
+    int64_t strideA[ORACLE_MAX_DIMS], strideB[ORACLE_MAX_DIMS];
     int64_t i[ORACLE_MAX_DIMS] = {0};
-    int err = oracle_size_b(N, sizeA, perm, sizeB);
+    int err = outer_strides(N, sizeA, perm, outerSizeA, outerSizeB, strideA, strideB);
     if (err) return err;
     if (numel_of(N, sizeA) == 0) return 0;
-    fortran_strides(N, sizeA, strideA);
-    fortran_strides(N, sizeB, strideB);
     do {
         int64_t offA, offB;
         offsets(N, i, perm, strideA, strideB, &offA, &offB);
         B[offB] = update_f64(A[offA], beta == 0.0 ? 0.0 : B[offB], alpha, beta);
     } while (next_index(N, sizeA, i));
     return 0;
+}
+
+/* Compact tensors: outer sizes equal the sizes. */
+int oracle_transpose_f32(int N, const int64_t *sizeA, const int32_t *perm,
+                         float alpha, float beta, const float *A, float *B)
+{
+    return oracle_transpose_outer_f32(N, sizeA, perm, 0, 0, alpha, beta, A, B);
+}
+
+int oracle_transpose_f64(int N, const int64_t *sizeA, const int32_t *perm,
+                         double alpha, double beta, const double *A, double *B)
+{
+    return oracle_transpose_outer_f64(N, sizeA, perm, 0, 0, alpha, beta, A, B);
 }
 
 /* Expected B values at a list of B offsets, computed one by one: each B

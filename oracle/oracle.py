@@ -54,11 +54,16 @@ class OracleLib:
                                              ctypes.c_float, vp, vp]
         lib.oracle_transpose_f64.argtypes = [ctypes.c_int, i64p, i32p, ctypes.c_double,
                                              ctypes.c_double, vp, vp]
+        lib.oracle_transpose_outer_f32.argtypes = [ctypes.c_int, i64p, i32p, i64p, i64p,
+                                                   ctypes.c_float, ctypes.c_float, vp, vp]
+        lib.oracle_transpose_outer_f64.argtypes = [ctypes.c_int, i64p, i32p, i64p, i64p,
+                                                   ctypes.c_double, ctypes.c_double, vp, vp]
         lib.oracle_sample_f32.argtypes = [ctypes.c_int, i64p, i32p, ctypes.c_float,
                                           ctypes.c_float, vp, vp, ctypes.c_int64, i64p, vp]
         lib.oracle_sample_f64.argtypes = [ctypes.c_int, i64p, i32p, ctypes.c_double,
                                           ctypes.c_double, vp, vp, ctypes.c_int64, i64p, vp]
         for f in ("oracle_size_b", "oracle_transpose_f32", "oracle_transpose_f64",
+                  "oracle_transpose_outer_f32", "oracle_transpose_outer_f64",
                   "oracle_sample_f32", "oracle_sample_f64"):
             getattr(lib, f).restype = ctypes.c_int
         self.lib = lib
@@ -101,6 +106,43 @@ class OracleLib:
             raise ValueError(f"invalid problem (oracle error {err})")
         return out
 
+    def transpose_outer(self, A: np.ndarray, size_a, perm, outer_a, outer_b,
+                        alpha: float = 1.0, beta: float = 0.0,
+                        B: np.ndarray | None = None) -> np.ndarray:
+        """Eq. (1) on sub-tensors (Fig. 3).  ``A`` and ``B`` are flat arrays
+        whose first elements are the sub-tensors' first elements, with the
+        Fortran strides of the enclosing extents ``outer_a`` (A's index
+        order) and ``outer_b`` (B's index order); each must cover its
+        sub-tensor's footprint.  ``B`` (zeros if None) is not modified; a new
+        array is returned in which only the sub-tensor's elements changed."""
+        dtype = A.dtype
+        if dtype not in (np.float32, np.float64):
+            raise TypeError("oracle supports float32 and float64")
+        n, sz, pm = _problem(size_a, perm)
+        if len(outer_a) != n or len(outer_b) != n:
+            raise ValueError("outer sizes must have N entries")
+        size_b = [size_a[p] for p in perm]
+        if A.ndim != 1 or A.size < footprint(size_a, outer_a) or not A.flags.c_contiguous:
+            raise ValueError("A must be a flat contiguous array covering the sub-tensor")
+        if B is None:
+            out = np.zeros(footprint(size_b, outer_b), dtype=dtype)
+        else:
+            out = B.copy()
+        if out.ndim != 1 or out.size < footprint(size_b, outer_b) or out.dtype != dtype:
+            raise ValueError("B must be a flat array covering the sub-tensor")
+        oa = (ctypes.c_int64 * n)(*[int(x) for x in outer_a])
+        ob = (ctypes.c_int64 * n)(*[int(x) for x in outer_b])
+        if dtype == np.float32:
+            err = self.lib.oracle_transpose_outer_f32(n, sz, pm, oa, ob, float(np.float32(alpha)),
+                                                      float(np.float32(beta)), A.ctypes.data,
+                                                      out.ctypes.data)
+        else:
+            err = self.lib.oracle_transpose_outer_f64(n, sz, pm, oa, ob, float(alpha),
+                                                      float(beta), A.ctypes.data, out.ctypes.data)
+        if err:
+            raise ValueError(f"invalid problem (oracle error {err})")
+        return out
+
     def sample(self, A: np.ndarray, size_a, perm, alpha: float, beta: float,
                B_in: np.ndarray | None, offsets_b: np.ndarray) -> np.ndarray:
         """Expected B values at the given B offsets, computed one element at
@@ -126,6 +168,18 @@ class OracleLib:
         if err:
             raise ValueError(f"invalid problem or offset (oracle error {err})")
         return out
+
+
+def footprint(size, outer) -> int:
+    """Elements from a sub-tensor's first to its last element, inclusive,
+    in an enclosing Fortran-ordered tensor of extents ``outer``."""
+    if any(int(x) == 0 for x in size):
+        return 0
+    span, stride = 1, 1
+    for n, o in zip(size, outer):
+        span += (int(n) - 1) * stride
+        stride *= int(o)
+    return span
 
 
 def _numel(size_a) -> int:
@@ -173,3 +227,7 @@ def transpose(A, size_a, perm, alpha=1.0, beta=0.0, B=None):
 
 def sample(A, size_a, perm, alpha, beta, B_in, offsets_b):
     return default().sample(A, size_a, perm, alpha, beta, B_in, offsets_b)
+
+
+def transpose_outer(A, size_a, perm, outer_a, outer_b, alpha=1.0, beta=0.0, B=None):
+    return default().transpose_outer(A, size_a, perm, outer_a, outer_b, alpha, beta, B)

@@ -285,10 +285,78 @@ def pin_sample_matches_full(orc):
     assert np.array_equal(orc.sample(A, size_a, perm, 1.5, -0.5, B0, offs), full[offs])
 
 
+# --------------------------------------------------------------------------
+# Pins of sub-tensors with outer sizes (Section 3.1, Fig. 3)
+# --------------------------------------------------------------------------
+
+def _fortran_offset(index, outer):
+    off, stride = 0, 1
+    for i, o in zip(index, outer):
+        off += int(i) * stride
+        stride *= int(o)
+    return off
+
+
+def pin_fig3b_outer_sizes(orc):
+    """Fig. 3: the 8x16x16 sub-tensor of A (outer 16x32x32) transposed and
+    compacted into B (outer = size = 16x16x8), against numpy slicing."""
+    rows = {r[0]: r[1:] for r in golden("fig3b_input.txt")}
+    perm = tuple(int(x) for x in rows["perm"])
+    size_a = tuple(int(x) for x in rows["sizeA"])
+    outer_a = tuple(int(x) for x in rows["outerSizeA"])
+    outer_b = tuple(int(x) for x in rows["outerSizeB"])
+    A = np.arange(int(np.prod(outer_a)), dtype=np.float32)
+    B = orc.transpose_outer(A, size_a, perm, outer_a, outer_b)
+    sub = A.reshape(outer_a, order="F")[tuple(slice(0, n) for n in size_a)]
+    assert np.array_equal(B, np.transpose(sub, perm).ravel(order="F"))
+
+
+def pin_outer_sizes_numpy(orc):
+    """Random sub-tensors at random positions of larger tensors, compacted
+    and scattered: the sub-tensor of B equals numpy's transpose of the
+    sub-tensor of A, and every other element of B keeps its value."""
+    rng = np.random.default_rng(RNG_SEED + 9)
+    for it in range(40):
+        n = int(rng.integers(1, 5))
+        size_a = tuple(int(x) for x in rng.integers(1, 5, size=n))
+        perm = tuple(int(p) for p in rng.permutation(n))
+        size_b = tuple(size_a[p] for p in perm)
+        outer_a = tuple(s + int(rng.integers(0, 3)) for s in size_a)
+        outer_b = tuple(s + int(rng.integers(0, 3)) for s in size_b)
+        start_a = tuple(int(rng.integers(0, o - s + 1)) for s, o in zip(size_a, outer_a))
+        start_b = tuple(int(rng.integers(0, o - s + 1)) for s, o in zip(size_b, outer_b))
+        dtype = (np.float32, np.float64)[it % 2]
+        alpha, beta = ((1.0, 0.0), (1.5, -0.5), (-2.0, 0.25))[it % 3]
+        PA = _rand(rng, int(np.prod(outer_a)), dtype)
+        PB = _rand(rng, int(np.prod(outer_b)), dtype)
+        oa, ob = _fortran_offset(start_a, outer_a), _fortran_offset(start_b, outer_b)
+        got_tail = orc.transpose_outer(PA[oa:], size_a, perm, outer_a, outer_b, alpha, beta,
+                                       PB[ob:])
+        got = np.concatenate([PB[:ob], got_tail])
+        sl_a = tuple(slice(s, s + n) for s, n in zip(start_a, size_a))
+        sl_b = tuple(slice(s, s + n) for s, n in zip(start_b, size_b))
+        want = PB.reshape(outer_b, order="F").copy()
+        t = np.transpose(PA.reshape(outer_a, order="F")[sl_a], perm)
+        want[sl_b] = dtype(alpha) * t + dtype(beta) * want[sl_b] if beta != 0 else dtype(alpha) * t
+        assert np.array_equal(got, want.ravel(order="F")), (size_a, perm, outer_a, outer_b)
+
+
+def pin_outer_equal_to_size_is_compact(orc):
+    """Outer sizes equal to the sizes give the compact transposition."""
+    rng = np.random.default_rng(RNG_SEED + 10)
+    for size_a, perm in [((3, 4, 5), (2, 0, 1)), ((6, 7), (1, 0)), ((2, 3, 2, 5), (3, 1, 0, 2))]:
+        A = _rand(rng, int(np.prod(size_a)), np.float64)
+        B0 = _rand(rng, A.size, np.float64)
+        size_b = tuple(size_a[p] for p in perm)
+        assert np.array_equal(orc.transpose_outer(A, size_a, perm, size_a, size_b, 1.5, 0.5, B0),
+                              orc.transpose(A, size_a, perm, 1.5, 0.5, B0))
+
+
 PINS = [pin_fig1_strides, pin_fig3b_sizes, pin_fn4_fusion, pin_table1_notation,
         pin_numpy_transpose, pin_identity_is_axpby, pin_matrix_transpose, pin_brute_force,
         pin_two_roundings, pin_inverse_roundtrip, pin_hit_once,
-        pin_beta_zero_does_not_read_b, pin_alpha_zero_still_reads_a, pin_sample_matches_full]
+        pin_beta_zero_does_not_read_b, pin_alpha_zero_still_reads_a, pin_sample_matches_full,
+        pin_fig3b_outer_sizes, pin_outer_sizes_numpy, pin_outer_equal_to_size_is_compact]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
@@ -327,8 +395,12 @@ MUTANTS = {
     "perm_direction_inverted": [("b += i[perm[k]] * strideB[k];", "b += i[k] * strideB[perm[k]];")],
     "size_b_inverted": [("for (int k = 0; k < N; ++k) sizeB[k] = sizeA[perm[k]];",
                          "for (int k = 0; k < N; ++k) sizeB[perm[k]] = sizeA[k];")],
-    "b_strides_from_a_sizes": [("fortran_strides(N, sizeB, strideB);",
-                                "fortran_strides(N, sizeA, strideB);")],
+    "b_strides_from_a_sizes": [("fortran_strides(N, outerB, strideB);",
+                                "fortran_strides(N, outerA, strideB);")],
+    "outer_a_ignored": [("outerA[d] = outerSizeA ? outerSizeA[d] : sizeA[d];",
+                         "outerA[d] = sizeA[d];")],
+    "outer_b_in_a_order": [("outerB[d] = outerSizeB ? outerSizeB[d] : sizeB[d];",
+                            "outerB[d] = outerSizeB ? outerSizeB[perm[d]] : sizeB[d];")],
     "a_offset_uses_b_strides": [("for (int d = 0; d < N; ++d) a += i[d] * strideA[d];\n    for (int k",
                                  "for (int d = 0; d < N; ++d) a += i[d] * strideB[d];\n    for (int k")],
     "stride_off_by_one": [("stride[d] = stride[d - 1] * size[d - 1];",
