@@ -105,6 +105,8 @@ typedef struct {
     int32_t vec_b;                     /* vector width of B accesses */
     int32_t lds_pitch;                 /* TILE: LDS row pitch in elements */
     int32_t rows_per_pass;             /* TILE: tile rows staged through LDS at once */
+    int64_t footprint_a;               /* elements from A's first to its last element */
+    int64_t footprint_b;               /* the same for B (numel for compact tensors) */
     int32_t lds_bytes;                 /* LDS per workgroup */
     int64_t tiles;                     /* TILE: tiles; STREAM, AXPBY: 16-byte vectors;
                                           GENERIC: elements */
@@ -145,18 +147,42 @@ hptt_status_t hptt_create_plan_ex(hptt_plan_t *plan, const int32_t *perm, int32_
                                   hptt_dtype_t dtype, const hptt_options_t *options);
 
 /*
+ * As hptt_create_plan_ex, for sub-tensors (Section 3.1, Fig. 3): A and B are
+ * parts of larger enclosing tensors, like a BLAS leading dimension, which
+ * allows transposing-and-compacting and transposing-and-scattering.
+ *
+ *   outerSizeA  N extents of the tensor enclosing A, in A's index order, each
+ *               >= sizeA[d]; NULL means A is compact.
+ *   outerSizeB  N extents of the tensor enclosing B, in B's index order, each
+ *               >= sizeB[k] = sizeA[perm[k]]; NULL means B is compact.
+ * Strides are the Fortran strides of the enclosing extents.  hptt_exec then
+ * takes pointers to the sub-tensors' first elements; elements of the
+ * enclosing B outside the sub-tensor are neither read nor written.  Indices
+ * are merged into superindices only where they lie back to back in both
+ * tensors.  Errors as hptt_create_plan_ex; an outer extent below the extent
+ * it encloses is HPTT_ERROR_INVALID_ARGUMENT.
+ */
+hptt_status_t hptt_create_plan_outer(hptt_plan_t *plan, const int32_t *perm, int32_t N,
+                                     const int64_t *sizeA, const int64_t *outerSizeA,
+                                     const int64_t *outerSizeB, double alpha, double beta,
+                                     hptt_dtype_t dtype, const hptt_options_t *options);
+
+/*
  * Execute a plan (Fig. 3b's plan->exec()): queue the transposition of A into B
  * on `stream` and return without waiting.
  *
- *   A  device pointer to numel elements of dtype (read only).
- *   B  device pointer to numel elements of dtype; read only when beta != 0.
+ *   A  device pointer to numel elements of dtype (read only); for a sub-tensor
+ *      plan, to its first element, with footprint_a elements addressable.
+ *   B  device pointer to numel elements of dtype, read only when beta != 0;
+ *      for a sub-tensor plan, to its first element (footprint_b addressable).
  *   stream  HIP stream (0 = the null stream).
  * A and B must be aligned to the element size.  Pointers aligned to 16 bytes
  * get 16-byte vector accesses; others get narrower ones (still correct).
  * The plan is not modified, so one plan may execute concurrently on several
  * streams.  numel == 0 returns HPTT_SUCCESS without a launch.
  * Errors: HPTT_ERROR_INVALID_ARGUMENT (null plan; null or misaligned A or B),
- * HPTT_ERROR_OVERLAP (the byte ranges of A and B intersect), HPTT_ERROR_HIP
+ * HPTT_ERROR_OVERLAP (the byte ranges of A and B intersect; for sub-tensors
+ * the ranges from first to last element), HPTT_ERROR_HIP
  * (the launch failed; see hptt_last_hip_error).
  */
 hptt_status_t hptt_exec(hptt_plan_t plan, const void *A, void *B, hipStream_t stream);

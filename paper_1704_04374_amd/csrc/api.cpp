@@ -7,14 +7,16 @@
 
 extern "C" {
 
-hptt_status_t hptt_create_plan_ex(hptt_plan_t* plan, const int32_t* perm, int32_t N,
-                                  const int64_t* sizeA, double alpha, double beta,
-                                  hptt_dtype_t dtype, const hptt_options_t* options) {
+hptt_status_t hptt_create_plan_outer(hptt_plan_t* plan, const int32_t* perm, int32_t N,
+                                     const int64_t* sizeA, const int64_t* outerSizeA,
+                                     const int64_t* outerSizeB, double alpha, double beta,
+                                     hptt_dtype_t dtype, const hptt_options_t* options) {
     if (!plan) return HPTT_ERROR_INVALID_ARGUMENT;
     *plan = nullptr;
     hptt_plan_s* p = new (std::nothrow) hptt_plan_s;
     if (!p) return HPTT_ERROR_OUT_OF_MEMORY;
-    hptt_status_t st = hptt::build_plan(perm, N, sizeA, alpha, beta, dtype, options, p);
+    hptt_status_t st = hptt::build_plan(perm, N, sizeA, outerSizeA, outerSizeB, alpha, beta,
+                                        dtype, options, p);
     if (st != HPTT_SUCCESS) {
         delete p;
         return st;
@@ -23,10 +25,18 @@ hptt_status_t hptt_create_plan_ex(hptt_plan_t* plan, const int32_t* perm, int32_
     return HPTT_SUCCESS;
 }
 
+hptt_status_t hptt_create_plan_ex(hptt_plan_t* plan, const int32_t* perm, int32_t N,
+                                  const int64_t* sizeA, double alpha, double beta,
+                                  hptt_dtype_t dtype, const hptt_options_t* options) {
+    return hptt_create_plan_outer(plan, perm, N, sizeA, nullptr, nullptr, alpha, beta, dtype,
+                                  options);
+}
+
 hptt_status_t hptt_create_plan(hptt_plan_t* plan, const int32_t* perm, int32_t N,
                                const int64_t* sizeA, double alpha, double beta,
                                hptt_dtype_t dtype) {
-    return hptt_create_plan_ex(plan, perm, N, sizeA, alpha, beta, dtype, nullptr);
+    return hptt_create_plan_outer(plan, perm, N, sizeA, nullptr, nullptr, alpha, beta, dtype,
+                                  nullptr);
 }
 
 hptt_status_t hptt_destroy_plan(hptt_plan_t plan) {

@@ -93,6 +93,7 @@ struct StreamArgs {
     FastDiv W[3];               // vectors per row for V = 1, 2, 4
     FastDiv oExt[kMaxDims];     // extents of B positions 1.. (B order)
     int64_t oStrideA[kMaxDims]; // A strides of the indices at those positions
+    int64_t oStrideB[kMaxDims]; // B strides of those positions
 };
 
 constexpr int log2_width(int v) { return v >= 4 ? 2 : v >= 2 ? 1 : 0; }
@@ -105,6 +106,7 @@ struct GenericArgs {
     FastDiv bExt[kMaxDims];     // extents of B positions (used when numel < 2^32)
     int64_t bExt64[kMaxDims];   // the same extents as 64-bit values
     int64_t bStrideA[kMaxDims]; // A stride of the index at each B position
+    int64_t bStrideB[kMaxDims]; // B stride of each B position
 };
 
 }  // namespace hptt

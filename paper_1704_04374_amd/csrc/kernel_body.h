@@ -255,14 +255,16 @@ __host__ __device__ inline void stream_items(const StreamArgs& g, uint32_t first
         if (ok[u]) {
             uint32_t r = fast_div(uint32_t(item), W);
             col[u] = int64_t(uint32_t(item) - r * W.d) * V;
-            offB[u] = int64_t(r) * g.rowLen + col[u];
-            int64_t a = 0;
+            int64_t a = 0, b = 0;
             for (int k = 0; k < g.nO; ++k) {
                 uint32_t q = fast_div(r, g.oExt[k]);
-                a += int64_t(r - q * g.oExt[k].d) * g.oStrideA[k];
+                const int64_t j = int64_t(r - q * g.oExt[k].d);
+                a += j * g.oStrideA[k];
+                b += j * g.oStrideB[k];
                 r = q;
             }
             offA[u] = a + col[u];
+            offB[u] = b + col[u];
             if (col[u] + V <= g.rowLen) {
                 x[u] = Mem::template ld<T, V, (HINT & kNtLoad) != 0>(A, offA[u]);
                 if (MODE == kAxpby) y[u] = Mem::template ld<T, V, false>(B, offB[u]);
@@ -332,26 +334,33 @@ __host__ __device__ inline void axpby_items(int64_t numel, int64_t first, int ti
 // Fallback: one B element per thread, any shape
 // ---------------------------------------------------------------------------
 
+// Element e (in B order) is split into B's multi-index; its offsets in A and
+// B follow from both tensors' strides.
 template <class Mem, typename T, int MODE, int HINT, bool BIG>
 __host__ __device__ inline void generic_elem(const GenericArgs& g, int64_t e, const T* A, T* B,
                                              T alpha, T beta) {
-    int64_t offA = 0;
+    int64_t offA = 0, offB = 0;
     if (BIG) {
         int64_t x = e;
         for (int k = 0; k < g.n; ++k) {
-            offA += (x % g.bExt64[k]) * g.bStrideA[k];
+            const int64_t j = x % g.bExt64[k];
+            offA += j * g.bStrideA[k];
+            offB += j * g.bStrideB[k];
             x /= g.bExt64[k];
         }
     } else {
         uint32_t x = uint32_t(e);
         for (int k = 0; k < g.n; ++k) {
             uint32_t q = fast_div(x, g.bExt[k]);
-            offA += int64_t(x - q * g.bExt[k].d) * g.bStrideA[k];
+            const int64_t j = int64_t(x - q * g.bExt[k].d);
+            offA += j * g.bStrideA[k];
+            offB += j * g.bStrideB[k];
             x = q;
         }
     }
-    T b = MODE == kAxpby ? Mem::template ld1<T>(B, e) : T(0);
-    Mem::template st1<(HINT & kNtStore) != 0, T>(B, e, update<MODE>(Mem::template ld1<T>(A, offA), b, alpha, beta));
+    T b = MODE == kAxpby ? Mem::template ld1<T>(B, offB) : T(0);
+    Mem::template st1<(HINT & kNtStore) != 0, T>(
+        B, offB, update<MODE>(Mem::template ld1<T>(A, offA), b, alpha, beta));
 }
 
 }  // namespace hptt

@@ -266,8 +266,9 @@ hptt_status_t hptt_exec(hptt_plan_t plan, const void* A, void* B, hipStream_t st
     const uintptr_t a = reinterpret_cast<uintptr_t>(A), b = reinterpret_cast<uintptr_t>(B);
     const uintptr_t elem = uintptr_t(in.elem_bytes);
     if (a % elem != 0 || b % elem != 0) return HPTT_ERROR_INVALID_ARGUMENT;
-    const uintptr_t bytes = uintptr_t(in.numel) * elem;
-    if (a < b + bytes && b < a + bytes) return HPTT_ERROR_OVERLAP;
+    const uintptr_t bytesA = uintptr_t(in.footprint_a) * elem;
+    const uintptr_t bytesB = uintptr_t(in.footprint_b) * elem;
+    if (a < b + bytesB && b < a + bytesA) return HPTT_ERROR_OVERLAP;
     if (plan->dtype == HPTT_FLOAT32) return hptt::launch<float>(plan, A, B, stream);
     return hptt::launch<double>(plan, A, B, stream);
 }

@@ -43,7 +43,7 @@ int32_t vec_width(int64_t gran, int elem, int32_t cap) {
 }
 
 // The fused problem: M indices of A with extents n, B position k holding
-// fused A index p[k], and the compact strides of every A index in A and B.
+// fused A index p[k], and the strides of every A index in A and in B.
 struct Fused {
     int M;
     int64_t n[kMaxDims];
@@ -53,65 +53,93 @@ struct Fused {
 };
 
 // Drop extent-1 indices, then merge maximal groups of B positions whose A
-// indices are consecutive and increasing: such a group is contiguous in both
-// tensors and behaves as one index (Section 3.1, footnote 4).
-void fuse(const int32_t* perm, int32_t N, const int64_t* sizeA, Fused& f) {
+// indices are consecutive and increasing and lie back to back in memory in
+// both tensors (each stride equals the previous stride times the previous
+// extent): such a group behaves as one index (Section 3.1, footnote 4).
+// Strides are the Fortran strides of the enclosing extents (the outer sizes
+// of Fig. 3); compact tensors have outer sizes equal to their sizes, and then
+// every group of consecutive indices qualifies.
+void fuse(const int32_t* perm, int32_t N, const int64_t* sizeA, const int64_t* outerA,
+          const int64_t* outerB, Fused& f) {
+    int64_t strideA[kMaxDims], strideB[kMaxDims];  // per original A index
+    int64_t s = 1;
+    for (int d = 0; d < N; ++d) {
+        strideA[d] = s;
+        s *= outerA[d];
+    }
+    s = 1;
+    for (int k = 0; k < N; ++k) {
+        strideB[perm[k]] = s;
+        s *= outerB[k];
+    }
     int32_t newIdx[kMaxDims];
     int kept = 0;
     for (int d = 0; d < N; ++d) newIdx[d] = sizeA[d] > 1 ? kept++ : -1;
-    int64_t n[kMaxDims];
+    int64_t n[kMaxDims], sA[kMaxDims], sB[kMaxDims];
     int32_t p[kMaxDims];
     int m = 0;
     for (int d = 0; d < N; ++d)
-        if (sizeA[d] > 1) n[newIdx[d]] = sizeA[d];
+        if (newIdx[d] >= 0) {
+            n[newIdx[d]] = sizeA[d];
+            sA[newIdx[d]] = strideA[d];
+            sB[newIdx[d]] = strideB[d];
+        }
     for (int k = 0; k < N; ++k)
         if (newIdx[perm[k]] >= 0) p[m++] = newIdx[perm[k]];
-    if (m == 0) {  // every extent is 1
+    if (m == 0) {  // every extent is 1: one element
         f.M = 1;
         f.n[0] = 1;
         f.p[0] = 0;
-    } else {
-        // groups in B order: first A index and extent
-        int32_t first[kMaxDims];
-        int64_t ext[kMaxDims];
-        int G = 0;
-        for (int k = 0; k < m; ++k) {
-            if (k > 0 && p[k] == p[k - 1] + 1) {
-                ext[G - 1] *= n[p[k]];
-            } else {
-                first[G] = p[k];
-                ext[G] = n[p[k]];
-                ++G;
-            }
+        f.sA[0] = f.sB[0] = 1;
+        return;
+    }
+    // groups in B order: first A index and extent
+    int32_t first[kMaxDims];
+    int64_t ext[kMaxDims];
+    int G = 0;
+    for (int k = 0; k < m; ++k) {
+        const int32_t a = p[k], prev = k > 0 ? p[k - 1] : -1;
+        const bool join = k > 0 && a == prev + 1 && sA[a] == sA[prev] * n[prev] &&
+                          sB[a] == sB[prev] * n[prev];
+        if (join) {
+            ext[G - 1] *= n[a];
+        } else {
+            first[G] = a;
+            ext[G] = n[a];
+            ++G;
         }
-        // fused A index of a group = rank of its first A index
-        for (int g = 0; g < G; ++g) {
-            int rank = 0;
-            for (int h = 0; h < G; ++h) rank += first[h] < first[g];
-            f.p[g] = rank;
-            f.n[rank] = ext[g];
-        }
-        f.M = G;
     }
-    int64_t s = 1;
-    for (int d = 0; d < f.M; ++d) {
-        f.sA[d] = s;
-        s *= f.n[d];
+    // fused A index of a group = rank of its first A index
+    for (int g = 0; g < G; ++g) {
+        int rank = 0;
+        for (int h = 0; h < G; ++h) rank += first[h] < first[g];
+        f.p[g] = rank;
+        f.n[rank] = ext[g];
+        f.sA[rank] = sA[first[g]];
+        f.sB[rank] = sB[first[g]];
     }
-    s = 1;
-    for (int k = 0; k < f.M; ++k) {
-        f.sB[f.p[k]] = s;
-        s *= f.n[f.p[k]];
-    }
+    f.M = G;
 }
 
-// Chunk of an index of extent n that extends a run whose inner part has
-// `inner` elements, aiming at a run of `target` elements.  With `aligned`,
-// only chunks whose runs start and end on 128-byte lines qualify (no line is
-// then shared between workgroups); returns 0 if there is none.  Among the
-// candidates: no partial edge tile first, then the length closest to target,
-// where falling short counts double.
-int64_t choose_chunk(int64_t inner, int64_t n, int64_t target, int elem, bool aligned) {
+// gcd of the strides (in one tensor) of the fused A indices in `which` that
+// have extent > 1; 0 if there are none.
+int64_t stride_gcd(const Fused& f, const int64_t* stride, const bool* which) {
+    int64_t g = 0;
+    for (int d = 0; d < f.M; ++d)
+        if (which[d] && f.n[d] > 1) g = gcd64(g, stride[d]);
+    return g;
+}
+
+// Chunk of an index of extent n that extends a contiguous run whose inner
+// part has `inner` elements, aiming at a run of `target` elements.  Runs then
+// start at multiples of gcd(chunk stride, `other`), where `other` is the gcd
+// of the strides of every index outside the run.  With `aligned`, only chunks
+// whose runs start and end on 128-byte lines qualify (no line is then shared
+// between workgroups); returns 0 if there is none.  Among the candidates: no
+// partial edge tile first, then the length closest to target, where falling
+// short counts double.
+int64_t choose_chunk(int64_t inner, int64_t n, int64_t other, int64_t target, int elem,
+                     bool aligned) {
     int64_t best = 0;
     double bestScore = 1e30;
     // Line-aligned chunks are multiples of `step` and may be long, up to
@@ -121,7 +149,7 @@ int64_t choose_chunk(int64_t inner, int64_t n, int64_t target, int elem, bool al
     const int64_t kmax = aligned ? kLdsMax / (inner * elem) : (4 * target) / inner;
     for (int64_t k = step; k <= n && (k == 1 || k <= kmax); k += step) {
         const int64_t run = inner * k;
-        const int64_t gran = inner * gcd64(k, n);
+        const int64_t gran = gcd64(k < n ? run : 0, other);
         const bool lineAligned = (gran * elem) % kLine == 0 && (run * elem) % kLine == 0;
         if (aligned && !lineAligned) continue;
         // a run shorter than the target costs twice as much as a longer one
@@ -145,12 +173,20 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     memset(&t, 0, sizeof(t));
     const int M = f.M;
     const int p0 = f.p[0];  // A index that is B's stride-1 index (never 0 here)
-    // A run: A indices 0, 1, ... (never reaching p0), the last possibly chunked.
+    // Both runs need a stride-1 index (a sub-tensor whose first extent is 1
+    // may have none once that index is dropped).
+    if (f.sA[0] != 1 || f.sB[p0] != 1) return false;
+    bool outside[kMaxDims];
+    // A run: A indices 0, 1, ... (never reaching p0) while they lie back to
+    // back in A, the last possibly chunked.
     int64_t inner = 1;
     int d = 0;
-    while (d < p0 - 1 && inner * f.n[d] <= tA) inner *= f.n[d++];
+    while (d < p0 - 1 && inner * f.n[d] <= tA && f.sA[d + 1] == f.sA[d] * f.n[d])
+        inner *= f.n[d++];
+    for (int j = 0; j < M; ++j) outside[j] = j > d;
     int64_t cChunk = f.n[d];
-    if (inner * f.n[d] > tA) cChunk = choose_chunk(inner, f.n[d], tA, elem, alignA);
+    if (inner * f.n[d] > tA)
+        cChunk = choose_chunk(inner, f.n[d], stride_gcd(f, f.sA, outside), tA, elem, alignA);
     if (cChunk == 0) return false;
     const int nC = d + 1;
     t.nC = nC;
@@ -161,12 +197,18 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
         set_div(t.cExt[k], k == nC - 1 ? cChunk : f.n[k]);
         t.cStrideB[k] = f.sB[k];
     }
-    // B run: B positions 0, 1, ... up to (not into) an index of the A run.
+    // B run: B positions 0, 1, ... up to (not into) an index of the A run,
+    // while they lie back to back in B.
     inner = 1;
     int k = 0;
-    while (k + 1 < M && f.p[k + 1] >= nC && inner * f.n[f.p[k]] <= tB) inner *= f.n[f.p[k++]];
+    while (k + 1 < M && f.p[k + 1] >= nC && inner * f.n[f.p[k]] <= tB &&
+           f.sB[f.p[k + 1]] == f.sB[f.p[k]] * f.n[f.p[k]])
+        inner *= f.n[f.p[k++]];
+    for (int j = 0; j < M; ++j) outside[j] = true;
+    for (int j = 0; j <= k; ++j) outside[f.p[j]] = false;
     int64_t rChunk = f.n[f.p[k]];
-    if (inner * rChunk > tB) rChunk = choose_chunk(inner, f.n[f.p[k]], tB, elem, alignB);
+    if (inner * rChunk > tB)
+        rChunk = choose_chunk(inner, f.n[f.p[k]], stride_gcd(f, f.sB, outside), tB, elem, alignB);
     if (rChunk == 0) return false;
     const int nR = k + 1;
     t.nR = nR;
@@ -267,16 +309,20 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
 bool setup_stream(const Fused& f, int elem, const hptt_options_t& opt, StreamArgs& s,
                   hptt_plan_info_t& info) {
     memset(&s, 0, sizeof(s));
+    if (f.sA[0] != 1 || f.sB[0] != 1) return false;
     s.rowLen = f.n[0];
     int64_t rows = 1;
     for (int d = 1; d < f.M; ++d) rows *= f.n[d];
     s.numRows = rows;
     s.nO = f.M - 1;
+    int64_t gran = s.rowLen;  // every row starts on a multiple of gran in both tensors
     for (int k = 1; k < f.M; ++k) {
         set_div(s.oExt[k - 1], f.n[f.p[k]]);
         s.oStrideA[k - 1] = f.sA[f.p[k]];
+        s.oStrideB[k - 1] = f.sB[f.p[k]];
+        gran = gcd64(gran, gcd64(s.oStrideA[k - 1], s.oStrideB[k - 1]));
     }
-    const int32_t v = vec_width(s.rowLen, elem, opt.max_vec);
+    const int32_t v = vec_width(gran, elem, opt.max_vec);
     for (int w = 0; w < 3; ++w) {  // every width hptt_exec may launch with
         const int64_t W = (s.rowLen + (1 << w) - 1) >> w;
         const int64_t items = rows * W;
@@ -299,12 +345,21 @@ void setup_generic(const Fused& f, int64_t numel, GenericArgs& g) {
         g.bExt64[k] = e;
         if (e < (int64_t(1) << 32)) set_div(g.bExt[k], e);
         g.bStrideA[k] = f.sA[f.p[k]];
+        g.bStrideB[k] = f.sB[f.p[k]];
     }
+}
+
+// Elements from a tensor's first to its last element, inclusive.
+int64_t footprint(const Fused& f, const int64_t* stride) {
+    int64_t span = 1;
+    for (int d = 0; d < f.M; ++d) span += (f.n[d] - 1) * stride[d];
+    return span;
 }
 
 }  // namespace
 
-hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, double alpha,
+hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
+                         const int64_t* outerSizeA, const int64_t* outerSizeB, double alpha,
                          double beta, hptt_dtype_t dtype, const hptt_options_t* options,
                          hptt_plan_s* plan) {
     if (!perm || !sizeA || !plan) return HPTT_ERROR_INVALID_ARGUMENT;
@@ -316,6 +371,19 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, d
         seen[perm[k]] = true;
         if (sizeA[k] < 0) return HPTT_ERROR_INVALID_ARGUMENT;
     }
+    // Enclosing extents (Fig. 3's outer sizes): each at least the extent it
+    // encloses; NULL means compact.
+    int64_t outerA[kMaxDims], outerB[kMaxDims];
+    int64_t spanA = 1, spanB = 1;
+    for (int k = 0; k < N; ++k) {
+        outerA[k] = outerSizeA ? outerSizeA[k] : sizeA[k];
+        outerB[k] = outerSizeB ? outerSizeB[k] : sizeA[perm[k]];
+        if (outerA[k] < sizeA[k] || outerB[k] < sizeA[perm[k]]) return HPTT_ERROR_INVALID_ARGUMENT;
+        if (outerA[k] > 0 && spanA > (int64_t(1) << 60) / outerA[k]) return HPTT_ERROR_INVALID_ARGUMENT;
+        if (outerB[k] > 0 && spanB > (int64_t(1) << 60) / outerB[k]) return HPTT_ERROR_INVALID_ARGUMENT;
+        spanA *= outerA[k] > 0 ? outerA[k] : 1;
+        spanB *= outerB[k] > 0 ? outerB[k] : 1;
+    }
     hptt_options_t opt;
     memset(&opt, 0, sizeof(opt));
     if (options) opt = *options;
@@ -323,7 +391,8 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, d
         opt.kernel == HPTT_KERNEL_NONE || opt.run_a < 0 || opt.run_b < 0 || opt.max_vec < 0 ||
         opt.store_hint < 0 || opt.store_hint > 2 || opt.load_hint < 0 || opt.load_hint > 2 ||
         opt.lds_pad < -1 || opt.lds_pad > 64 || opt.max_blocks < 0 || opt.tile_order < 0 ||
-        opt.tile_order > 3 || opt.row_passes < 0 || opt.row_passes > 64 || opt.exact_runs < 0 || opt.exact_runs > 1)
+        opt.tile_order > 3 || opt.row_passes < 0 || opt.row_passes > 64 || opt.exact_runs < 0 ||
+        opt.exact_runs > 1)
         return HPTT_ERROR_INVALID_ARGUMENT;
 
     const int elem = dtype == HPTT_FLOAT32 ? 4 : 8;
@@ -355,7 +424,9 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, d
             f.p[d] = perm[d];
         }
     } else {
-        fuse(perm, N, sizeA, f);
+        fuse(perm, N, sizeA, outerA, outerB, f);
+        info.footprint_a = footprint(f, f.sA);
+        info.footprint_b = footprint(f, f.sB);
     }
     info.ndim = f.M;
     for (int d = 0; d < f.M; ++d) {
@@ -367,14 +438,19 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, d
         return HPTT_SUCCESS;
     }
 
-    const bool identity = f.M == 1;
-    const bool kept = f.p[0] == 0;
+    // Classes: one fused index -> flat axpby (only when that index has stride
+    // 1 in both tensors: a sub-tensor whose first extent is 1 can leave a
+    // strided one); A's stride-1 index also B's -> stream; otherwise tiles.
+    // Anything a class cannot serve goes to the generic kernel.
+    const bool single = f.M == 1;
+    const bool unit = f.sA[0] == 1 && f.sB[0] == 1;
+    const bool kept = !single && f.p[0] == 0;
     hptt_kernel_t k = opt.kernel;
-    if (k == HPTT_KERNEL_AXPBY && !identity) return HPTT_ERROR_UNSUPPORTED;
-    if (k == HPTT_KERNEL_STREAM && (!kept || identity)) return HPTT_ERROR_UNSUPPORTED;
-    if (k == HPTT_KERNEL_TILE && kept) return HPTT_ERROR_UNSUPPORTED;
+    if (k == HPTT_KERNEL_AXPBY && !(single && unit)) return HPTT_ERROR_UNSUPPORTED;
+    if (k == HPTT_KERNEL_STREAM && !kept) return HPTT_ERROR_UNSUPPORTED;
+    if (k == HPTT_KERNEL_TILE && (single || kept)) return HPTT_ERROR_UNSUPPORTED;
     if (k == HPTT_KERNEL_AUTO) {
-        if (identity) k = HPTT_KERNEL_AXPBY;
+        if (single) k = unit ? HPTT_KERNEL_AXPBY : HPTT_KERNEL_GENERIC;
         else if (kept) k = f.n[0] * elem >= 64 ? HPTT_KERNEL_STREAM : HPTT_KERNEL_GENERIC;
         else k = HPTT_KERNEL_TILE;
     }

@@ -17,7 +17,9 @@ struct hptt_plan_s {
 namespace hptt {
 
 // Fill *plan for Eq. (1); no HIP call.  options may be NULL.
-hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA, double alpha,
+// outerSizeA / outerSizeB may be NULL (compact tensors).
+hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
+                         const int64_t* outerSizeA, const int64_t* outerSizeB, double alpha,
                          double beta, hptt_dtype_t dtype, const hptt_options_t* options,
                          hptt_plan_s* plan);
 

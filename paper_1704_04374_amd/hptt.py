@@ -52,6 +52,7 @@ class PlanInfo(ctypes.Structure):
                 ("dims_a", ctypes.c_int32), ("dims_b", ctypes.c_int32),
                 ("vec_a", ctypes.c_int32), ("vec_b", ctypes.c_int32),
                 ("lds_pitch", ctypes.c_int32), ("rows_per_pass", ctypes.c_int32),
+                ("footprint_a", ctypes.c_int64), ("footprint_b", ctypes.c_int64),
                 ("lds_bytes", ctypes.c_int32),
                 ("tiles", ctypes.c_int64), ("grid", ctypes.c_int64), ("block", ctypes.c_int32),
                 ("hints", ctypes.c_int32), ("mode", ctypes.c_int32),
@@ -64,14 +65,16 @@ class PlanInfo(ctypes.Structure):
                 "elem_bytes": self.elem_bytes, "run_a": self.run_a, "run_b": self.run_b,
                 "dims_a": self.dims_a, "dims_b": self.dims_b, "vec_a": self.vec_a,
                 "vec_b": self.vec_b, "lds_pitch": self.lds_pitch,
-                "rows_per_pass": self.rows_per_pass, "lds_bytes": self.lds_bytes,
+                "rows_per_pass": self.rows_per_pass, "footprint_a": self.footprint_a,
+                "footprint_b": self.footprint_b, "lds_bytes": self.lds_bytes,
                 "tiles": self.tiles, "grid": self.grid, "block": self.block,
                 "hints": self.hints, "mode": MODES[self.mode],
                 "tile_order": self.tile_order}
 
 
 # Every entry point declared in include/hptt.h and include/hptt_yardstick.h.
-EXPORTS = ("hptt_create_plan", "hptt_create_plan_ex", "hptt_exec", "hptt_destroy_plan",
+EXPORTS = ("hptt_create_plan", "hptt_create_plan_ex", "hptt_create_plan_outer", "hptt_exec",
+           "hptt_destroy_plan",
            "hptt_plan_info", "hptt_describe_plan", "hptt_status_string",
            "hptt_last_hip_error", "hptt_yardstick_copy", "hptt_yardstick_axpby",
            "hptt_yardstick_fill", "hptt_yardstick_read")
@@ -85,13 +88,16 @@ def _declare(lib: ctypes.CDLL, gpu: bool) -> ctypes.CDLL:
     lib.hptt_create_plan.argtypes = [ctypes.POINTER(vp), i32p, ctypes.c_int32, i64p,
                                      ctypes.c_double, ctypes.c_double, ctypes.c_int]
     lib.hptt_create_plan_ex.argtypes = lib.hptt_create_plan.argtypes + [ctypes.POINTER(Options)]
+    lib.hptt_create_plan_outer.argtypes = [ctypes.POINTER(vp), i32p, ctypes.c_int32, i64p, i64p,
+                                           i64p, ctypes.c_double, ctypes.c_double, ctypes.c_int,
+                                           ctypes.POINTER(Options)]
     lib.hptt_destroy_plan.argtypes = [vp]
     lib.hptt_plan_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]
     lib.hptt_describe_plan.argtypes = [vp, ctypes.c_char_p, ctypes.c_size_t]
     lib.hptt_status_string.argtypes = [ctypes.c_int]
     lib.hptt_status_string.restype = ctypes.c_char_p
-    for f in ("hptt_create_plan", "hptt_create_plan_ex", "hptt_destroy_plan", "hptt_plan_info",
-              "hptt_describe_plan"):
+    for f in ("hptt_create_plan", "hptt_create_plan_ex", "hptt_create_plan_outer",
+              "hptt_destroy_plan", "hptt_plan_info", "hptt_describe_plan"):
         getattr(lib, f).restype = st
     if gpu:
         lib.hptt_exec.argtypes = [vp, vp, vp, vp]
@@ -144,10 +150,13 @@ def _check(status: int, what: str):
 
 class Plan:
     """A plan for Eq. (1): perm[k] is the A index at position k of B (0-based),
-    tensors are compact and Fortran-ordered (first index fastest)."""
+    tensors are Fortran-ordered (first index fastest).  With ``outer_size_a``
+    (A's index order) and/or ``outer_size_b`` (B's index order) A and B are
+    sub-tensors of larger tensors of those extents (Fig. 3)."""
 
     def __init__(self, perm, size_a, alpha: float = 1.0, beta: float = 0.0, dtype="f32",
-                 options: Options | None = None, lib: ctypes.CDLL | None = None, **knobs):
+                 options: Options | None = None, lib: ctypes.CDLL | None = None,
+                 outer_size_a=None, outer_size_b=None, **knobs):
         self._lib = lib if lib is not None else library()
         self._handle = None
         n = len(perm)
@@ -164,7 +173,18 @@ class Plan:
             options = options or Options()
             for k, v in knobs.items():
                 setattr(options, k, KERNEL_IDS[v] if k == "kernel" and isinstance(v, str) else v)
-        if options is None:
+        self.outer_size_a = None if outer_size_a is None else tuple(int(x) for x in outer_size_a)
+        self.outer_size_b = None if outer_size_b is None else tuple(int(x) for x in outer_size_b)
+        if self.outer_size_a is not None or self.outer_size_b is not None:
+            oa = None if self.outer_size_a is None else (ctypes.c_int64 * n)(*self.outer_size_a)
+            ob = None if self.outer_size_b is None else (ctypes.c_int64 * n)(*self.outer_size_b)
+            for o in (self.outer_size_a, self.outer_size_b):
+                if o is not None and len(o) != n:
+                    raise ValueError("outer sizes need one extent per index")
+            st = self._lib.hptt_create_plan_outer(ctypes.byref(handle), pm, n, sz, oa, ob,
+                                                  self.alpha, self.beta, DTYPES[self.dtype],
+                                                  None if options is None else ctypes.byref(options))
+        elif options is None:
             st = self._lib.hptt_create_plan(ctypes.byref(handle), pm, n, sz, self.alpha,
                                             self.beta, DTYPES[self.dtype])
         else:
@@ -233,8 +253,11 @@ class Plan:
     def _check_tensor(self, t, name):
         if not t.is_cuda:
             raise ValueError(f"{name} must be a device tensor")
-        if t.numel() != self.numel or not t.is_contiguous():
-            raise ValueError(f"{name} must be contiguous with {self.numel} elements")
+        info = self.info
+        need = info["footprint_a"] if name == "A" else info["footprint_b"]
+        if not t.is_contiguous() or t.numel() < need or (
+                self.outer_size_a is None and self.outer_size_b is None and t.numel() != need):
+            raise ValueError(f"{name} must be contiguous and cover {need} elements")
         if _dtype_id(t.dtype) != DTYPES[self.dtype]:
             raise ValueError(f"{name} has dtype {t.dtype}, plan is {self.dtype}")
 

@@ -39,7 +39,7 @@ def plan(perm, size_a, alpha=1.0, beta=0.0, dtype="f32", **knobs):
 def run(p, A=None, B=None, va=0, vb=0, counts=False, block_stride=1):
     """Emulate hptt_exec; B is updated in place.  Returns (errors, msg, counts)."""
     lib = library()
-    cnt = np.zeros(p.numel, dtype=np.uint8) if counts else None
+    cnt = np.zeros(p.info["footprint_b"], dtype=np.uint8) if counts else None
     msg = ctypes.create_string_buffer(512)
     err = lib.hptt_emulate_exec(p.handle, None if A is None else A.ctypes.data,
                                 None if B is None else B.ctypes.data, va, vb,

@@ -27,7 +27,8 @@
 namespace {
 
 struct EmuState {
-    int64_t numel = 0;
+    int64_t numelA = 0;   // elements addressable from A (its footprint)
+    int64_t numelB = 0;   // elements addressable from B
     const void* A = nullptr;
     void* B = nullptr;
     bool readsB = false;
@@ -55,7 +56,10 @@ bool check_global(const T* p, int64_t off, int V, bool isStore) {
     if (!isA && !isB) { fail("access to an unknown buffer", off, V); return false; }
     if (isA && isStore) { fail("store into A", off, V); return false; }
     if (isB && !isStore && !S->readsB) { fail("B read although beta == 0", off, V); return false; }
-    if (off < 0 || off + V > S->numel) { fail(isA ? "A offset out of bounds" : "B offset out of bounds", off, V); return false; }
+    if (off < 0 || off + V > (isA ? S->numelA : S->numelB)) {
+        fail(isA ? "A offset out of bounds" : "B offset out of bounds", off, V);
+        return false;
+    }
     if (off % V != 0) { fail("misaligned vector access", off, V); return false; }
     return true;
 }
@@ -239,13 +243,15 @@ extern "C" {
 // narrower ones as hptt_exec does for less aligned pointers.  counts (numel
 // bytes, or NULL) is incremented at every B element written.  Only
 // workgroups 0, block_stride, 2*block_stride, ... are run.  Returns the
-// number of violations; the first is described in msg.
+// number of violations; the first is described in msg.  For sub-tensor plans
+// A, B and counts cover the footprints (info.footprint_a, footprint_b).
 int64_t hptt_emulate_exec(hptt_plan_t plan, const void* A, void* B, int32_t va, int32_t vb,
                           uint8_t* counts, int64_t block_stride, char* msg, size_t msglen) {
     if (!plan) return -1;
     EmuState st;
     S = &st;
-    st.numel = plan->info.numel;
+    st.numelA = plan->info.footprint_a;
+    st.numelB = plan->info.footprint_b;
     st.dry = (A == nullptr && B == nullptr);
     st.A = st.dry ? kDryA : A;
     st.B = st.dry ? kDryB : B;
@@ -254,7 +260,7 @@ int64_t hptt_emulate_exec(hptt_plan_t plan, const void* A, void* B, int32_t va, 
     if (va <= 0) va = plan->info.vec_a;
     if (vb <= 0) vb = plan->info.vec_b;
     if (block_stride < 1) block_stride = 1;
-    if (plan->info.kernel != HPTT_KERNEL_NONE && st.numel > 0) {
+    if (plan->info.kernel != HPTT_KERNEL_NONE && plan->info.numel > 0) {
         if (plan->dtype == HPTT_FLOAT32)
             run<float>(plan, static_cast<const float*>(st.A), static_cast<float*>(st.B), va, vb, block_stride);
         else

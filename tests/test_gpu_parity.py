@@ -230,3 +230,89 @@ def test_yardsticks():
     hptt.yardstick_fill(z, n * 4, 0)
     torch.cuda.synchronize()
     assert z.abs().sum().item() == 0
+
+
+# --------------------------------------------------------------------------
+# Sub-tensors with outer sizes (Section 3.1, Fig. 3)
+# --------------------------------------------------------------------------
+
+def _fortran_offset(index, outer):
+    off, stride = 0, 1
+    for i, o in zip(index, outer):
+        off += int(i) * stride
+        stride *= int(o)
+    return off
+
+
+def _run_outer(size_a, perm, outer_a, outer_b, start_a, start_b, alpha, beta, dtype, rng,
+               **knobs):
+    p = hptt.create_plan(perm, size_a, alpha, beta, dtype, outer_size_a=outer_a,
+                         outer_size_b=outer_b, **knobs)
+    npd = NUMPY_DTYPE[dtype]
+    PA = _rand(rng, int(np.prod(outer_a)), dtype)
+    PB = _rand(rng, int(np.prod(outer_b)), dtype)
+    oa, ob = _fortran_offset(start_a, outer_a), _fortran_offset(start_b, outer_b)
+    want = np.concatenate([PB[:ob], orc.transpose_outer(PA[oa:], size_a, perm, outer_a, outer_b,
+                                                        alpha, beta, PB[ob:])])
+    dA = torch.from_numpy(PA).cuda()
+    dB = torch.from_numpy(PB).cuda()
+    p.exec(dA[oa:], dB[ob:])
+    torch.cuda.synchronize()
+    _assert_parity(dB.cpu().numpy(), want.astype(npd), dtype, "outer " + p.describe())
+    return p
+
+
+def test_fig3b_sub_tensor_on_gpu():
+    """Fig. 3b: the 8x16x16 sub-tensor of a 16x32x32 tensor, compacted."""
+    rng = np.random.default_rng(3)
+    _run_outer((8, 16, 16), (2, 1, 0), (16, 32, 32), (16, 16, 8), (0, 0, 0), (0, 0, 0),
+               1.0, 0.0, "f32", rng)
+    # the same sub-tensor taken from the middle of A, and scattered back
+    _run_outer((8, 16, 16), (2, 1, 0), (16, 32, 32), (16, 32, 16), (5, 9, 11), (0, 7, 3),
+               1.5, 0.5, "f64", rng)
+
+
+@pytest.mark.parametrize("knobs", [dict(), dict(kernel="generic"), dict(run_a=8, run_b=8)],
+                         ids=["default", "generic", "small_tiles"])
+def test_sub_tensors_random(knobs):
+    rng = np.random.default_rng(77)
+    kinds = set()
+    for it in range(60):
+        n = int(rng.integers(1, 6))
+        size_a = tuple(int(x) for x in rng.choice([1, 2, 3, 5, 8, 17, 33, 64, 65], size=n))
+        if np.prod(size_a) > (1 << 17):
+            continue
+        perm = tuple(int(p) for p in rng.permutation(n))
+        size_b = tuple(size_a[p] for p in perm)
+        outer_a = tuple(s + int(rng.choice([0, 0, 1, 3, 8])) for s in size_a)
+        outer_b = tuple(s + int(rng.choice([0, 0, 1, 3, 8])) for s in size_b)
+        start_a = tuple(int(rng.integers(0, o - s + 1)) for s, o in zip(size_a, outer_a))
+        start_b = tuple(int(rng.integers(0, o - s + 1)) for s, o in zip(size_b, outer_b))
+        dtype = ("f32", "f64")[it % 2]
+        alpha, beta = ((1.0, 0.0), (1.5, 0.0), (-0.3, 1.25), (2.0, 0.5))[it % 4]
+        p = _run_outer(size_a, perm, outer_a, outer_b, start_a, start_b, alpha, beta, dtype,
+                       rng, **knobs)
+        kinds.add(p.info["kernel"])
+    if not knobs:
+        assert {"tile", "generic"} <= kinds
+
+
+def test_large_sub_tensor_compact():
+    """A 4096 x 8192 block of an 8192 x 8192 matrix, transposed and compacted
+    (the shape of the sub-tensor benchmark), against one-by-one samples."""
+    outer_a, size_a, perm = (8192, 8192), (4096, 8192), (1, 0)
+    start_a = (2048, 0)
+    g = torch.Generator(device="cuda").manual_seed(9)
+    PA = torch.rand(8192 * 8192, device="cuda", generator=g)
+    B = torch.full((4096 * 8192,), float("nan"), device="cuda")
+    oa = _fortran_offset(start_a, outer_a)
+    p = hptt.create_plan(perm, size_a, outer_size_a=outer_a)
+    p.exec(PA[oa:], B)
+    torch.cuda.synchronize()
+    got = B.cpu().numpy()
+    assert not np.isnan(got).any()
+    hA = PA.cpu().numpy()
+    rng = np.random.default_rng(1)
+    j = rng.integers(0, 8192, 4000)      # B index 0 (A's index 1)
+    i = rng.integers(0, 4096, 4000)      # B index 1 (A's index 0)
+    assert np.array_equal(got[j + 8192 * i], hA[(start_a[0] + i) + 8192 * j])

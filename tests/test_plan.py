@@ -230,3 +230,46 @@ def test_plan_creation_is_quick():
         for _ in range(10):
             hptt.create_plan(perm, size)
         assert (time.perf_counter() - t0) / 10 < 2e-3, size
+
+
+# --------------------------------------------------------------------------
+# Sub-tensors with outer sizes (Section 3.1, Fig. 3)
+# --------------------------------------------------------------------------
+
+def test_fig3b_outer_plan():
+    rows = {r[0]: r[1:] for r in golden("fig3b_input.txt")}
+    perm = tuple(int(x) for x in rows["perm"])
+    size_a = tuple(int(x) for x in rows["sizeA"])
+    outer_a = tuple(int(x) for x in rows["outerSizeA"])
+    outer_b = tuple(int(x) for x in rows["outerSizeB"])
+    info = hptt.create_plan(perm, size_a, outer_size_a=outer_a, outer_size_b=outer_b).info
+    # A's sub-tensor spans from (0,0,0) to (7,15,15) of the 16x32x32 tensor
+    assert info["footprint_a"] == 1 + 7 * 1 + 15 * 16 + 15 * 16 * 32
+    assert info["footprint_b"] == 16 * 16 * 8
+    assert info["ndim"] == 3 and info["kernel"] == "tile"
+
+
+@pytest.mark.parametrize("outer_a,outer_b,fsize,fperm", [
+    ((4, 5, 6), (5, 6, 4), (4, 30), (1, 0)),        # compact: A1, A2 fuse
+    ((4, 8, 6), (5, 6, 4), (4, 5, 6), (1, 2, 0)),   # A1 padded in A: no fusion
+    ((4, 5, 6), (7, 6, 4), (4, 5, 6), (1, 2, 0)),   # B's first index padded: no fusion
+    ((4, 5, 6), (5, 6, 9), (4, 30), (1, 0)),        # padding only on B's last index
+    ((9, 5, 6), (5, 6, 4), (4, 30), (1, 0)),        # padding on A0 does not stop A1+A2
+])
+def test_outer_fusion(outer_a, outer_b, fsize, fperm):
+    info = hptt.create_plan((1, 2, 0), (4, 5, 6), outer_size_a=outer_a, outer_size_b=outer_b).info
+    assert info["size"] == fsize and info["perm"] == fperm
+
+
+def test_outer_smaller_than_size_rejected():
+    with pytest.raises(hptt.HpttError):
+        hptt.create_plan((1, 0), (4, 5), outer_size_a=(3, 5))
+    with pytest.raises(hptt.HpttError):
+        hptt.create_plan((1, 0), (4, 5), outer_size_b=(5, 3))
+
+
+def test_strided_single_index_uses_generic():
+    """A sub-tensor whose first extent is 1 leaves a strided index after the
+    extent-1 index is dropped; the flat kernel must not serve it."""
+    info = hptt.create_plan((0, 1), (1, 7), outer_size_a=(3, 7)).info
+    assert info["kernel"] == "generic" and info["footprint_a"] == 1 + 6 * 3
