@@ -152,10 +152,16 @@ def measure_workload(torch, hptt, w, steps, warmup, reps, flush_buf, sink, full:
     tdt = torch.float32 if w.dtype == "f32" else torch.float64
     gen = torch.Generator(device="cuda").manual_seed(w.seed_a)
     k = rotation(w)
-    As = [torch.rand(w.numel, dtype=tdt, device="cuda", generator=gen) * 2 - 1 for _ in range(k)]
-    Bs = [torch.rand(w.numel, dtype=tdt, device="cuda", generator=gen) * 2 - 1 for _ in range(k)]
+    # enclosing tensors; A and B below are the sub-tensors' first elements
+    PA = [torch.rand(w.parent_numel_a, dtype=tdt, device="cuda", generator=gen) * 2 - 1
+          for _ in range(k)]
+    PB = [torch.rand(w.parent_numel_b, dtype=tdt, device="cuda", generator=gen) * 2 - 1
+          for _ in range(k)]
+    As = [x[w.offset_a:] for x in PA]
+    Bs = [x[w.offset_b:] for x in PB]
     t0 = time.perf_counter()
-    plan = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype)
+    plan = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype, outer_size_a=w.outer_a,
+                            outer_size_b=w.outer_b)
     plan_us = (time.perf_counter() - t0) * 1e6
     moved = w.moved_bytes
     S = w.tensor_bytes
@@ -172,7 +178,7 @@ def measure_workload(torch, hptt, w, steps, warmup, reps, flush_buf, sink, full:
         hptt.yardstick_copy(As[i % k], Bs[i % k], S)
 
     def memcpy(i):
-        Bs[i % k].copy_(As[i % k])
+        Bs[i % k][:w.numel].copy_(As[i % k][:w.numel])
 
     def axpby(i):
         hptt.yardstick_axpby(w.dtype, w.alpha, As[i % k], w.beta, Bs[i % k], w.numel)
@@ -208,7 +214,7 @@ def measure_workload(torch, hptt, w, steps, warmup, reps, flush_buf, sink, full:
         }
         out["cold"]["median_pct_of_copy"] = (100 * out["cold"]["median_gbs"]
                                              / out["cold"]["copy_median_gbs"])
-    del As, Bs
+    del As, Bs, PA, PB
     torch.cuda.empty_cache()
     return out
 
@@ -375,7 +381,7 @@ def main():
     import torch
 
     from paper_1704_04374_amd import hptt
-    from paper_1704_04374_amd.workloads import BY_NAME, WORKLOADS
+    from paper_1704_04374_amd.workloads import BY_NAME, SUBTENSOR_WORKLOADS, WORKLOADS
 
     if not os.path.exists(hptt.LIB_PATH):
         from paper_1704_04374_amd import build
@@ -394,7 +400,7 @@ def main():
           f"of copy", file=sys.stderr, flush=True)
     per = {}
     if not args.only_headline:
-        for w in WORKLOADS:
+        for w in WORKLOADS + SUBTENSOR_WORKLOADS:
             r = headline if w.name == head.name else measure_workload(
                 torch, hptt, w, args.steps, args.warmup, args.reps, flush_buf, sink, full=True)
             per[w.name] = {k: (round(v, 2) if isinstance(v, float) else v) for k, v in r.items()}

@@ -30,6 +30,12 @@ class Workload:
     beta: float
     seed_a: int
     seed_b: int | None      # prior B contents (only when beta != 0)
+    # Sub-tensors (Fig. 3): extents of the enclosing tensors (A's / B's index
+    # order) and the sub-tensors' first multi-indices in them; None = compact.
+    outer_a: tuple | None = None
+    outer_b: tuple | None = None
+    start_a: tuple | None = None
+    start_b: tuple | None = None
 
     @property
     def numel(self) -> int:
@@ -58,9 +64,31 @@ class Workload:
         """lambda * S: bytes an ideal implementation moves through memory."""
         return self.lam * self.tensor_bytes
 
+    @property
+    def parent_numel_a(self) -> int:
+        return prod(self.outer_a) if self.outer_a else self.numel
+
+    @property
+    def parent_numel_b(self) -> int:
+        return prod(self.outer_b) if self.outer_b else self.numel
+
+    @property
+    def offset_a(self) -> int:
+        """Element offset of A's sub-tensor in its enclosing tensor."""
+        return _fortran_offset(self.start_a, self.outer_a) if self.start_a else 0
+
+    @property
+    def offset_b(self) -> int:
+        return _fortran_offset(self.start_b, self.outer_b) if self.start_b else 0
+
     def describe(self) -> str:
-        return (f"{self.name}: {self.dtype} A{self.size_a} perm{list(self.perm)} -> "
-                f"B{self.size_b}, alpha={self.alpha}, beta={self.beta}")
+        d = (f"{self.name}: {self.dtype} A{self.size_a} perm{list(self.perm)} -> "
+             f"B{self.size_b}, alpha={self.alpha}, beta={self.beta}")
+        if self.outer_a:
+            d += f", A inside {self.outer_a} at {self.start_a}"
+        if self.outer_b:
+            d += f", B inside {self.outer_b} at {self.start_b}"
+        return d
 
 
 WORKLOADS = [
@@ -74,7 +102,25 @@ WORKLOADS = [
              1.0, 1.0, 5, 6),
 ]
 
-BY_NAME = {w.name: w for w in WORKLOADS}
+# Sub-tensor workloads (Section 3.1, Fig. 3): transpose-and-compact and its
+# reverse, transpose-and-scatter, on a half of an 8192 x 8192 fp32 matrix.
+SUBTENSOR_WORKLOADS = [
+    Workload("compact_4096x8192_of_8192x8192_f32", "f32", (4096, 8192), (1, 0), 1.0, 0.0, 7,
+             None, outer_a=(8192, 8192), start_a=(2048, 0)),
+    Workload("scatter_4096x8192_into_8192x8192_f32", "f32", (4096, 8192), (1, 0), 1.0, 0.0, 8,
+             None, outer_b=(8192, 8192), start_b=(0, 2048)),
+]
+
+BY_NAME = {w.name: w for w in WORKLOADS + SUBTENSOR_WORKLOADS}
+
+
+def _fortran_offset(index, outer) -> int:
+    off, stride = 0, 1
+    for i, o in zip(index, outer):
+        off += int(i) * stride
+        stride *= int(o)
+    return off
+
 
 TORCH_DTYPE = {"f32": torch.float32, "f64": torch.float64}
 NUMPY_DTYPE = {"f32": np.float32, "f64": np.float64}
