@@ -146,7 +146,8 @@ def rotation(w) -> int:
     return max(2, min(8, -(-ROTATE_BYTES // per_set)))
 
 
-def measure_workload(torch, hptt, w, steps, warmup, reps, flush_buf, sink, full: bool):
+def measure_workload(torch, hptt, w, steps, warmup, reps, flush_buf, sink, full: bool,
+                     tune_s: float = 0.0):
     """Time one workload: the transposition and its same-run yardsticks, all
     over the same rotating buffer sets."""
     tdt = torch.float32 if w.dtype == "f32" else torch.float64
@@ -214,6 +215,22 @@ def measure_workload(torch, hptt, w, steps, warmup, reps, flush_buf, sink, full:
         }
         out["cold"]["median_pct_of_copy"] = (100 * out["cold"]["median_gbs"]
                                              / out["cold"]["copy_median_gbs"])
+    if tune_s > 0:
+        # the autotune path (Section 3.1), timed like the quick path's plan
+        t0 = time.perf_counter()
+        tuned, rep = hptt.autotune_plan(w.perm, w.size_a, As[0], Bs[0], w.alpha, w.beta,
+                                        w.dtype, timeout=tune_s, outer_size_a=w.outer_a,
+                                        outer_size_b=w.outer_b)
+        tune_wall = time.perf_counter() - t0
+        truns = [tuned.launcher(As[j].data_ptr(), Bs[j].data_ptr(), stream) for j in range(k)]
+        tms = time_launches(torch, lambda i: truns[i % k](), steps, warmup)[1]
+        out["autotune"] = {
+            "seconds": round(tune_wall, 2), "candidates": rep["candidates"],
+            "timed": rep["timed"], "plan": tuned.describe(),
+            "knobs": {n: v for n, v in rep["options"].items() if v},
+            "kernel_gbs": round(gbs(moved, tms), 1),
+            "speedup_vs_quick": round(ms / tms, 3),
+        }
     del As, Bs, PA, PB
     torch.cuda.empty_cache()
     return out
@@ -353,6 +370,8 @@ def main():
     ap.add_argument("--only-headline", action="store_true",
                     help="time only the headline workload (for profiler runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--autotune", type=float, default=2.0, metavar="SECONDS",
+                    help="also tune each named workload for this long (0: skip)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     ap.add_argument("--summarize-trace", metavar="TRACE_DIR")
     ap.add_argument("--pmc-command", default="")
@@ -395,17 +414,22 @@ def main():
 
     preheat(torch, hptt)
     headline = measure_workload(torch, hptt, head, args.steps, args.warmup, args.reps, flush_buf,
-                                sink, full=not args.only_headline)
+                                sink, full=not args.only_headline,
+                                tune_s=0.0 if args.only_headline else args.autotune)
     print(f"[bench] {head.name}: {headline['gbs']:.0f} GB/s, {headline['pct_of_copy']:.1f}% "
           f"of copy", file=sys.stderr, flush=True)
     per = {}
     if not args.only_headline:
         for w in WORKLOADS + SUBTENSOR_WORKLOADS:
             r = headline if w.name == head.name else measure_workload(
-                torch, hptt, w, args.steps, args.warmup, args.reps, flush_buf, sink, full=True)
+                torch, hptt, w, args.steps, args.warmup, args.reps, flush_buf, sink, full=True,
+                tune_s=args.autotune)
             per[w.name] = {k: (round(v, 2) if isinstance(v, float) else v) for k, v in r.items()}
+            tuned = r.get("autotune")
             print(f"[bench] {w.name}: kernel {r['kernel_gbs']:.0f} GB/s, "
-                  f"{r['pct_of_copy']:.1f}% of copy, {r['pct_of_hbm_peak']:.1f}% of peak",
+                  f"{r['pct_of_copy']:.1f}% of copy, {r['pct_of_hbm_peak']:.1f}% of peak"
+                  + (f"; autotuned {tuned['kernel_gbs']:.0f} GB/s ({tuned['timed']} of "
+                     f"{tuned['candidates']} plans timed)" if tuned else ""),
                   file=sys.stderr, flush=True)
 
     traffic = load_traffic(headline["kernel_class"], head.name)

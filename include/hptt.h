@@ -167,6 +167,53 @@ hptt_status_t hptt_create_plan_outer(hptt_plan_t *plan, const int32_t *perm, int
                                      const int64_t *outerSizeB, double alpha, double beta,
                                      hptt_dtype_t dtype, const hptt_options_t *options);
 
+/* What hptt_create_plan_autotune did. */
+typedef struct {
+    int32_t candidates;      /* distinct plans generated */
+    int32_t timed;           /* plans timed before the timeout */
+    int32_t from_cache;      /* 1 when the problem was tuned earlier in this process */
+    float default_ms;        /* the quick path's plan, best of three launches */
+    float best_ms;           /* the winner, best of three launches */
+    hptt_options_t options;  /* the winner's knobs (all zero: the quick path's plan) */
+} hptt_autotune_report_t;
+
+/*
+ * The autotune path of plan creation (Section 3.1): generate candidate plans
+ * (tile shapes, tile orders, cache hints), rank them with the quick path's
+ * plan first, then time them on the caller's own tensors, from good to bad,
+ * until timeout_seconds have passed, and return a plan with the fastest one's
+ * knobs for the given alpha and beta.  Like the paper, timing runs with
+ * alpha = 0 and beta = 1, so B is rewritten with its own value and A is read
+ * and multiplied by zero; A must hold no inf or NaN (footnote 5), and a -0.0
+ * in B may come back as +0.0.  The winner is cached per problem (perm,
+ * extents, outer sizes, dtype, update mode, device) for the life of the
+ * process; a cached problem returns at once without launching anything.
+ *
+ *   A, B     device pointers as for hptt_exec (used only for timing).
+ *   stream   stream the timing launches are queued on; this call waits for it.
+ *   timeout_seconds  <= 0 returns the quick path's plan (or the cached one).
+ *   report   may be NULL.
+ * Errors: as hptt_create_plan_outer and hptt_exec.
+ */
+hptt_status_t hptt_create_plan_autotune(hptt_plan_t *plan, const int32_t *perm, int32_t N,
+                                        const int64_t *sizeA, const int64_t *outerSizeA,
+                                        const int64_t *outerSizeB, double alpha, double beta,
+                                        hptt_dtype_t dtype, const void *A, void *B,
+                                        hipStream_t stream, double timeout_seconds,
+                                        hptt_autotune_report_t *report);
+
+/* The candidate knobs hptt_create_plan_autotune would time for a problem, in
+ * its order, written to options[0 .. min(count, max_options) - 1].  Returns
+ * the count, or minus a status code for an invalid problem.  Makes no HIP
+ * call. */
+int32_t hptt_autotune_candidates(const int32_t *perm, int32_t N, const int64_t *sizeA,
+                                 const int64_t *outerSizeA, const int64_t *outerSizeB,
+                                 double alpha, double beta, hptt_dtype_t dtype,
+                                 hptt_options_t *options, int32_t max_options);
+
+/* Drop every cached autotuning result of this process. */
+hptt_status_t hptt_forget_wisdom(void);
+
 /*
  * Execute a plan (Fig. 3b's plan->exec()): queue the transposition of A into B
  * on `stream` and return without waiting.

@@ -21,7 +21,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libhptt.so")
 
 ARCH = "gfx950"
-SOURCES = ["kernels.hip", "yardstick.hip", "api.cpp", "plan.cpp"]
+SOURCES = ["kernels.hip", "yardstick.hip", "api.cpp", "plan.cpp", "autotune.cpp"]
 
 # -ffp-contract=off: alpha*a + beta*b is two roundings and an add, never an
 # FMA.  The packed-fp32 feature is switched off for every HIP file.

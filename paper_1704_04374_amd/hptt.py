@@ -43,6 +43,19 @@ class Options(ctypes.Structure):
                 ("exact_runs", ctypes.c_int32), ("row_passes", ctypes.c_int32)]
 
 
+class AutotuneReport(ctypes.Structure):
+    """hptt_autotune_report_t"""
+    _fields_ = [("candidates", ctypes.c_int32), ("timed", ctypes.c_int32),
+                ("from_cache", ctypes.c_int32), ("default_ms", ctypes.c_float),
+                ("best_ms", ctypes.c_float), ("options", Options)]
+
+    def as_dict(self) -> dict:
+        return {"candidates": self.candidates, "timed": self.timed,
+                "from_cache": bool(self.from_cache), "default_ms": self.default_ms,
+                "best_ms": self.best_ms,
+                "options": {name: getattr(self.options, name) for name, _ in Options._fields_}}
+
+
 class PlanInfo(ctypes.Structure):
     """hptt_plan_info_t"""
     _fields_ = [("ndim", ctypes.c_int32), ("size", ctypes.c_int64 * MAX_DIMS),
@@ -73,8 +86,9 @@ class PlanInfo(ctypes.Structure):
 
 
 # Every entry point declared in include/hptt.h and include/hptt_yardstick.h.
-EXPORTS = ("hptt_create_plan", "hptt_create_plan_ex", "hptt_create_plan_outer", "hptt_exec",
-           "hptt_destroy_plan",
+EXPORTS = ("hptt_create_plan", "hptt_create_plan_ex", "hptt_create_plan_outer",
+           "hptt_create_plan_autotune", "hptt_autotune_candidates", "hptt_forget_wisdom",
+           "hptt_exec", "hptt_destroy_plan",
            "hptt_plan_info", "hptt_describe_plan", "hptt_status_string",
            "hptt_last_hip_error", "hptt_yardstick_copy", "hptt_yardstick_axpby",
            "hptt_yardstick_fill", "hptt_yardstick_read")
@@ -100,6 +114,16 @@ def _declare(lib: ctypes.CDLL, gpu: bool) -> ctypes.CDLL:
               "hptt_destroy_plan", "hptt_plan_info", "hptt_describe_plan"):
         getattr(lib, f).restype = st
     if gpu:
+        lib.hptt_autotune_candidates.argtypes = [i32p, ctypes.c_int32, i64p, i64p, i64p,
+                                                 ctypes.c_double, ctypes.c_double, ctypes.c_int,
+                                                 ctypes.POINTER(Options), ctypes.c_int32]
+        lib.hptt_autotune_candidates.restype = ctypes.c_int32
+        lib.hptt_create_plan_autotune.argtypes = [ctypes.POINTER(vp), i32p, ctypes.c_int32, i64p,
+                                                  i64p, i64p, ctypes.c_double, ctypes.c_double,
+                                                  ctypes.c_int, vp, vp, vp, ctypes.c_double,
+                                                  ctypes.POINTER(AutotuneReport)]
+        lib.hptt_create_plan_autotune.restype = st
+        lib.hptt_forget_wisdom.restype = st
         lib.hptt_exec.argtypes = [vp, vp, vp, vp]
         lib.hptt_exec.restype = st
         lib.hptt_last_hip_error.restype = ctypes.c_int32
@@ -313,3 +337,48 @@ def yardstick_read(buf, nbytes: int, sink, stream=None):
     _check(library().hptt_yardstick_read(ctypes.c_void_p(buf.data_ptr()), nbytes,
                                          ctypes.c_void_p(sink.data_ptr()),
                                          ctypes.c_void_p(_stream(stream))), "hptt_yardstick_read")
+
+
+def _sizes(values, n):
+    return None if values is None else (ctypes.c_int64 * n)(*[int(x) for x in values])
+
+
+def autotune_candidates(perm, size_a, alpha=1.0, beta=0.0, dtype="f32", outer_size_a=None,
+                        outer_size_b=None, max_options: int = 256) -> list:
+    """The knobs hptt_create_plan_autotune would time, in its order."""
+    n = len(perm)
+    out = (Options * max_options)()
+    cnt = library().hptt_autotune_candidates(
+        (ctypes.c_int32 * n)(*perm), n, (ctypes.c_int64 * n)(*size_a), _sizes(outer_size_a, n),
+        _sizes(outer_size_b, n), float(alpha), float(beta), _dtype_id(dtype), out, max_options)
+    if cnt < 0:
+        raise HpttError(-cnt, "hptt_autotune_candidates")
+    return [{name: getattr(out[i], name) for name, _ in Options._fields_}
+            for i in range(min(cnt, max_options))]
+
+
+def autotune_plan(perm, size_a, A, B, alpha=1.0, beta=0.0, dtype="f32", timeout=1.0,
+                  outer_size_a=None, outer_size_b=None, stream=None):
+    """A plan tuned on the device tensors A and B (which keep their values)
+    within ``timeout`` seconds; returns (Plan, report dict)."""
+    plan = Plan(perm, size_a, alpha, beta, dtype, outer_size_a=outer_size_a,
+                outer_size_b=outer_size_b)
+    plan._check_tensor(A, "A")   # the tuner launches on A and B: check them first
+    plan._check_tensor(B, "B")
+    n = len(plan.perm)
+    handle = ctypes.c_void_p()
+    rep = AutotuneReport()
+    st = plan._lib.hptt_create_plan_autotune(
+        ctypes.byref(handle), (ctypes.c_int32 * n)(*plan.perm), n,
+        (ctypes.c_int64 * n)(*plan.size_a), _sizes(plan.outer_size_a, n),
+        _sizes(plan.outer_size_b, n), plan.alpha, plan.beta, DTYPES[plan.dtype],
+        ctypes.c_void_p(A.data_ptr()), ctypes.c_void_p(B.data_ptr()),
+        ctypes.c_void_p(_stream(stream)), float(timeout), ctypes.byref(rep))
+    _check(st, "hptt_create_plan_autotune")
+    plan._lib.hptt_destroy_plan(plan._handle)
+    plan._handle = handle
+    return plan, rep.as_dict()
+
+
+def forget_wisdom():
+    _check(library().hptt_forget_wisdom(), "hptt_forget_wisdom")

@@ -1,0 +1,118 @@
+"""The autotune path (Section 3.1) on an MI355X, through the C ABI: the
+tuner leaves A and B as they were, its plan matches the oracle bit for bit,
+and a tuned problem is served from the process-wide cache."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as orc
+from paper_1704_04374_amd import hptt
+from paper_1704_04374_amd.workloads import BY_NAME, NUMPY_DTYPE, inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _rand(rng, n, dtype):
+    return (rng.integers(-(1 << 20), 1 << 20, size=n) / float(1 << 20)).astype(NUMPY_DTYPE[dtype])
+
+
+def _bits(t: torch.Tensor) -> np.ndarray:
+    a = t.cpu().numpy()
+    return a.view(np.uint32 if a.dtype == np.float32 else np.uint64)
+
+
+@pytest.mark.parametrize("name", ["transpose2d_8192x8192_f32",
+                                  "transpose4d_96x96x96x96_keep1_f64"])
+def test_autotune_full_size(name):
+    """Tune on the workload's own tensors: A and B bit for bit unchanged,
+    the tuned plan's result equal to the oracle's, the second request served
+    from the cache without timing anything."""
+    w = BY_NAME[name]
+    _say(f"[autotune] {w.describe()}")
+    hptt.forget_wisdom()
+    A, B0 = inputs(w)
+    if B0 is None:
+        B0 = torch.full_like(A, 0.75)
+    want = orc.transpose(A.numpy(), w.size_a, w.perm, w.alpha, w.beta,
+                         B0.numpy() if w.beta != 0 else None)
+    dA, dB = A.cuda(), B0.cuda()
+    a_bits, b_bits = _bits(dA), _bits(dB)
+    plan, rep = hptt.autotune_plan(w.perm, w.size_a, dA, dB, w.alpha, w.beta, w.dtype,
+                                   timeout=1.5)
+    torch.cuda.synchronize()
+    _say(f"[autotune] {rep}")
+    assert rep["candidates"] >= 1 and 1 <= rep["timed"] <= rep["candidates"]
+    assert not rep["from_cache"]
+    assert 0 < rep["best_ms"] <= rep["default_ms"]
+    assert np.array_equal(_bits(dA), a_bits) and np.array_equal(_bits(dB), b_bits)
+    plan.exec(dA, dB)
+    torch.cuda.synchronize()
+    assert np.array_equal(dB.cpu().numpy(), want), plan.describe()
+    again, rep2 = hptt.autotune_plan(w.perm, w.size_a, dA, dB, w.alpha, w.beta, w.dtype,
+                                     timeout=1.5)
+    assert rep2["from_cache"] and rep2["timed"] == 0
+    assert rep2["options"] == rep["options"]
+    assert again.describe() == plan.describe()
+
+
+def test_autotune_small_problems_and_sub_tensors():
+    """Small ragged problems of every kernel class (and a sub-tensor pair):
+    tuned plans equal the oracle, tensors untouched by tuning."""
+    rng = np.random.default_rng(11)
+    hptt.forget_wisdom()
+    cases = [((97, 65, 33), (2, 0, 1), 1.0, 0.0, "f32", None, None),
+             ((1000, 1032), (1, 0), -0.5, 1.25, "f64", None, None),
+             ((3, 2, 40, 33, 17), (4, 2, 0, 3, 1), 1.0, 1.0, "f32", None, None),
+             ((24, 13, 9, 10), (0, 3, 2, 1), 2.0, 0.5, "f64", None, None),
+             ((4100,), (0,), 1.5, 0.0, "f32", None, None),
+             ((300, 200), (1, 0), 1.0, 0.0, "f32", (333, 250), (210, 320))]
+    for size_a, perm, alpha, beta, dtype, outer_a, outer_b in cases:
+        _say(f"[autotune] {size_a} perm {perm} alpha {alpha} beta {beta} {dtype} "
+             f"outer {outer_a} {outer_b}")
+        size_b = tuple(size_a[p] for p in perm)
+        na = int(np.prod(outer_a or size_a))
+        nb = int(np.prod(outer_b or size_b))
+        A = _rand(rng, na, dtype)
+        B0 = _rand(rng, nb, dtype)
+        B0[B0 == 0] = 0.5                      # -0.0 could come back as +0.0
+        want = orc.transpose_outer(A, size_a, perm, outer_a or size_a, outer_b or size_b, alpha,
+                                   beta, B0)
+        dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B0).cuda()
+        plan, rep = hptt.autotune_plan(perm, size_a, dA, dB, alpha, beta, dtype, timeout=0.2,
+                                       outer_size_a=outer_a, outer_size_b=outer_b)
+        torch.cuda.synchronize()
+        assert np.array_equal(dB.cpu().numpy().view(np.uint8), B0.view(np.uint8)), rep
+        assert np.array_equal(dA.cpu().numpy().view(np.uint8), A.view(np.uint8))
+        plan.exec(dA, dB)
+        torch.cuda.synchronize()
+        assert np.array_equal(dB.cpu().numpy(), want), (plan.describe(), rep)
+
+
+def test_autotune_zero_timeout_and_cache_reset():
+    rng = np.random.default_rng(3)
+    hptt.forget_wisdom()
+    size_a, perm = (512, 384), (1, 0)
+    A = torch.from_numpy(_rand(rng, 512 * 384, "f32")).cuda()
+    B = torch.zeros_like(A)
+    plan, rep = hptt.autotune_plan(perm, size_a, A, B, timeout=0)
+    assert rep["timed"] == 0 and not any(rep["options"].values())
+    assert plan.describe() == hptt.create_plan(perm, size_a).describe()
+    _, rep = hptt.autotune_plan(perm, size_a, A, B, timeout=0.1)
+    assert rep["timed"] >= 1 and not rep["from_cache"]
+    _, rep = hptt.autotune_plan(perm, size_a, A, B, timeout=0.1)
+    assert rep["from_cache"]
+    hptt.forget_wisdom()
+    _, rep = hptt.autotune_plan(perm, size_a, A, B, timeout=0.1)
+    assert not rep["from_cache"]
+    # another update mode of the same shape is another problem
+    _, rep = hptt.autotune_plan(perm, size_a, A, B, 1.0, 1.0, timeout=0.1)
+    assert not rep["from_cache"]
+    # an empty problem needs no tuning and no tensors
+    empty = hptt.Plan((1, 0), (0, 5))
+    assert empty.info["kernel"] == "none"
