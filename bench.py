@@ -360,6 +360,47 @@ def summarize_trace(trace_dir: str, workload: str, command: str, out_path: str):
     print("\n".join(lines))
 
 
+def run_sweep(torch, hptt, args, flush_buf, sink) -> dict:
+    """The 57-case sweep (Section 4, Figs. 6 and 7): every case with beta != 0
+    against the same-run axpby yardstick (the paper's SAXPY), with and
+    without autotuning, and again with beta = 0 against the copy yardstick."""
+    from dataclasses import replace
+
+    from paper_1704_04374_amd.workloads import sweep57
+    cases = []
+    for w in sweep57(beta=1.0):
+        r = measure_workload(torch, hptt, w, args.steps, args.warmup, 0, flush_buf, sink,
+                             full=False, tune_s=args.autotune)
+        w0 = replace(w, name=w.name, beta=0.0, seed_b=None)
+        r0 = measure_workload(torch, hptt, w0, args.steps, args.warmup, 0, flush_buf, sink,
+                              full=False)
+        c = {"case": w.name, "kernel": r["kernel_class"], "plan": r["plan"],
+             "gbs": round(r["kernel_gbs"], 1), "pct_of_axpby": round(r["pct_of_axpby"], 1),
+             "pct_of_hbm_peak": round(r["pct_of_hbm_peak"], 1),
+             "beta0_gbs": round(r0["kernel_gbs"], 1), "beta0_pct_of_copy": round(r0["pct_of_copy"], 1)}
+        if "autotune" in r:
+            c["tuned_gbs"] = r["autotune"]["kernel_gbs"]
+            c["tuned_speedup"] = r["autotune"]["speedup_vs_quick"]
+            c["tuned_knobs"] = r["autotune"]["knobs"]
+        cases.append(c)
+        print(f"[sweep] {w.name}: {c['kernel']} {c['gbs']:.0f} GB/s = {c['pct_of_axpby']:.1f}% of "
+              f"axpby; beta=0 {c['beta0_pct_of_copy']:.1f}% of copy"
+              + (f"; tuned x{c['tuned_speedup']:.3f}" if "tuned_speedup" in c else ""),
+              file=sys.stderr, flush=True)
+
+    def stats(key):
+        v = [c[key] for c in cases if key in c]
+        return {"mean": round(statistics.mean(v), 3), "median": round(statistics.median(v), 3),
+                "min": round(min(v), 3), "max": round(max(v), 3)} if v else None
+    return {"sweep": "57 seeded fp32 transpositions, 2-D to 6-D, 200 MB per tensor",
+            "steps": args.steps, "warmup": args.warmup, "autotune_seconds": args.autotune,
+            "pct_of_axpby": stats("pct_of_axpby"), "beta0_pct_of_copy": stats("beta0_pct_of_copy"),
+            "pct_of_hbm_peak": stats("pct_of_hbm_peak"), "tuned_speedup": stats("tuned_speedup"),
+            "kernels": {k: sum(c["kernel"] == k for c in cases) for k in
+                        sorted(set(c["kernel"] for c in cases))},
+            "cases": cases}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -372,6 +413,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--autotune", type=float, default=2.0, metavar="SECONDS",
                     help="also tune each named workload for this long (0: skip)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="run the 57-case sweep instead and print its summary as JSON")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     ap.add_argument("--summarize-trace", metavar="TRACE_DIR")
     ap.add_argument("--pmc-command", default="")
@@ -413,6 +456,9 @@ def main():
           file=sys.stderr, flush=True)
 
     preheat(torch, hptt)
+    if args.sweep:
+        print(json.dumps(run_sweep(torch, hptt, args, flush_buf, sink)), flush=True)
+        return 0
     headline = measure_workload(torch, hptt, head, args.steps, args.warmup, args.reps, flush_buf,
                                 sink, full=not args.only_headline,
                                 tune_s=0.0 if args.only_headline else args.autotune)

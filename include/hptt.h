@@ -172,9 +172,11 @@ typedef struct {
     int32_t candidates;      /* distinct plans generated */
     int32_t timed;           /* plans timed before the timeout */
     int32_t from_cache;      /* 1 when the problem was tuned earlier in this process */
-    float default_ms;        /* the quick path's plan, best of three launches */
-    float best_ms;           /* the winner, best of three launches */
-    hptt_options_t options;  /* the winner's knobs (all zero: the quick path's plan) */
+    int32_t flushed;         /* 1 when each timed launch started with cold caches */
+    int32_t own_mode;        /* 1 when beta = 0 plans were timed writing a scratch tensor */
+    float default_ms;        /* the quick path's plan, median of three launches */
+    float best_ms;           /* the chosen plan, median of three launches */
+    hptt_options_t options;  /* the chosen plan's knobs (all zero: the quick path's plan) */
 } hptt_autotune_report_t;
 
 /*
@@ -182,15 +184,24 @@ typedef struct {
  * (tile shapes, tile orders, cache hints), rank them with the quick path's
  * plan first, then time them on the caller's own tensors, from good to bad,
  * until timeout_seconds have passed, and return a plan with the fastest one's
- * knobs for the given alpha and beta.  Like the paper, timing runs with
- * alpha = 0 and beta = 1, so B is rewritten with its own value and A is read
- * and multiplied by zero; A must hold no inf or NaN (footnote 5), and a -0.0
- * in B may come back as +0.0.  The winner is cached per problem (perm,
+ * knobs for the given alpha and beta (the quick path's plan unless another
+ * is at least 1 % faster).  Each plan is timed in the update mode it will
+ * run in, as the median of three launches that each start after a 512 MiB
+ * read has evicted the tensors from the caches.  The caller's data are not
+ * changed: with beta != 0 timing runs, like the paper's, with alpha = 0 and
+ * beta = 1, so B is rewritten with its own value and A is read and multiplied
+ * by zero (A must then hold no inf or NaN, footnote 5, and a -0.0 in B may
+ * come back as +0.0); with beta = 0 the plans write a scratch tensor and B is
+ * not touched.  The scratch memory (the flush buffer and, for beta = 0, a
+ * tensor of B's footprint) is allocated for the call and freed before it
+ * returns; without it, timing falls back to warm caches and the paper's
+ * alpha = 0, beta = 1 on B.  The chosen plan is cached per problem (perm,
  * extents, outer sizes, dtype, update mode, device) for the life of the
  * process; a cached problem returns at once without launching anything.
  *
  *   A, B     device pointers as for hptt_exec (used only for timing).
- *   stream   stream the timing launches are queued on; this call waits for it.
+ *   stream   stream the timing launches are queued on; this call waits for it
+ *            (and, through hipFree of the scratch memory, for the device).
  *   timeout_seconds  <= 0 returns the quick path's plan (or the cached one).
  *   report   may be NULL.
  * Errors: as hptt_create_plan_outer and hptt_exec.

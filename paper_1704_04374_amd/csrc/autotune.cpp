@@ -1,9 +1,13 @@
 // The autotune path of plan creation (Section 3.1): generate candidate plans,
 // rank them with the heuristic plan first, then time them on the caller's own
 // tensors, from good to bad, until a timeout, and keep the fastest (FFTW
-// style).  Timing runs with alpha = 0 and beta = 1, so B is rewritten with
-// its own value and A is read and multiplied by zero (Section 3.1; A must not
-// hold inf or NaN, footnote 5).  Winners are cached per problem for the life
+// style).  Timing never changes the caller's data: with beta != 0 it runs with
+// alpha = 0 and beta = 1, so B is rewritten with its own value and A is read
+// and multiplied by zero (Section 3.1; A must not hold inf or NaN, footnote
+// 5); with beta = 0 the plans write a scratch tensor instead, so that they are
+// timed in the mode they will run in.  A 512 MiB read between timed launches
+// evicts the tensors from the last-level cache, as the paper's measurements
+// clear the caches (Section 4).  Winners are cached per problem for the life
 // of the process.
 #include <hip/hip_runtime_api.h>
 
@@ -14,6 +18,7 @@
 #include <string>
 #include <vector>
 
+#include "hptt_yardstick.h"
 #include "plan.h"
 
 namespace hptt {
@@ -126,6 +131,37 @@ int autotune_candidates(const int32_t* perm, int32_t N, const int64_t* sizeA,
     return n;
 }
 
+namespace {
+
+constexpr size_t kFlushBytes = size_t(512) << 20;  // two last-level caches (256 MB each)
+constexpr int kReps = 3;
+constexpr float kMargin = 0.99f;  // leave the quick plan only for a 1 % gain
+
+// Device memory the tuner borrows for its measurements and returns at the end.
+struct Scratch {
+    void* flush = nullptr;  // read between timed launches so they start cold
+    void* sink = nullptr;   // checksums of the flush reads
+    void* out = nullptr;    // a stand-in for B when beta = 0
+    ~Scratch() {
+        if (flush) (void)hipFree(flush);
+        if (sink) (void)hipFree(sink);
+        if (out) (void)hipFree(out);
+    }
+};
+
+bool try_alloc(void** p, size_t bytes) {
+    if (hipMalloc(p, bytes) == hipSuccess) return true;
+    *p = nullptr;
+    (void)hipGetLastError();  // an allocation failure is not an error of the caller's
+    return false;
+}
+
+float median3(float a, float b, float c) {
+    return a > b ? (b > c ? b : (a > c ? c : a)) : (a > c ? a : (b > c ? c : b));
+}
+
+}  // namespace
+
 hptt_status_t autotune(hptt_plan_t* planOut, const int32_t* perm, int32_t N, const int64_t* sizeA,
                        const int64_t* outerA, const int64_t* outerB, double alpha, double beta,
                        hptt_dtype_t dtype, const void* A, void* B, hipStream_t stream,
@@ -134,12 +170,12 @@ hptt_status_t autotune(hptt_plan_t* planOut, const int32_t* perm, int32_t N, con
     if (!planOut) return HPTT_ERROR_INVALID_ARGUMENT;
     *planOut = nullptr;
     if (report) memset(report, 0, sizeof(*report));
-    {   // nothing to tune when there is nothing to move
-        hptt_plan_s base;
+    hptt_plan_s base;
+    {
         const hptt_status_t st =
             build_plan(perm, N, sizeA, outerA, outerB, alpha, beta, dtype, nullptr, &base);
         if (st != HPTT_SUCCESS) return st;
-        if (base.info.kernel == HPTT_KERNEL_NONE)
+        if (base.info.kernel == HPTT_KERNEL_NONE)  // nothing to move, nothing to tune
             return hptt_create_plan_outer(planOut, perm, N, sizeA, outerA, outerB, alpha, beta,
                                           dtype, nullptr);
     }
@@ -163,7 +199,19 @@ hptt_status_t autotune(hptt_plan_t* planOut, const int32_t* perm, int32_t N, con
         const int nc = autotune_candidates(perm, N, sizeA, outerA, outerB, alpha, beta, dtype,
                                            cand.data(), kMaxCandidates);
         if (nc < 0) return hptt_status_t(-nc);
-        if (nc > 0 && (!A || !B)) return HPTT_ERROR_INVALID_ARGUMENT;
+        if (!A || !B) return HPTT_ERROR_INVALID_ARGUMENT;
+        // Time in the caller's own update mode.  With beta != 0 that is the
+        // paper's alpha = 0, beta = 1 on B itself (B keeps its value); with
+        // beta = 0 the plan writes a scratch tensor and B is not touched.
+        // Without memory for the scratch tensor, fall back to the paper's way.
+        Scratch scratch;
+        const size_t elem = dtype == HPTT_FLOAT32 ? 4 : 8;
+        const bool ownMode =
+            mode != kAxpby && try_alloc(&scratch.out, size_t(base.info.footprint_b) * elem);
+        const double tAlpha = ownMode ? alpha : 0.0, tBeta = ownMode ? beta : 1.0;
+        void* const target = ownMode ? scratch.out : B;
+        const bool flush = try_alloc(&scratch.flush, kFlushBytes) &&
+                           try_alloc(&scratch.sink, 4096 * sizeof(uint32_t));
         hipEvent_t e0, e1;
         if (hipEventCreate(&e0) != hipSuccess) return HPTT_ERROR_HIP;
         if (hipEventCreate(&e1) != hipSuccess) {
@@ -171,34 +219,36 @@ hptt_status_t autotune(hptt_plan_t* planOut, const int32_t* perm, int32_t N, con
             return HPTT_ERROR_HIP;
         }
         const auto t0 = clock::now();
-        float bestMs = 0.f;
+        float bestMs = 0.f, quickMs = 0.f;
         hptt_status_t err = HPTT_SUCCESS;
         int timed = 0;
-        for (int c = 0; c < nc; ++c) {
-            // non-destructive timing plan: alpha = 0, beta = 1
+        for (int c = 0; c < nc && err == HPTT_SUCCESS; ++c) {
             hptt_plan_s tp;
-            if (build_plan(perm, N, sizeA, outerA, outerB, 0.0, 1.0, dtype, &cand[c], &tp) !=
+            if (build_plan(perm, N, sizeA, outerA, outerB, tAlpha, tBeta, dtype, &cand[c], &tp) !=
                 HPTT_SUCCESS)
                 continue;
-            float ms = 0.f;
-            err = hptt_exec(&tp, A, B, stream);  // warm-up
-            for (int r = 0; r < 3 && err == HPTT_SUCCESS; ++r) {
-                if (hipEventRecord(e0, stream) != hipSuccess) err = HPTT_ERROR_HIP;
-                if (err == HPTT_SUCCESS) err = hptt_exec(&tp, A, B, stream);
+            float ms[kReps] = {};
+            err = hptt_exec(&tp, A, target, stream);  // warm-up
+            for (int r = 0; r < kReps && err == HPTT_SUCCESS; ++r) {
+                if (flush)
+                    err = hptt_yardstick_read(scratch.flush, kFlushBytes, scratch.sink, stream);
+                if (err == HPTT_SUCCESS && hipEventRecord(e0, stream) != hipSuccess)
+                    err = HPTT_ERROR_HIP;
+                if (err == HPTT_SUCCESS) err = hptt_exec(&tp, A, target, stream);
                 if (err == HPTT_SUCCESS && hipEventRecord(e1, stream) != hipSuccess)
                     err = HPTT_ERROR_HIP;
                 if (err == HPTT_SUCCESS && hipEventSynchronize(e1) != hipSuccess)
                     err = HPTT_ERROR_HIP;
-                float one = 0.f;
-                if (err == HPTT_SUCCESS && hipEventElapsedTime(&one, e0, e1) != hipSuccess)
+                if (err == HPTT_SUCCESS && hipEventElapsedTime(&ms[r], e0, e1) != hipSuccess)
                     err = HPTT_ERROR_HIP;
-                if (r == 0 || one < ms) ms = one;  // best of three
             }
             if (err != HPTT_SUCCESS) break;
+            const float m = median3(ms[0], ms[1], ms[2]);
             ++timed;
-            if (c == 0 && report) report->default_ms = ms;
-            if (timed == 1 || ms < bestMs) {
-                bestMs = ms;
+            if (c == 0) {
+                quickMs = bestMs = m;
+            } else if (m < bestMs && m < kMargin * quickMs) {
+                bestMs = m;
                 best = cand[c];
             }
             const double elapsed = std::chrono::duration<double>(clock::now() - t0).count();
@@ -210,7 +260,10 @@ hptt_status_t autotune(hptt_plan_t* planOut, const int32_t* perm, int32_t N, con
         if (report) {
             report->candidates = nc;
             report->timed = timed;
+            report->default_ms = quickMs;
             report->best_ms = bestMs;
+            report->flushed = flush ? 1 : 0;
+            report->own_mode = ownMode ? 1 : 0;
         }
         std::lock_guard<std::mutex> lock(g_mutex);
         g_wisdom[key] = best;

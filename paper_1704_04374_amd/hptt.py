@@ -46,12 +46,14 @@ class Options(ctypes.Structure):
 class AutotuneReport(ctypes.Structure):
     """hptt_autotune_report_t"""
     _fields_ = [("candidates", ctypes.c_int32), ("timed", ctypes.c_int32),
-                ("from_cache", ctypes.c_int32), ("default_ms", ctypes.c_float),
+                ("from_cache", ctypes.c_int32), ("flushed", ctypes.c_int32),
+                ("own_mode", ctypes.c_int32), ("default_ms", ctypes.c_float),
                 ("best_ms", ctypes.c_float), ("options", Options)]
 
     def as_dict(self) -> dict:
         return {"candidates": self.candidates, "timed": self.timed,
-                "from_cache": bool(self.from_cache), "default_ms": self.default_ms,
+                "from_cache": bool(self.from_cache), "flushed": bool(self.flushed),
+                "own_mode": bool(self.own_mode), "default_ms": self.default_ms,
                 "best_ms": self.best_ms,
                 "options": {name: getattr(self.options, name) for name, _ in Options._fields_}}
 

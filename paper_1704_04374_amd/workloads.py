@@ -140,6 +140,42 @@ def inputs(w: Workload):
     return A, B
 
 
+# The paper's benchmark: 57 transpositions of 2-D to 6-D tensors of roughly
+# 200 MB each, single precision, reported for beta != 0 unless stated
+# (Section 4).  Its case list is not printed; this seeded generator stands in
+# for it with the same dimension range, tensor size and precision.
+SWEEP_DIMS = {2: 5, 3: 10, 4: 14, 5: 14, 6: 14}      # 57 cases
+SWEEP_BYTES = 200 * 1000 * 1000
+
+
+def sweep57(seed: int = 1704, beta: float = 1.0, alpha: float = 1.0) -> list:
+    """57 seeded fp32 workloads, ``SWEEP_BYTES`` per tensor (within 3 %).
+    Extents are log-uniform shares of the element count (every extent >= 2,
+    so each index is a real one and small leading extents occur); perms are
+    uniform over the non-identity permutations, so the stride-1 index is
+    kept in about 1/N of the cases."""
+    rng = np.random.default_rng(seed)
+    target = SWEEP_BYTES // 4
+    out = []
+    for n, count in SWEEP_DIMS.items():
+        for c in range(count):
+            while True:
+                w = rng.dirichlet(np.ones(n))
+                ext = [max(2, int(round(target ** x))) for x in w]
+                ext[-1] = max(2, int(round(target / prod(ext[:-1]))))
+                if abs(prod(ext) / target - 1) <= 0.03:
+                    break
+            while True:
+                perm = tuple(int(p) for p in rng.permutation(n))
+                if perm != tuple(range(n)):
+                    break
+            name = f"sweep{n}d_{c:02d}_" + "x".join(map(str, ext)) + "_p" + "".join(map(str, perm))
+            out.append(Workload(name, "f32", tuple(ext), perm, alpha, beta,
+                                seed * 1000 + len(out), None if beta == 0 else seed * 1000 + 500
+                                + len(out)))
+    return out
+
+
 def random_problem(rng: np.random.Generator, max_dims: int = 6,
                    extents=(1, 2, 3, 5, 7, 17, 33, 64, 65), max_numel: int = 1 << 20):
     """A random (size_a, perm) pair for sweeps, with at most ``max_numel`` elements."""

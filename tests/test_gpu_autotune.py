@@ -48,7 +48,8 @@ def test_autotune_full_size(name):
     torch.cuda.synchronize()
     _say(f"[autotune] {rep}")
     assert rep["candidates"] >= 1 and 1 <= rep["timed"] <= rep["candidates"]
-    assert not rep["from_cache"]
+    assert not rep["from_cache"] and rep["flushed"]
+    assert rep["own_mode"] == (w.beta == 0)     # beta = 0: timed into a scratch tensor
     assert 0 < rep["best_ms"] <= rep["default_ms"]
     assert np.array_equal(_bits(dA), a_bits) and np.array_equal(_bits(dB), b_bits)
     plan.exec(dA, dB)
@@ -87,6 +88,7 @@ def test_autotune_small_problems_and_sub_tensors():
         plan, rep = hptt.autotune_plan(perm, size_a, dA, dB, alpha, beta, dtype, timeout=0.2,
                                        outer_size_a=outer_a, outer_size_b=outer_b)
         torch.cuda.synchronize()
+        assert rep["own_mode"] == (beta == 0) and rep["flushed"], rep
         assert np.array_equal(dB.cpu().numpy().view(np.uint8), B0.view(np.uint8)), rep
         assert np.array_equal(dA.cpu().numpy().view(np.uint8), A.view(np.uint8))
         plan.exec(dA, dB)
