@@ -5,6 +5,8 @@ sizes as a dry run of bounds, alignment and coverage -- before any of them
 is timed on a GPU."""
 from __future__ import annotations
 
+import itertools
+
 import numpy as np
 import pytest
 
@@ -113,11 +115,14 @@ def test_every_candidate_full_size_dry_run(w):
                                      w.outer_a, w.outer_b)
     rng = np.random.default_rng(len(cands))
     whole = set(int(i) for i in rng.choice(len(cands), size=min(3, len(cands)), replace=False))
-    for i, c in enumerate(cands):
-        p = emu.plan(w.perm, w.size_a, 0.0, 1.0, w.dtype, outer_size_a=w.outer_a,
+    # the tuner times beta = 0 plans as they are (into a scratch tensor) and
+    # others with alpha = 0, beta = 1 (also beta = 0 plans when it has no
+    # memory for the scratch tensor)
+    modes = ([(w.alpha, w.beta)] if w.beta == 0 else []) + [(0.0, 1.0)]
+    for (i, c), (j, (alpha, beta)) in itertools.product(enumerate(cands), enumerate(modes)):
+        p = emu.plan(w.perm, w.size_a, alpha, beta, w.dtype, outer_size_a=w.outer_a,
                      outer_size_b=w.outer_b, **_knobs(c))
-        grid = p.info["grid"]
-        stride = 1 if i in whole else max(1, grid // 97)
+        stride = 1 if (i in whole and j == 0) else max(1, p.info["grid"] // 97)
         err, msg, cnt = emu.run(p, counts=True, block_stride=stride)
         assert err == 0, f"{c}: {p.describe()}: {msg}"
         assert cnt.max() <= 1, f"{c}: {p.describe()}"
