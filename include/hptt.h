@@ -172,7 +172,7 @@ typedef struct {
     int32_t candidates;      /* distinct plans generated */
     int32_t timed;           /* plans timed before the timeout */
     int32_t from_cache;      /* 1 when the problem was tuned earlier in this process */
-    int32_t flushed;         /* 1 when each timed launch started with cold caches */
+    int32_t flushed;         /* 1 when launches were timed cold, with their write-backs */
     int32_t own_mode;        /* 1 when beta = 0 plans were timed writing a scratch tensor */
     float default_ms;        /* the quick path's plan, median of three launches */
     float best_ms;           /* the chosen plan, median of three launches */
@@ -187,15 +187,18 @@ typedef struct {
  * knobs for the given alpha and beta (the quick path's plan unless another
  * is at least 1 % faster).  Each plan is timed in the update mode it will
  * run in, as the median of three launches that each start after a 512 MiB
- * read has evicted the tensors from the caches.  The caller's data are not
+ * read has evicted the tensors from the caches; each timed span also holds a
+ * second such read, which writes back what the launch left dirty in the
+ * caches (its clean time is subtracted), so that plans whose stores stay in
+ * the caches are charged for them as in back-to-back use.  The caller's data are not
  * changed: with beta != 0 timing runs, like the paper's, with alpha = 0 and
  * beta = 1, so B is rewritten with its own value and A is read and multiplied
  * by zero (A must then hold no inf or NaN, footnote 5, and a -0.0 in B may
  * come back as +0.0); with beta = 0 the plans write a scratch tensor and B is
  * not touched.  The scratch memory (the flush buffer and, for beta = 0, a
  * tensor of B's footprint) is allocated for the call and freed before it
- * returns; without it, timing falls back to warm caches and the paper's
- * alpha = 0, beta = 1 on B.  The chosen plan is cached per problem (perm,
+ * returns; without it, timing falls back to bursts of four back-to-back
+ * launches and the paper's alpha = 0, beta = 1 on B.  The chosen plan is cached per problem (perm,
  * extents, outer sizes, dtype, update mode, device) for the life of the
  * process; a cached problem returns at once without launching anything.
  *

@@ -43,6 +43,8 @@ def _compile(src: str) -> str:
     cmd = [hipcc(), *COMMON, "-c", os.path.join(CSRC, src), "-o", obj]
     if src.endswith(".hip"):
         cmd[1:1] = ["-x", "hip", *HIP_ONLY]
+    else:  # host code only: no device pass
+        cmd[1:1] = ["-x", "hip", f"--offload-arch={ARCH}", "--offload-host-only"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compiling {src} failed:\n{' '.join(cmd)}\n{r.stdout}{r.stderr}")

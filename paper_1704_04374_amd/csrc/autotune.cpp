@@ -135,6 +135,7 @@ namespace {
 
 constexpr size_t kFlushBytes = size_t(512) << 20;  // two last-level caches (256 MB each)
 constexpr int kReps = 3;
+constexpr int kBurst = 4;
 constexpr float kMargin = 0.99f;  // leave the quick plan only for a 1 % gain
 
 // Device memory the tuner borrows for its measurements and returns at the end.
@@ -215,35 +216,50 @@ hptt_status_t autotune(hptt_plan_t* planOut, const int32_t* perm, int32_t N, con
         hipEvent_t e0, e1;
         if (hipEventCreate(&e0) != hipSuccess) return HPTT_ERROR_HIP;
         if (hipEventCreate(&e1) != hipSuccess) {
-            hipEventDestroy(e0);
+            (void)hipEventDestroy(e0);
             return HPTT_ERROR_HIP;
         }
+        // One measurement: [flush] e0 launch(es) [flush] e1.  The second flush
+        // is inside the timed span: it writes back the lines the launch left
+        // dirty in the caches, a cost a lone launch with write-back stores
+        // would hide and back-to-back launches pay.  Its clean time is
+        // measured alone and subtracted.  Without flush memory: kBurst
+        // launches back to back.
+        auto span = [&](hptt_plan_s* tp, float* ms) -> hptt_status_t {
+            hptt_status_t e = HPTT_SUCCESS;
+            if (flush) e = hptt_yardstick_read(scratch.flush, kFlushBytes, scratch.sink, stream);
+            if (e == HPTT_SUCCESS && hipEventRecord(e0, stream) != hipSuccess) e = HPTT_ERROR_HIP;
+            for (int b = 0; b < (flush ? 1 : kBurst) && e == HPTT_SUCCESS; ++b)
+                if (tp) e = hptt_exec(tp, A, target, stream);
+            if (e == HPTT_SUCCESS && flush)
+                e = hptt_yardstick_read(scratch.flush, kFlushBytes, scratch.sink, stream);
+            if (e == HPTT_SUCCESS && hipEventRecord(e1, stream) != hipSuccess) e = HPTT_ERROR_HIP;
+            if (e == HPTT_SUCCESS && hipEventSynchronize(e1) != hipSuccess) e = HPTT_ERROR_HIP;
+            if (e == HPTT_SUCCESS && hipEventElapsedTime(ms, e0, e1) != hipSuccess)
+                e = HPTT_ERROR_HIP;
+            return e;
+        };
+        auto measure = [&](hptt_plan_s* tp, float* out) -> hptt_status_t {
+            float ms[kReps] = {};
+            hptt_status_t e = HPTT_SUCCESS;
+            for (int r = 0; r < kReps && e == HPTT_SUCCESS; ++r) e = span(tp, &ms[r]);
+            *out = median3(ms[0], ms[1], ms[2]);
+            return e;
+        };
         const auto t0 = clock::now();
-        float bestMs = 0.f, quickMs = 0.f;
-        hptt_status_t err = HPTT_SUCCESS;
+        float bestMs = 0.f, quickMs = 0.f, flushMs = 0.f;
+        hptt_status_t err = flush ? measure(nullptr, &flushMs) : HPTT_SUCCESS;
         int timed = 0;
         for (int c = 0; c < nc && err == HPTT_SUCCESS; ++c) {
             hptt_plan_s tp;
             if (build_plan(perm, N, sizeA, outerA, outerB, tAlpha, tBeta, dtype, &cand[c], &tp) !=
                 HPTT_SUCCESS)
                 continue;
-            float ms[kReps] = {};
             err = hptt_exec(&tp, A, target, stream);  // warm-up
-            for (int r = 0; r < kReps && err == HPTT_SUCCESS; ++r) {
-                if (flush)
-                    err = hptt_yardstick_read(scratch.flush, kFlushBytes, scratch.sink, stream);
-                if (err == HPTT_SUCCESS && hipEventRecord(e0, stream) != hipSuccess)
-                    err = HPTT_ERROR_HIP;
-                if (err == HPTT_SUCCESS) err = hptt_exec(&tp, A, target, stream);
-                if (err == HPTT_SUCCESS && hipEventRecord(e1, stream) != hipSuccess)
-                    err = HPTT_ERROR_HIP;
-                if (err == HPTT_SUCCESS && hipEventSynchronize(e1) != hipSuccess)
-                    err = HPTT_ERROR_HIP;
-                if (err == HPTT_SUCCESS && hipEventElapsedTime(&ms[r], e0, e1) != hipSuccess)
-                    err = HPTT_ERROR_HIP;
-            }
+            float m = 0.f;
+            if (err == HPTT_SUCCESS) err = measure(&tp, &m);
             if (err != HPTT_SUCCESS) break;
-            const float m = median3(ms[0], ms[1], ms[2]);
+            m = flush ? m - flushMs : m / kBurst;
             ++timed;
             if (c == 0) {
                 quickMs = bestMs = m;
@@ -254,8 +270,8 @@ hptt_status_t autotune(hptt_plan_t* planOut, const int32_t* perm, int32_t N, con
             const double elapsed = std::chrono::duration<double>(clock::now() - t0).count();
             if (elapsed >= timeoutSeconds) break;
         }
-        hipEventDestroy(e0);
-        hipEventDestroy(e1);
+        (void)hipEventDestroy(e0);
+        (void)hipEventDestroy(e1);
         if (err != HPTT_SUCCESS) return err;
         if (report) {
             report->candidates = nc;
