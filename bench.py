@@ -405,6 +405,55 @@ def run_sweep(torch, hptt, args, flush_buf, sink) -> dict:
             "cases": cases}
 
 
+def run_contractions(torch, args) -> dict:
+    """Contractions by transposition - GEMM - transposition against
+    torch.einsum on the same tensors (the speedup of Eq. 3, with einsum in
+    the role of the framework without this library's transpositions)."""
+    from paper_1704_04374_amd.contraction import Contraction
+    from paper_1704_04374_amd.workloads import CONTRACTIONS
+    tdt = {"f32": torch.float32, "f64": torch.float64}
+    out = []
+    for w in CONTRACTIONS:
+        gen = torch.Generator(device="cuda").manual_seed(w.seed + 1)
+        A = torch.rand(w.numel(w.modes_a), dtype=tdt[w.dtype], device="cuda", generator=gen)
+        B = torch.rand(w.numel(w.modes_b), dtype=tdt[w.dtype], device="cuda", generator=gen)
+        C = torch.zeros(w.numel(w.modes_c), dtype=tdt[w.dtype], device="cuda")
+        t0 = time.perf_counter()
+        p = Contraction(w.modes_c, w.modes_a, w.size(w.modes_a), w.modes_b, w.size(w.modes_b),
+                        w.alpha, w.beta, w.dtype)
+        plan_us = (time.perf_counter() - t0) * 1e6
+        p.workspace()
+        # torch's view of a Fortran tensor: the same memory, modes reversed
+        ta = A.view(*reversed(w.size(w.modes_a)))
+        tb = B.view(*reversed(w.size(w.modes_b)))
+        eq = f"{w.modes_a[::-1]},{w.modes_b[::-1]}->{w.modes_c[::-1]}"
+
+        def ours(i):
+            p.exec(A, B, C)
+
+        def theirs(i):
+            torch.einsum(eq, ta, tb).contiguous()
+
+        steps = max(5, args.steps // 10)
+        ms_ours = time_launches(torch, ours, steps, 3)[1]
+        ms_theirs = time_launches(torch, theirs, steps, 3)[1]
+        info = p.info
+        r = {"contraction": w.name, "spec": w.spec, "dtype": w.dtype, "plan": p.describe(),
+             "plan_create_us": round(plan_us, 1), "ms": round(ms_ours, 4),
+             "einsum_ms": round(ms_theirs, 4), "speedup_vs_einsum": round(ms_theirs / ms_ours, 3),
+             "tflops": round(info["flops"] / ms_ours / 1e9, 2),
+             "einsum_tflops": round(info["flops"] / ms_theirs / 1e9, 2),
+             "transposed_bytes": int(info["bytes_transposed"])}
+        out.append(r)
+        print(f"[contract] {w.name}: {r['ms']:.3f} ms ({r['tflops']} TFLOP/s) vs einsum "
+              f"{r['einsum_ms']:.3f} ms: x{r['speedup_vs_einsum']}", file=sys.stderr, flush=True)
+        del A, B, C, p
+        torch.cuda.empty_cache()
+    sp = [r["speedup_vs_einsum"] for r in out]
+    return {"contractions": out, "speedup_vs_einsum": {
+        "mean": round(statistics.mean(sp), 3), "max": max(sp), "min": min(sp)}}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -419,6 +468,8 @@ def main():
                     help="also tune each named workload for this long (0: skip)")
     ap.add_argument("--sweep", action="store_true",
                     help="run the 57-case sweep instead and print its summary as JSON")
+    ap.add_argument("--contractions", action="store_true",
+                    help="time the contraction workloads against torch.einsum instead")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     ap.add_argument("--summarize-trace", metavar="TRACE_DIR")
     ap.add_argument("--pmc-command", default="")
@@ -462,6 +513,9 @@ def main():
     preheat(torch, hptt)
     if args.sweep:
         print(json.dumps(run_sweep(torch, hptt, args, flush_buf, sink)), flush=True)
+        return 0
+    if args.contractions:
+        print(json.dumps(run_contractions(torch, args)), flush=True)
         return 0
     headline = measure_workload(torch, hptt, head, args.steps, args.warmup, args.reps, flush_buf,
                                 sink, full=not args.only_headline,

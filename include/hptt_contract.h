@@ -21,10 +21,10 @@
  * ordered [rows, columns, batch] or [columns, rows, batch].  Among the
  * layouts that qualify, the plan picks the one that moves the fewest bytes.
  *
- * Ownership: plans are opaque, immutable after creation and own their
- * transposition plans and their rocBLAS handle (created at the first
- * execution on the device current then).  The caller owns all tensors and
- * the workspace.
+ * Ownership: plans are opaque and own their transposition plans and their
+ * rocBLAS handle, which the first execution creates on the device current
+ * then (and an execution on another device replaces); execute a plan from
+ * one host thread at a time.  The caller owns all tensors and the workspace.
  */
 #ifndef HPTT_CONTRACT_H
 #define HPTT_CONTRACT_H
@@ -47,9 +47,17 @@ typedef struct {
     int32_t transpose_b;      /* 1: B is transposed into the workspace first */
     int32_t transpose_c;      /* 1: the product goes to the workspace, then is transposed into C */
     int32_t swap;             /* 1: the product is formed as C^T = B^T A^T */
-    int32_t op_p;             /* 1: the first GEMM operand is read transposed */
-    int32_t op_q;             /* 1: the second GEMM operand is read transposed */
+    int32_t op_p;             /* 1: the first GEMM operand (A, or B when swapped) is read
+                                 transposed: stored [K, X, L] instead of [X, K, L] */
+    int32_t op_q;             /* 1: the second GEMM operand is read transposed: stored
+                                 [Y, K, L] instead of [K, Y, L] */
     int64_t gemm_m, gemm_n, gemm_k, batch;   /* GEMM shape (column-major) and batch count */
+    int64_t ld_p, ld_q, ld_c;                 /* leading dimensions of the GEMM operands */
+    int64_t stride_p, stride_q, stride_c;     /* elements between batch entries */
+    char modes_x[17];         /* GEMM rows (M modes, or N modes when swapped), in order */
+    char modes_y[17];         /* GEMM columns */
+    char modes_k[17];         /* contracted modes */
+    char modes_l[17];         /* batch modes */
     int64_t workspace_bytes;  /* device workspace hptt_contraction_exec needs */
     double flops;             /* 2 * m * n * k * batch */
     double bytes_transposed;  /* bytes read and written by the transpositions */

@@ -68,6 +68,41 @@ def contract(A: np.ndarray, modes_a: str, size_a, B: np.ndarray, modes_b: str, s
     return np.asarray(out).reshape(-1, order="F")
 
 
+def contract_sample(A: np.ndarray, modes_a: str, size_a, B: np.ndarray, modes_b: str, size_b,
+                    modes_c: str, offsets_c, alpha: float = 1.0, beta: float = 0.0,
+                    C: np.ndarray | None = None):
+    """(value, magnitude) of C at the given Fortran offsets of C, each
+    computed on its own from the definition: split the offset into C's
+    mode indices, fix those modes in A and B, and sum the products over the
+    contracted modes (for tensors too large to contract whole on the CPU)."""
+    ext = extents(modes_a, size_a, modes_b, size_b)
+    size_c = [ext[m] for m in modes_c]
+    ta, tb = _tensor(A, size_a), _tensor(B, size_b)
+    con = "".join(m for m in modes_a if m in modes_b and m not in modes_c)
+    vals, mags = [], []
+    for off in np.asarray(offsets_c, dtype=np.int64):
+        idx, rest = {}, int(off)
+        for m, n in zip(modes_c, size_c):
+            idx[m] = rest % n
+            rest //= n
+        sa = tuple(idx.get(m, slice(None)) for m in modes_a)
+        sb = tuple(idx.get(m, slice(None)) for m in modes_b)
+        ra = "".join(m for m in modes_a if m not in idx)
+        rb = "".join(m for m in modes_b if m not in idx)
+        xa, xb = ta[sa], tb[sb]
+        dot = float(np.einsum(f"{ra},{rb}->", xa, xb, optimize=False)) if con else float(xa * xb)
+        mag = (float(np.einsum(f"{ra},{rb}->", np.abs(xa), np.abs(xb), optimize=False)) if con
+               else float(abs(xa * xb)))
+        v, g = float(alpha) * dot, abs(float(alpha)) * mag
+        if beta != 0:
+            c0 = float(np.asarray(C, dtype=np.float64)[off])
+            v += float(beta) * c0
+            g += abs(float(beta)) * abs(c0)
+        vals.append(v)
+        mags.append(g)
+    return np.array(vals), np.array(mags)
+
+
 def magnitude(A: np.ndarray, modes_a: str, size_a, B: np.ndarray, modes_b: str, size_b,
               modes_c: str, alpha: float = 1.0, beta: float = 0.0,
               C: np.ndarray | None = None) -> np.ndarray:

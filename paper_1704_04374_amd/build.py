@@ -19,6 +19,10 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libhptt.so")
+# Contractions (transposition - GEMM - transposition) link rocBLAS, so they
+# live in a library of their own on top of libhptt.so.
+CONTRACT_LIB = os.path.join(PKG, "libhptt_contract.so")
+CONTRACT_SOURCES = ["contract.cpp"]
 
 ARCH = "gfx950"
 SOURCES = ["kernels.hip", "yardstick.hip", "api.cpp", "plan.cpp", "autotune.cpp"]
@@ -62,8 +66,18 @@ def build(verbose: bool = False) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"linking libhptt.so failed:\n{' '.join(cmd)}\n{r.stdout}{r.stderr}")
     os.replace(tmp, LIB)
+    with cf.ThreadPoolExecutor(max_workers=len(CONTRACT_SOURCES)) as ex:
+        cobjs = list(ex.map(_compile, CONTRACT_SOURCES))
+    tmp = CONTRACT_LIB + ".tmp"
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *cobjs, "-o", tmp, f"-L{PKG}",
+           "-lhptt", "-lrocblas", "-Wl,-rpath,$ORIGIN"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"linking libhptt_contract.so failed:\n{' '.join(cmd)}\n"
+                           f"{r.stdout}{r.stderr}")
+    os.replace(tmp, CONTRACT_LIB)
     if verbose:
-        print(f"built {LIB}")
+        print(f"built {LIB} and {CONTRACT_LIB}")
     return LIB
 
 

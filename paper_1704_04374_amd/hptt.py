@@ -24,6 +24,7 @@ KERNEL_IDS = {v: k for k, v in KERNELS.items()}
 MODES = {0: "copy", 1: "scale", 2: "axpby"}
 
 SUCCESS = 0
+HIP_ERROR = 5
 STATUS = {0: "HPTT_SUCCESS", 1: "HPTT_ERROR_INVALID_ARGUMENT", 2: "HPTT_ERROR_UNSUPPORTED",
           3: "HPTT_ERROR_OVERLAP", 4: "HPTT_ERROR_OUT_OF_MEMORY", 5: "HPTT_ERROR_HIP"}
 
@@ -260,7 +261,7 @@ class Plan:
             stream = stream.cuda_stream
         st = self._lib.hptt_exec(self._handle, ctypes.c_void_p(a), ctypes.c_void_p(b),
                                  ctypes.c_void_p(stream))
-        if st == 5:
+        if st == HIP_ERROR:
             raise HpttError(st, f"hptt_exec (hipError {self._lib.hptt_last_hip_error()})")
         _check(st, "hptt_exec")
 

@@ -176,6 +176,62 @@ def sweep57(seed: int = 1704, beta: float = 1.0, alpha: float = 1.0) -> list:
     return out
 
 
+@dataclass(frozen=True)
+class ContractionWorkload:
+    """C[modes_c] = alpha * A[modes_a] . B[modes_b] + beta * C (Fortran order)."""
+    name: str
+    modes_c: str
+    modes_a: str
+    modes_b: str
+    extents: tuple           # ((mode, extent), ...)
+    dtype: str = "f64"
+    alpha: float = 1.0
+    beta: float = 0.0
+    seed: int = 0
+
+    def ext(self) -> dict:
+        return dict(self.extents)
+
+    def size(self, modes: str) -> tuple:
+        e = self.ext()
+        return tuple(e[m] for m in modes)
+
+    def numel(self, modes: str) -> int:
+        return prod(self.size(modes))
+
+    @property
+    def spec(self) -> str:
+        return f"{self.modes_c}={self.modes_a}*{self.modes_b}"
+
+    @property
+    def flops(self) -> int:
+        e = self.ext()
+        return 2 * prod(e[m] for m in set(self.modes_a) | set(self.modes_b))
+
+
+def _cw(name, spec, dtype="f64", **ext):
+    c, ab = spec.split("=")
+    a, b = ab.split("*")
+    return ContractionWorkload(name, c, a, b, tuple(sorted(ext.items())), dtype)
+
+
+# Contractions standing in for the tensor-contraction experiment of Section
+# 4.1 (double precision, like Fig. 9), whose case list is not in the paper:
+# from bandwidth-bound (few contracted elements, large C) to compute-bound
+# (long contractions), plus a pure matrix product that needs no transposition.
+CONTRACTIONS = [
+    _cw("abcd_aebf_dfce", "abcd=aebf*dfce", a=72, b=72, c=72, d=72, e=4, f=4),
+    _cw("abcd_ebad_ce", "abcd=ebad*ce", a=48, b=48, c=256, d=48, e=16),
+    _cw("abc_bda_dc", "abc=bda*dc", a=512, b=256, c=256, d=24),
+    _cw("abcde_efbad_cf", "abcde=efbad*cf", a=24, b=24, c=96, d=24, e=24, f=32),
+    _cw("abcd_dbea_ec", "abcd=dbea*ec", a=96, b=64, c=96, d=64, e=64),
+    _cw("ab_acd_dbc", "ab=acd*dbc", a=2048, b=2048, c=64, d=64),
+    _cw("abc_adec_ebd", "abc=adec*ebd", a=96, b=96, c=96, d=96, e=96),
+    _cw("ij_ik_kj", "ij=ik*kj", i=4096, j=4096, k=4096),
+]
+CONTRACTIONS_BY_NAME = {w.name: w for w in CONTRACTIONS}
+
+
 def random_problem(rng: np.random.Generator, max_dims: int = 6,
                    extents=(1, 2, 3, 5, 7, 17, 33, 64, 65), max_numel: int = 1 << 20):
     """A random (size_a, perm) pair for sweeps, with at most ``max_numel`` elements."""

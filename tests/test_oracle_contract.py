@@ -106,6 +106,22 @@ def test_identity_contraction_is_a_transposition():
     assert np.array_equal(got, want)
 
 
+@pytest.mark.parametrize("case", CASES, ids=lambda c: f"{c[0]}*{c[2]}->{c[4]}")
+def test_sample_agrees_with_whole_contraction(case):
+    """The one-element-at-a-time definition against the whole-tensor one."""
+    ma, sa, mb, sb, mc = case
+    rng = np.random.default_rng(11)
+    A, B = _rand(rng, int(np.prod(sa))), _rand(rng, int(np.prod(sb)))
+    ext = oc.extents(ma, sa, mb, sb)
+    nc = int(np.prod([ext[m] for m in mc]))
+    C = _rand(rng, nc)
+    whole = oc.contract(A, ma, sa, B, mb, sb, mc, -1.25, 0.5, C)
+    mag = oc.magnitude(A, ma, sa, B, mb, sb, mc, -1.25, 0.5, C)
+    offs = np.arange(nc)
+    vals, mags = oc.contract_sample(A, ma, sa, B, mb, sb, mc, offs, -1.25, 0.5, C)
+    assert np.array_equal(vals, whole) and np.array_equal(mags, mag)
+
+
 def test_linearity_in_alpha_and_beta():
     rng = np.random.default_rng(4)
     sa, sb = (3, 4, 2), (4, 5)

@@ -14,14 +14,19 @@ from paper_1704_04374_amd import hptt
 from paper_1704_04374_amd.workloads import WORKLOADS, BY_NAME
 
 
-def _declared_functions():
+def _declared_functions(headers=("hptt.h", "hptt_yardstick.h")):
     names = set()
-    for path in glob.glob(os.path.join(ROOT, "include", "*.h")):
-        text = open(path).read()
+    for name in headers:
+        text = open(os.path.join(ROOT, "include", name)).read()
         text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
         text = re.sub(r"//[^\n]*", "", text)
         names.update(re.findall(r"\b(hptt_[a-z0-9_]+)\s*\(", text))
     return names
+
+
+def test_every_header_is_checked():
+    assert sorted(os.path.basename(p) for p in glob.glob(os.path.join(ROOT, "include", "*.h"))) \
+        == ["hptt.h", "hptt_contract.h", "hptt_yardstick.h"]
 
 
 def test_library_exports_every_declared_symbol():
@@ -31,6 +36,16 @@ def test_library_exports_every_declared_symbol():
     for name in sorted(declared):
         assert hasattr(lib, name), f"{name} declared but not exported"
     assert declared == set(hptt.EXPORTS)
+
+
+def test_contraction_library_exports_every_declared_symbol():
+    from paper_1704_04374_amd import contraction
+    lib = ctypes.CDLL(contraction.LIB_PATH)
+    declared = _declared_functions(("hptt_contract.h",))
+    assert declared
+    for name in sorted(declared):
+        assert hasattr(lib, name), f"{name} declared but not exported"
+    assert declared == set(contraction.EXPORTS)
 
 
 def test_status_strings():
