@@ -87,6 +87,10 @@ typedef struct {
                               where runs then do not start on 128-byte lines */
     int32_t row_passes;    /* TILE: N > 1 = stage each tile through LDS in N passes
                               over its rows (less LDS, one more barrier per pass) */
+    int32_t depth;         /* TILE: tiles stacked per workgroup along one more index;
+                              0 = as many as a small tile needs, 1 = none */
+    int32_t min_tile;      /* TILE: smallest tile (elements) worth a workgroup round;
+                              smaller tiles get longer runs or depth; 0 = 16 KiB worth */
 } hptt_options_t;
 
 /* What the plan builder decided; for inspection and tests. */
@@ -101,7 +105,8 @@ typedef struct {
     int64_t run_b;                     /* TILE: B-run (rows); STREAM: kept row length */
     int32_t dims_a;                    /* TILE: fused A indices inside the A run */
     int32_t dims_b;                    /* TILE: fused B positions inside the B run */
-    int32_t vec_a;                     /* vector width of A accesses for 16-byte aligned bases */
+    int32_t vec_a;                     /* vector width of A accesses (TILE: runs that start
+                                          off the vector grid are shifted onto it) */
     int32_t vec_b;                     /* vector width of B accesses */
     int32_t lds_pitch;                 /* TILE: LDS row pitch in elements */
     int32_t rows_per_pass;             /* TILE: tile rows staged through LDS at once */
@@ -117,6 +122,7 @@ typedef struct {
     int32_t mode;                      /* 0 raw copy, 1 scale (beta = 0), 2 alpha*A + beta*B */
     int32_t tile_order;                /* TILE: 1 grid-digit order, 2 diagonal, 3 diagonal
                                           with contiguous tile ranges per XCD */
+    int32_t depth;                     /* TILE: tiles stacked per workgroup round */
 } hptt_plan_info_t;
 
 /*

@@ -78,26 +78,31 @@ int autotune_candidates(const int32_t* perm, int32_t N, const int64_t* sizeA,
     if (base.info.kernel == HPTT_KERNEL_TILE) {
         const int32_t aBytes[] = {0, 256, 1024, 128};
         const int32_t bBytes[] = {0, 256, 512};
+        // the smallest tile worth a workgroup round: default, twice, none
+        const int32_t minTile[] = {0, 32768 / elem, 1};
         std::vector<std::pair<int, hptt_options_t>> var;
         for (int ia = 0; ia < 4; ++ia)
             for (int ib = 0; ib < 3; ++ib)
                 for (int ord = 0; ord < 2; ++ord)
                     for (int ex = 0; ex < 2; ++ex)
-                        for (int h = 0; h < 5; ++h) {
-                            hptt_options_t v;
-                            memset(&v, 0, sizeof(v));
-                            v.run_a = aBytes[ia] / elem;
-                            v.run_b = bBytes[ib] ? bBytes[ib] / elem : 0;
-                            if (ia == 0 && ib != 0) v.run_a = 512 / elem;
-                            if (ib == 0 && ia != 0) v.run_b = 128 / elem;
-                            v.tile_order = ord ? 1 : 0;
-                            v.exact_runs = ex;
-                            v.store_hint = hintsStore[h];
-                            v.load_hint = hintsLoad[h];
-                            const int changed = (ia != 0) + (ib != 0) + ord + ex + (h != 0);
-                            if (changed) var.push_back({changed, v});
-                        }
-        for (int c = 1; c <= 5; ++c)
+                        for (int mt = 0; mt < 3; ++mt)
+                            for (int h = 0; h < 5; ++h) {
+                                hptt_options_t v;
+                                memset(&v, 0, sizeof(v));
+                                v.run_a = aBytes[ia] / elem;
+                                v.run_b = bBytes[ib] ? bBytes[ib] / elem : 0;
+                                if (ia == 0 && ib != 0) v.run_a = 512 / elem;
+                                if (ib == 0 && ia != 0) v.run_b = 128 / elem;
+                                v.tile_order = ord ? 1 : 0;
+                                v.exact_runs = ex;
+                                v.min_tile = minTile[mt];
+                                v.store_hint = hintsStore[h];
+                                v.load_hint = hintsLoad[h];
+                                const int changed =
+                                    (ia != 0) + (ib != 0) + ord + ex + (mt != 0) + (h != 0);
+                                if (changed) var.push_back({changed, v});
+                            }
+        for (int c = 1; c <= 6; ++c)
             for (auto& pv : var)
                 if (pv.first == c) cand.push_back(pv.second);
     } else if (base.info.kernel == HPTT_KERNEL_STREAM || base.info.kernel == HPTT_KERNEL_AXPBY) {

@@ -68,6 +68,22 @@ struct TileArgs {
     int32_t xcdSplit;    // 1: tile numbers dealt so that each XCD gets a contiguous range
     int32_t alignedA;    // 1 when every A run is whole 128-byte lines (set by the plan builder)
     int32_t subRows;     // rows staged through LDS per pass (runB, or runB / passes)
+    // Depth: nZ tiles that differ only in one more index are staged together
+    // (stacked rows z*subRows + r in LDS), so that tiles of a few hundred
+    // elements still give a workgroup a few thousand.  nZ = 1: no depth.
+    int32_t nZ;
+    int32_t gDepth;      // grid digit that counts chunks of nZ along that index, or -1
+    int64_t zLast;       // extent of that index
+    int64_t zStrideA;    // its stride in A
+    int64_t zStrideB;    // its stride in B
+    FastDiv zRows;       // subRows: splits a stacked row into (depth, row)
+    FastDiv zCols;       // runA: splits a stacked column into (depth, column)
+    // Vector grid.  runsOnGridA = 1 when every A run starts on a multiple of
+    // the A vector width (plan time); misA = element offset of the A base
+    // pointer from that grid (launch time).  Otherwise each run's vectors are
+    // shifted onto the grid, with partial vectors at both ends.  Same for B.
+    int32_t runsOnGridA, runsOnGridB;
+    int32_t misA, misB;
     int64_t cInner, cChunk, cLast;  // valid columns = cInner * min(cChunk, cLast - j*cChunk)
     int64_t rInner, rChunk, rLast;  // valid rows    = rInner * min(rChunk, rLast - j*rChunk)
     FastDiv cExt[kMaxDims];         // tile extents of the A-run indices

@@ -39,10 +39,11 @@ __host__ __device__ __forceinline__ I imin(I a, I b) { return a < b ? a : b; }
 // ---------------------------------------------------------------------------
 
 struct TileBase {
-    int64_t a;          // offset of the tile's first element in A
-    int64_t b;          // offset of the tile's first element in B
-    int64_t validCols;  // columns (A-run elements) inside the tensor
-    int64_t validRows;  // rows (B-run elements) inside the tensor
+    int64_t a;           // offset of the tile's first element in A
+    int64_t b;           // offset of the tile's first element in B
+    int64_t validCols;   // columns (A-run elements) inside the tensor
+    int64_t validRows;   // rows (B-run elements) inside the tensor
+    int64_t validDepth;  // stacked tiles inside the tensor
 };
 
 // Split the tile number into grid digits (fastest first).  With g.skew the
@@ -65,6 +66,7 @@ __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
     tb.b = 0;
     tb.validCols = g.runA;
     tb.validRows = g.runB;
+    tb.validDepth = g.nZ;
     uint32_t j0 = 0;
     for (int k = 0; k < g.nG; ++k) {
         uint32_t q = fast_div(t, g.gExt[k]);
@@ -81,6 +83,7 @@ __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
         tb.b += j * g.gStrideB[k];
         if (k == g.gChunkC) tb.validCols = g.cInner * imin(g.cChunk, g.cLast - j * g.cChunk);
         if (k == g.gChunkR) tb.validRows = g.rInner * imin(g.rChunk, g.rLast - j * g.rChunk);
+        if (k == g.gDepth) tb.validDepth = imin(int64_t(g.nZ), g.zLast - j * g.nZ);
     }
     return tb;
 }
@@ -117,118 +120,159 @@ __host__ __device__ inline void tile_tables(const TileArgs& g, int tid, int64_t*
 // 16 measured within noise of each other on MI355X; 8 was best on average).
 constexpr int kBatch = 8;
 
-// Load phase of the pass over tile rows [r0, r0 + subRows): the tile's rows
-// are contiguous runs of A.  Thread tid takes the vectors tid, tid + kBlock,
-// ... of the (row, vector) space, vector fastest, so a wave reads whole runs.
-// The vectors land in LDS at [row - r0][column].
+// Load phase of the pass over tile rows [r0, r0 + subRows) of each of the
+// nZ stacked tiles: the rows are contiguous runs of A.  Stacked row R holds
+// row r = R mod subRows of depth z = R / subRows and lands in LDS row R.
+// Thread tid takes the vectors tid, tid + kBlock, ... of the (stacked row,
+// vector) space, vector fastest, so a wave reads whole runs.  Vectors sit on
+// the A vector grid: a run that starts off it is covered by one more vector,
+// its first and last ones partial (element loads).
 template <class Mem, typename T, int VA, int HINT>
 __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb, int64_t r0,
                                           int tid, const T* A, T* lds, const int64_t* rowOffA) {
-    const int64_t W = (g.runA + VA - 1) / VA;  // vectors per row
+    const bool shift = !g.runsOnGridA || g.misA != 0;
+    const int64_t W = (g.runA + (shift ? VA - 1 : 0) + VA - 1) / VA;  // vectors per row
     const int64_t rows = imin(int64_t(g.subRows), tb.validRows - r0);  // rows of this pass
-    int64_t r = tid / W, c = tid % W;
-    const int64_t dr = kBlock / W, dc = kBlock % W;
-    while (r < g.subRows) {
+    const int64_t stacked = int64_t(g.nZ) * g.subRows;
+    int64_t R = tid / W, c = tid % W;
+    const int64_t dR = kBlock / W, dc = kBlock % W;
+    while (R < stacked) {
         Vec<T, VA> v[kBatch];
-        int64_t rr[kBatch], cc[kBatch];
+        int64_t at[kBatch], cc[kBatch];
+        bool ok[kBatch];
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
-            rr[u] = r;
-            cc[u] = c * VA;
-            if (r < rows && cc[u] < tb.validCols) {
-                const int64_t off = tb.a + Mem::template lds_ld<int64_t>(rowOffA, r0 + r) + cc[u];
-                if (cc[u] + VA <= tb.validCols) {
-                    v[u] = Mem::template ld<T, VA, (HINT & kNtLoad) != 0>(A, off);
-                } else {
-                    for (int e = 0; e < VA; ++e)
-                        if (cc[u] + e < tb.validCols) v[u].v[e] = Mem::template ld1<T>(A, off + e);
+            int64_t z = 0, r = R;
+            if (g.nZ > 1) {
+                z = int64_t(fast_div(uint32_t(R), g.zRows));
+                r = R - z * g.subRows;
+            }
+            ok[u] = R < stacked && r < rows && z < tb.validDepth;
+            cc[u] = 0;
+            at[u] = 0;
+            if (ok[u]) {
+                const int64_t start =
+                    tb.a + Mem::template lds_ld<int64_t>(rowOffA, r0 + r) + z * g.zStrideA;
+                const int64_t d = shift ? ((start + g.misA) & (VA - 1)) : 0;
+                cc[u] = c * VA - d;
+                ok[u] = cc[u] + VA > 0 && cc[u] < tb.validCols;
+                at[u] = R * g.pitch + cc[u];
+                if (ok[u]) {
+                    if (cc[u] >= 0 && cc[u] + VA <= tb.validCols) {
+                        v[u] = Mem::template ld<T, VA, (HINT & kNtLoad) != 0>(A, start + cc[u]);
+                    } else {
+                        for (int e = 0; e < VA; ++e)
+                            if (cc[u] + e >= 0 && cc[u] + e < tb.validCols)
+                                v[u].v[e] = Mem::template ld1<T>(A, start + cc[u] + e);
+                    }
                 }
             }
             c += dc;
-            r += dr;
+            R += dR;
             if (c >= W) {
                 c -= W;
-                r += 1;
+                R += 1;
             }
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
-            if (rr[u] < rows && cc[u] < tb.validCols) {
-                const int64_t base = rr[u] * g.pitch + cc[u];
+            if (ok[u]) {
 #pragma unroll
                 for (int e = 0; e < VA; ++e)
-                    if (cc[u] + e < tb.validCols) Mem::template lds_st<T>(lds, base + e, v[u].v[e]);
+                    if (cc[u] + e >= 0 && cc[u] + e < tb.validCols)
+                        Mem::template lds_st<T>(lds, at[u] + e, v[u].v[e]);
             }
         }
     }
 }
 
 // Store phase of the same pass: the tile's columns are contiguous runs of B,
-// of which this pass writes rows [r0, r0 + subRows).  Thread tid takes the
-// vectors tid, tid + kBlock, ... of the (column, vector) space, vector
+// of which this pass writes rows [r0, r0 + subRows).  Stacked column Q is
+// column q = Q mod runA of depth z = Q / runA.  Thread tid takes the vectors
+// tid, tid + kBlock, ... of the (stacked column, vector) space, vector
 // fastest, gathers each vector's VB elements from consecutive LDS rows, and
-// writes it to B (reading B first when beta != 0).
+// writes it to B (reading B first when beta != 0).  Vectors sit on the B
+// vector grid, as in the load phase.
 template <class Mem, typename T, int VB, int MODE, int HINT>
 __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb, int64_t r0,
                                            int tid, T* B, const T* lds, const int64_t* colOffB,
                                            T alpha, T beta) {
-    const int64_t W = (g.subRows + VB - 1) / VB;  // vectors per column in this pass
+    const bool shift = !g.runsOnGridB || g.misB != 0;
+    const int64_t W = (g.subRows + (shift ? VB - 1 : 0) + VB - 1) / VB;  // vectors per column
     const int64_t rows = imin(int64_t(g.subRows), tb.validRows - r0);
-    int64_t q = tid / W, s = tid % W;
-    const int64_t dq = kBlock / W, ds = kBlock % W;
-    while (q < g.runA) {
+    const int64_t cols = int64_t(g.nZ) * g.runA;
+    int64_t Q = tid / W, s = tid % W;
+    const int64_t dQ = kBlock / W, ds = kBlock % W;
+    while (Q < cols) {
         Vec<T, VB> x[kBatch], y[kBatch];
-        int64_t qq[kBatch], ss[kBatch], off[kBatch];
+        int64_t ss[kBatch], off[kBatch];
+        bool ok[kBatch];
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
-            qq[u] = q;
-            ss[u] = s * VB;
+            int64_t z = 0, q = Q;
+            if (g.nZ > 1) {
+                z = int64_t(fast_div(uint32_t(Q), g.zCols));
+                q = Q - z * g.runA;
+            }
+            ok[u] = Q < cols && q < tb.validCols && z < tb.validDepth;
+            ss[u] = 0;
             off[u] = 0;
-            if (q < tb.validCols && ss[u] < rows) {
-                off[u] = tb.b + Mem::template lds_ld<int64_t>(colOffB, q) + r0 + ss[u];
+            if (ok[u]) {
+                const int64_t start =
+                    tb.b + Mem::template lds_ld<int64_t>(colOffB, q) + z * g.zStrideB + r0;
+                const int64_t d = shift ? ((start + g.misB) & (VB - 1)) : 0;
+                ss[u] = s * VB - d;
+                ok[u] = ss[u] + VB > 0 && ss[u] < rows;
+                off[u] = start + ss[u];
+                if (ok[u]) {
+                    const int64_t base = (z * g.subRows + ss[u]) * g.pitch + q;
 #pragma unroll
-                for (int e = 0; e < VB; ++e)
-                    if (ss[u] + e < rows)
-                        x[u].v[e] = Mem::template lds_ld<T>(lds, (ss[u] + e) * g.pitch + q);
-                if (MODE == kAxpby) {
-                    if (ss[u] + VB <= rows) {
-                        y[u] = Mem::template ld<T, VB, false>(B, off[u]);
-                    } else {
-                        for (int e = 0; e < VB; ++e)
-                            if (ss[u] + e < rows) y[u].v[e] = Mem::template ld1<T>(B, off[u] + e);
+                    for (int e = 0; e < VB; ++e)
+                        if (ss[u] + e >= 0 && ss[u] + e < rows)
+                            x[u].v[e] = Mem::template lds_ld<T>(lds, base + e * g.pitch);
+                    if (MODE == kAxpby) {
+                        if (ss[u] >= 0 && ss[u] + VB <= rows) {
+                            y[u] = Mem::template ld<T, VB, false>(B, off[u]);
+                        } else {
+                            for (int e = 0; e < VB; ++e)
+                                if (ss[u] + e >= 0 && ss[u] + e < rows)
+                                    y[u].v[e] = Mem::template ld1<T>(B, off[u] + e);
+                        }
                     }
                 }
             }
             s += ds;
-            q += dq;
+            Q += dQ;
             if (s >= W) {
                 s -= W;
-                q += 1;
+                Q += 1;
             }
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
-            if (qq[u] < tb.validCols && ss[u] < rows) {
-                Vec<T, VB> z;
+            if (ok[u]) {
+                Vec<T, VB> zv;
 #pragma unroll
                 for (int e = 0; e < VB; ++e)
-                    z.v[e] = update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
-                if (ss[u] + VB <= rows) {
-                    Mem::template st<(HINT & kNtStore) != 0, T, VB>(B, off[u], z);
+                    zv.v[e] = update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
+                if (ss[u] >= 0 && ss[u] + VB <= rows) {
+                    Mem::template st<(HINT & kNtStore) != 0, T, VB>(B, off[u], zv);
                 } else {
                     for (int e = 0; e < VB; ++e)
-                        if (ss[u] + e < rows)
-                            Mem::template st1<(HINT & kNtStore) != 0, T>(B, off[u] + e, z.v[e]);
+                        if (ss[u] + e >= 0 && ss[u] + e < rows)
+                            Mem::template st1<(HINT & kNtStore) != 0, T>(B, off[u] + e, zv.v[e]);
                 }
             }
         }
     }
 }
 
-// LDS layout of kernel T: rowOffA[runB], colOffB[runA], then subRows rows of
-// the tile.  A tile with runB > subRows is staged in passes of subRows rows.
+// LDS layout of kernel T: rowOffA[runB], colOffB[runA], then nZ * subRows
+// rows of the tile.  A tile with runB > subRows is staged in passes of
+// subRows rows (never with depth).
 __host__ __device__ inline int64_t tile_lds_bytes(const TileArgs& g, int elem) {
-    return (g.runA + g.runB) * int64_t(sizeof(int64_t)) + int64_t(g.subRows) * g.pitch * elem;
+    return (g.runA + g.runB) * int64_t(sizeof(int64_t)) +
+           int64_t(g.nZ) * g.subRows * g.pitch * elem;
 }
 
 // ---------------------------------------------------------------------------

@@ -222,8 +222,18 @@ template <typename T>
 hptt_status_t launch(const hptt_plan_s* p, const void* A, void* B, hipStream_t stream) {
     const hptt_plan_info_t& in = p->info;
     const int elem = int(sizeof(T));
-    const int va = aligned_width(in.vec_a, reinterpret_cast<uintptr_t>(A), elem);
-    const int vb = aligned_width(in.vec_b, reinterpret_cast<uintptr_t>(B), elem);
+    const uintptr_t pa = reinterpret_cast<uintptr_t>(A), pb = reinterpret_cast<uintptr_t>(B);
+    // The tile kernel keeps its widths and shifts its runs onto the vector
+    // grid of the actual pointers; the others narrow to the pointers' alignment.
+    const bool tile = in.kernel == HPTT_KERNEL_TILE;
+    const int va = tile ? in.vec_a : aligned_width(in.vec_a, pa, elem);
+    const int vb = tile ? in.vec_b : aligned_width(in.vec_b, pb, elem);
+    TileArgs targs;
+    if (tile) {
+        targs = p->tile;
+        targs.misA = int32_t((pa / uintptr_t(elem)) % uintptr_t(va));
+        targs.misB = int32_t((pb / uintptr_t(elem)) % uintptr_t(vb));
+    }
     const void* fn = select_mode<T>(p, va, vb);
     if (!fn) return HPTT_ERROR_INVALID_ARGUMENT;
     const T* a = static_cast<const T*>(A);
@@ -234,7 +244,7 @@ hptt_status_t launch(const hptt_plan_s* p, const void* A, void* B, hipStream_t s
     int64_t numel = in.numel;
     switch (in.kernel) {
         case HPTT_KERNEL_TILE:
-            args[2] = const_cast<TileArgs*>(&p->tile);
+            args[2] = &targs;
             lds = size_t(in.lds_bytes);
             break;
         case HPTT_KERNEL_STREAM:

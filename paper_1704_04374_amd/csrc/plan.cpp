@@ -12,7 +12,8 @@
 namespace hptt {
 
 int64_t tile_lds_bytes_host(const TileArgs& t, int elem) {
-    return (t.runA + t.runB) * int64_t(sizeof(int64_t)) + int64_t(t.subRows) * t.pitch * elem;
+    return (t.runA + t.runB) * int64_t(sizeof(int64_t)) +
+           int64_t(t.nZ) * t.subRows * t.pitch * elem;
 }
 
 namespace {
@@ -21,6 +22,8 @@ constexpr int64_t kLdsMax = 64 * 1024;     // LDS a kernel-T workgroup may use
 constexpr int64_t kLdsBudget = 40 * 1024;  // preferred: at least 4 workgroups per CU
 constexpr int64_t kLine = 128;             // L2 cache line of gfx950
 constexpr int64_t kVecBytes = 16;          // widest global access per lane (dwordx4)
+constexpr int64_t kMinTileBytes = 16 * 1024;  // a workgroup round below this is mostly overhead
+constexpr double kMinGrid = 2048;          // workgroups a larger tile must still leave (8 per CU)
 
 int64_t gcd64(int64_t a, int64_t b) {
     if (a < 0) a = -a;
@@ -39,6 +42,19 @@ int32_t vec_width(int64_t gran, int elem, int32_t cap) {
     int32_t v = int32_t(kVecBytes / elem);
     while (cap > 0 && v > cap) v /= 2;
     while (v > 1 && gran % v != 0) v /= 2;
+    return v;
+}
+
+// Vector width of a tile run of `run` elements whose starts have gcd `gran`:
+// the tile kernel shifts runs that start off the vector grid onto it, so the
+// width is limited by the run length, not by the alignment: a run on the grid
+// takes vectors up to its length, a run off it needs two vectors' worth (its
+// first and last vectors are partial).
+int32_t run_vec_width(int64_t run, int64_t gran, int elem, int32_t cap) {
+    int32_t v = int32_t(kVecBytes / elem);
+    while (cap > 0 && v > cap) v /= 2;
+    const bool onGrid = gran % v == 0;
+    while (v > 1 && (onGrid ? run < v : run < 2 * v)) v /= 2;
     return v;
 }
 
@@ -168,7 +184,7 @@ void set_div(FastDiv& f, int64_t d) { f = make_fastdiv(uint32_t(d)); }
 // Kernel T set-up for targets tA (A-run) and tB (B-run).  Returns false if the
 // tile does not fit the LDS budget or the grid is too large.
 bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_options_t& opt,
-                bool alignA, bool alignB, int64_t ldsBudget, TileArgs& t,
+                bool alignA, bool alignB, int64_t ldsBudget, int64_t minTile, TileArgs& t,
                 hptt_plan_info_t& info) {
     memset(&t, 0, sizeof(t));
     const int M = f.M;
@@ -249,6 +265,56 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
         t.gStrideB[g] = f.sB[a];
         ++g;
     }
+    // LDS pitch: an odd number of elements by default, so the column-wise
+    // reads of the store phase spread over the LDS banks.
+    int64_t pad = t.runA % 2 == 0 ? 1 : 0;
+    if (opt.lds_pad > 0) pad = opt.lds_pad;
+    if (opt.lds_pad < 0) pad = 0;
+    t.pitch = int32_t(t.runA + pad);
+    // Depth: a tile smaller than `minTile` elements stacks nZ tiles along the
+    // grid index closest to contiguous in both tensors (smallest sum of
+    // strides), in one LDS round, as long as kMinGrid workgroups remain.
+    // Not with row passes.
+    t.nZ = 1;
+    t.gDepth = -1;
+    const int64_t area = t.runA * t.runB;
+    double tilesBefore = 1;
+    for (int j = 0; j < g; ++j) tilesBefore *= double(ext[j]);
+    int64_t wantZ = opt.depth > 0 ? opt.depth : (minTile + area - 1) / area;
+    if (opt.depth == 0 && double(wantZ) > tilesBefore / kMinGrid)
+        wantZ = int64_t(tilesBefore / kMinGrid);
+    if (opt.row_passes > 1) wantZ = 1;
+    if (wantZ > 1) {
+        // among the indices long enough for wantZ the one with the smallest
+        // strides; if none is, the longest
+        int best = -1;
+        for (int j = 0; j < g; ++j) {
+            if (j == t.gChunkC || j == t.gChunkR || ext[j] < 2) continue;
+            const bool longJ = ext[j] >= wantZ, longB = best >= 0 && ext[best] >= wantZ;
+            if (best < 0 || (longJ && !longB) ||
+                (longJ == longB && (longJ ? t.gStrideA[j] + t.gStrideB[j] <
+                                                t.gStrideA[best] + t.gStrideB[best]
+                                          : ext[j] > ext[best])))
+                best = j;
+        }
+        if (best >= 0) {
+            const int64_t perTile = t.runB * t.pitch * elem;
+            const int64_t tables = (t.runA + t.runB) * int64_t(sizeof(int64_t));
+            int64_t z = wantZ < ext[best] ? wantZ : ext[best];
+            if (tables + z * perTile > ldsBudget) z = (ldsBudget - tables) / perTile;
+            if (z >= 2) {
+                t.nZ = int32_t(z);
+                t.gDepth = best;
+                t.zLast = ext[best];
+                t.zStrideA = t.gStrideA[best];
+                t.zStrideB = t.gStrideB[best];
+                ext[best] = (ext[best] + z - 1) / z;
+                t.gStrideA[best] *= z;
+                t.gStrideB[best] *= z;
+            }
+        }
+    }
+    info.depth = t.nZ;
     t.nG = g;
     t.skew = (g >= 2 && opt.tile_order != 1) ? 1 : 0;
     t.xcdSplit = opt.tile_order == 3 ? 1 : 0;
@@ -260,26 +326,27 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
         if (tiles >= (uint64_t(1) << 32)) return false;
     }
     t.numTiles = uint32_t(tiles);
-    // LDS pitch: an odd number of elements by default, so the column-wise
-    // reads of the store phase spread over the LDS banks.
-    int64_t pad = t.runA % 2 == 0 ? 1 : 0;
-    if (opt.lds_pad > 0) pad = opt.lds_pad;
-    if (opt.lds_pad < 0) pad = 0;
-    t.pitch = int32_t(t.runA + pad);
-    // Vector widths: every A run must start on a multiple of vec_a elements,
-    // every B run on a multiple of vec_b.
+    // Vector widths: A runs start at multiples of granA elements, B runs at
+    // multiples of granB (relative to the tensors' first elements).
     int64_t granA = 0, granB = 0;
     for (int j = 0; j < g; ++j)
         if (ext[j] > 1) {
             granA = gcd64(granA, t.gStrideA[j]);
             granB = gcd64(granB, t.gStrideB[j]);
         }
+    if (t.nZ > 1) {
+        granA = gcd64(granA, t.zStrideA);
+        granB = gcd64(granB, t.zStrideB);
+    }
     for (int j = 0; j < nR; ++j)
         if (t.rExt[j].d > 1) granA = gcd64(granA, t.rStrideA[j]);
     for (int j = 0; j < nC; ++j)
         if (t.cExt[j].d > 1) granB = gcd64(granB, t.cStrideB[j]);
-    info.vec_a = vec_width(granA, elem, opt.max_vec);
-    info.vec_b = vec_width(granB, elem, opt.max_vec);
+    info.vec_a = run_vec_width(t.runA, granA, elem, opt.max_vec);
+    info.vec_b = run_vec_width(t.runB, granB, elem, opt.max_vec);
+    t.runsOnGridA = granA % info.vec_a == 0 ? 1 : 0;
+    t.runsOnGridB = granB % info.vec_b == 0 ? 1 : 0;
+    t.misA = t.misB = 0;
     // A runs that start and end on 128-byte lines share no line with another
     // tile, so they can be read with non-temporal loads.
     t.alignedA = (granA == 0 || (granA * elem) % kLine == 0) && (t.runA * elem) % kLine == 0;
@@ -293,6 +360,8 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
         const int64_t want = (t.runB + opt.row_passes - 1) / opt.row_passes;
         t.subRows = int32_t((want + info.vec_b - 1) / info.vec_b * info.vec_b);
     }
+    set_div(t.zRows, t.subRows);
+    set_div(t.zCols, t.runA);
     const int64_t lds = tile_lds_bytes_host(t, elem);
     if (lds > ldsBudget) return false;
     info.run_a = t.runA;
@@ -391,7 +460,8 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
         opt.kernel == HPTT_KERNEL_NONE || opt.run_a < 0 || opt.run_b < 0 || opt.max_vec < 0 ||
         opt.store_hint < 0 || opt.store_hint > 2 || opt.load_hint < 0 || opt.load_hint > 2 ||
         opt.lds_pad < -1 || opt.lds_pad > 64 || opt.max_blocks < 0 || opt.tile_order < 0 ||
-        opt.tile_order > 3 || opt.row_passes < 0 || opt.row_passes > 64 || opt.exact_runs < 0 ||
+        opt.tile_order > 3 || opt.row_passes < 0 || opt.row_passes > 64 || opt.depth < 0 ||
+        opt.depth > 4096 || opt.min_tile < 0 || opt.exact_runs < 0 ||
         opt.exact_runs > 1)
         return HPTT_ERROR_INVALID_ARGUMENT;
 
@@ -476,6 +546,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
                                 {true, true, kLdsMax},     {false, false, kLdsMax}};
         const Stage* st = opt.exact_runs ? forced : stages;
         const int nst = opt.exact_runs ? 1 : 6;
+        const int64_t minTile = opt.min_tile > 0 ? opt.min_tile : kMinTileBytes / elem;
         int64_t tA = tA0, tB = tB0;
         Stage chosen = st[0];
         bool ok = false;
@@ -485,11 +556,42 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
             chosen = st[s];
             for (int attempt = 0; attempt < 24 && !ok; ++attempt) {
                 ok = setup_tile(f, elem, tA, tB, opt, chosen.alignA, chosen.alignB, chosen.budget,
-                                plan->tile, info);
+                                minTile, plan->tile, info);
                 if (!ok) {
                     if (tA >= tB && tA > 1) tA /= 2;
                     else if (tB > 1) tB /= 2;
                     else break;
+                }
+            }
+        }
+        // A tile below minTile elements whose A run is cut short by the
+        // tensor (its leading extents end before the target) lets its B run
+        // grow instead, and the other way round: longer runs beat stacking.
+        if (ok && opt.run_a == 0 && opt.run_b == 0 && opt.exact_runs == 0) {
+            const int64_t runA = plan->tile.runA, runB = plan->tile.runB;
+            if (runA * runB < minTile && double(plan->tile.numTiles) * plan->tile.nZ >= kMinGrid) {
+                int64_t gA = tA, gB = tB;
+                if (runA < tA) gB = (minTile + runA - 1) / runA;
+                else if (runB < tB) gA = (minTile + runB - 1) / runB;
+                TileArgs keep = plan->tile;
+                hptt_plan_info_t keepInfo = info;
+                bool grown = false;
+                for (int attempt = 0; attempt < 8 && !grown && (gA != tA || gB != tB); ++attempt) {
+                    grown = setup_tile(f, elem, gA, gB, opt, false, false, kLdsBudget, minTile,
+                                       plan->tile, info) &&
+                            plan->tile.runA * plan->tile.runB > runA * runB &&
+                            double(plan->tile.numTiles) * plan->tile.nZ >= kMinGrid;
+                    if (!grown) {
+                        if (gB > tB) gB = gB / 2 > tB ? gB / 2 : tB;
+                        else if (gA > tA) gA = gA / 2 > tA ? gA / 2 : tA;
+                    }
+                }
+                if (grown) {
+                    tA = gA;
+                    tB = gB;
+                } else {
+                    plan->tile = keep;
+                    info = keepInfo;
                 }
             }
         }
@@ -502,7 +604,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
             if (tA >= tB) tA /= 2;
             else tB /= 2;
             if (!setup_tile(f, elem, tA, tB, opt, chosen.alignA, chosen.alignB, kLdsMax,
-                            plan->tile, info) ||
+                            minTile, plan->tile, info) ||
                 plan->tile.numTiles <= keep.numTiles) {
                 plan->tile = keep;
                 info = keepInfo;

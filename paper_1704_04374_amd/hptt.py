@@ -41,7 +41,8 @@ class Options(ctypes.Structure):
                 ("max_vec", ctypes.c_int32), ("store_hint", ctypes.c_int32),
                 ("load_hint", ctypes.c_int32), ("lds_pad", ctypes.c_int32),
                 ("max_blocks", ctypes.c_int32), ("tile_order", ctypes.c_int32),
-                ("exact_runs", ctypes.c_int32), ("row_passes", ctypes.c_int32)]
+                ("exact_runs", ctypes.c_int32), ("row_passes", ctypes.c_int32),
+                ("depth", ctypes.c_int32), ("min_tile", ctypes.c_int32)]
 
 
 class AutotuneReport(ctypes.Structure):
@@ -72,7 +73,7 @@ class PlanInfo(ctypes.Structure):
                 ("lds_bytes", ctypes.c_int32),
                 ("tiles", ctypes.c_int64), ("grid", ctypes.c_int64), ("block", ctypes.c_int32),
                 ("hints", ctypes.c_int32), ("mode", ctypes.c_int32),
-                ("tile_order", ctypes.c_int32)]
+                ("tile_order", ctypes.c_int32), ("depth", ctypes.c_int32)]
 
     def as_dict(self) -> dict:
         n = self.ndim
@@ -85,7 +86,7 @@ class PlanInfo(ctypes.Structure):
                 "footprint_b": self.footprint_b, "lds_bytes": self.lds_bytes,
                 "tiles": self.tiles, "grid": self.grid, "block": self.block,
                 "hints": self.hints, "mode": MODES[self.mode],
-                "tile_order": self.tile_order}
+                "tile_order": self.tile_order, "depth": self.depth}
 
 
 # Every entry point declared in include/hptt.h and include/hptt_yardstick.h.

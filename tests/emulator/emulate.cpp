@@ -29,6 +29,8 @@ namespace {
 struct EmuState {
     int64_t numelA = 0;   // elements addressable from A (its footprint)
     int64_t numelB = 0;   // elements addressable from B
+    int64_t misA = 0;     // element offset of A's base from the vector grid
+    int64_t misB = 0;
     const void* A = nullptr;
     void* B = nullptr;
     bool readsB = false;
@@ -60,7 +62,10 @@ bool check_global(const T* p, int64_t off, int V, bool isStore) {
         fail(isA ? "A offset out of bounds" : "B offset out of bounds", off, V);
         return false;
     }
-    if (off % V != 0) { fail("misaligned vector access", off, V); return false; }
+    if ((off + (isA ? S->misA : S->misB)) % V != 0) {
+        fail("misaligned vector access", off, V);
+        return false;
+    }
     return true;
 }
 
@@ -123,7 +128,9 @@ void clear_written(int64_t from, int64_t to) {
 template <typename T, int VA, int VB, int MODE, int NT>
 void emu_tile(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     using namespace hptt;
-    const TileArgs& g = p->tile;
+    TileArgs g = p->tile;  // with the base pointers' offsets from the vector grid, as at launch
+    g.misA = int32_t(S->misA % VA);
+    g.misB = int32_t(S->misB % VB);
     const T alpha = T(p->alpha), beta = T(p->beta);
     const int64_t ldsBytes = p->info.lds_bytes;
     const int64_t tableBytes = (g.runA + g.runB) * int64_t(sizeof(int64_t));
@@ -240,18 +247,24 @@ extern "C" {
 
 // Emulate hptt_exec of `plan` on host buffers A and B (or, with both NULL,
 // only the offsets).  va/vb = 0 use the plan's vector widths, others force
-// narrower ones as hptt_exec does for less aligned pointers.  counts (numel
+// narrower ones as hptt_exec does for less aligned pointers (stream and axpby
+// kernels).  misA/misB: the base pointers' element offsets from the 16-byte
+// grid, which the tile kernel shifts its runs by (vector accesses are checked
+// for alignment relative to that grid).  counts (numel
 // bytes, or NULL) is incremented at every B element written.  Only
 // workgroups 0, block_stride, 2*block_stride, ... are run.  Returns the
 // number of violations; the first is described in msg.  For sub-tensor plans
 // A, B and counts cover the footprints (info.footprint_a, footprint_b).
 int64_t hptt_emulate_exec(hptt_plan_t plan, const void* A, void* B, int32_t va, int32_t vb,
-                          uint8_t* counts, int64_t block_stride, char* msg, size_t msglen) {
+                          uint8_t* counts, int64_t block_stride, char* msg, size_t msglen,
+                          int32_t misA, int32_t misB) {
     if (!plan) return -1;
     EmuState st;
     S = &st;
     st.numelA = plan->info.footprint_a;
     st.numelB = plan->info.footprint_b;
+    st.misA = misA;
+    st.misB = misB;
     st.dry = (A == nullptr && B == nullptr);
     st.A = st.dry ? kDryA : A;
     st.B = st.dry ? kDryB : B;

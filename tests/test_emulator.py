@@ -8,6 +8,7 @@ import numpy as np
 import pytest
 
 from oracle import oracle as orc
+from paper_1704_04374_amd import hptt
 from paper_1704_04374_amd.workloads import WORKLOADS, random_problem
 from emulator import emu
 
@@ -188,3 +189,61 @@ def test_outer_sizes_match_oracle(knobs):
         strides = np.cumprod((1,) + outer_b[:-1])
         mask[(idx * np.array(strides)[:, None]).sum(axis=0)] = True
         assert np.all(cnt[mask] == 1) and np.all(cnt[~mask] == 0), p.describe()
+
+
+@pytest.mark.parametrize("mis", [(1, 0), (0, 3), (2, 1), (3, 2)], ids=lambda m: f"misA{m[0]}_misB{m[1]}")
+def test_tile_runs_shifted_onto_the_vector_grid(mis):
+    """Base pointers off the 16-byte grid: the tile kernel keeps its vector
+    widths and shifts every run onto the grid, with partial vectors at both
+    ends.  Bit-exact against the oracle; every vector access aligned."""
+    rng = np.random.default_rng(100 + 4 * mis[0] + mis[1])
+    seen = 0
+    for it in range(80):
+        size_a, perm = random_problem(rng, max_dims=5, max_numel=30000)
+        dtype = "f32" if it % 2 == 0 else "f64"
+        alpha, beta = CASES[it % len(CASES)]
+        p = emu.plan(perm, size_a, alpha, beta, dtype)
+        if p.info["kernel"] != "tile":
+            continue
+        seen += 1
+        per = 4 if dtype == "f32" else 2
+        _check(p, size_a, perm, alpha, beta, dtype, rng, mis_a=mis[0] % per, mis_b=mis[1] % per)
+    assert seen >= 20
+
+
+@pytest.mark.parametrize("knobs", [dict(depth=2), dict(depth=3), dict(depth=7),
+                                   dict(depth=5, max_vec=2), dict(min_tile=64),
+                                   dict(min_tile=1 << 16), dict(run_a=4, run_b=4, depth=9)],
+                         ids=lambda k: "_".join(f"{a}{b}" for a, b in k.items()))
+def test_stacked_tiles_match_oracle(knobs):
+    """Tiles stacked along one more index (depth), forced or chosen by the
+    minimum tile size, with ragged last stacks: bit-exact, each B element
+    written once."""
+    rng = np.random.default_rng(7 + sum(knobs.values()))
+    stacked = 0
+    for it in range(80):
+        size_a, perm = random_problem(rng, max_dims=6, extents=(1, 2, 3, 5, 7, 9, 17, 33),
+                                      max_numel=40000)
+        dtype = "f32" if it % 2 == 0 else "f64"
+        alpha, beta = CASES[it % len(CASES)]
+        try:
+            p = emu.plan(perm, size_a, alpha, beta, dtype, kernel="tile", **knobs)
+        except hptt.HpttError:
+            continue
+        stacked += p.info["depth"] > 1
+        _check(p, size_a, perm, alpha, beta, dtype, rng, mis_a=it % 3 % (4 if dtype == "f32" else 2))
+    assert stacked >= 5 or "depth" not in knobs
+
+
+def test_small_tiles_grow_or_stack():
+    """Leading extents too short for the target runs: the planner lengthens
+    the other run or stacks tiles until a workgroup round holds at least
+    min_tile elements (when the grid stays large)."""
+    for size, perm in [((4, 11, 385, 2952), (1, 0, 2, 3)), ((2, 26250, 4, 238), (1, 3, 0, 2)),
+                       ((2, 3, 2, 995, 4188), (2, 3, 0, 1, 4)), ((184, 2, 135870), (1, 0, 2)),
+                       ((70, 5, 98, 1458), (1, 0, 2, 3))]:
+        p = hptt.Plan(perm, size, 1.0, 1.0, "f32")
+        i = p.info
+        assert i["run_a"] * i["run_b"] * i["depth"] >= 2048, p.describe()
+        err, msg, _ = emu.run(emu.plan(perm, size, 1.0, 1.0, "f32"), block_stride=97)
+        assert err == 0, msg
