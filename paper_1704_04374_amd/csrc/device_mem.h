@@ -1,0 +1,64 @@
+// Memory policy of the device kernels: plain global and LDS accesses.  A
+// vector of V elements is one global_load/store of V*sizeof(T) bytes; the
+// plan only asks for widths that keep every such access aligned.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "kernel_body.h"
+
+namespace hptt {
+namespace {
+
+struct DeviceMem {
+    template <typename T, int V, bool NT>
+    __device__ __forceinline__ static Vec<T, V> ld(const T* p, int64_t off) {
+        Vec<T, V> r;
+        if constexpr (V == 1) {
+            r.v[0] = NT ? __builtin_nontemporal_load(p + off) : p[off];
+        } else {
+            typedef T vt __attribute__((ext_vector_type(V)));
+            const vt x = NT ? __builtin_nontemporal_load(reinterpret_cast<const vt*>(p + off))
+                            : *reinterpret_cast<const vt*>(p + off);
+#pragma unroll
+            for (int e = 0; e < V; ++e) r.v[e] = x[e];
+        }
+        return r;
+    }
+    template <typename T>
+    __device__ __forceinline__ static T ld1(const T* p, int64_t off) {
+        return p[off];
+    }
+    template <bool NT, typename T>
+    __device__ __forceinline__ static void st1(T* p, int64_t off, T v) {
+        if constexpr (NT) __builtin_nontemporal_store(v, p + off);
+        else p[off] = v;
+    }
+    template <bool NT, typename T, int V>
+    __device__ __forceinline__ static void st(T* p, int64_t off, const Vec<T, V>& v) {
+        if constexpr (V == 1) {
+            st1<NT, T>(p, off, v.v[0]);
+        } else {
+            typedef T vt __attribute__((ext_vector_type(V)));
+            vt x;
+#pragma unroll
+            for (int e = 0; e < V; ++e) x[e] = v.v[e];
+            if constexpr (NT) __builtin_nontemporal_store(x, reinterpret_cast<vt*>(p + off));
+            else *reinterpret_cast<vt*>(p + off) = x;
+        }
+    }
+    template <typename T>
+    __device__ __forceinline__ static T lds_ld(const T* l, int64_t i) {
+        return l[i];
+    }
+    template <typename T>
+    __device__ __forceinline__ static void lds_st(T* l, int64_t i, T v) {
+        l[i] = v;
+    }
+};
+
+template <typename T>
+constexpr int kMaxVec = int(16 / sizeof(T));
+
+}  // namespace
+}  // namespace hptt

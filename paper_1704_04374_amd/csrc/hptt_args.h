@@ -112,6 +112,14 @@ struct StreamArgs {
     int64_t oStrideB[kMaxDims]; // B strides of those positions
 };
 
+// Kernel T needs its general variant when a run starts off its vector grid
+// (runs shifted, partial vectors at both ends) or when tiles are stacked;
+// otherwise the specialised variant, compiled without either, is launched.
+// g.misA / g.misB must already hold the launch's pointer offsets.
+__host__ __device__ inline bool tile_is_general(const TileArgs& g) {
+    return !g.runsOnGridA || !g.runsOnGridB || g.misA != 0 || g.misB != 0 || g.nZ > 1;
+}
+
 constexpr int log2_width(int v) { return v >= 4 ? 2 : v >= 2 ? 1 : 0; }
 
 // Fallback: one element per thread in B order, any shape.

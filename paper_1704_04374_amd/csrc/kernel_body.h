@@ -126,14 +126,17 @@ constexpr int kBatch = 8;
 // Thread tid takes the vectors tid, tid + kBlock, ... of the (stacked row,
 // vector) space, vector fastest, so a wave reads whole runs.  Vectors sit on
 // the A vector grid: a run that starts off it is covered by one more vector,
-// its first and last ones partial (element loads).
-template <class Mem, typename T, int VA, int HINT>
+// its first and last ones partial (element loads).  GEN = false compiles the
+// common case without either (tile_is_general() is false): every run starts
+// on the grid and nZ = 1.
+template <class Mem, typename T, int VA, int HINT, bool GEN>
 __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb, int64_t r0,
                                           int tid, const T* A, T* lds, const int64_t* rowOffA) {
-    const bool shift = !g.runsOnGridA || g.misA != 0;
+    const bool shift = GEN && (!g.runsOnGridA || g.misA != 0);
+    const bool depth = GEN && g.nZ > 1;
     const int64_t W = (g.runA + (shift ? VA - 1 : 0) + VA - 1) / VA;  // vectors per row
     const int64_t rows = imin(int64_t(g.subRows), tb.validRows - r0);  // rows of this pass
-    const int64_t stacked = int64_t(g.nZ) * g.subRows;
+    const int64_t stacked = depth ? int64_t(g.nZ) * g.subRows : int64_t(g.subRows);
     int64_t R = tid / W, c = tid % W;
     const int64_t dR = kBlock / W, dc = kBlock % W;
     while (R < stacked) {
@@ -143,26 +146,25 @@ __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb,
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             int64_t z = 0, r = R;
-            if (g.nZ > 1) {
+            if (depth) {
                 z = int64_t(fast_div(uint32_t(R), g.zRows));
                 r = R - z * g.subRows;
             }
-            ok[u] = R < stacked && r < rows && z < tb.validDepth;
-            cc[u] = 0;
+            ok[u] = R < stacked && r < rows && (!depth || z < tb.validDepth);
+            cc[u] = c * VA;
             at[u] = 0;
             if (ok[u]) {
-                const int64_t start =
-                    tb.a + Mem::template lds_ld<int64_t>(rowOffA, r0 + r) + z * g.zStrideA;
-                const int64_t d = shift ? ((start + g.misA) & (VA - 1)) : 0;
-                cc[u] = c * VA - d;
-                ok[u] = cc[u] + VA > 0 && cc[u] < tb.validCols;
+                int64_t start = tb.a + Mem::template lds_ld<int64_t>(rowOffA, r0 + r);
+                if (depth) start += z * g.zStrideA;
+                if (shift) cc[u] -= (start + g.misA) & (VA - 1);
+                ok[u] = (!shift || cc[u] + VA > 0) && cc[u] < tb.validCols;
                 at[u] = R * g.pitch + cc[u];
                 if (ok[u]) {
-                    if (cc[u] >= 0 && cc[u] + VA <= tb.validCols) {
+                    if ((!shift || cc[u] >= 0) && cc[u] + VA <= tb.validCols) {
                         v[u] = Mem::template ld<T, VA, (HINT & kNtLoad) != 0>(A, start + cc[u]);
                     } else {
                         for (int e = 0; e < VA; ++e)
-                            if (cc[u] + e >= 0 && cc[u] + e < tb.validCols)
+                            if ((!shift || cc[u] + e >= 0) && cc[u] + e < tb.validCols)
                                 v[u].v[e] = Mem::template ld1<T>(A, start + cc[u] + e);
                     }
                 }
@@ -179,7 +181,7 @@ __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb,
             if (ok[u]) {
 #pragma unroll
                 for (int e = 0; e < VA; ++e)
-                    if (cc[u] + e >= 0 && cc[u] + e < tb.validCols)
+                    if ((!shift || cc[u] + e >= 0) && cc[u] + e < tb.validCols)
                         Mem::template lds_st<T>(lds, at[u] + e, v[u].v[e]);
             }
         }
@@ -193,14 +195,15 @@ __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb,
 // fastest, gathers each vector's VB elements from consecutive LDS rows, and
 // writes it to B (reading B first when beta != 0).  Vectors sit on the B
 // vector grid, as in the load phase.
-template <class Mem, typename T, int VB, int MODE, int HINT>
+template <class Mem, typename T, int VB, int MODE, int HINT, bool GEN>
 __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb, int64_t r0,
                                            int tid, T* B, const T* lds, const int64_t* colOffB,
                                            T alpha, T beta) {
-    const bool shift = !g.runsOnGridB || g.misB != 0;
+    const bool shift = GEN && (!g.runsOnGridB || g.misB != 0);
+    const bool depth = GEN && g.nZ > 1;
     const int64_t W = (g.subRows + (shift ? VB - 1 : 0) + VB - 1) / VB;  // vectors per column
     const int64_t rows = imin(int64_t(g.subRows), tb.validRows - r0);
-    const int64_t cols = int64_t(g.nZ) * g.runA;
+    const int64_t cols = depth ? int64_t(g.nZ) * g.runA : g.runA;
     int64_t Q = tid / W, s = tid % W;
     const int64_t dQ = kBlock / W, ds = kBlock % W;
     while (Q < cols) {
@@ -210,32 +213,31 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             int64_t z = 0, q = Q;
-            if (g.nZ > 1) {
+            if (depth) {
                 z = int64_t(fast_div(uint32_t(Q), g.zCols));
                 q = Q - z * g.runA;
             }
-            ok[u] = Q < cols && q < tb.validCols && z < tb.validDepth;
-            ss[u] = 0;
+            ok[u] = Q < cols && q < tb.validCols && (!depth || z < tb.validDepth);
+            ss[u] = s * VB;
             off[u] = 0;
             if (ok[u]) {
-                const int64_t start =
-                    tb.b + Mem::template lds_ld<int64_t>(colOffB, q) + z * g.zStrideB + r0;
-                const int64_t d = shift ? ((start + g.misB) & (VB - 1)) : 0;
-                ss[u] = s * VB - d;
-                ok[u] = ss[u] + VB > 0 && ss[u] < rows;
+                int64_t start = tb.b + Mem::template lds_ld<int64_t>(colOffB, q) + r0;
+                if (depth) start += z * g.zStrideB;
+                if (shift) ss[u] -= (start + g.misB) & (VB - 1);
+                ok[u] = (!shift || ss[u] + VB > 0) && ss[u] < rows;
                 off[u] = start + ss[u];
                 if (ok[u]) {
-                    const int64_t base = (z * g.subRows + ss[u]) * g.pitch + q;
+                    const int64_t base = ((depth ? z * g.subRows : 0) + ss[u]) * g.pitch + q;
 #pragma unroll
                     for (int e = 0; e < VB; ++e)
-                        if (ss[u] + e >= 0 && ss[u] + e < rows)
+                        if ((!shift || ss[u] + e >= 0) && ss[u] + e < rows)
                             x[u].v[e] = Mem::template lds_ld<T>(lds, base + e * g.pitch);
                     if (MODE == kAxpby) {
-                        if (ss[u] >= 0 && ss[u] + VB <= rows) {
+                        if ((!shift || ss[u] >= 0) && ss[u] + VB <= rows) {
                             y[u] = Mem::template ld<T, VB, false>(B, off[u]);
                         } else {
                             for (int e = 0; e < VB; ++e)
-                                if (ss[u] + e >= 0 && ss[u] + e < rows)
+                                if ((!shift || ss[u] + e >= 0) && ss[u] + e < rows)
                                     y[u].v[e] = Mem::template ld1<T>(B, off[u] + e);
                         }
                     }
@@ -255,11 +257,11 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
 #pragma unroll
                 for (int e = 0; e < VB; ++e)
                     zv.v[e] = update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
-                if (ss[u] >= 0 && ss[u] + VB <= rows) {
+                if ((!shift || ss[u] >= 0) && ss[u] + VB <= rows) {
                     Mem::template st<(HINT & kNtStore) != 0, T, VB>(B, off[u], zv);
                 } else {
                     for (int e = 0; e < VB; ++e)
-                        if (ss[u] + e >= 0 && ss[u] + e < rows)
+                        if ((!shift || ss[u] + e >= 0) && ss[u] + e < rows)
                             Mem::template st1<(HINT & kNtStore) != 0, T>(B, off[u] + e, zv.v[e]);
                 }
             }

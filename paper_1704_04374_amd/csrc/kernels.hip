@@ -1,90 +1,20 @@
-// Device half of the C ABI: the gfx950 kernels and hptt_exec.
+// Device half of the C ABI: the streaming, axpby and generic gfx950 kernels,
+// and hptt_exec.
 //
 // Each kernel is a thin __global__ wrapper around the phase functions of
 // kernel_body.h, instantiated for the element type, the vector widths of the
-// A and B accesses, the update mode of Eq. (1) and the store hint.
+// A and B accesses, the update mode of Eq. (1) and the cache hints.  The
+// tile kernel (tile_kernel.h) is instantiated in tile_*.hip.
 #include <hip/hip_runtime.h>
 
-#include "kernel_body.h"
+#include "device_mem.h"
 #include "plan.h"
+#include "tile_kernel.h"
 
 namespace hptt {
 namespace {
 
 thread_local int32_t g_last_hip_error = 0;
-
-// Plain global and LDS accesses.  A vector of V elements is one
-// global_load/store of V*sizeof(T) bytes; the plan only asks for widths that
-// keep every such access aligned.
-struct DeviceMem {
-    template <typename T, int V, bool NT>
-    __device__ __forceinline__ static Vec<T, V> ld(const T* p, int64_t off) {
-        Vec<T, V> r;
-        if constexpr (V == 1) {
-            r.v[0] = NT ? __builtin_nontemporal_load(p + off) : p[off];
-        } else {
-            typedef T vt __attribute__((ext_vector_type(V)));
-            const vt x = NT ? __builtin_nontemporal_load(reinterpret_cast<const vt*>(p + off))
-                            : *reinterpret_cast<const vt*>(p + off);
-#pragma unroll
-            for (int e = 0; e < V; ++e) r.v[e] = x[e];
-        }
-        return r;
-    }
-    template <typename T>
-    __device__ __forceinline__ static T ld1(const T* p, int64_t off) {
-        return p[off];
-    }
-    template <bool NT, typename T>
-    __device__ __forceinline__ static void st1(T* p, int64_t off, T v) {
-        if constexpr (NT) __builtin_nontemporal_store(v, p + off);
-        else p[off] = v;
-    }
-    template <bool NT, typename T, int V>
-    __device__ __forceinline__ static void st(T* p, int64_t off, const Vec<T, V>& v) {
-        if constexpr (V == 1) {
-            st1<NT, T>(p, off, v.v[0]);
-        } else {
-            typedef T vt __attribute__((ext_vector_type(V)));
-            vt x;
-#pragma unroll
-            for (int e = 0; e < V; ++e) x[e] = v.v[e];
-            if constexpr (NT) __builtin_nontemporal_store(x, reinterpret_cast<vt*>(p + off));
-            else *reinterpret_cast<vt*>(p + off) = x;
-        }
-    }
-    template <typename T>
-    __device__ __forceinline__ static T lds_ld(const T* l, int64_t i) {
-        return l[i];
-    }
-    template <typename T>
-    __device__ __forceinline__ static void lds_st(T* l, int64_t i, T v) {
-        l[i] = v;
-    }
-};
-
-template <typename T, int VA, int VB, int MODE, int HINT>
-__global__ __launch_bounds__(kBlock) void tile_kernel(const T* __restrict__ A, T* __restrict__ B,
-                                                      const TileArgs g, T alpha, T beta) {
-    extern __shared__ int64_t smem[];
-    int64_t* rowOffA = smem;
-    int64_t* colOffB = smem + g.runB;
-    T* lds = reinterpret_cast<T*>(colOffB + g.runA);
-    const int tid = int(threadIdx.x);
-    tile_tables<DeviceMem>(g, tid, rowOffA, colOffB);
-    __syncthreads();
-    bool first = true;
-    for (uint32_t t = blockIdx.x; t < g.numTiles; t += gridDim.x) {
-        const TileBase tb = tile_base(g, t);
-        for (int64_t r0 = 0; r0 < tb.validRows; r0 += g.subRows) {
-            if (!first) __syncthreads();  // the previous pass's LDS reads are done
-            first = false;
-            tile_load<DeviceMem, T, VA, HINT>(g, tb, r0, tid, A, lds, rowOffA);
-            __syncthreads();
-            tile_store<DeviceMem, T, VB, MODE, HINT>(g, tb, r0, tid, B, lds, colOffB, alpha, beta);
-        }
-    }
-}
 
 template <typename T, int V, int MODE, int HINT>
 __global__ __launch_bounds__(kBlock) void stream_kernel(const T* __restrict__ A,
@@ -120,34 +50,6 @@ __global__ __launch_bounds__(kBlock) void generic_kernel(const T* __restrict__ A
 // Template selection: (mode, store hint) x vector widths -> kernel address
 // ---------------------------------------------------------------------------
 
-template <typename T>
-constexpr int kMaxVec = int(16 / sizeof(T));
-
-template <typename T, int VA, int MODE, int HINT>
-const void* tile_fn_vb(int vb) {
-    switch (vb) {
-        case 1: return reinterpret_cast<const void*>(&tile_kernel<T, VA, 1, MODE, HINT>);
-        case 2: return reinterpret_cast<const void*>(&tile_kernel<T, VA, 2, MODE, HINT>);
-        case 4:
-            if constexpr (kMaxVec<T> >= 4)
-                return reinterpret_cast<const void*>(&tile_kernel<T, VA, 4, MODE, HINT>);
-            return nullptr;
-    }
-    return nullptr;
-}
-
-template <typename T, int MODE, int HINT>
-const void* tile_fn(int va, int vb) {
-    switch (va) {
-        case 1: return tile_fn_vb<T, 1, MODE, HINT>(vb);
-        case 2: return tile_fn_vb<T, 2, MODE, HINT>(vb);
-        case 4:
-            if constexpr (kMaxVec<T> >= 4) return tile_fn_vb<T, 4, MODE, HINT>(vb);
-            return nullptr;
-    }
-    return nullptr;
-}
-
 template <typename T, int MODE, int HINT>
 const void* stream_fn(int v) {
     switch (v) {
@@ -180,11 +82,11 @@ const void* generic_fn(bool big) {
                : reinterpret_cast<const void*>(&generic_kernel<T, MODE, HINT, false>);
 }
 
-// Kernel address for the plan's class, with the given vector widths.
+// Kernel address for the plan's class, with the given vector widths (the
+// tile kernel is picked by launch()).
 template <typename T, int MODE, int HINT>
 const void* select(const hptt_plan_s* p, int va, int vb) {
     switch (p->info.kernel) {
-        case HPTT_KERNEL_TILE: return tile_fn<T, MODE, HINT>(va, vb);
         case HPTT_KERNEL_STREAM: return stream_fn<T, MODE, HINT>(va < vb ? va : vb);
         case HPTT_KERNEL_AXPBY: return axpby_fn<T, MODE, HINT>(va < vb ? va : vb);
         case HPTT_KERNEL_GENERIC:
@@ -234,7 +136,14 @@ hptt_status_t launch(const hptt_plan_s* p, const void* A, void* B, hipStream_t s
         targs.misA = int32_t((pa / uintptr_t(elem)) % uintptr_t(va));
         targs.misB = int32_t((pb / uintptr_t(elem)) % uintptr_t(vb));
     }
-    const void* fn = select_mode<T>(p, va, vb);
+    const void* fn = nullptr;
+    if (tile) {
+        const bool general = tile_is_general(targs);
+        fn = sizeof(T) == 4 ? tile_kernel_f32(general, in.mode, in.hints, va, vb)
+                            : tile_kernel_f64(general, in.mode, in.hints, va, vb);
+    } else {
+        fn = select_mode<T>(p, va, vb);
+    }
     if (!fn) return HPTT_ERROR_INVALID_ARGUMENT;
     const T* a = static_cast<const T*>(A);
     T* b = static_cast<T*>(B);

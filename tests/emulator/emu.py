@@ -24,7 +24,7 @@ def library():
         lib.hptt_emulate_exec.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                           ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                           ctypes.c_int64, ctypes.c_char_p, ctypes.c_size_t,
-                                          ctypes.c_int32, ctypes.c_int32]
+                                          ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
         lib.hptt_emulate_exec.restype = ctypes.c_int64
         lib.hptt_emulate_check_fastdiv.argtypes = [ctypes.c_uint32, ctypes.c_uint64, ctypes.c_uint64]
         lib.hptt_emulate_check_fastdiv.restype = ctypes.c_int64
@@ -37,15 +37,17 @@ def plan(perm, size_a, alpha=1.0, beta=0.0, dtype="f32", **knobs):
     return Plan(perm, size_a, alpha, beta, dtype, lib=library(), **knobs)
 
 
-def run(p, A=None, B=None, va=0, vb=0, counts=False, block_stride=1, mis_a=0, mis_b=0):
+def run(p, A=None, B=None, va=0, vb=0, counts=False, block_stride=1, mis_a=0, mis_b=0,
+        general=False):
     """Emulate hptt_exec; B is updated in place.  mis_a/mis_b: element offsets
-    of the base pointers from the 16-byte grid (tile kernel).  Returns
-    (errors, msg, counts)."""
+    of the base pointers from the 16-byte grid (tile kernel); general: run the
+    tile kernel's general variant even where the specialised one would run.
+    Returns (errors, msg, counts)."""
     lib = library()
     cnt = np.zeros(p.info["footprint_b"], dtype=np.uint8) if counts else None
     msg = ctypes.create_string_buffer(512)
     err = lib.hptt_emulate_exec(p.handle, None if A is None else A.ctypes.data,
                                 None if B is None else B.ctypes.data, va, vb,
                                 None if cnt is None else cnt.ctypes.data, block_stride, msg,
-                                len(msg), mis_a, mis_b)
+                                len(msg), mis_a, mis_b, int(general))
     return err, msg.value.decode(), cnt

@@ -31,6 +31,7 @@ struct EmuState {
     int64_t numelB = 0;   // elements addressable from B
     int64_t misA = 0;     // element offset of A's base from the vector grid
     int64_t misB = 0;
+    bool forceGeneral = false;  // run kernel T's general variant on any plan
     const void* A = nullptr;
     void* B = nullptr;
     bool readsB = false;
@@ -124,9 +125,9 @@ void clear_written(int64_t from, int64_t to) {
     memset(S->written.data() + from, 0, size_t(to - from));
 }
 
-// Mirrors tile_kernel in kernels.hip.
-template <typename T, int VA, int VB, int MODE, int NT>
-void emu_tile(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
+// Mirrors tile_kernel in tile_kernel.h, in the variant GEN.
+template <typename T, int VA, int VB, int MODE, int NT, bool GEN>
+void emu_tile_variant(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     using namespace hptt;
     TileArgs g = p->tile;  // with the base pointers' offsets from the vector grid, as at launch
     g.misA = int32_t(S->misA % VA);
@@ -148,13 +149,25 @@ void emu_tile(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
             for (int64_t r0 = 0; r0 < tb.validRows && S->errors == 0; r0 += g.subRows) {
                 clear_written(tableBytes, ldsBytes);
                 for (int tid = 0; tid < kBlock; ++tid)
-                    tile_load<HostMem, T, VA, NT>(g, tb, r0, tid, A, lds, rowOffA);
+                    tile_load<HostMem, T, VA, NT, GEN>(g, tb, r0, tid, A, lds, rowOffA);
                 for (int tid = 0; tid < kBlock; ++tid)
-                    tile_store<HostMem, T, VB, MODE, NT>(g, tb, r0, tid, B, lds, colOffB, alpha,
-                                                         beta);
+                    tile_store<HostMem, T, VB, MODE, NT, GEN>(g, tb, r0, tid, B, lds, colOffB,
+                                                              alpha, beta);
             }
         }
     }
+}
+
+// The variant hptt_exec would launch (or the general one when forced).
+template <typename T, int VA, int VB, int MODE, int NT>
+void emu_tile(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
+    hptt::TileArgs g = p->tile;
+    g.misA = int32_t(S->misA % VA);
+    g.misB = int32_t(S->misB % VB);
+    if (S->forceGeneral || hptt::tile_is_general(g))
+        emu_tile_variant<T, VA, VB, MODE, NT, true>(p, A, B, blockStride);
+    else
+        emu_tile_variant<T, VA, VB, MODE, NT, false>(p, A, B, blockStride);
 }
 
 // Mirrors stream_kernel in kernels.hip.
@@ -250,17 +263,20 @@ extern "C" {
 // narrower ones as hptt_exec does for less aligned pointers (stream and axpby
 // kernels).  misA/misB: the base pointers' element offsets from the 16-byte
 // grid, which the tile kernel shifts its runs by (vector accesses are checked
-// for alignment relative to that grid).  counts (numel
+// for alignment relative to that grid).  general = 1 runs the tile kernel's
+// general variant even where hptt_exec would launch the specialised one.
+// counts (numel
 // bytes, or NULL) is incremented at every B element written.  Only
 // workgroups 0, block_stride, 2*block_stride, ... are run.  Returns the
 // number of violations; the first is described in msg.  For sub-tensor plans
 // A, B and counts cover the footprints (info.footprint_a, footprint_b).
 int64_t hptt_emulate_exec(hptt_plan_t plan, const void* A, void* B, int32_t va, int32_t vb,
                           uint8_t* counts, int64_t block_stride, char* msg, size_t msglen,
-                          int32_t misA, int32_t misB) {
+                          int32_t misA, int32_t misB, int32_t general) {
     if (!plan) return -1;
     EmuState st;
     S = &st;
+    st.forceGeneral = general != 0;
     st.numelA = plan->info.footprint_a;
     st.numelB = plan->info.footprint_b;
     st.misA = misA;

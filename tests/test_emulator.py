@@ -61,6 +61,23 @@ def test_random_problems_match_oracle():
         _check(p, size_a, perm, alpha, beta, dtype, rng)
 
 
+def test_general_tile_variant_on_every_plan():
+    """The tile kernel's general variant (shifted runs, stacked tiles) is also
+    correct on plans where hptt_exec launches the specialised one."""
+    rng = np.random.default_rng(2018)
+    seen = 0
+    for it in range(80):
+        size_a, perm = random_problem(rng, max_dims=6, max_numel=40000)
+        dtype = "f32" if it % 2 == 0 else "f64"
+        alpha, beta = CASES[it % len(CASES)]
+        p = emu.plan(perm, size_a, alpha, beta, dtype)
+        if p.info["kernel"] != "tile":
+            continue
+        seen += 1
+        _check(p, size_a, perm, alpha, beta, dtype, rng, general=True)
+    assert seen >= 20
+
+
 @pytest.mark.parametrize("knobs", [
     dict(kernel="generic"),
     dict(run_a=4, run_b=4),
