@@ -82,7 +82,8 @@ typedef struct {
     int32_t tile_order;    /* TILE: 1 = tiles in grid-digit order, 2 = diagonal
                               (second grid digit rotated by the first), 3 =
                               diagonal, with each XCD given a contiguous range
-                              of tiles */
+                              of tiles, 4 = grid-digit order with contiguous
+                              ranges per XCD */
     int32_t exact_runs;    /* TILE: 1 = chunk the runs to the target lengths even
                               where runs then do not start on 128-byte lines */
     int32_t row_passes;    /* TILE: N > 1 = stage each tile through LDS in N passes
@@ -91,6 +92,9 @@ typedef struct {
                               0 = as many as a small tile needs, 1 = none */
     int32_t min_tile;      /* TILE: smallest tile (elements) worth a workgroup round;
                               smaller tiles get longer runs or depth; 0 = 16 KiB worth */
+    int32_t block;         /* TILE: threads per workgroup, 256 or 1024, when the
+                              launch can take the specialised tile kernel (the
+                              general one always runs 256); 0 = choose */
 } hptt_options_t;
 
 /* What the plan builder decided; for inspection and tests. */
@@ -116,12 +120,14 @@ typedef struct {
     int64_t tiles;                     /* TILE: tiles; STREAM, AXPBY: 16-byte vectors;
                                           GENERIC: elements */
     int64_t grid;                      /* workgroups launched */
-    int32_t block;                     /* threads per workgroup */
+    int32_t block;                     /* threads per workgroup (TILE: of the specialised
+                                          variant; the general one runs 256) */
     int32_t hints;                     /* bit 0: non-temporal B stores; bit 1:
                                           non-temporal A loads */
     int32_t mode;                      /* 0 raw copy, 1 scale (beta = 0), 2 alpha*A + beta*B */
     int32_t tile_order;                /* TILE: 1 grid-digit order, 2 diagonal, 3 diagonal
-                                          with contiguous tile ranges per XCD */
+                                          with contiguous tile ranges per XCD, 4
+                                          grid-digit order with such ranges */
     int32_t depth;                     /* TILE: tiles stacked per workgroup round */
 } hptt_plan_info_t;
 

@@ -28,7 +28,7 @@ CFLAGS = ["-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared", "-st
 
 def compile_source(src: str, out: str) -> str:
     """Compile an oracle source file into a shared library at ``out``."""
-    tmp = out + ".tmp"
+    tmp = f"{out}.tmp{os.getpid()}"  # one per process: test workers may build at once
     subprocess.check_call(["gcc", *CFLAGS, src, "-o", tmp])
     os.replace(tmp, out)
     return out

@@ -11,6 +11,7 @@ namespace hptt {
 
 constexpr int kMaxDims = 16;  // = HPTT_MAX_DIMS
 constexpr int kBlock = 256;   // threads per workgroup: 4 waves of 64
+constexpr int kBigBlock = 1024;  // kernel T's large workgroup: 16 waves, for large tiles
 constexpr int kItems = 4;     // vectors per lane of the streaming kernels
 constexpr int kXcds = 8;      // MI355X: workgroups are dealt to 8 XCDs round robin
 
@@ -67,6 +68,7 @@ struct TileArgs {
     int32_t skew;        // 1: grid digit 1 is shifted by digit 0 (diagonal tile order)
     int32_t xcdSplit;    // 1: tile numbers dealt so that each XCD gets a contiguous range
     int32_t alignedA;    // 1 when every A run is whole 128-byte lines (set by the plan builder)
+    int32_t alignedB;    // 1 when every B run is whole 128-byte lines
     int32_t subRows;     // rows staged through LDS per pass (runB, or runB / passes)
     // Depth: nZ tiles that differ only in one more index are staged together
     // (stacked rows z*subRows + r in LDS), so that tiles of a few hundred
@@ -84,6 +86,9 @@ struct TileArgs {
     // shifted onto the grid, with partial vectors at both ends.  Same for B.
     int32_t runsOnGridA, runsOnGridB;
     int32_t misA, misB;
+    // 1 when every offset inside a tile (table entry plus position in the
+    // run) is below 2^31, so the specialised variant can use 32-bit offsets.
+    int32_t offsets32;
     int64_t cInner, cChunk, cLast;  // valid columns = cInner * min(cChunk, cLast - j*cChunk)
     int64_t rInner, rChunk, rLast;  // valid rows    = rInner * min(rChunk, rLast - j*rChunk)
     FastDiv cExt[kMaxDims];         // tile extents of the A-run indices
@@ -113,11 +118,13 @@ struct StreamArgs {
 };
 
 // Kernel T needs its general variant when a run starts off its vector grid
-// (runs shifted, partial vectors at both ends) or when tiles are stacked;
-// otherwise the specialised variant, compiled without either, is launched.
-// g.misA / g.misB must already hold the launch's pointer offsets.
+// (runs shifted, partial vectors at both ends), when tiles are stacked, or
+// when offsets inside a tile need 64 bits; otherwise the specialised
+// variant, compiled without any of these, is launched.  g.misA / g.misB must
+// already hold the launch's pointer offsets.
 __host__ __device__ inline bool tile_is_general(const TileArgs& g) {
-    return !g.runsOnGridA || !g.runsOnGridB || g.misA != 0 || g.misB != 0 || g.nZ > 1;
+    return !g.runsOnGridA || !g.runsOnGridB || g.misA != 0 || g.misB != 0 || g.nZ > 1 ||
+           !g.offsets32;
 }
 
 constexpr int log2_width(int v) { return v >= 4 ? 2 : v >= 2 ? 1 : 0; }

@@ -91,10 +91,10 @@ __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
 // Offset tables shared by every tile of the launch: rowOffA[r] is the A
 // offset of row r (a B-run position) and colOffB[c] the B offset of column c
 // (an A-run position), both relative to the tile origin.
-template <class Mem>
+template <class Mem, int BLOCK = kBlock>
 __host__ __device__ inline void tile_tables(const TileArgs& g, int tid, int64_t* rowOffA,
                                             int64_t* colOffB) {
-    for (int64_t r = tid; r < g.runB; r += kBlock) {
+    for (int64_t r = tid; r < g.runB; r += BLOCK) {
         uint32_t x = uint32_t(r);
         int64_t off = 0;
         for (int k = 0; k < g.nR; ++k) {
@@ -104,7 +104,7 @@ __host__ __device__ inline void tile_tables(const TileArgs& g, int tid, int64_t*
         }
         Mem::template lds_st<int64_t>(rowOffA, r, off);
     }
-    for (int64_t c = tid; c < g.runA; c += kBlock) {
+    for (int64_t c = tid; c < g.runA; c += BLOCK) {
         uint32_t x = uint32_t(c);
         int64_t off = 0;
         for (int k = 0; k < g.nC; ++k) {
@@ -120,6 +120,144 @@ __host__ __device__ inline void tile_tables(const TileArgs& g, int tid, int64_t*
 // 16 measured within noise of each other on MI355X; 8 was best on average).
 constexpr int kBatch = 8;
 
+// Batch of the specialised tile phases for a workgroup of BLOCK threads: a
+// 1024-thread workgroup (16 waves) keeps fewer vectors per lane, so that two
+// of them fit a CU's registers (at most 64 VGPRs per lane).
+constexpr int tile_batch(int block) { return block >= 1024 ? 4 : kBatch; }
+
+// Specialised load phase (tile_is_general() false): every run starts on the
+// A vector grid, nZ = 1, and offsets inside a tile fit 32 bits, so the
+// per-vector arithmetic is 32-bit around one 64-bit tile base pointer.  The
+// second sweep of a batch recomputes each vector's position from the batch's
+// start instead of keeping it, so only the data stays live between the two
+// (fewer registers, more resident waves).  Same thread-to-vector map as
+// tile_load.
+template <class Mem, typename T, int VA, int HINT, int BLOCK>
+__host__ __device__ inline void tile_load_fast(const TileArgs& g, const TileBase& tb, int r0,
+                                               int tid, const T* A, T* lds,
+                                               const int64_t* rowOffA) {
+    constexpr int NB = tile_batch(BLOCK);
+    const int W = (int(g.runA) + VA - 1) / VA;  // vectors per row
+    const int rows = int(imin(int64_t(g.subRows), tb.validRows - r0));
+    const int vcols = int(tb.validCols);
+    const T* Ab = A + tb.a;
+    int R = tid / W, c = tid % W;
+    const int dR = BLOCK / W, dc = BLOCK % W;
+    while (R < g.subRows) {
+        Vec<T, VA> v[NB];
+        const int R0 = R, c0 = c;
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const int cc = c * VA;
+            const int n = R < rows ? imin(VA, vcols - cc) : 0;  // valid elements
+            if (n > 0) {
+                const int off = int(Mem::template lds_ld<int64_t>(rowOffA, r0 + R)) + cc;
+                if (n == VA) {
+                    v[u] = Mem::template ld<T, VA, (HINT & kNtLoad) != 0>(Ab, off);
+                } else {
+                    for (int e = 0; e < VA; ++e)
+                        if (e < n) v[u].v[e] = Mem::template ld1<T>(Ab, off + e);
+                }
+            }
+            c += dc;
+            R += dR;
+            if (c >= W) {
+                c -= W;
+                R += 1;
+            }
+        }
+        R = R0;
+        c = c0;
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const int cc = c * VA;
+            const int n = R < rows ? imin(VA, vcols - cc) : 0;
+            const int at = R * g.pitch + cc;
+#pragma unroll
+            for (int e = 0; e < VA; ++e)
+                if (e < n) Mem::template lds_st<T>(lds, at + e, v[u].v[e]);
+            c += dc;
+            R += dR;
+            if (c >= W) {
+                c -= W;
+                R += 1;
+            }
+        }
+    }
+}
+
+// Specialised store phase, the counterpart of tile_load_fast.
+template <class Mem, typename T, int VB, int MODE, int HINT, int BLOCK>
+__host__ __device__ inline void tile_store_fast(const TileArgs& g, const TileBase& tb, int r0,
+                                                int tid, T* B, const T* lds,
+                                                const int64_t* colOffB, T alpha, T beta) {
+    constexpr int NB = tile_batch(BLOCK);
+    const int W = (g.subRows + VB - 1) / VB;  // vectors per column
+    const int rows = int(imin(int64_t(g.subRows), tb.validRows - r0));
+    const int vcols = int(tb.validCols);
+    T* Bb = B + tb.b + r0;
+    int q = tid / W, s = tid % W;
+    const int dq = BLOCK / W, ds = BLOCK % W;
+    while (q < int(g.runA)) {
+        Vec<T, VB> x[NB], y[NB];
+        const int q0 = q, s0 = s;
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const int ss = s * VB;
+            const int n = q < vcols ? imin(VB, rows - ss) : 0;
+            if (n > 0) {
+                const int base = ss * g.pitch + q;
+#pragma unroll
+                for (int e = 0; e < VB; ++e)
+                    if (e < n) x[u].v[e] = Mem::template lds_ld<T>(lds, base + e * g.pitch);
+                if (MODE == kAxpby) {
+                    const int off = int(Mem::template lds_ld<int64_t>(colOffB, q)) + ss;
+                    if (n == VB) {
+                        y[u] = Mem::template ld<T, VB, false>(Bb, off);
+                    } else {
+                        for (int e = 0; e < VB; ++e)
+                            if (e < n) y[u].v[e] = Mem::template ld1<T>(Bb, off + e);
+                    }
+                }
+            }
+            s += ds;
+            q += dq;
+            if (s >= W) {
+                s -= W;
+                q += 1;
+            }
+        }
+        q = q0;
+        s = s0;
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const int ss = s * VB;
+            const int n = q < vcols ? imin(VB, rows - ss) : 0;
+            if (n > 0) {
+                const int off = int(Mem::template lds_ld<int64_t>(colOffB, q)) + ss;
+                Vec<T, VB> zv;
+#pragma unroll
+                for (int e = 0; e < VB; ++e)
+                    zv.v[e] =
+                        update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
+                if (n == VB) {
+                    Mem::template st<(HINT & kNtStore) != 0, T, VB>(Bb, off, zv);
+                } else {
+                    for (int e = 0; e < VB; ++e)
+                        if (e < n)
+                            Mem::template st1<(HINT & kNtStore) != 0, T>(Bb, off + e, zv.v[e]);
+                }
+            }
+            s += ds;
+            q += dq;
+            if (s >= W) {
+                s -= W;
+                q += 1;
+            }
+        }
+    }
+}
+
 // Load phase of the pass over tile rows [r0, r0 + subRows) of each of the
 // nZ stacked tiles: the rows are contiguous runs of A.  Stacked row R holds
 // row r = R mod subRows of depth z = R / subRows and lands in LDS row R.
@@ -128,10 +266,15 @@ constexpr int kBatch = 8;
 // the A vector grid: a run that starts off it is covered by one more vector,
 // its first and last ones partial (element loads).  GEN = false compiles the
 // common case without either (tile_is_general() is false): every run starts
-// on the grid and nZ = 1.
-template <class Mem, typename T, int VA, int HINT, bool GEN>
+// on the grid and nZ = 1 (tile_load_fast).
+template <class Mem, typename T, int VA, int HINT, bool GEN, int BLOCK = kBlock>
 __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb, int64_t r0,
                                           int tid, const T* A, T* lds, const int64_t* rowOffA) {
+    static_assert(!GEN || BLOCK == kBlock, "the general variant runs kBlock threads");
+    if constexpr (!GEN) {
+        tile_load_fast<Mem, T, VA, HINT, BLOCK>(g, tb, int(r0), tid, A, lds, rowOffA);
+        return;
+    }
     const bool shift = GEN && (!g.runsOnGridA || g.misA != 0);
     const bool depth = GEN && g.nZ > 1;
     const int64_t W = (g.runA + (shift ? VA - 1 : 0) + VA - 1) / VA;  // vectors per row
@@ -195,10 +338,16 @@ __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb,
 // fastest, gathers each vector's VB elements from consecutive LDS rows, and
 // writes it to B (reading B first when beta != 0).  Vectors sit on the B
 // vector grid, as in the load phase.
-template <class Mem, typename T, int VB, int MODE, int HINT, bool GEN>
+template <class Mem, typename T, int VB, int MODE, int HINT, bool GEN, int BLOCK = kBlock>
 __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb, int64_t r0,
                                            int tid, T* B, const T* lds, const int64_t* colOffB,
                                            T alpha, T beta) {
+    static_assert(!GEN || BLOCK == kBlock, "the general variant runs kBlock threads");
+    if constexpr (!GEN) {
+        tile_store_fast<Mem, T, VB, MODE, HINT, BLOCK>(g, tb, int(r0), tid, B, lds, colOffB, alpha,
+                                                       beta);
+        return;
+    }
     const bool shift = GEN && (!g.runsOnGridB || g.misB != 0);
     const bool depth = GEN && g.nZ > 1;
     const int64_t W = (g.subRows + (shift ? VB - 1 : 0) + VB - 1) / VB;  // vectors per column

@@ -137,10 +137,20 @@ hptt_status_t launch(const hptt_plan_s* p, const void* A, void* B, hipStream_t s
         targs.misB = int32_t((pb / uintptr_t(elem)) % uintptr_t(vb));
     }
     const void* fn = nullptr;
+    int block = kBlock;
     if (tile) {
+        // the general variant (less aligned pointers, stacking) runs kBlock threads
         const bool general = tile_is_general(targs);
-        fn = sizeof(T) == 4 ? tile_kernel_f32(general, in.mode, in.hints, va, vb)
-                            : tile_kernel_f64(general, in.mode, in.hints, va, vb);
+        block = general ? kBlock : in.block;
+        // Runs that are whole lines relative to the tensors' first elements
+        // are not whole lines in memory when those are not on a line: lines
+        // are then shared between tiles, so no non-temporal hint (see the
+        // plan builder).
+        int hints = in.hints;
+        if (pb % 128 != 0) hints &= ~kNtStore;
+        if (pa % 128 != 0) hints &= ~kNtLoad;
+        fn = sizeof(T) == 4 ? tile_kernel_f32(general, in.mode, hints, va, vb, block)
+                            : tile_kernel_f64(general, in.mode, hints, va, vb, block);
     } else {
         fn = select_mode<T>(p, va, vb);
     }
@@ -164,7 +174,11 @@ hptt_status_t launch(const hptt_plan_s* p, const void* A, void* B, hipStream_t s
         case HPTT_KERNEL_GENERIC: args[2] = const_cast<GenericArgs*>(&p->generic); break;
         default: return HPTT_ERROR_INVALID_ARGUMENT;
     }
-    hipError_t err = hipLaunchKernel(fn, dim3(uint32_t(in.grid)), dim3(kBlock), args, lds, stream);
+    hipError_t err = hipSuccess;
+    if (lds > 64 * 1024)  // gfx950 has 160 KiB of LDS per CU; above 64 KiB it must be asked for
+        err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+    if (err == hipSuccess)
+        err = hipLaunchKernel(fn, dim3(uint32_t(in.grid)), dim3(block), args, lds, stream);
     if (err != hipSuccess) {
         g_last_hip_error = int32_t(err);
         return HPTT_ERROR_HIP;

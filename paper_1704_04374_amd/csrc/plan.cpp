@@ -19,6 +19,7 @@ int64_t tile_lds_bytes_host(const TileArgs& t, int elem) {
 namespace {
 
 constexpr int64_t kLdsMax = 64 * 1024;     // LDS a kernel-T workgroup may use
+constexpr int64_t kLdsMaxBig = 152 * 1024; // ... with kBigBlock threads (one per CU)
 constexpr int64_t kLdsBudget = 40 * 1024;  // preferred: at least 4 workgroups per CU
 constexpr int64_t kLine = 128;             // L2 cache line of gfx950
 constexpr int64_t kVecBytes = 16;          // widest global access per lane (dwordx4)
@@ -151,9 +152,9 @@ int64_t stride_gcd(const Fused& f, const int64_t* stride, const bool* which) {
 // start at multiples of gcd(chunk stride, `other`), where `other` is the gcd
 // of the strides of every index outside the run.  With `aligned`, only chunks
 // whose runs start and end on 128-byte lines qualify (no line is then shared
-// between workgroups); returns 0 if there is none.  Among the candidates: no
-// partial edge tile first, then the length closest to target, where falling
-// short counts double.
+// between workgroups); returns 0 if there is none.  Among the candidates: the
+// length closest to target, where falling short counts double and a partial
+// last chunk counts by the share of lanes it leaves idle.
 int64_t choose_chunk(int64_t inner, int64_t n, int64_t other, int64_t target, int elem,
                      bool aligned) {
     int64_t best = 0;
@@ -168,9 +169,13 @@ int64_t choose_chunk(int64_t inner, int64_t n, int64_t other, int64_t target, in
         const int64_t gran = gcd64(k < n ? run : 0, other);
         const bool lineAligned = (gran * elem) % kLine == 0 && (run * elem) % kLine == 0;
         if (aligned && !lineAligned) continue;
-        // a run shorter than the target costs twice as much as a longer one
+        // a run shorter than the target costs twice as much as a longer one;
+        // a chunk that does not divide the extent costs the share of the
+        // chunks' elements its last, partial chunk leaves idle
         const double ratio = log2(double(run) / double(target));
-        const double score = (n % k != 0 ? 2.0 : 0.0) + (ratio < 0 ? -2.0 * ratio : ratio);
+        const int64_t chunks = (n + k - 1) / k;
+        const double idle = double(chunks * k - n) / double(chunks * k);
+        const double score = 6.0 * idle + (ratio < 0 ? -2.0 * ratio : ratio);
         if (score < bestScore) {
             bestScore = score;
             best = k;
@@ -316,9 +321,9 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     }
     info.depth = t.nZ;
     t.nG = g;
-    t.skew = (g >= 2 && opt.tile_order != 1) ? 1 : 0;
-    t.xcdSplit = opt.tile_order == 3 ? 1 : 0;
-    info.tile_order = t.xcdSplit ? 3 : t.skew ? 2 : 1;
+    t.skew = (g >= 2 && opt.tile_order != 1 && opt.tile_order != 4) ? 1 : 0;
+    t.xcdSplit = (opt.tile_order == 3 || opt.tile_order == 4) ? 1 : 0;
+    info.tile_order = t.xcdSplit ? (t.skew ? 3 : 4) : t.skew ? 2 : 1;
     for (int j = 0; j < g; ++j) {
         if (ext[j] >= (int64_t(1) << 32)) return false;
         set_div(t.gExt[j], ext[j]);
@@ -350,6 +355,7 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     // A runs that start and end on 128-byte lines share no line with another
     // tile, so they can be read with non-temporal loads.
     t.alignedA = (granA == 0 || (granA * elem) % kLine == 0) && (t.runA * elem) % kLine == 0;
+    t.alignedB = (granB == 0 || (granB * elem) % kLine == 0) && (t.runB * elem) % kLine == 0;
     // Rows staged through LDS per pass: the whole tile by default.  Staging a
     // tile in several passes keeps its run lengths with less LDS, but each
     // pass adds a barrier round trip; on MI355X that cost more than it saved
@@ -362,6 +368,13 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     }
     set_div(t.zRows, t.subRows);
     set_div(t.zCols, t.runA);
+    // Largest offset inside a tile: the last row's A offset plus the run,
+    // and the last column's B offset plus the B run.
+    int64_t maxRowA = 0, maxColB = 0;
+    for (int j = 0; j < nR; ++j) maxRowA += (int64_t(t.rExt[j].d) - 1) * t.rStrideA[j];
+    for (int j = 0; j < nC; ++j) maxColB += (int64_t(t.cExt[j].d) - 1) * t.cStrideB[j];
+    t.offsets32 = (maxRowA + t.runA < (int64_t(1) << 31) && maxColB + t.runB < (int64_t(1) << 31))
+                      ? 1 : 0;
     const int64_t lds = tile_lds_bytes_host(t, elem);
     if (lds > ldsBudget) return false;
     info.run_a = t.runA;
@@ -460,9 +473,9 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
         opt.kernel == HPTT_KERNEL_NONE || opt.run_a < 0 || opt.run_b < 0 || opt.max_vec < 0 ||
         opt.store_hint < 0 || opt.store_hint > 2 || opt.load_hint < 0 || opt.load_hint > 2 ||
         opt.lds_pad < -1 || opt.lds_pad > 64 || opt.max_blocks < 0 || opt.tile_order < 0 ||
-        opt.tile_order > 3 || opt.row_passes < 0 || opt.row_passes > 64 || opt.depth < 0 ||
+        opt.tile_order > 4 || opt.row_passes < 0 || opt.row_passes > 64 || opt.depth < 0 ||
         opt.depth > 4096 || opt.min_tile < 0 || opt.exact_runs < 0 ||
-        opt.exact_runs > 1)
+        opt.exact_runs > 1 || (opt.block != 0 && opt.block != kBlock && opt.block != kBigBlock))
         return HPTT_ERROR_INVALID_ARGUMENT;
 
     const int elem = dtype == HPTT_FLOAT32 ? 4 : 8;
@@ -540,7 +553,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
         const int64_t tA0 = opt.run_a > 0 ? opt.run_a : 512 / elem;
         const int64_t tB0 = opt.run_b > 0 ? opt.run_b : kLine / elem;
         struct Stage { bool alignA, alignB; int64_t budget; };
-        const Stage forced[] = {{false, false, kLdsMax}};
+        const Stage forced[] = {{false, false, opt.block == kBigBlock ? kLdsMaxBig : kLdsMax}};
         const Stage stages[] = {{true, true, kLdsBudget},  {false, true, kLdsBudget},
                                 {true, false, kLdsBudget}, {false, false, kLdsBudget},
                                 {true, true, kLdsMax},     {false, false, kLdsMax}};
@@ -595,6 +608,35 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
                 }
             }
         }
+        // B runs that cannot start and end on 128-byte lines leave a partly
+        // written line at each end, shared with the neighbouring tile; runs
+        // of four lines halve the share of such lines against one-line runs
+        // (MI355X, 3251-element B rows: 64x128 tiles 1.3x faster than
+        // 128x32), so the A run gives way to a longer B run.
+        if (ok && !plan->tile.alignedB && opt.run_a == 0 && opt.run_b == 0 &&
+            opt.exact_runs == 0) {
+            const int64_t runB = plan->tile.runB;
+            TileArgs keep = plan->tile;
+            hptt_plan_info_t keepInfo = info;
+            const int64_t lB = 4 * kLine / elem;
+            bool longer = false;
+            // A runs of two lines, else one (a B-run length that divides the
+            // index may need the room)
+            for (int64_t lA = 2 * kLine / elem; runB < lB && lA >= kLine / elem && !longer;
+                 lA /= 2) {
+                longer = setup_tile(f, elem, lA, lB, opt, false, false, kLdsBudget, minTile,
+                                    plan->tile, info) &&
+                         plan->tile.runB > runB;
+                if (longer) {
+                    tA = lA;
+                    tB = lB;
+                }
+            }
+            if (!longer) {
+                plan->tile = keep;
+                info = keepInfo;
+            }
+        }
         // Small problems: shorter runs (down to one 128-byte line) for more
         // tiles, so that more CUs take part.
         while (ok && opt.run_a == 0 && opt.run_b == 0 && plan->tile.numTiles < 512 &&
@@ -617,6 +659,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
         } else {
             const int64_t grid = plan->tile.numTiles;
             info.grid = grid < maxBlocks ? grid : maxBlocks;
+            info.block = opt.block > 0 ? opt.block : kBlock;
         }
     }
     if (k == HPTT_KERNEL_STREAM) {
@@ -647,10 +690,14 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
         info.grid = grid < maxBlocks ? grid : maxBlocks;
     }
     // Cache hints.  Every element is touched once, so by default B is written
-    // and A read with non-temporal hints, except A runs that share 128-byte
-    // lines with a neighbouring tile (the neighbour would miss the line).
+    // and A read with non-temporal hints, except runs that share 128-byte
+    // lines with a neighbouring tile: an A line read non-temporally is gone
+    // when the neighbour wants it, and a partly written B line stored
+    // non-temporally reaches HBM as a partial write instead of being merged
+    // with the neighbour's part in L2 (2-3.5x slower on MI355X).
     const bool loadOk = k != HPTT_KERNEL_TILE || plan->tile.alignedA;
-    const bool ntStore = opt.store_hint != 2;
+    const bool storeOk = k != HPTT_KERNEL_TILE || plan->tile.alignedB;
+    const bool ntStore = opt.store_hint == 1 || (opt.store_hint == 0 && storeOk);
     const bool ntLoad = opt.load_hint == 1 || (opt.load_hint == 0 && loadOk && k != HPTT_KERNEL_GENERIC);
     info.hints = (ntStore ? kNtStore : 0) | (ntLoad ? kNtLoad : 0);
     info.kernel = k;

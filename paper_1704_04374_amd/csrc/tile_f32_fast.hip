@@ -3,8 +3,8 @@
 
 namespace hptt {
 
-const void* tile_kernel_f32_fast(int mode, int hints, int va, int vb) {
-    return tile_kernel_address<float, false>(mode, hints, va, vb);
+const void* tile_kernel_f32_fast(int mode, int hints, int va, int vb, int block) {
+    return tile_kernel_address<float, false>(mode, hints, va, vb, block);
 }
 
 }  // namespace hptt

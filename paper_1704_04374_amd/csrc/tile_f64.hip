@@ -4,17 +4,17 @@
 
 namespace hptt {
 
-const void* tile_kernel_f32_fast(int mode, int hints, int va, int vb);
-const void* tile_kernel_f32_general(int mode, int hints, int va, int vb);
+const void* tile_kernel_f32_fast(int mode, int hints, int va, int vb, int block);
+const void* tile_kernel_f32_general(int mode, int hints, int va, int vb, int block);
 
-const void* tile_kernel_f32(bool general, int mode, int hints, int va, int vb) {
-    return general ? tile_kernel_f32_general(mode, hints, va, vb)
-                   : tile_kernel_f32_fast(mode, hints, va, vb);
+const void* tile_kernel_f32(bool general, int mode, int hints, int va, int vb, int block) {
+    return general ? tile_kernel_f32_general(mode, hints, va, vb, block)
+                   : tile_kernel_f32_fast(mode, hints, va, vb, block);
 }
 
-const void* tile_kernel_f64(bool general, int mode, int hints, int va, int vb) {
-    return general ? tile_kernel_address<double, true>(mode, hints, va, vb)
-                   : tile_kernel_address<double, false>(mode, hints, va, vb);
+const void* tile_kernel_f64(bool general, int mode, int hints, int va, int vb, int block) {
+    return general ? tile_kernel_address<double, true>(mode, hints, va, vb, block)
+                   : tile_kernel_address<double, false>(mode, hints, va, vb, block);
 }
 
 }  // namespace hptt

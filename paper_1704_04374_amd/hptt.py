@@ -42,7 +42,8 @@ class Options(ctypes.Structure):
                 ("load_hint", ctypes.c_int32), ("lds_pad", ctypes.c_int32),
                 ("max_blocks", ctypes.c_int32), ("tile_order", ctypes.c_int32),
                 ("exact_runs", ctypes.c_int32), ("row_passes", ctypes.c_int32),
-                ("depth", ctypes.c_int32), ("min_tile", ctypes.c_int32)]
+                ("depth", ctypes.c_int32), ("min_tile", ctypes.c_int32),
+                ("block", ctypes.c_int32)]
 
 
 class AutotuneReport(ctypes.Structure):

@@ -21,7 +21,7 @@ def build() -> str:
     hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
     srcs = [os.path.join(HERE, "emulate.cpp"), os.path.join(CSRC, "plan.cpp"),
             os.path.join(CSRC, "api.cpp")]
-    tmp = LIB + ".tmp"
+    tmp = f"{LIB}.tmp{os.getpid()}"  # one per process: test workers may build at once
     cmd = [hipcc, "-x", "hip", "--offload-host-only", "-O2", "-g", "-std=c++17", "-fPIC",
            "-shared", "-ffp-contract=off", "-Wall", f"-I{INCLUDE}", f"-I{CSRC}", *srcs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -52,11 +52,26 @@ void fail(const char* what, long long a, long long b) {
     if (S->errors++ == 0) snprintf(S->msg, sizeof(S->msg), "%s (%lld, %lld)", what, a, b);
 }
 
+// Whether p points at one of the n elements from base on; its offset from
+// base goes to *rel.
 template <typename T>
-bool check_global(const T* p, int64_t off, int V, bool isStore) {
-    const bool isA = static_cast<const void*>(p) == S->A;
-    const bool isB = static_cast<const void*>(p) == S->B;
+bool points_into(const T* p, const void* base, int64_t n, int64_t* rel) {
+    const intptr_t d = reinterpret_cast<intptr_t>(p) - reinterpret_cast<intptr_t>(base);
+    if (d < 0 || d % intptr_t(sizeof(T)) != 0 || d / intptr_t(sizeof(T)) >= n) return false;
+    *rel = d / intptr_t(sizeof(T));
+    return true;
+}
+
+// Kernels may address a tensor from its first element or from a pointer
+// inside it (a tile's base); off is turned into an offset from the first
+// element before every check.
+template <typename T>
+bool check_global(const T* p, int64_t& off, int V, bool isStore) {
+    int64_t rel = 0;
+    const bool isA = points_into(p, S->A, S->numelA, &rel);
+    const bool isB = !isA && points_into(p, S->B, S->numelB, &rel);
     if (!isA && !isB) { fail("access to an unknown buffer", off, V); return false; }
+    off += rel;
     if (isA && isStore) { fail("store into A", off, V); return false; }
     if (isB && !isStore && !S->readsB) { fail("B read although beta == 0", off, V); return false; }
     if (off < 0 || off + V > (isA ? S->numelA : S->numelB)) {
@@ -84,28 +99,32 @@ struct HostMem {
     static hptt::Vec<T, V> ld(const T* p, int64_t off) {
         hptt::Vec<T, V> r;
         memset(&r, 0, sizeof(r));
-        if (check_global(p, off, V, false) && !S->dry) memcpy(&r, p + off, sizeof(r));
+        int64_t at = off;  // offset from the tensor's first element
+        if (check_global(p, at, V, false) && !S->dry) memcpy(&r, p + off, sizeof(r));
         return r;
     }
     template <typename T>
     static T ld1(const T* p, int64_t off) {
         T r = T(0);
-        if (check_global(p, off, 1, false) && !S->dry) r = p[off];
+        int64_t at = off;
+        if (check_global(p, at, 1, false) && !S->dry) r = p[off];
         return r;
     }
     template <bool NT, typename T, int V>
     static void st(T* p, int64_t off, const hptt::Vec<T, V>& v) {
-        if (!check_global(p, off, V, true)) return;
+        int64_t at = off;
+        if (!check_global(p, at, V, true)) return;
         if (!S->dry) memcpy(p + off, &v, sizeof(v));
         if (S->counts)
             for (int e = 0; e < V; ++e)
-                if (S->counts[off + e] < 255) ++S->counts[off + e];
+                if (S->counts[at + e] < 255) ++S->counts[at + e];
     }
     template <bool NT, typename T>
     static void st1(T* p, int64_t off, T v) {
-        if (!check_global(p, off, 1, true)) return;
+        int64_t at = off;
+        if (!check_global(p, at, 1, true)) return;
         if (!S->dry) p[off] = v;
-        if (S->counts && S->counts[off] < 255) ++S->counts[off];
+        if (S->counts && S->counts[at] < 255) ++S->counts[at];
     }
     template <typename T>
     static T lds_ld(const T* l, int64_t i) {
@@ -125,8 +144,8 @@ void clear_written(int64_t from, int64_t to) {
     memset(S->written.data() + from, 0, size_t(to - from));
 }
 
-// Mirrors tile_kernel in tile_kernel.h, in the variant GEN.
-template <typename T, int VA, int VB, int MODE, int NT, bool GEN>
+// Mirrors tile_kernel in tile_kernel.h, in the variant GEN with BLOCK threads.
+template <typename T, int VA, int VB, int MODE, int NT, bool GEN, int BLOCK>
 void emu_tile_variant(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     using namespace hptt;
     TileArgs g = p->tile;  // with the base pointers' offsets from the vector grid, as at launch
@@ -143,31 +162,36 @@ void emu_tile_variant(const hptt_plan_s* p, const T* A, T* B, int64_t blockStrid
     const int64_t grid = p->info.grid;
     for (int64_t blk = 0; blk < grid && S->errors == 0; blk += blockStride) {
         clear_written(0, ldsBytes);
-        for (int tid = 0; tid < kBlock; ++tid) tile_tables<HostMem>(g, tid, rowOffA, colOffB);
+        for (int tid = 0; tid < BLOCK; ++tid) tile_tables<HostMem, BLOCK>(g, tid, rowOffA, colOffB);
         for (int64_t t = blk; t < g.numTiles && S->errors == 0; t += grid) {
             const TileBase tb = tile_base(g, uint32_t(t));
             for (int64_t r0 = 0; r0 < tb.validRows && S->errors == 0; r0 += g.subRows) {
                 clear_written(tableBytes, ldsBytes);
-                for (int tid = 0; tid < kBlock; ++tid)
-                    tile_load<HostMem, T, VA, NT, GEN>(g, tb, r0, tid, A, lds, rowOffA);
-                for (int tid = 0; tid < kBlock; ++tid)
-                    tile_store<HostMem, T, VB, MODE, NT, GEN>(g, tb, r0, tid, B, lds, colOffB,
-                                                              alpha, beta);
+                for (int tid = 0; tid < BLOCK; ++tid)
+                    tile_load<HostMem, T, VA, NT, GEN, BLOCK>(g, tb, r0, tid, A, lds, rowOffA);
+                for (int tid = 0; tid < BLOCK; ++tid)
+                    tile_store<HostMem, T, VB, MODE, NT, GEN, BLOCK>(g, tb, r0, tid, B, lds,
+                                                                     colOffB, alpha, beta);
             }
         }
     }
 }
 
-// The variant hptt_exec would launch (or the general one when forced).
+// The variant and workgroup size hptt_exec would launch (or the general
+// variant when forced).
 template <typename T, int VA, int VB, int MODE, int NT>
 void emu_tile(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
+    using hptt::kBlock;
+    using hptt::kBigBlock;
     hptt::TileArgs g = p->tile;
     g.misA = int32_t(S->misA % VA);
     g.misB = int32_t(S->misB % VB);
     if (S->forceGeneral || hptt::tile_is_general(g))
-        emu_tile_variant<T, VA, VB, MODE, NT, true>(p, A, B, blockStride);
+        emu_tile_variant<T, VA, VB, MODE, NT, true, kBlock>(p, A, B, blockStride);
+    else if (p->info.block == kBigBlock)
+        emu_tile_variant<T, VA, VB, MODE, NT, false, kBigBlock>(p, A, B, blockStride);
     else
-        emu_tile_variant<T, VA, VB, MODE, NT, false>(p, A, B, blockStride);
+        emu_tile_variant<T, VA, VB, MODE, NT, false, kBlock>(p, A, B, blockStride);
 }
 
 // Mirrors stream_kernel in kernels.hip.

@@ -92,6 +92,7 @@ def test_general_tile_variant_on_every_plan():
     dict(load_hint=1, store_hint=1),
     dict(tile_order=1),
     dict(tile_order=3),
+    dict(tile_order=4),
     dict(row_passes=2),
     dict(row_passes=3, max_blocks=7),
     dict(row_passes=5, run_a=8, run_b=40),
@@ -101,6 +102,10 @@ def test_general_tile_variant_on_every_plan():
     dict(run_a=64, run_b=64),
     dict(run_a=512, run_b=8),
     dict(exact_runs=1, run_a=6, run_b=10),
+    dict(block=1024),
+    dict(block=1024, run_a=96, run_b=160),
+    dict(block=1024, row_passes=2, max_blocks=9),
+    dict(block=1024, tile_order=3),
 ])
 def test_knobs_match_oracle(knobs):
     rng = np.random.default_rng(11)
@@ -141,8 +146,10 @@ def test_small_workload_matches_oracle(w):
 
 
 @pytest.mark.parametrize("knobs", [dict(), dict(tile_order=1), dict(tile_order=3),
-                                   dict(row_passes=3)],
-                         ids=["default", "digit_order", "xcd_order", "three_passes"])
+                                   dict(tile_order=4), dict(block=1024), dict(row_passes=3)],
+                         ids=["default", "digit_order", "xcd_order", "xcd_digit_order",
+                              "block1024",
+                              "three_passes"])
 @pytest.mark.parametrize("w", WORKLOADS, ids=lambda w: w.name)
 def test_full_size_geometry(w, knobs):
     """Dry run of every workgroup of each full-size workload: every offset in

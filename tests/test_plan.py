@@ -184,8 +184,9 @@ def test_null_arguments():
 
 @pytest.mark.parametrize("field,value", [("kernel", 9), ("kernel", 1), ("run_a", -1),
                                          ("store_hint", 3), ("load_hint", -1), ("lds_pad", 65),
-                                         ("max_blocks", -2), ("tile_order", 4), ("exact_runs", 2),
-                                         ("row_passes", -1), ("row_passes", 65)])
+                                         ("max_blocks", -2), ("tile_order", 5), ("exact_runs", 2),
+                                         ("row_passes", -1), ("row_passes", 65), ("block", 512),
+                                         ("block", -1)])
 def test_invalid_options(field, value):
     opt = hptt.Options()
     setattr(opt, field, value)
