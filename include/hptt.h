@@ -95,6 +95,8 @@ typedef struct {
     int32_t block;         /* TILE: threads per workgroup, 256 or 1024, when the
                               launch can take the specialised tile kernel (the
                               general one always runs 256); 0 = choose */
+    int32_t skew;          /* TILE: diagonal orders rotate the second grid digit by
+                              skew times the first; 0 = 1 */
 } hptt_options_t;
 
 /* What the plan builder decided; for inspection and tests. */

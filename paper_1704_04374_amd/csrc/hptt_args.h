@@ -65,7 +65,7 @@ struct TileArgs {
     uint32_t numTiles;
     int32_t gChunkC;     // grid digit that counts chunks of the last A-run index, or -1
     int32_t gChunkR;     // grid digit that counts chunks of the last B-run index, or -1
-    int32_t skew;        // 1: grid digit 1 is shifted by digit 0 (diagonal tile order)
+    int32_t skew;        // s > 0: grid digit 1 is shifted by s times digit 0 (diagonal order)
     int32_t xcdSplit;    // 1: tile numbers dealt so that each XCD gets a contiguous range
     int32_t alignedA;    // 1 when every A run is whole 128-byte lines (set by the plan builder)
     int32_t alignedB;    // 1 when every B run is whole 128-byte lines

@@ -46,8 +46,8 @@ struct TileBase {
     int64_t validDepth;  // stacked tiles inside the tensor
 };
 
-// Split the tile number into grid digits (fastest first).  With g.skew the
-// second digit is rotated by the first (j1 <- (j1 + j0) mod n1), a bijection
+// Split the tile number into grid digits (fastest first).  With g.skew = s the
+// second digit is rotated by the first (j1 <- (j1 + s*j0) mod n1), a bijection
 // of the tiles: workgroups that run at the same time then start their B runs
 // (and A runs) at many different offsets modulo a power-of-two stride instead
 // of one, which spreads their traffic over the HBM channels.
@@ -74,7 +74,8 @@ __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
         t = q;
         if (k == 0) j0 = jj;
         if (k == 1 && g.skew) {
-            const uint32_t r = j0 - fast_div(j0, g.gExt[1]) * g.gExt[1].d;  // j0 mod n1
+            const uint32_t js = j0 * uint32_t(g.skew);  // below 2^32: checked by the plan
+            const uint32_t r = js - fast_div(js, g.gExt[1]) * g.gExt[1].d;  // (s*j0) mod n1
             jj += r;
             if (jj >= g.gExt[1].d) jj -= g.gExt[1].d;
         }

@@ -321,7 +321,9 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     }
     info.depth = t.nZ;
     t.nG = g;
-    t.skew = (g >= 2 && opt.tile_order != 1 && opt.tile_order != 4) ? 1 : 0;
+    t.skew = (g >= 2 && opt.tile_order != 1 && opt.tile_order != 4) ? (opt.skew > 0 ? opt.skew : 1)
+                                                                     : 0;
+    if (t.skew > 1 && uint64_t(ext[0]) * uint64_t(t.skew) >= (uint64_t(1) << 32)) t.skew = 1;
     t.xcdSplit = (opt.tile_order == 3 || opt.tile_order == 4) ? 1 : 0;
     info.tile_order = t.xcdSplit ? (t.skew ? 3 : 4) : t.skew ? 2 : 1;
     for (int j = 0; j < g; ++j) {
@@ -475,7 +477,8 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
         opt.lds_pad < -1 || opt.lds_pad > 64 || opt.max_blocks < 0 || opt.tile_order < 0 ||
         opt.tile_order > 4 || opt.row_passes < 0 || opt.row_passes > 64 || opt.depth < 0 ||
         opt.depth > 4096 || opt.min_tile < 0 || opt.exact_runs < 0 ||
-        opt.exact_runs > 1 || (opt.block != 0 && opt.block != kBlock && opt.block != kBigBlock))
+        opt.exact_runs > 1 || (opt.block != 0 && opt.block != kBlock && opt.block != kBigBlock) ||
+        opt.skew < 0 || opt.skew > 1024)
         return HPTT_ERROR_INVALID_ARGUMENT;
 
     const int elem = dtype == HPTT_FLOAT32 ? 4 : 8;

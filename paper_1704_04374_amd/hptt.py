@@ -43,7 +43,7 @@ class Options(ctypes.Structure):
                 ("max_blocks", ctypes.c_int32), ("tile_order", ctypes.c_int32),
                 ("exact_runs", ctypes.c_int32), ("row_passes", ctypes.c_int32),
                 ("depth", ctypes.c_int32), ("min_tile", ctypes.c_int32),
-                ("block", ctypes.c_int32)]
+                ("block", ctypes.c_int32), ("skew", ctypes.c_int32)]
 
 
 class AutotuneReport(ctypes.Structure):

@@ -106,6 +106,8 @@ def test_general_tile_variant_on_every_plan():
     dict(block=1024, run_a=96, run_b=160),
     dict(block=1024, row_passes=2, max_blocks=9),
     dict(block=1024, tile_order=3),
+    dict(skew=3),
+    dict(skew=7, tile_order=3),
 ])
 def test_knobs_match_oracle(knobs):
     rng = np.random.default_rng(11)

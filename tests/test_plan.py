@@ -186,7 +186,7 @@ def test_null_arguments():
                                          ("store_hint", 3), ("load_hint", -1), ("lds_pad", 65),
                                          ("max_blocks", -2), ("tile_order", 5), ("exact_runs", 2),
                                          ("row_passes", -1), ("row_passes", 65), ("block", 512),
-                                         ("block", -1)])
+                                         ("block", -1), ("skew", -1), ("skew", 1025)])
 def test_invalid_options(field, value):
     opt = hptt.Options()
     setattr(opt, field, value)
