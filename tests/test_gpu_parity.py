@@ -104,7 +104,10 @@ def test_random_sweep():
                                    dict(tile_order=1), dict(tile_order=3), dict(run_a=512, run_b=8),
                                    dict(row_passes=3), dict(row_passes=2, max_blocks=5),
                                    dict(run_a=64, run_b=64, max_blocks=5),
-                                   dict(exact_runs=1, run_a=6, run_b=10)],
+                                   dict(exact_runs=1, run_a=6, run_b=10),
+                                   dict(block=1024), dict(block=1024, run_a=64, run_b=64),
+                                   dict(block=1024, max_blocks=5), dict(tile_order=4),
+                                   dict(skew=3), dict(store_hint=2, load_hint=2)],
                          ids=lambda k: ",".join(f"{a}={b}" for a, b in k.items()))
 def test_forced_variants(knobs):
     rng = np.random.default_rng(99)
@@ -112,6 +115,31 @@ def test_forced_variants(knobs):
                          ((24, 20, 16, 5, 3), (4, 2, 0, 3, 1)), ((3, 2, 64, 9, 32), (4, 2, 0, 3, 1))]:
         for dtype, (alpha, beta) in (("f32", (1.0, 0.0)), ("f64", (1.5, -0.5))):
             _run_case(size_a, perm, alpha, beta, dtype, rng, **knobs)
+
+
+@pytest.mark.parametrize("name,knobs", [
+    ("transpose6d_24x20x16x24x18x20_f32", dict(exact_runs=1, run_a=96, run_b=160, block=1024)),
+    ("transpose6d_24x20x16x24x18x20_f32", dict(exact_runs=1, run_a=96, run_b=320, block=1024)),
+    ("transpose5d_3x2x640x480x96_f32", dict(exact_runs=1, run_a=192, run_b=96, block=1024)),
+    ("transpose2d_8192x8192_f32", dict(block=1024, tile_order=4))],
+    ids=lambda x: x if isinstance(x, str) else ",".join(f"{a}={b}" for a, b in x.items()))
+def test_large_tiles_full_size(name, knobs):
+    """1024-thread workgroups and tiles above 64 KiB of LDS, at full size,
+    against the whole oracle result."""
+    from paper_1704_04374_amd.workloads import BY_NAME
+    w = BY_NAME[name]
+    _say(f"[parity] {w.describe()} {knobs}")
+    A, B0 = inputs(w)
+    if B0 is None:
+        B0 = torch.full_like(A, float("nan"))
+    want = orc.transpose(A.numpy(), w.size_a, w.perm, w.alpha, w.beta,
+                         B0.numpy() if w.beta != 0 else None)
+    p = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype, **knobs)
+    assert p.info["block"] == 1024
+    dA, dB = A.cuda(), B0.cuda()
+    p.exec(dA, dB)
+    torch.cuda.synchronize()
+    _assert_parity(dB.cpu().numpy(), want, w.dtype, p.describe())
 
 
 def test_stream_kernel_variants():
