@@ -12,7 +12,13 @@ namespace hptt {
 constexpr int kMaxDims = 16;  // = HPTT_MAX_DIMS
 constexpr int kBlock = 256;   // threads per workgroup: 4 waves of 64
 constexpr int kBigBlock = 1024;  // kernel T's large workgroup: 16 waves, for large tiles
-constexpr int kItems = 4;     // vectors per lane of the streaming kernels
+// Vectors of v elements per lane of the streaming kernels: one 16-byte
+// vector's worth, so a lane keeps 16 bytes in flight at any width.  Measured
+// on MI355X: with 16-byte vectors one per lane beats four (96^4 fp64 rows
+// 5.96 vs 5.49 TB/s, a flat fp64 copy 6.38 vs 5.85), and with one element
+// per vector four per lane beat one, two or sixteen.
+constexpr int items_per_lane(int elem, int v) { return 16 / (elem * v) > 1 ? 16 / (elem * v) : 1; }
+constexpr int kMaxItems = 4;  // items_per_lane(4, 1): the most any width takes
 constexpr int kXcds = 8;      // MI355X: workgroups are dealt to 8 XCDs round robin
 
 // Unsigned division of n < 2^32 by a divisor 1 <= d < 2^32 fixed at plan

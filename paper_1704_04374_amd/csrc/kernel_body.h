@@ -432,19 +432,21 @@ __host__ __device__ inline int64_t tile_lds_bytes(const TileArgs& g, int elem) {
 // ---------------------------------------------------------------------------
 
 
-// Block `blk` handles items [blk*kBlock*kItems, (blk+1)*kBlock*kItems); lane
-// tid takes items first + u*kBlock + tid, so each wave covers consecutive B
+// Block `blk` handles items [blk*kBlock*NI, (blk+1)*kBlock*NI), NI =
+// items_per_lane; lane tid takes items first + u*kBlock + tid, so each wave
+// covers consecutive B
 // vectors.  All loads of a lane are issued before its first store.
 template <class Mem, typename T, int V, int MODE, int HINT>
 __host__ __device__ inline void stream_items(const StreamArgs& g, uint32_t first, int tid,
                                              const T* A, T* B, T alpha, T beta) {
     const FastDiv& W = g.W[log2_width(V)];
     const uint32_t numItems = g.numItems[log2_width(V)];
-    Vec<T, V> x[kItems], y[kItems];
-    int64_t offA[kItems], offB[kItems], col[kItems];
-    bool ok[kItems];
+    constexpr int NI = items_per_lane(int(sizeof(T)), V);
+    Vec<T, V> x[NI], y[NI];
+    int64_t offA[NI], offB[NI], col[NI];
+    bool ok[NI];
 #pragma unroll
-    for (int u = 0; u < kItems; ++u) {
+    for (int u = 0; u < NI; ++u) {
         const uint64_t item = uint64_t(first) + uint64_t(u) * kBlock + uint64_t(tid);
         ok[u] = item < numItems;
         offA[u] = offB[u] = col[u] = 0;
@@ -474,7 +476,7 @@ __host__ __device__ inline void stream_items(const StreamArgs& g, uint32_t first
         }
     }
 #pragma unroll
-    for (int u = 0; u < kItems; ++u) {
+    for (int u = 0; u < NI; ++u) {
         if (!ok[u]) continue;
         Vec<T, V> z;
 #pragma unroll
@@ -494,14 +496,15 @@ __host__ __device__ inline void stream_items(const StreamArgs& g, uint32_t first
 // ---------------------------------------------------------------------------
 
 // Lane tid of the block starting at vector `first` takes vectors
-// first + u*kBlock + tid; vector i covers elements [i*V, i*V + V), the last
-// one possibly partial.
+// first + u*kBlock + tid, u < items_per_lane; vector i covers elements
+// [i*V, i*V + V), the last one possibly partial.
 template <class Mem, typename T, int V, int MODE, int HINT>
 __host__ __device__ inline void axpby_items(int64_t numel, int64_t first, int tid, const T* A,
                                             T* B, T alpha, T beta) {
-    Vec<T, V> x[kItems], y[kItems];
+    constexpr int NI = items_per_lane(int(sizeof(T)), V);
+    Vec<T, V> x[NI], y[NI];
 #pragma unroll
-    for (int u = 0; u < kItems; ++u) {
+    for (int u = 0; u < NI; ++u) {
         const int64_t off = (first + int64_t(u) * kBlock + tid) * V;
         if (off + V <= numel) {
             x[u] = Mem::template ld<T, V, (HINT & kNtLoad) != 0>(A, off);
@@ -509,7 +512,7 @@ __host__ __device__ inline void axpby_items(int64_t numel, int64_t first, int ti
         }
     }
 #pragma unroll
-    for (int u = 0; u < kItems; ++u) {
+    for (int u = 0; u < NI; ++u) {
         const int64_t off = (first + int64_t(u) * kBlock + tid) * V;
         if (off + V <= numel) {
             Vec<T, V> z;

@@ -20,9 +20,10 @@ template <typename T, int V, int MODE, int HINT>
 __global__ __launch_bounds__(kBlock) void stream_kernel(const T* __restrict__ A,
                                                         T* __restrict__ B, const StreamArgs g,
                                                         T alpha, T beta) {
-    const uint64_t step = uint64_t(gridDim.x) * kBlock * kItems;
+    constexpr uint64_t per = uint64_t(kBlock) * items_per_lane(int(sizeof(T)), V);
+    const uint64_t step = uint64_t(gridDim.x) * per;
     const uint64_t items = g.numItems[log2_width(V)];
-    for (uint64_t first = uint64_t(blockIdx.x) * kBlock * kItems; first < items; first += step)
+    for (uint64_t first = uint64_t(blockIdx.x) * per; first < items; first += step)
         stream_items<DeviceMem, T, V, MODE, HINT>(g, uint32_t(first), int(threadIdx.x), A, B, alpha,
                                                   beta);
 }
@@ -31,9 +32,10 @@ template <typename T, int V, int MODE, int HINT>
 __global__ __launch_bounds__(kBlock) void axpby_kernel(const T* __restrict__ A,
                                                        T* __restrict__ B, const int64_t numel,
                                                        T alpha, T beta) {
+    constexpr int64_t per = int64_t(kBlock) * items_per_lane(int(sizeof(T)), V);
     const int64_t vecs = (numel + V - 1) / V;
-    const int64_t step = int64_t(gridDim.x) * kBlock * kItems;
-    for (int64_t first = int64_t(blockIdx.x) * kBlock * kItems; first < vecs; first += step)
+    const int64_t step = int64_t(gridDim.x) * per;
+    for (int64_t first = int64_t(blockIdx.x) * per; first < vecs; first += step)
         axpby_items<DeviceMem, T, V, MODE, HINT>(numel, first, int(threadIdx.x), A, B, alpha, beta);
 }
 

@@ -410,7 +410,7 @@ bool setup_stream(const Fused& f, int elem, const hptt_options_t& opt, StreamArg
     for (int w = 0; w < 3; ++w) {  // every width hptt_exec may launch with
         const int64_t W = (s.rowLen + (1 << w) - 1) >> w;
         const int64_t items = rows * W;
-        if (items >= (int64_t(1) << 32) - int64_t(kBlock) * kItems) return false;
+        if (items >= (int64_t(1) << 32) - int64_t(kBlock) * kMaxItems) return false;
         set_div(s.W[w], W);
         s.numItems[w] = uint32_t(items);
     }
@@ -670,7 +670,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
             if (opt.kernel == HPTT_KERNEL_STREAM) return HPTT_ERROR_UNSUPPORTED;
             k = HPTT_KERNEL_GENERIC;
         } else {
-            const int64_t per = int64_t(kBlock) * kItems;
+            const int64_t per = int64_t(kBlock) * items_per_lane(elem, info.vec_a);
             const int64_t grid = (info.tiles + per - 1) / per;
             info.grid = grid < maxBlocks ? grid : maxBlocks;
         }
@@ -678,7 +678,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
     if (k == HPTT_KERNEL_AXPBY) {
         info.vec_a = info.vec_b = vec_width(0, elem, opt.max_vec);
         const int64_t vecs = (numel + info.vec_a - 1) / info.vec_a;
-        const int64_t per = int64_t(kBlock) * kItems;
+        const int64_t per = int64_t(kBlock) * items_per_lane(elem, info.vec_a);
         info.tiles = vecs;
         int64_t grid = (vecs + per - 1) / per;
         if (grid > (int64_t(1) << 30)) grid = int64_t(1) << 30;

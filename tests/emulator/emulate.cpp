@@ -200,9 +200,10 @@ void emu_stream(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     using namespace hptt;
     const StreamArgs& g = p->stream;
     const T alpha = T(p->alpha), beta = T(p->beta);
-    const uint64_t grid = uint64_t(p->info.grid), step = grid * kBlock * kItems;
+    const uint64_t per = uint64_t(kBlock) * items_per_lane(int(sizeof(T)), V);
+    const uint64_t grid = uint64_t(p->info.grid), step = grid * per;
     for (uint64_t blk = 0; blk < grid && S->errors == 0; blk += uint64_t(blockStride))
-        for (uint64_t first = blk * kBlock * kItems;
+        for (uint64_t first = blk * per;
              first < g.numItems[log2_width(V)] && S->errors == 0; first += step)
             for (int tid = 0; tid < kBlock; ++tid)
                 stream_items<HostMem, T, V, MODE, NT>(g, uint32_t(first), tid, A, B, alpha, beta);
@@ -213,9 +214,10 @@ template <typename T, int V, int MODE, int NT>
 void emu_axpby(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     using namespace hptt;
     const int64_t numel = p->info.numel, vecs = (numel + V - 1) / V;
-    const int64_t grid = p->info.grid, step = grid * kBlock * kItems;
+    const int64_t per = int64_t(kBlock) * items_per_lane(int(sizeof(T)), V);
+    const int64_t grid = p->info.grid, step = grid * per;
     for (int64_t blk = 0; blk < grid && S->errors == 0; blk += blockStride)
-        for (int64_t first = blk * kBlock * kItems; first < vecs; first += step)
+        for (int64_t first = blk * per; first < vecs; first += step)
             for (int tid = 0; tid < kBlock; ++tid)
                 axpby_items<HostMem, T, V, MODE, NT>(numel, first, tid, A, B, T(p->alpha), T(p->beta));
 }
