@@ -126,6 +126,10 @@ constexpr int kBatch = 8;
 // of them fit a CU's registers (at most 64 VGPRs per lane).
 constexpr int tile_batch(int block) { return block >= 1024 ? 4 : kBatch; }
 
+// Batch of the specialised store phase when it also reads B (beta != 0):
+// its B vectors double the registers a batch holds.
+constexpr int kAxpbyStoreBatch = 2;
+
 // Specialised load phase (tile_is_general() false): every run starts on the
 // A vector grid, nZ = 1, and offsets inside a tile fit 32 bits, so the
 // per-vector arithmetic is 32-bit around one 64-bit tile base pointer.  The
@@ -192,7 +196,7 @@ template <class Mem, typename T, int VB, int MODE, int HINT, int BLOCK>
 __host__ __device__ inline void tile_store_fast(const TileArgs& g, const TileBase& tb, int r0,
                                                 int tid, T* B, const T* lds,
                                                 const int64_t* colOffB, T alpha, T beta) {
-    constexpr int NB = tile_batch(BLOCK);
+    constexpr int NB = MODE == kAxpby ? kAxpbyStoreBatch : tile_batch(BLOCK);
     const int W = (g.subRows + VB - 1) / VB;  // vectors per column
     const int rows = int(imin(int64_t(g.subRows), tb.validRows - r0));
     const int vcols = int(tb.validCols);
