@@ -353,6 +353,7 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
                                                        beta);
         return;
     }
+    constexpr int NB = MODE == kAxpby ? kAxpbyStoreBatch : kBatch;
     const bool shift = GEN && (!g.runsOnGridB || g.misB != 0);
     const bool depth = GEN && g.nZ > 1;
     const int64_t W = (g.subRows + (shift ? VB - 1 : 0) + VB - 1) / VB;  // vectors per column
@@ -361,11 +362,11 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
     int64_t Q = tid / W, s = tid % W;
     const int64_t dQ = kBlock / W, ds = kBlock % W;
     while (Q < cols) {
-        Vec<T, VB> x[kBatch], y[kBatch];
-        int64_t ss[kBatch], off[kBatch];
-        bool ok[kBatch];
+        Vec<T, VB> x[NB], y[NB];
+        int64_t ss[NB], off[NB];
+        bool ok[NB];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
+        for (int u = 0; u < NB; ++u) {
             int64_t z = 0, q = Q;
             if (depth) {
                 z = int64_t(fast_div(uint32_t(Q), g.zCols));
@@ -405,7 +406,7 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
             }
         }
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
+        for (int u = 0; u < NB; ++u) {
             if (ok[u]) {
                 Vec<T, VB> zv;
 #pragma unroll
