@@ -97,6 +97,11 @@ typedef struct {
                               general one always runs 256); 0 = choose */
     int32_t skew;          /* TILE: diagonal orders rotate the second grid digit by
                               skew times the first; 0 = 1 */
+    int32_t shear;         /* TILE: B runs that cannot be whole 128-byte lines are
+                              sheared onto lines (each column's run starts on the
+                              line at or below the chunk); 0 = where they apply
+                              and the problem is not small, 1 = wherever they
+                              apply, 2 = never */
 } hptt_options_t;
 
 /* What the plan builder decided; for inspection and tests. */
@@ -131,6 +136,8 @@ typedef struct {
                                           with contiguous tile ranges per XCD, 4
                                           grid-digit order with such ranges */
     int32_t depth;                     /* TILE: tiles stacked per workgroup round */
+    int32_t shear;                     /* TILE: extra rows staged for sheared B runs
+                                          (0: runs not sheared) */
 } hptt_plan_info_t;
 
 /*

@@ -95,6 +95,19 @@ struct TileArgs {
     // 1 when every offset inside a tile (table entry plus position in the
     // run) is below 2^31, so the specialised variant can use 32-bit offsets.
     int32_t offsets32;
+    // Sheared B runs (general variant; one B-run index, no stacking, no row
+    // passes).  With shear = lineB - 1 > 0 the B run of column q starts at
+    // the 128-byte line of B at or below the chunk's first row, i.e. it is
+    // shifted back by d_q = (B address of the column, in elements) mod lineB,
+    // so every line of B is written whole by one tile; the tile stages shear
+    // rows more (staged row R holds run index rowBase + R - shear, rowBase =
+    // j * runB for chunk j) and the run's index of extent rowsB has one
+    // chunk more.  misLineB = element offset of the B base pointer from a
+    // line (launch time).
+    int32_t shear;
+    int32_t lineB;
+    int32_t misLineB;
+    int64_t rowsB;
     int64_t cInner, cChunk, cLast;  // valid columns = cInner * min(cChunk, cLast - j*cChunk)
     int64_t rInner, rChunk, rLast;  // valid rows    = rInner * min(rChunk, rLast - j*rChunk)
     FastDiv cExt[kMaxDims];         // tile extents of the A-run indices
@@ -124,13 +137,14 @@ struct StreamArgs {
 };
 
 // Kernel T needs its general variant when a run starts off its vector grid
-// (runs shifted, partial vectors at both ends), when tiles are stacked, or
-// when offsets inside a tile need 64 bits; otherwise the specialised
+// (runs shifted, partial vectors at both ends), when tiles are stacked or
+// their B runs sheared, or when offsets inside a tile need 64 bits;
+// otherwise the specialised
 // variant, compiled without any of these, is launched.  g.misA / g.misB must
 // already hold the launch's pointer offsets.
 __host__ __device__ inline bool tile_is_general(const TileArgs& g) {
     return !g.runsOnGridA || !g.runsOnGridB || g.misA != 0 || g.misB != 0 || g.nZ > 1 ||
-           !g.offsets32;
+           !g.offsets32 || g.shear > 0;
 }
 
 constexpr int log2_width(int v) { return v >= 4 ? 2 : v >= 2 ? 1 : 0; }

@@ -44,6 +44,7 @@ struct TileBase {
     int64_t validCols;   // columns (A-run elements) inside the tensor
     int64_t validRows;   // rows (B-run elements) inside the tensor
     int64_t validDepth;  // stacked tiles inside the tensor
+    int64_t rowBase;     // sheared B runs: run index of the chunk's first row
 };
 
 // Split the tile number into grid digits (fastest first).  With g.skew = s the
@@ -67,6 +68,7 @@ __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
     tb.validCols = g.runA;
     tb.validRows = g.runB;
     tb.validDepth = g.nZ;
+    tb.rowBase = 0;
     uint32_t j0 = 0;
     for (int k = 0; k < g.nG; ++k) {
         uint32_t q = fast_div(t, g.gExt[k]);
@@ -83,7 +85,13 @@ __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
         tb.a += j * g.gStrideA[k];
         tb.b += j * g.gStrideB[k];
         if (k == g.gChunkC) tb.validCols = g.cInner * imin(g.cChunk, g.cLast - j * g.cChunk);
-        if (k == g.gChunkR) tb.validRows = g.rInner * imin(g.rChunk, g.rLast - j * g.rChunk);
+        if (k == g.gChunkR) {
+            // a sheared chunk reaches shear rows back and always has work
+            // (its count is that of the rows plus shear), so it takes one
+            // full pass; its rows are checked one by one
+            tb.validRows = g.shear ? g.runB : g.rInner * imin(g.rChunk, g.rLast - j * g.rChunk);
+            tb.rowBase = j * g.runB;
+        }
         if (k == g.gDepth) tb.validDepth = imin(int64_t(g.nZ), g.zLast - j * g.nZ);
     }
     return tb;
@@ -91,17 +99,23 @@ __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
 
 // Offset tables shared by every tile of the launch: rowOffA[r] is the A
 // offset of row r (a B-run position) and colOffB[c] the B offset of column c
-// (an A-run position), both relative to the tile origin.
+// (an A-run position), both relative to the tile origin.  With sheared B
+// runs the row table covers the shear rows before the chunk too:
+// rowOffA[R] is the offset of run index R - shear (one B-run index).
 template <class Mem, int BLOCK = kBlock>
 __host__ __device__ inline void tile_tables(const TileArgs& g, int tid, int64_t* rowOffA,
                                             int64_t* colOffB) {
-    for (int64_t r = tid; r < g.runB; r += BLOCK) {
-        uint32_t x = uint32_t(r);
+    for (int64_t r = tid; r < g.runB + g.shear; r += BLOCK) {
         int64_t off = 0;
-        for (int k = 0; k < g.nR; ++k) {
-            uint32_t q = fast_div(x, g.rExt[k]);
-            off += int64_t(x - q * g.rExt[k].d) * g.rStrideA[k];
-            x = q;
+        if (g.shear) {
+            off = (r - g.shear) * g.rStrideA[0];
+        } else {
+            uint32_t x = uint32_t(r);
+            for (int k = 0; k < g.nR; ++k) {
+                uint32_t q = fast_div(x, g.rExt[k]);
+                off += int64_t(x - q * g.rExt[k].d) * g.rStrideA[k];
+                x = q;
+            }
         }
         Mem::template lds_st<int64_t>(rowOffA, r, off);
     }
@@ -284,7 +298,8 @@ __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb,
     const bool depth = GEN && g.nZ > 1;
     const int64_t W = (g.runA + (shift ? VA - 1 : 0) + VA - 1) / VA;  // vectors per row
     const int64_t rows = imin(int64_t(g.subRows), tb.validRows - r0);  // rows of this pass
-    const int64_t stacked = depth ? int64_t(g.nZ) * g.subRows : int64_t(g.subRows);
+    // staged rows: with shear, the shear rows before the chunk come first
+    const int64_t stacked = (depth ? int64_t(g.nZ) * g.subRows : int64_t(g.subRows)) + g.shear;
     int64_t R = tid / W, c = tid % W;
     const int64_t dR = kBlock / W, dc = kBlock % W;
     while (R < stacked) {
@@ -298,7 +313,10 @@ __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb,
                 z = int64_t(fast_div(uint32_t(R), g.zRows));
                 r = R - z * g.subRows;
             }
-            ok[u] = R < stacked && r < rows && (!depth || z < tb.validDepth);
+            // with shear, staged row R is run index rowBase + R - shear
+            const int64_t G = tb.rowBase + R - g.shear;
+            const bool rowOk = g.shear ? (G >= 0 && G < g.rowsB) : r < rows;
+            ok[u] = R < stacked && rowOk && (!depth || z < tb.validDepth);
             cc[u] = c * VA;
             at[u] = 0;
             if (ok[u]) {
@@ -354,10 +372,18 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
         return;
     }
     constexpr int NB = MODE == kAxpby ? kAxpbyStoreBatch : kBatch;
-    const bool shift = GEN && (!g.runsOnGridB || g.misB != 0);
-    const bool depth = GEN && g.nZ > 1;
-    const int64_t W = (g.subRows + (shift ? VB - 1 : 0) + VB - 1) / VB;  // vectors per column
+    // B side: with shear, each column's run starts on the line at or below
+    // the chunk's first row (d = the column's offset from that line); else,
+    // without the vector grid, vectors are shifted onto it (d < VB).
+    const bool sheared = g.shear > 0;
+    const bool shift = !sheared && (!g.runsOnGridB || g.misB != 0);
+    const bool depth = g.nZ > 1;
+    const int64_t W = sheared ? g.runB / VB
+                              : (g.subRows + (shift ? VB - 1 : 0) + VB - 1) / VB;  // per column
     const int64_t rows = imin(int64_t(g.subRows), tb.validRows - r0);
+    // element ss + e of a column's run exists when lo <= ss + e < hi
+    const int64_t lo = sheared ? -tb.rowBase : 0;
+    const int64_t hi = sheared ? g.rowsB - tb.rowBase : rows;
     const int64_t cols = depth ? int64_t(g.nZ) * g.runA : g.runA;
     int64_t Q = tid / W, s = tid % W;
     const int64_t dQ = kBlock / W, ds = kBlock % W;
@@ -378,21 +404,23 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
             if (ok[u]) {
                 int64_t start = tb.b + Mem::template lds_ld<int64_t>(colOffB, q) + r0;
                 if (depth) start += z * g.zStrideB;
-                if (shift) ss[u] -= (start + g.misB) & (VB - 1);
-                ok[u] = (!shift || ss[u] + VB > 0) && ss[u] < rows;
+                if (sheared) ss[u] -= (start + g.misLineB) & (g.lineB - 1);
+                else if (shift) ss[u] -= (start + g.misB) & (VB - 1);
+                ok[u] = ss[u] + VB > lo && ss[u] < hi;
                 off[u] = start + ss[u];
                 if (ok[u]) {
-                    const int64_t base = ((depth ? z * g.subRows : 0) + ss[u]) * g.pitch + q;
+                    const int64_t base =
+                        ((depth ? z * g.subRows : 0) + ss[u] + g.shear) * g.pitch + q;
 #pragma unroll
                     for (int e = 0; e < VB; ++e)
-                        if ((!shift || ss[u] + e >= 0) && ss[u] + e < rows)
+                        if (ss[u] + e >= lo && ss[u] + e < hi)
                             x[u].v[e] = Mem::template lds_ld<T>(lds, base + e * g.pitch);
                     if (MODE == kAxpby) {
-                        if ((!shift || ss[u] >= 0) && ss[u] + VB <= rows) {
+                        if (ss[u] >= lo && ss[u] + VB <= hi) {
                             y[u] = Mem::template ld<T, VB, false>(B, off[u]);
                         } else {
                             for (int e = 0; e < VB; ++e)
-                                if ((!shift || ss[u] + e >= 0) && ss[u] + e < rows)
+                                if (ss[u] + e >= lo && ss[u] + e < hi)
                                     y[u].v[e] = Mem::template ld1<T>(B, off[u] + e);
                         }
                     }
@@ -412,11 +440,11 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
 #pragma unroll
                 for (int e = 0; e < VB; ++e)
                     zv.v[e] = update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
-                if ((!shift || ss[u] >= 0) && ss[u] + VB <= rows) {
+                if (ss[u] >= lo && ss[u] + VB <= hi) {
                     Mem::template st<(HINT & kNtStore) != 0, T, VB>(B, off[u], zv);
                 } else {
                     for (int e = 0; e < VB; ++e)
-                        if ((!shift || ss[u] + e >= 0) && ss[u] + e < rows)
+                        if (ss[u] + e >= lo && ss[u] + e < hi)
                             Mem::template st1<(HINT & kNtStore) != 0, T>(B, off[u] + e, zv.v[e]);
                 }
             }
@@ -424,12 +452,12 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
     }
 }
 
-// LDS layout of kernel T: rowOffA[runB], colOffB[runA], then nZ * subRows
-// rows of the tile.  A tile with runB > subRows is staged in passes of
-// subRows rows (never with depth).
+// LDS layout of kernel T: rowOffA[runB + shear], colOffB[runA], then
+// nZ * subRows + shear rows of the tile.  A tile with runB > subRows is
+// staged in passes of subRows rows (never with depth or shear).
 __host__ __device__ inline int64_t tile_lds_bytes(const TileArgs& g, int elem) {
-    return (g.runA + g.runB) * int64_t(sizeof(int64_t)) +
-           int64_t(g.nZ) * g.subRows * g.pitch * elem;
+    return (g.runA + g.runB + g.shear) * int64_t(sizeof(int64_t)) +
+           (int64_t(g.nZ) * g.subRows + g.shear) * g.pitch * elem;
 }
 
 // ---------------------------------------------------------------------------

@@ -137,6 +137,7 @@ hptt_status_t launch(const hptt_plan_s* p, const void* A, void* B, hipStream_t s
         targs = p->tile;
         targs.misA = int32_t((pa / uintptr_t(elem)) % uintptr_t(va));
         targs.misB = int32_t((pb / uintptr_t(elem)) % uintptr_t(vb));
+        if (targs.shear) targs.misLineB = int32_t((pb / uintptr_t(elem)) % uintptr_t(targs.lineB));
     }
     const void* fn = nullptr;
     int block = kBlock;

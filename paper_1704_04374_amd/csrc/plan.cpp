@@ -12,8 +12,8 @@
 namespace hptt {
 
 int64_t tile_lds_bytes_host(const TileArgs& t, int elem) {
-    return (t.runA + t.runB) * int64_t(sizeof(int64_t)) +
-           int64_t(t.nZ) * t.subRows * t.pitch * elem;
+    return (t.runA + t.runB + t.shear) * int64_t(sizeof(int64_t)) +
+           (int64_t(t.nZ) * t.subRows + t.shear) * t.pitch * elem;
 }
 
 namespace {
@@ -190,8 +190,9 @@ void set_div(FastDiv& f, int64_t d) { f = make_fastdiv(uint32_t(d)); }
 // tile does not fit the LDS budget or the grid is too large.
 bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_options_t& opt,
                 bool alignA, bool alignB, int64_t ldsBudget, int64_t minTile, TileArgs& t,
-                hptt_plan_info_t& info) {
+                hptt_plan_info_t& info, bool shear = false) {
     memset(&t, 0, sizeof(t));
+    const int64_t lineB = kLine / elem;
     const int M = f.M;
     const int p0 = f.p[0];  // A index that is B's stride-1 index (never 0 here)
     // Both runs need a stride-1 index (a sub-tensor whose first extent is 1
@@ -228,8 +229,15 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     for (int j = 0; j < M; ++j) outside[j] = true;
     for (int j = 0; j <= k; ++j) outside[f.p[j]] = false;
     int64_t rChunk = f.n[f.p[k]];
-    if (inner * rChunk > tB)
+    if (shear) {
+        // sheared B runs: one B-run index, chunks of whole lines, and more
+        // than one chunk (a run that covers its index needs no shear)
+        if (k != 0) return false;
+        rChunk = tB >= lineB ? tB / lineB * lineB : lineB;
+        if (rChunk >= f.n[f.p[k]]) return false;
+    } else if (inner * rChunk > tB) {
         rChunk = choose_chunk(inner, f.n[f.p[k]], stride_gcd(f, f.sB, outside), tB, elem, alignB);
+    }
     if (rChunk == 0) return false;
     const int nR = k + 1;
     t.nR = nR;
@@ -258,7 +266,9 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     }
     if (t.rChunk < t.rLast) {
         const int a = f.p[nR - 1];
-        ext[g] = (t.rLast + t.rChunk - 1) / t.rChunk;
+        // sheared runs start up to lineB - 1 rows early: one chunk more at most
+        const int64_t span = t.rLast + (shear ? lineB - 1 : 0);
+        ext[g] = (span + t.rChunk - 1) / t.rChunk;
         t.gStrideA[g] = t.rChunk * f.sA[a];
         t.gStrideB[g] = t.rChunk * f.sB[a];
         t.gChunkR = g++;
@@ -288,7 +298,7 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     int64_t wantZ = opt.depth > 0 ? opt.depth : (minTile + area - 1) / area;
     if (opt.depth == 0 && double(wantZ) > tilesBefore / kMinGrid)
         wantZ = int64_t(tilesBefore / kMinGrid);
-    if (opt.row_passes > 1) wantZ = 1;
+    if (opt.row_passes > 1 || shear) wantZ = 1;
     if (wantZ > 1) {
         // among the indices long enough for wantZ the one with the smallest
         // strides; if none is, the longest
@@ -349,6 +359,12 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
         if (t.rExt[j].d > 1) granA = gcd64(granA, t.rStrideA[j]);
     for (int j = 0; j < nC; ++j)
         if (t.cExt[j].d > 1) granB = gcd64(granB, t.cStrideB[j]);
+    if (shear) {
+        t.shear = int32_t(lineB - 1);
+        t.lineB = int32_t(lineB);
+        t.rowsB = t.rLast;
+        granB = lineB;  // sheared runs start on lines
+    }
     info.vec_a = run_vec_width(t.runA, granA, elem, opt.max_vec);
     info.vec_b = run_vec_width(t.runB, granB, elem, opt.max_vec);
     t.runsOnGridA = granA % info.vec_a == 0 ? 1 : 0;
@@ -358,6 +374,7 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     // tile, so they can be read with non-temporal loads.
     t.alignedA = (granA == 0 || (granA * elem) % kLine == 0) && (t.runA * elem) % kLine == 0;
     t.alignedB = (granB == 0 || (granB * elem) % kLine == 0) && (t.runB * elem) % kLine == 0;
+    info.shear = t.shear;
     // Rows staged through LDS per pass: the whole tile by default.  Staging a
     // tile in several passes keeps its run lengths with less LDS, but each
     // pass adds a barrier round trip; on MI355X that cost more than it saved
@@ -478,7 +495,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
         opt.tile_order > 4 || opt.row_passes < 0 || opt.row_passes > 64 || opt.depth < 0 ||
         opt.depth > 4096 || opt.min_tile < 0 || opt.exact_runs < 0 ||
         opt.exact_runs > 1 || (opt.block != 0 && opt.block != kBlock && opt.block != kBigBlock) ||
-        opt.skew < 0 || opt.skew > 1024)
+        opt.skew < 0 || opt.skew > 1024 || opt.shear < 0 || opt.shear > 2)
         return HPTT_ERROR_INVALID_ARGUMENT;
 
     const int elem = dtype == HPTT_FLOAT32 ? 4 : 8;
@@ -640,9 +657,55 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
                 info = keepInfo;
             }
         }
+        // B runs that still cannot be whole lines are sheared: each column's
+        // run starts on the line at or below the chunk's first row, so no
+        // line of B is written by two tiles, at the price of lineB - 1 more
+        // A rows staged per tile.
+        if (ok && !plan->tile.alignedB && opt.shear != 2 && opt.exact_runs == 0 &&
+            opt.row_passes <= 1 && opt.depth <= 1) {
+            TileArgs keep = plan->tile;
+            hptt_plan_info_t keepInfo = info;
+            const int64_t lineB = kLine / elem;
+            const int64_t sA = opt.run_a > 0 ? opt.run_a : lineB;
+            int64_t sB = opt.run_b > 0 ? opt.run_b : 4 * lineB;
+            bool sheared = setup_tile(f, elem, sA, sB, opt, false, false, kLdsBudget, minTile,
+                                      plan->tile, info, true);
+            // an A run cut short by its extent lets the B run grow towards
+            // the smallest tile worth a workgroup round
+            const int64_t area0 = keep.runA * keep.runB * keep.nZ;
+            if (sheared && opt.run_b == 0 && plan->tile.runA * plan->tile.runB < minTile) {
+                TileArgs t1 = plan->tile;
+                hptt_plan_info_t i1 = info;
+                const int64_t want = (minTile / plan->tile.runA + lineB - 1) / lineB * lineB;
+                if (!setup_tile(f, elem, sA, want, opt, false, false, kLdsBudget, minTile,
+                                plan->tile, info, true)) {
+                    plan->tile = t1;
+                    info = i1;
+                } else {
+                    sB = want;
+                }
+            }
+            // Shearing pays where the run's index spans many chunks: its
+            // extra chunk and its lineB - 1 extra rows per chunk are then a
+            // small share (sweep on MI355X: +1 to +10 points of the copy
+            // rate from 8 chunks up, -3 to -13 below 6; likewise A runs of
+            // a few elements lost).  opt.shear = 1 shears wherever it can.
+            const bool pays =
+                sheared && (opt.shear == 1 ||
+                            (plan->tile.rowsB >= 8 * plan->tile.runB && plan->tile.runA >= 8));
+            const int64_t area = plan->tile.runA * plan->tile.runB;
+            if (!pays || (area < minTile && area < area0)) {
+                plan->tile = keep;
+                info = keepInfo;
+            } else {
+                tA = sA;
+                tB = sB;
+            }
+        }
         // Small problems: shorter runs (down to one 128-byte line) for more
         // tiles, so that more CUs take part.
         while (ok && opt.run_a == 0 && opt.run_b == 0 && plan->tile.numTiles < 512 &&
+               !(opt.shear == 1 && plan->tile.shear > 0) &&
                (tA * elem > kLine || tB * elem > kLine)) {
             TileArgs keep = plan->tile;
             hptt_plan_info_t keepInfo = info;
@@ -720,12 +783,12 @@ void describe_plan(const hptt_plan_s* p, char* buf, size_t len) {
     snprintf(buf, len,
              "kernel=%s dtype=%s mode=%s fused=(%s) perm=(%s) run_a=%lld run_b=%lld "
              "dims_a=%d dims_b=%d vec=%d/%d pitch=%d rows=%d lds=%d tiles=%lld grid=%lld block=%d "
-             "hints=%d order=%d",
+             "hints=%d order=%d shear=%d",
              kKernel[in.kernel], p->dtype == HPTT_FLOAT32 ? "f32" : "f64", kMode[in.mode], shape,
              perm, (long long)in.run_a, (long long)in.run_b, in.dims_a, in.dims_b, in.vec_a,
              in.vec_b, in.lds_pitch, in.rows_per_pass, in.lds_bytes, (long long)in.tiles,
              (long long)in.grid,
-             in.block, in.hints, in.tile_order);
+             in.block, in.hints, in.tile_order, in.shear);
 }
 
 }  // namespace hptt

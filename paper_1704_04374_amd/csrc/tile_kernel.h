@@ -28,7 +28,7 @@ __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(BLOCK >= 
 void tile_kernel(const T* __restrict__ A, T* __restrict__ B, const TileArgs g, T alpha, T beta) {
     extern __shared__ int64_t smem[];
     int64_t* rowOffA = smem;
-    int64_t* colOffB = smem + g.runB;
+    int64_t* colOffB = smem + g.runB + g.shear;
     T* lds = reinterpret_cast<T*>(colOffB + g.runA);
     const int tid = int(threadIdx.x);
     tile_tables<DeviceMem, BLOCK>(g, tid, rowOffA, colOffB);

@@ -151,13 +151,14 @@ void emu_tile_variant(const hptt_plan_s* p, const T* A, T* B, int64_t blockStrid
     TileArgs g = p->tile;  // with the base pointers' offsets from the vector grid, as at launch
     g.misA = int32_t(S->misA % VA);
     g.misB = int32_t(S->misB % VB);
+    if (g.shear) g.misLineB = int32_t(S->misB % g.lineB);
     const T alpha = T(p->alpha), beta = T(p->beta);
     const int64_t ldsBytes = p->info.lds_bytes;
-    const int64_t tableBytes = (g.runA + g.runB) * int64_t(sizeof(int64_t));
+    const int64_t tableBytes = (g.runA + g.runB + g.shear) * int64_t(sizeof(int64_t));
     S->lds.assign(size_t(ldsBytes), 0);
     S->written.assign(size_t(ldsBytes), 0);
     int64_t* rowOffA = reinterpret_cast<int64_t*>(S->lds.data());
-    int64_t* colOffB = rowOffA + g.runB;
+    int64_t* colOffB = rowOffA + g.runB + g.shear;
     T* lds = reinterpret_cast<T*>(colOffB + g.runA);
     const int64_t grid = p->info.grid;
     for (int64_t blk = 0; blk < grid && S->errors == 0; blk += blockStride) {

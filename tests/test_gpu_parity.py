@@ -142,6 +142,39 @@ def test_large_tiles_full_size(name, knobs):
     _assert_parity(dB.cpu().numpy(), want, w.dtype, p.describe())
 
 
+def test_sheared_b_runs():
+    """B runs sheared onto 128-byte lines, small (forced) and at sweep size,
+    including tensors that start off a line."""
+    rng = np.random.default_rng(41)
+    sheared = 0
+    for size_a, perm in [((397, 125), (1, 0)), ((153, 10, 325), (2, 0, 1)),
+                         ((65, 33, 129), (2, 0, 1))]:
+        for dtype, (alpha, beta) in (("f32", (1.0, 0.0)), ("f64", (1.5, -0.5)),
+                                     ("f32", (2.0, 0.5))):
+            p = _run_case(size_a, perm, alpha, beta, dtype, rng, shear=1)
+            sheared += p.info["shear"] > 0
+    assert sheared >= 6
+    for size_a, perm in [((39792, 1257), (1, 0)), ((1538, 10, 3251), (2, 0, 1))]:
+        p = _run_case(size_a, perm, 1.0, 0.0, "f32", rng)
+        assert p.info["shear"] == 31
+    # tensors one and three elements past a line
+    p = hptt.create_plan((1, 0), (397, 125), 1.5, 0.5, "f64", shear=1)
+    for off in (1, 3):
+        n = p.numel
+        A = _rand(rng, n, "f64")
+        B0 = _rand(rng, n, "f64")
+        want = orc.transpose(A, (397, 125), (1, 0), 1.5, 0.5, B0)
+        dA = torch.zeros(n + 8, dtype=torch.float64, device="cuda")
+        dB = torch.zeros(n + 8, dtype=torch.float64, device="cuda")
+        dA[off:off + n] = torch.from_numpy(A).cuda()
+        dB[off:off + n] = torch.from_numpy(B0).cuda()
+        p.exec(dA[off:off + n], dB[off:off + n])
+        torch.cuda.synchronize()
+        got = dB.cpu().numpy()
+        _assert_parity(got[off:off + n], want, "f64", f"offset {off}: {p.describe()}")
+        assert np.all(got[:off] == 0) and np.all(got[off + n:] == 0)
+
+
 def test_stream_kernel_variants():
     rng = np.random.default_rng(5)
     for size_a, perm in [((96, 7, 9, 5), (0, 3, 2, 1)), ((33, 8, 8), (0, 2, 1)),

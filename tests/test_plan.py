@@ -186,7 +186,8 @@ def test_null_arguments():
                                          ("store_hint", 3), ("load_hint", -1), ("lds_pad", 65),
                                          ("max_blocks", -2), ("tile_order", 5), ("exact_runs", 2),
                                          ("row_passes", -1), ("row_passes", 65), ("block", 512),
-                                         ("block", -1), ("skew", -1), ("skew", 1025)])
+                                         ("block", -1), ("skew", -1), ("skew", 1025),
+                                         ("shear", 3), ("shear", -1)])
 def test_invalid_options(field, value):
     opt = hptt.Options()
     setattr(opt, field, value)
@@ -289,3 +290,17 @@ def test_strided_single_index_uses_generic():
     extent-1 index is dropped; the flat kernel must not serve it."""
     info = hptt.create_plan((0, 1), (1, 7), outer_size_a=(3, 7)).info
     assert info["kernel"] == "generic" and info["footprint_a"] == 1 + 6 * 3
+
+
+def test_shear_only_where_b_runs_cannot_be_lines():
+    """B runs are sheared onto lines only where they cannot be whole lines
+    otherwise; never on the named workloads; never with shear = 2."""
+    for w in WORKLOADS:
+        assert hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype).info["shear"] == 0
+    p = hptt.create_plan((1, 0), (39792, 1257), 1.0, 0.0, "f32")
+    assert p.info["shear"] == 31 and p.info["run_b"] % 32 == 0
+    assert p.info["hints"] & 1  # whole lines: non-temporal stores again
+    p64 = hptt.create_plan((1, 0), (39792, 1257), 1.0, 0.0, "f64")
+    assert p64.info["shear"] == 15
+    assert hptt.create_plan((1, 0), (39792, 1257), 1.0, 0.0, "f32", shear=2).info["shear"] == 0
+    assert hptt.create_plan((1, 0), (39792, 1280), 1.0, 0.0, "f32").info["shear"] == 0
