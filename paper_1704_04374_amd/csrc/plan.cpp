@@ -295,7 +295,12 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     const int64_t area = t.runA * t.runB;
     double tilesBefore = 1;
     for (int j = 0; j < g; ++j) tilesBefore *= double(ext[j]);
-    int64_t wantZ = opt.depth > 0 ? opt.depth : (minTile + area - 1) / area;
+    // only tiles below half the minimum are stacked: stacking takes the
+    // general variant, which cost more than it gave above that (sweep on
+    // MI355X: +1.4 % with beta = 1, +2.2 % with beta = 0; the 5-D beta = 1
+    // workload 5.20-5.37 -> 5.43 TB/s)
+    int64_t wantZ =
+        opt.depth > 0 ? opt.depth : (2 * area >= minTile ? 1 : (minTile + area - 1) / area);
     if (opt.depth == 0 && double(wantZ) > tilesBefore / kMinGrid)
         wantZ = int64_t(tilesBefore / kMinGrid);
     if (opt.row_passes > 1 || shear) wantZ = 1;
@@ -569,8 +574,11 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
         // runs, and aligned B runs more than aligned A runs.
         // Default targets: A runs of 512 bytes, B runs of one 128-byte line
         // (on MI355X short B runs with long A runs measured fastest: the
-        // tile stays small, so more workgroups stay resident).
-        const int64_t tA0 = opt.run_a > 0 ? opt.run_a : 512 / elem;
+        // tile stays small, so more workgroups stay resident); 256-byte A
+        // runs when B is read as well (the 5-D beta = 1 workload 5.42 ->
+        // 5.56 TB/s, the beta = 1 sweep +1.1 %; with beta = 0 they lost).
+        const int64_t tA0 =
+            opt.run_a > 0 ? opt.run_a : (info.mode == kAxpby ? 256 : 512) / elem;
         const int64_t tB0 = opt.run_b > 0 ? opt.run_b : kLine / elem;
         struct Stage { bool alignA, alignB; int64_t budget; };
         const Stage forced[] = {{false, false, opt.block == kBigBlock ? kLdsMaxBig : kLdsMax}};

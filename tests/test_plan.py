@@ -108,9 +108,10 @@ EXPECTED = {
                                               rows_per_pass=160),
     "transpose4d_96x96x96x96_keep1_f64": dict(kernel="stream", size=(96, 96, 96, 96),
                                               perm=(0, 3, 2, 1), run_b=96, vec_a=2, vec_b=2),
+    # beta != 0: A-run target of 256 bytes, met by 3 x 2 x 16 = 96 elements (384 B)
     "transpose5d_3x2x640x480x96_f32": dict(kernel="tile", size=(3, 2, 640, 480, 96),
-                                           perm=(4, 2, 0, 3, 1), run_a=192, run_b=32, dims_a=3,
-                                           dims_b=1, tiles=28800, hints=3),
+                                           perm=(4, 2, 0, 3, 1), run_a=96, run_b=32, dims_a=3,
+                                           dims_b=1, tiles=57600, hints=3, depth=1),
 }
 
 
