@@ -136,15 +136,18 @@ struct StreamArgs {
     int64_t oStrideB[kMaxDims]; // B strides of those positions
 };
 
-// Kernel T needs its general variant when a run starts off its vector grid
-// (runs shifted, partial vectors at both ends), when tiles are stacked or
-// their B runs sheared, or when offsets inside a tile need 64 bits;
-// otherwise the specialised
-// variant, compiled without any of these, is launched.  g.misA / g.misB must
-// already hold the launch's pointer offsets.
-__host__ __device__ inline bool tile_is_general(const TileArgs& g) {
-    return !g.runsOnGridA || !g.runsOnGridB || g.misA != 0 || g.misB != 0 || g.nZ > 1 ||
-           !g.offsets32 || g.shear > 0;
+// Compiled variants of kernel T, picked per launch by tile_variant():
+// kFast when every run starts on its vector grid for the actual pointers,
+// kShifted when some do not (runs shifted onto the grid, partial vectors at
+// both ends), both with 32-bit offsets inside a tile, no stacking and no
+// shear; kGeneral otherwise (stacked tiles, sheared B runs, 64-bit offsets).
+// g.misA / g.misB must already hold the launch's pointer offsets.
+enum TileVariant : int { kFast = 0, kShifted = 1, kGeneral = 2 };
+
+__host__ __device__ inline int tile_variant(const TileArgs& g) {
+    if (g.nZ > 1 || !g.offsets32 || g.shear > 0) return kGeneral;
+    if (!g.runsOnGridA || !g.runsOnGridB || g.misA != 0 || g.misB != 0) return kShifted;
+    return kFast;
 }
 
 constexpr int log2_width(int v) { return v >= 4 ? 2 : v >= 2 ? 1 : 0; }

@@ -144,40 +144,49 @@ constexpr int tile_batch(int block) { return block >= 1024 ? 4 : kBatch; }
 // its B vectors double the registers a batch holds.
 constexpr int kAxpbyStoreBatch = 2;
 
-// Specialised load phase (tile_is_general() false): every run starts on the
-// A vector grid, nZ = 1, and offsets inside a tile fit 32 bits, so the
-// per-vector arithmetic is 32-bit around one 64-bit tile base pointer.  The
-// second sweep of a batch recomputes each vector's position from the batch's
-// start instead of keeping it, so only the data stays live between the two
-// (fewer registers, more resident waves).  Same thread-to-vector map as
-// tile_load.
-template <class Mem, typename T, int VA, int HINT, int BLOCK>
+// Specialised load phase (variant kFast, or kShifted with SHIFT): nZ = 1, no
+// shear, and offsets inside a tile fit 32 bits, so the per-vector
+// arithmetic is 32-bit around one 64-bit tile base pointer.  Without SHIFT
+// every run starts on the A vector grid; with SHIFT a run that starts off it
+// is covered by one more vector, its first and last ones partial.  The
+// second sweep of a batch recomputes each vector's position from the
+// batch's start instead of keeping it (only the shifted column is kept), so
+// little besides the data stays live between the two (fewer registers, more
+// resident waves).  Same thread-to-vector map as tile_load.
+template <class Mem, typename T, int VA, int HINT, int BLOCK, bool SHIFT>
 __host__ __device__ inline void tile_load_fast(const TileArgs& g, const TileBase& tb, int r0,
                                                int tid, const T* A, T* lds,
                                                const int64_t* rowOffA) {
     constexpr int NB = tile_batch(BLOCK);
-    const int W = (int(g.runA) + VA - 1) / VA;  // vectors per row
+    const bool shift = SHIFT && (!g.runsOnGridA || g.misA != 0);
+    const int W = (int(g.runA) + (shift ? VA - 1 : 0) + VA - 1) / VA;  // vectors per row
     const int rows = int(imin(int64_t(g.subRows), tb.validRows - r0));
     const int vcols = int(tb.validCols);
     const T* Ab = A + tb.a;
+    // element offset of the tile origin from the A vector grid
+    const int ta = shift ? int((tb.a + g.misA) & (VA - 1)) : 0;
     int R = tid / W, c = tid % W;
     const int dR = BLOCK / W, dc = BLOCK % W;
     while (R < g.subRows) {
         Vec<T, VA> v[NB];
+        int ccs[SHIFT ? NB : 1];
         const int R0 = R, c0 = c;
 #pragma unroll
         for (int u = 0; u < NB; ++u) {
-            const int cc = c * VA;
-            const int n = R < rows ? imin(VA, vcols - cc) : 0;  // valid elements
-            if (n > 0) {
-                const int off = int(Mem::template lds_ld<int64_t>(rowOffA, r0 + R)) + cc;
-                if (n == VA) {
+            int cc = c * VA;
+            if (R < rows) {
+                const int rowOff = int(Mem::template lds_ld<int64_t>(rowOffA, r0 + R));
+                if (shift) cc -= (ta + rowOff) & (VA - 1);
+                const int off = rowOff + cc;
+                if (cc >= 0 && cc + VA <= vcols) {
                     v[u] = Mem::template ld<T, VA, (HINT & kNtLoad) != 0>(Ab, off);
                 } else {
                     for (int e = 0; e < VA; ++e)
-                        if (e < n) v[u].v[e] = Mem::template ld1<T>(Ab, off + e);
+                        if (cc + e >= 0 && cc + e < vcols)
+                            v[u].v[e] = Mem::template ld1<T>(Ab, off + e);
                 }
             }
+            if constexpr (SHIFT) ccs[u] = cc;
             c += dc;
             R += dR;
             if (c >= W) {
@@ -189,12 +198,14 @@ __host__ __device__ inline void tile_load_fast(const TileArgs& g, const TileBase
         c = c0;
 #pragma unroll
         for (int u = 0; u < NB; ++u) {
-            const int cc = c * VA;
-            const int n = R < rows ? imin(VA, vcols - cc) : 0;
-            const int at = R * g.pitch + cc;
+            int cc = c * VA;
+            if constexpr (SHIFT) cc = ccs[u];
+            if (R < rows) {
+                const int at = R * g.pitch + cc;
 #pragma unroll
-            for (int e = 0; e < VA; ++e)
-                if (e < n) Mem::template lds_st<T>(lds, at + e, v[u].v[e]);
+                for (int e = 0; e < VA; ++e)
+                    if (cc + e >= 0 && cc + e < vcols) Mem::template lds_st<T>(lds, at + e, v[u].v[e]);
+            }
             c += dc;
             R += dR;
             if (c >= W) {
@@ -206,39 +217,48 @@ __host__ __device__ inline void tile_load_fast(const TileArgs& g, const TileBase
 }
 
 // Specialised store phase, the counterpart of tile_load_fast.
-template <class Mem, typename T, int VB, int MODE, int HINT, int BLOCK>
+template <class Mem, typename T, int VB, int MODE, int HINT, int BLOCK, bool SHIFT>
 __host__ __device__ inline void tile_store_fast(const TileArgs& g, const TileBase& tb, int r0,
                                                 int tid, T* B, const T* lds,
                                                 const int64_t* colOffB, T alpha, T beta) {
     constexpr int NB = MODE == kAxpby ? kAxpbyStoreBatch : tile_batch(BLOCK);
-    const int W = (g.subRows + VB - 1) / VB;  // vectors per column
+    const bool shift = SHIFT && (!g.runsOnGridB || g.misB != 0);
+    const int W = (g.subRows + (shift ? VB - 1 : 0) + VB - 1) / VB;  // vectors per column
     const int rows = int(imin(int64_t(g.subRows), tb.validRows - r0));
     const int vcols = int(tb.validCols);
     T* Bb = B + tb.b + r0;
+    // element offset of this pass's origin from the B vector grid
+    const int tbm = shift ? int((tb.b + r0 + g.misB) & (VB - 1)) : 0;
     int q = tid / W, s = tid % W;
     const int dq = BLOCK / W, ds = BLOCK % W;
     while (q < int(g.runA)) {
         Vec<T, VB> x[NB], y[NB];
+        int sss[SHIFT ? NB : 1];
         const int q0 = q, s0 = s;
 #pragma unroll
         for (int u = 0; u < NB; ++u) {
-            const int ss = s * VB;
-            const int n = q < vcols ? imin(VB, rows - ss) : 0;
-            if (n > 0) {
+            int ss = s * VB;
+            if (q < vcols) {
+                int colOff = 0;
+                if (shift || MODE == kAxpby) colOff = int(Mem::template lds_ld<int64_t>(colOffB, q));
+                if (shift) ss -= (tbm + colOff) & (VB - 1);
                 const int base = ss * g.pitch + q;
 #pragma unroll
                 for (int e = 0; e < VB; ++e)
-                    if (e < n) x[u].v[e] = Mem::template lds_ld<T>(lds, base + e * g.pitch);
+                    if (ss + e >= 0 && ss + e < rows)
+                        x[u].v[e] = Mem::template lds_ld<T>(lds, base + e * g.pitch);
                 if (MODE == kAxpby) {
-                    const int off = int(Mem::template lds_ld<int64_t>(colOffB, q)) + ss;
-                    if (n == VB) {
+                    const int off = colOff + ss;
+                    if (ss >= 0 && ss + VB <= rows) {
                         y[u] = Mem::template ld<T, VB, false>(Bb, off);
                     } else {
                         for (int e = 0; e < VB; ++e)
-                            if (e < n) y[u].v[e] = Mem::template ld1<T>(Bb, off + e);
+                            if (ss + e >= 0 && ss + e < rows)
+                                y[u].v[e] = Mem::template ld1<T>(Bb, off + e);
                     }
                 }
             }
+            if constexpr (SHIFT) sss[u] = ss;
             s += ds;
             q += dq;
             if (s >= W) {
@@ -250,20 +270,20 @@ __host__ __device__ inline void tile_store_fast(const TileArgs& g, const TileBas
         s = s0;
 #pragma unroll
         for (int u = 0; u < NB; ++u) {
-            const int ss = s * VB;
-            const int n = q < vcols ? imin(VB, rows - ss) : 0;
-            if (n > 0) {
+            int ss = s * VB;
+            if constexpr (SHIFT) ss = sss[u];
+            if (q < vcols && ss + VB > 0 && ss < rows) {
                 const int off = int(Mem::template lds_ld<int64_t>(colOffB, q)) + ss;
                 Vec<T, VB> zv;
 #pragma unroll
                 for (int e = 0; e < VB; ++e)
                     zv.v[e] =
                         update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
-                if (n == VB) {
+                if (ss >= 0 && ss + VB <= rows) {
                     Mem::template st<(HINT & kNtStore) != 0, T, VB>(Bb, off, zv);
                 } else {
                     for (int e = 0; e < VB; ++e)
-                        if (e < n)
+                        if (ss + e >= 0 && ss + e < rows)
                             Mem::template st1<(HINT & kNtStore) != 0, T>(Bb, off + e, zv.v[e]);
                 }
             }
@@ -283,19 +303,19 @@ __host__ __device__ inline void tile_store_fast(const TileArgs& g, const TileBas
 // Thread tid takes the vectors tid, tid + kBlock, ... of the (stacked row,
 // vector) space, vector fastest, so a wave reads whole runs.  Vectors sit on
 // the A vector grid: a run that starts off it is covered by one more vector,
-// its first and last ones partial (element loads).  GEN = false compiles the
-// common case without either (tile_is_general() is false): every run starts
-// on the grid and nZ = 1 (tile_load_fast).
-template <class Mem, typename T, int VA, int HINT, bool GEN, int BLOCK = kBlock>
+// its first and last ones partial (element loads).  Variants kFast and
+// kShifted (see tile_variant) take tile_load_fast instead.
+template <class Mem, typename T, int VA, int HINT, int VAR, int BLOCK = kBlock>
 __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb, int64_t r0,
                                           int tid, const T* A, T* lds, const int64_t* rowOffA) {
-    static_assert(!GEN || BLOCK == kBlock, "the general variant runs kBlock threads");
-    if constexpr (!GEN) {
-        tile_load_fast<Mem, T, VA, HINT, BLOCK>(g, tb, int(r0), tid, A, lds, rowOffA);
+    static_assert(VAR == kFast || BLOCK == kBlock, "only the kFast variant runs kBigBlock");
+    if constexpr (VAR != kGeneral) {
+        tile_load_fast<Mem, T, VA, HINT, BLOCK, VAR == kShifted>(g, tb, int(r0), tid, A, lds,
+                                                                 rowOffA);
         return;
     }
-    const bool shift = GEN && (!g.runsOnGridA || g.misA != 0);
-    const bool depth = GEN && g.nZ > 1;
+    const bool shift = !g.runsOnGridA || g.misA != 0;
+    const bool depth = g.nZ > 1;
     const int64_t W = (g.runA + (shift ? VA - 1 : 0) + VA - 1) / VA;  // vectors per row
     const int64_t rows = imin(int64_t(g.subRows), tb.validRows - r0);  // rows of this pass
     // staged rows: with shear, the shear rows before the chunk come first
@@ -361,14 +381,14 @@ __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb,
 // fastest, gathers each vector's VB elements from consecutive LDS rows, and
 // writes it to B (reading B first when beta != 0).  Vectors sit on the B
 // vector grid, as in the load phase.
-template <class Mem, typename T, int VB, int MODE, int HINT, bool GEN, int BLOCK = kBlock>
+template <class Mem, typename T, int VB, int MODE, int HINT, int VAR, int BLOCK = kBlock>
 __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb, int64_t r0,
                                            int tid, T* B, const T* lds, const int64_t* colOffB,
                                            T alpha, T beta) {
-    static_assert(!GEN || BLOCK == kBlock, "the general variant runs kBlock threads");
-    if constexpr (!GEN) {
-        tile_store_fast<Mem, T, VB, MODE, HINT, BLOCK>(g, tb, int(r0), tid, B, lds, colOffB, alpha,
-                                                       beta);
+    static_assert(VAR == kFast || BLOCK == kBlock, "only the kFast variant runs kBigBlock");
+    if constexpr (VAR != kGeneral) {
+        tile_store_fast<Mem, T, VB, MODE, HINT, BLOCK, VAR == kShifted>(g, tb, int(r0), tid, B, lds,
+                                                                        colOffB, alpha, beta);
         return;
     }
     constexpr int NB = MODE == kAxpby ? kAxpbyStoreBatch : kBatch;

@@ -142,9 +142,9 @@ hptt_status_t launch(const hptt_plan_s* p, const void* A, void* B, hipStream_t s
     const void* fn = nullptr;
     int block = kBlock;
     if (tile) {
-        // the general variant (less aligned pointers, stacking) runs kBlock threads
-        const bool general = tile_is_general(targs);
-        block = general ? kBlock : in.block;
+        // only the kFast variant takes the plan's workgroup size
+        const int variant = tile_variant(targs);
+        block = variant == kFast ? in.block : kBlock;
         // Runs that are whole lines relative to the tensors' first elements
         // are not whole lines in memory when those are not on a line: lines
         // are then shared between tiles, so no non-temporal hint (see the
@@ -152,8 +152,8 @@ hptt_status_t launch(const hptt_plan_s* p, const void* A, void* B, hipStream_t s
         int hints = in.hints;
         if (pb % 128 != 0) hints &= ~kNtStore;
         if (pa % 128 != 0) hints &= ~kNtLoad;
-        fn = sizeof(T) == 4 ? tile_kernel_f32(general, in.mode, hints, va, vb, block)
-                            : tile_kernel_f64(general, in.mode, hints, va, vb, block);
+        fn = sizeof(T) == 4 ? tile_kernel_f32(variant, in.mode, hints, va, vb, block)
+                            : tile_kernel_f64(variant, in.mode, hints, va, vb, block);
     } else {
         fn = select_mode<T>(p, va, vb);
     }

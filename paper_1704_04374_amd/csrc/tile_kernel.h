@@ -1,8 +1,8 @@
 // Kernel T (stride-1 index moved) as a __global__ template, and the table
 // that maps (update mode, cache hints, vector widths) to one instantiation.
-// Each tile_*.hip file instantiates it for one element type and variant, so
-// the instantiations compile in parallel; kernels.hip only receives the
-// kernel addresses through tile_kernel_f32 / tile_kernel_f64.
+// Each tile_*.hip file instantiates it for one element type and variant (fp64:
+// all three), so the instantiations compile in parallel; kernels.hip only
+// receives the kernel addresses through tile_kernel_f32 / tile_kernel_f64.
 #pragma once
 
 #include "device_mem.h"
@@ -10,11 +10,11 @@
 namespace hptt {
 
 // Address of the tile kernel for (update mode, cache hints, vector widths,
-// workgroup size) in the general (see tile_is_general; 256 threads only) or
-// specialised variant (256 or 1024 threads), or nullptr for an unsupported
+// workgroup size) in variant kFast (256 or 1024 threads), kShifted or
+// kGeneral (256 threads; see tile_variant), or nullptr for an unsupported
 // combination.  Defined in tile_f64.hip.
-const void* tile_kernel_f32(bool general, int mode, int hints, int va, int vb, int block);
-const void* tile_kernel_f64(bool general, int mode, int hints, int va, int vb, int block);
+const void* tile_kernel_f32(int variant, int mode, int hints, int va, int vb, int block);
+const void* tile_kernel_f64(int variant, int mode, int hints, int va, int vb, int block);
 
 namespace {
 
@@ -23,7 +23,7 @@ namespace {
 // load A runs into LDS, barrier, and store B runs.  A 1024-thread workgroup
 // asks for 8 waves per SIMD, i.e. two workgroups per CU, which keeps its
 // registers at 64 VGPRs per lane.
-template <typename T, int VA, int VB, int MODE, int HINT, bool GEN, int BLOCK>
+template <typename T, int VA, int VB, int MODE, int HINT, int VAR, int BLOCK>
 __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(BLOCK >= 1024 ? 8 : 1)))
 void tile_kernel(const T* __restrict__ A, T* __restrict__ B, const TileArgs g, T alpha, T beta) {
     extern __shared__ int64_t smem[];
@@ -39,66 +39,66 @@ void tile_kernel(const T* __restrict__ A, T* __restrict__ B, const TileArgs g, T
         for (int64_t r0 = 0; r0 < tb.validRows; r0 += g.subRows) {
             if (!first) __syncthreads();  // the previous pass's LDS reads are done
             first = false;
-            tile_load<DeviceMem, T, VA, HINT, GEN, BLOCK>(g, tb, r0, tid, A, lds, rowOffA);
+            tile_load<DeviceMem, T, VA, HINT, VAR, BLOCK>(g, tb, r0, tid, A, lds, rowOffA);
             __syncthreads();
-            tile_store<DeviceMem, T, VB, MODE, HINT, GEN, BLOCK>(g, tb, r0, tid, B, lds, colOffB,
+            tile_store<DeviceMem, T, VB, MODE, HINT, VAR, BLOCK>(g, tb, r0, tid, B, lds, colOffB,
                                                                  alpha, beta);
         }
     }
 }
 
-template <typename T, int VA, int MODE, int HINT, bool GEN, int BLOCK>
+template <typename T, int VA, int MODE, int HINT, int VAR, int BLOCK>
 const void* tile_vb(int vb) {
     switch (vb) {
-        case 1: return reinterpret_cast<const void*>(&tile_kernel<T, VA, 1, MODE, HINT, GEN, BLOCK>);
-        case 2: return reinterpret_cast<const void*>(&tile_kernel<T, VA, 2, MODE, HINT, GEN, BLOCK>);
+        case 1: return reinterpret_cast<const void*>(&tile_kernel<T, VA, 1, MODE, HINT, VAR, BLOCK>);
+        case 2: return reinterpret_cast<const void*>(&tile_kernel<T, VA, 2, MODE, HINT, VAR, BLOCK>);
         case 4:
             if constexpr (kMaxVec<T> >= 4)
                 return reinterpret_cast<const void*>(
-                    &tile_kernel<T, VA, 4, MODE, HINT, GEN, BLOCK>);
+                    &tile_kernel<T, VA, 4, MODE, HINT, VAR, BLOCK>);
             return nullptr;
     }
     return nullptr;
 }
 
-template <typename T, int MODE, int HINT, bool GEN, int BLOCK>
+template <typename T, int MODE, int HINT, int VAR, int BLOCK>
 const void* tile_va(int va, int vb) {
     switch (va) {
-        case 1: return tile_vb<T, 1, MODE, HINT, GEN, BLOCK>(vb);
-        case 2: return tile_vb<T, 2, MODE, HINT, GEN, BLOCK>(vb);
+        case 1: return tile_vb<T, 1, MODE, HINT, VAR, BLOCK>(vb);
+        case 2: return tile_vb<T, 2, MODE, HINT, VAR, BLOCK>(vb);
         case 4:
-            if constexpr (kMaxVec<T> >= 4) return tile_vb<T, 4, MODE, HINT, GEN, BLOCK>(vb);
+            if constexpr (kMaxVec<T> >= 4) return tile_vb<T, 4, MODE, HINT, VAR, BLOCK>(vb);
             return nullptr;
     }
     return nullptr;
 }
 
-template <typename T, int MODE, bool GEN, int BLOCK>
+template <typename T, int MODE, int VAR, int BLOCK>
 const void* tile_hint(int hints, int va, int vb) {
     switch (hints) {
-        case 0: return tile_va<T, MODE, 0, GEN, BLOCK>(va, vb);
-        case kNtStore: return tile_va<T, MODE, kNtStore, GEN, BLOCK>(va, vb);
-        case kNtLoad: return tile_va<T, MODE, kNtLoad, GEN, BLOCK>(va, vb);
-        default: return tile_va<T, MODE, kNtStore | kNtLoad, GEN, BLOCK>(va, vb);
+        case 0: return tile_va<T, MODE, 0, VAR, BLOCK>(va, vb);
+        case kNtStore: return tile_va<T, MODE, kNtStore, VAR, BLOCK>(va, vb);
+        case kNtLoad: return tile_va<T, MODE, kNtLoad, VAR, BLOCK>(va, vb);
+        default: return tile_va<T, MODE, kNtStore | kNtLoad, VAR, BLOCK>(va, vb);
     }
 }
 
-template <typename T, bool GEN, int BLOCK>
+template <typename T, int VAR, int BLOCK>
 const void* tile_mode(int mode, int hints, int va, int vb) {
     switch (mode) {
-        case kCopy: return tile_hint<T, kCopy, GEN, BLOCK>(hints, va, vb);
-        case kScale: return tile_hint<T, kScale, GEN, BLOCK>(hints, va, vb);
-        default: return tile_hint<T, kAxpby, GEN, BLOCK>(hints, va, vb);
+        case kCopy: return tile_hint<T, kCopy, VAR, BLOCK>(hints, va, vb);
+        case kScale: return tile_hint<T, kScale, VAR, BLOCK>(hints, va, vb);
+        default: return tile_hint<T, kAxpby, VAR, BLOCK>(hints, va, vb);
     }
 }
 
-// The general variant exists for kBlock threads only; the specialised one
-// for kBlock and kBigBlock.
-template <typename T, bool GEN>
+// Variants kShifted and kGeneral exist for kBlock threads only; kFast for
+// kBlock and kBigBlock.
+template <typename T, int VAR>
 const void* tile_kernel_address(int mode, int hints, int va, int vb, int block) {
-    if (block == kBlock) return tile_mode<T, GEN, kBlock>(mode, hints, va, vb);
-    if constexpr (!GEN)
-        if (block == kBigBlock) return tile_mode<T, GEN, kBigBlock>(mode, hints, va, vb);
+    if (block == kBlock) return tile_mode<T, VAR, kBlock>(mode, hints, va, vb);
+    if constexpr (VAR == kFast)
+        if (block == kBigBlock) return tile_mode<T, VAR, kBigBlock>(mode, hints, va, vb);
     return nullptr;
 }
 

@@ -37,11 +37,15 @@ def plan(perm, size_a, alpha=1.0, beta=0.0, dtype="f32", **knobs):
     return Plan(perm, size_a, alpha, beta, dtype, lib=library(), **knobs)
 
 
+VARIANTS = {"fast": 0, "shifted": 1, "general": 2}
+
+
 def run(p, A=None, B=None, va=0, vb=0, counts=False, block_stride=1, mis_a=0, mis_b=0,
-        general=False):
+        variant=None):
     """Emulate hptt_exec; B is updated in place.  mis_a/mis_b: element offsets
-    of the base pointers from the 16-byte grid (tile kernel); general: run the
-    tile kernel's general variant even where the specialised one would run.
+    of the base pointers from the 16-byte grid (tile kernel); variant:
+    "general" (any plan) or "shifted" (plans the fast variant serves) runs the
+    tile kernel in that variant instead of the one hptt_exec would launch.
     Returns (errors, msg, counts)."""
     lib = library()
     cnt = np.zeros(p.info["footprint_b"], dtype=np.uint8) if counts else None
@@ -49,5 +53,6 @@ def run(p, A=None, B=None, va=0, vb=0, counts=False, block_stride=1, mis_a=0, mi
     err = lib.hptt_emulate_exec(p.handle, None if A is None else A.ctypes.data,
                                 None if B is None else B.ctypes.data, va, vb,
                                 None if cnt is None else cnt.ctypes.data, block_stride, msg,
-                                len(msg), mis_a, mis_b, int(general))
+                                len(msg), mis_a, mis_b,
+                                -1 if variant is None else VARIANTS[variant])
     return err, msg.value.decode(), cnt

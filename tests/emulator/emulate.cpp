@@ -31,7 +31,7 @@ struct EmuState {
     int64_t numelB = 0;   // elements addressable from B
     int64_t misA = 0;     // element offset of A's base from the vector grid
     int64_t misB = 0;
-    bool forceGeneral = false;  // run kernel T's general variant on any plan
+    int forceVariant = -1;  // >= 0: run kernel T in this variant (where it applies)
     const void* A = nullptr;
     void* B = nullptr;
     bool readsB = false;
@@ -144,8 +144,8 @@ void clear_written(int64_t from, int64_t to) {
     memset(S->written.data() + from, 0, size_t(to - from));
 }
 
-// Mirrors tile_kernel in tile_kernel.h, in the variant GEN with BLOCK threads.
-template <typename T, int VA, int VB, int MODE, int NT, bool GEN, int BLOCK>
+// Mirrors tile_kernel in tile_kernel.h, in variant VAR with BLOCK threads.
+template <typename T, int VA, int VB, int MODE, int NT, int VAR, int BLOCK>
 void emu_tile_variant(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     using namespace hptt;
     TileArgs g = p->tile;  // with the base pointers' offsets from the vector grid, as at launch
@@ -169,30 +169,34 @@ void emu_tile_variant(const hptt_plan_s* p, const T* A, T* B, int64_t blockStrid
             for (int64_t r0 = 0; r0 < tb.validRows && S->errors == 0; r0 += g.subRows) {
                 clear_written(tableBytes, ldsBytes);
                 for (int tid = 0; tid < BLOCK; ++tid)
-                    tile_load<HostMem, T, VA, NT, GEN, BLOCK>(g, tb, r0, tid, A, lds, rowOffA);
+                    tile_load<HostMem, T, VA, NT, VAR, BLOCK>(g, tb, r0, tid, A, lds, rowOffA);
                 for (int tid = 0; tid < BLOCK; ++tid)
-                    tile_store<HostMem, T, VB, MODE, NT, GEN, BLOCK>(g, tb, r0, tid, B, lds,
+                    tile_store<HostMem, T, VB, MODE, NT, VAR, BLOCK>(g, tb, r0, tid, B, lds,
                                                                      colOffB, alpha, beta);
             }
         }
     }
 }
 
-// The variant and workgroup size hptt_exec would launch (or the general
-// variant when forced).
+// The variant and workgroup size hptt_exec would launch, or a forced variant:
+// kGeneral serves any plan, kShifted any plan kFast serves.
 template <typename T, int VA, int VB, int MODE, int NT>
 void emu_tile(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
-    using hptt::kBlock;
-    using hptt::kBigBlock;
-    hptt::TileArgs g = p->tile;
+    using namespace hptt;
+    TileArgs g = p->tile;
     g.misA = int32_t(S->misA % VA);
     g.misB = int32_t(S->misB % VB);
-    if (S->forceGeneral || hptt::tile_is_general(g))
-        emu_tile_variant<T, VA, VB, MODE, NT, true, kBlock>(p, A, B, blockStride);
+    int var = tile_variant(g);
+    if (S->forceVariant == kGeneral || (S->forceVariant == kShifted && var == kFast))
+        var = S->forceVariant;
+    if (var == kGeneral)
+        emu_tile_variant<T, VA, VB, MODE, NT, kGeneral, kBlock>(p, A, B, blockStride);
+    else if (var == kShifted)
+        emu_tile_variant<T, VA, VB, MODE, NT, kShifted, kBlock>(p, A, B, blockStride);
     else if (p->info.block == kBigBlock)
-        emu_tile_variant<T, VA, VB, MODE, NT, false, kBigBlock>(p, A, B, blockStride);
+        emu_tile_variant<T, VA, VB, MODE, NT, kFast, kBigBlock>(p, A, B, blockStride);
     else
-        emu_tile_variant<T, VA, VB, MODE, NT, false, kBlock>(p, A, B, blockStride);
+        emu_tile_variant<T, VA, VB, MODE, NT, kFast, kBlock>(p, A, B, blockStride);
 }
 
 // Mirrors stream_kernel in kernels.hip.
@@ -290,8 +294,9 @@ extern "C" {
 // narrower ones as hptt_exec does for less aligned pointers (stream and axpby
 // kernels).  misA/misB: the base pointers' element offsets from the 16-byte
 // grid, which the tile kernel shifts its runs by (vector accesses are checked
-// for alignment relative to that grid).  general = 1 runs the tile kernel's
-// general variant even where hptt_exec would launch the specialised one.
+// for alignment relative to that grid).  variant >= 0 runs the tile kernel
+// in that variant (kGeneral on any plan, kShifted on plans kFast serves)
+// instead of the one hptt_exec would launch.
 // counts (numel
 // bytes, or NULL) is incremented at every B element written.  Only
 // workgroups 0, block_stride, 2*block_stride, ... are run.  Returns the
@@ -299,11 +304,11 @@ extern "C" {
 // A, B and counts cover the footprints (info.footprint_a, footprint_b).
 int64_t hptt_emulate_exec(hptt_plan_t plan, const void* A, void* B, int32_t va, int32_t vb,
                           uint8_t* counts, int64_t block_stride, char* msg, size_t msglen,
-                          int32_t misA, int32_t misB, int32_t general) {
+                          int32_t misA, int32_t misB, int32_t variant) {
     if (!plan) return -1;
     EmuState st;
     S = &st;
-    st.forceGeneral = general != 0;
+    st.forceVariant = variant;
     st.numelA = plan->info.footprint_a;
     st.numelB = plan->info.footprint_b;
     st.misA = misA;

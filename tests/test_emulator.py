@@ -100,8 +100,8 @@ def test_sheared_full_size_geometry():
 
 
 def test_general_tile_variant_on_every_plan():
-    """The tile kernel's general variant (shifted runs, stacked tiles) is also
-    correct on plans where hptt_exec launches the specialised one."""
+    """The tile kernel's general and shifted variants are also correct on
+    plans where hptt_exec launches another one."""
     rng = np.random.default_rng(2018)
     seen = 0
     for it in range(80):
@@ -112,7 +112,8 @@ def test_general_tile_variant_on_every_plan():
         if p.info["kernel"] != "tile":
             continue
         seen += 1
-        _check(p, size_a, perm, alpha, beta, dtype, rng, general=True)
+        _check(p, size_a, perm, alpha, beta, dtype, rng, variant="general")
+        _check(p, size_a, perm, alpha, beta, dtype, rng, variant="shifted")
     assert seen >= 20
 
 
