@@ -95,8 +95,8 @@ struct TileArgs {
     // 1 when every offset inside a tile (table entry plus position in the
     // run) is below 2^31, so the specialised variant can use 32-bit offsets.
     int32_t offsets32;
-    // Sheared B runs (general variant; one B-run index, no stacking, no row
-    // passes).  With shear = lineB - 1 > 0 the B run of column q starts at
+    // Sheared B runs (variants kShifted and kGeneral; one B-run index, no
+    // stacking, no row passes).  With shear = lineB - 1 > 0 the B run of column q starts at
     // the 128-byte line of B at or below the chunk's first row, i.e. it is
     // shifted back by d_q = (B address of the column, in elements) mod lineB,
     // so every line of B is written whole by one tile; the tile stages shear
@@ -139,14 +139,16 @@ struct StreamArgs {
 // Compiled variants of kernel T, picked per launch by tile_variant():
 // kFast when every run starts on its vector grid for the actual pointers,
 // kShifted when some do not (runs shifted onto the grid, partial vectors at
-// both ends), both with 32-bit offsets inside a tile, no stacking and no
-// shear; kGeneral otherwise (stacked tiles, sheared B runs, 64-bit offsets).
+// both ends) or B runs are sheared onto lines, both with 32-bit offsets
+// inside a tile and no stacking; kGeneral otherwise (stacked tiles, 64-bit
+// offsets).
 // g.misA / g.misB must already hold the launch's pointer offsets.
 enum TileVariant : int { kFast = 0, kShifted = 1, kGeneral = 2 };
 
 __host__ __device__ inline int tile_variant(const TileArgs& g) {
-    if (g.nZ > 1 || !g.offsets32 || g.shear > 0) return kGeneral;
-    if (!g.runsOnGridA || !g.runsOnGridB || g.misA != 0 || g.misB != 0) return kShifted;
+    if (g.nZ > 1 || !g.offsets32) return kGeneral;
+    if (!g.runsOnGridA || !g.runsOnGridB || g.misA != 0 || g.misB != 0 || g.shear > 0)
+        return kShifted;
     return kFast;
 }
 

@@ -144,12 +144,13 @@ constexpr int tile_batch(int block) { return block >= 1024 ? 4 : kBatch; }
 // its B vectors double the registers a batch holds.
 constexpr int kAxpbyStoreBatch = 2;
 
-// Specialised load phase (variant kFast, or kShifted with SHIFT): nZ = 1, no
-// shear, and offsets inside a tile fit 32 bits, so the per-vector
+// Specialised load phase (variant kFast, or kShifted with SHIFT): nZ = 1 and
+// offsets inside a tile fit 32 bits, so the per-vector
 // arithmetic is 32-bit around one 64-bit tile base pointer.  Without SHIFT
 // every run starts on the A vector grid; with SHIFT a run that starts off it
-// is covered by one more vector, its first and last ones partial.  The
-// second sweep of a batch recomputes each vector's position from the
+// is covered by one more vector, its first and last ones partial, and
+// sheared B runs stage g.shear rows more.  The second sweep of a batch
+// recomputes each vector's position from the
 // batch's start instead of keeping it (only the shifted column is kept), so
 // little besides the data stays live between the two (fewer registers, more
 // resident waves).  Same thread-to-vector map as tile_load.
@@ -165,16 +166,22 @@ __host__ __device__ inline void tile_load_fast(const TileArgs& g, const TileBase
     const T* Ab = A + tb.a;
     // element offset of the tile origin from the A vector grid
     const int ta = shift ? int((tb.a + g.misA) & (VA - 1)) : 0;
+    // sheared B runs: staged row R holds run index rowBase + R - sh, which
+    // must lie in [0, rowsB); otherwise row R exists when R < rows
+    const int sh = SHIFT ? g.shear : 0;
+    const int staged = g.subRows + sh;
+    const int rLo = sh ? sh - int(tb.rowBase) : 0;
+    const int rHi = sh ? int(g.rowsB - tb.rowBase) + sh : rows;
     int R = tid / W, c = tid % W;
     const int dR = BLOCK / W, dc = BLOCK % W;
-    while (R < g.subRows) {
+    while (R < staged) {
         Vec<T, VA> v[NB];
         int ccs[SHIFT ? NB : 1];
         const int R0 = R, c0 = c;
 #pragma unroll
         for (int u = 0; u < NB; ++u) {
             int cc = c * VA;
-            if (R < rows) {
+            if (R >= rLo && R < rHi && R < staged) {
                 const int rowOff = int(Mem::template lds_ld<int64_t>(rowOffA, r0 + R));
                 if (shift) cc -= (ta + rowOff) & (VA - 1);
                 const int off = rowOff + cc;
@@ -200,7 +207,7 @@ __host__ __device__ inline void tile_load_fast(const TileArgs& g, const TileBase
         for (int u = 0; u < NB; ++u) {
             int cc = c * VA;
             if constexpr (SHIFT) cc = ccs[u];
-            if (R < rows) {
+            if (R >= rLo && R < rHi && R < staged) {
                 const int at = R * g.pitch + cc;
 #pragma unroll
                 for (int e = 0; e < VA; ++e)
@@ -222,13 +229,23 @@ __host__ __device__ inline void tile_store_fast(const TileArgs& g, const TileBas
                                                 int tid, T* B, const T* lds,
                                                 const int64_t* colOffB, T alpha, T beta) {
     constexpr int NB = MODE == kAxpby ? kAxpbyStoreBatch : tile_batch(BLOCK);
-    const bool shift = SHIFT && (!g.runsOnGridB || g.misB != 0);
-    const int W = (g.subRows + (shift ? VB - 1 : 0) + VB - 1) / VB;  // vectors per column
-    const int rows = int(imin(int64_t(g.subRows), tb.validRows - r0));
+    // B runs sheared onto lines (each column's run starts on the line at or
+    // below the chunk's first row), or else shifted onto the vector grid
+    const bool sheared = SHIFT && g.shear > 0;
+    const bool shift = SHIFT && !sheared && (!g.runsOnGridB || g.misB != 0);
+    const int W = sheared ? int(g.runB) / VB
+                          : (g.subRows + (shift ? VB - 1 : 0) + VB - 1) / VB;  // per column
     const int vcols = int(tb.validCols);
+    // element ss of a column's run exists when rows0 <= ss < rows
+    const int rows0 = sheared ? -int(tb.rowBase) : 0;
+    const int rows = sheared ? int(g.rowsB - tb.rowBase)
+                             : int(imin(int64_t(g.subRows), tb.validRows - r0));
+    const int sh = sheared ? g.shear : 0;
     T* Bb = B + tb.b + r0;
-    // element offset of this pass's origin from the B vector grid
-    const int tbm = shift ? int((tb.b + r0 + g.misB) & (VB - 1)) : 0;
+    // element offset of this pass's origin from the B vector grid / line
+    const int tbm = shift ? int((tb.b + r0 + g.misB) & (VB - 1))
+                          : sheared ? int((tb.b + r0 + g.misLineB) & (g.lineB - 1)) : 0;
+    const int gridMask = sheared ? g.lineB - 1 : VB - 1;
     int q = tid / W, s = tid % W;
     const int dq = BLOCK / W, ds = BLOCK % W;
     while (q < int(g.runA)) {
@@ -240,20 +257,21 @@ __host__ __device__ inline void tile_store_fast(const TileArgs& g, const TileBas
             int ss = s * VB;
             if (q < vcols) {
                 int colOff = 0;
-                if (shift || MODE == kAxpby) colOff = int(Mem::template lds_ld<int64_t>(colOffB, q));
-                if (shift) ss -= (tbm + colOff) & (VB - 1);
-                const int base = ss * g.pitch + q;
+                if (shift || sheared || MODE == kAxpby)
+                    colOff = int(Mem::template lds_ld<int64_t>(colOffB, q));
+                if (shift || sheared) ss -= (tbm + colOff) & gridMask;
+                const int base = (ss + sh) * g.pitch + q;
 #pragma unroll
                 for (int e = 0; e < VB; ++e)
-                    if (ss + e >= 0 && ss + e < rows)
+                    if (ss + e >= rows0 && ss + e < rows)
                         x[u].v[e] = Mem::template lds_ld<T>(lds, base + e * g.pitch);
                 if (MODE == kAxpby) {
                     const int off = colOff + ss;
-                    if (ss >= 0 && ss + VB <= rows) {
+                    if (ss >= rows0 && ss + VB <= rows) {
                         y[u] = Mem::template ld<T, VB, false>(Bb, off);
                     } else {
                         for (int e = 0; e < VB; ++e)
-                            if (ss + e >= 0 && ss + e < rows)
+                            if (ss + e >= rows0 && ss + e < rows)
                                 y[u].v[e] = Mem::template ld1<T>(Bb, off + e);
                     }
                 }
@@ -272,18 +290,18 @@ __host__ __device__ inline void tile_store_fast(const TileArgs& g, const TileBas
         for (int u = 0; u < NB; ++u) {
             int ss = s * VB;
             if constexpr (SHIFT) ss = sss[u];
-            if (q < vcols && ss + VB > 0 && ss < rows) {
+            if (q < vcols && ss + VB > rows0 && ss < rows) {
                 const int off = int(Mem::template lds_ld<int64_t>(colOffB, q)) + ss;
                 Vec<T, VB> zv;
 #pragma unroll
                 for (int e = 0; e < VB; ++e)
                     zv.v[e] =
                         update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
-                if (ss >= 0 && ss + VB <= rows) {
+                if (ss >= rows0 && ss + VB <= rows) {
                     Mem::template st<(HINT & kNtStore) != 0, T, VB>(Bb, off, zv);
                 } else {
                     for (int e = 0; e < VB; ++e)
-                        if (ss + e >= 0 && ss + e < rows)
+                        if (ss + e >= rows0 && ss + e < rows)
                             Mem::template st1<(HINT & kNtStore) != 0, T>(Bb, off + e, zv.v[e]);
                 }
             }

@@ -693,14 +693,17 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
                     sB = want;
                 }
             }
-            // Shearing pays where the run's index spans many chunks: its
-            // extra chunk and its lineB - 1 extra rows per chunk are then a
-            // small share (sweep on MI355X: +1 to +10 points of the copy
-            // rate from 8 chunks up, -3 to -13 below 6; likewise A runs of
-            // a few elements lost).  opt.shear = 1 shears wherever it can.
-            const bool pays =
-                sheared && (opt.shear == 1 ||
-                            (plan->tile.rowsB >= 8 * plan->tile.runB && plan->tile.runA >= 8));
+            // Shearing pays unless its chunks leave many row slots idle: the
+            // extra chunk it may need is a large share of a short index
+            // (sweep on MI355X, sheared vs unsheared: +1 to +33 % where at
+            // most 13 % of the slots idle, 0 to +9 % at 19 %, -2 to -9 % at
+            // 23-31 %).  opt.shear = 1 shears wherever it can.
+            bool pays = sheared;
+            if (sheared && opt.shear != 1) {
+                const TileArgs& t = plan->tile;
+                const int64_t chunks = (t.rowsB + t.shear + t.runB - 1) / t.runB;
+                pays = 5 * (chunks * t.runB - t.rowsB) <= chunks * t.runB;  // idle <= 20 %
+            }
             const int64_t area = plan->tile.runA * plan->tile.runB;
             if (!pays || (area < minTile && area < area0)) {
                 plan->tile = keep;

@@ -52,26 +52,29 @@ void fail(const char* what, long long a, long long b) {
     if (S->errors++ == 0) snprintf(S->msg, sizeof(S->msg), "%s (%lld, %lld)", what, a, b);
 }
 
-// Whether p points at one of the n elements from base on; its offset from
-// base goes to *rel.
-template <typename T>
-bool points_into(const T* p, const void* base, int64_t n, int64_t* rel) {
-    const intptr_t d = reinterpret_cast<intptr_t>(p) - reinterpret_cast<intptr_t>(base);
-    if (d < 0 || d % intptr_t(sizeof(T)) != 0 || d / intptr_t(sizeof(T)) >= n) return false;
-    *rel = d / intptr_t(sizeof(T));
-    return true;
+// Distance in bytes from address p to the byte range [base, base + bytes).
+intptr_t distance(const void* p, const void* base, int64_t bytes) {
+    const intptr_t a = reinterpret_cast<intptr_t>(p), b = reinterpret_cast<intptr_t>(base);
+    if (a < b) return b - a;
+    if (a >= b + intptr_t(bytes)) return a - (b + intptr_t(bytes)) + 1;
+    return 0;
 }
 
-// Kernels may address a tensor from its first element or from a pointer
-// inside it (a tile's base); off is turned into an offset from the first
-// element before every check.
+// Kernels address a tensor from its first element or from a pointer near it
+// (a tile's base, which for a sheared chunk past a row's end may lie beyond
+// the tensor).  The tensor meant is the one the pointer is nearer to; the
+// element accessed must lie inside it.  off is turned into an offset from
+// that tensor's first element before every check.
 template <typename T>
 bool check_global(const T* p, int64_t& off, int V, bool isStore) {
-    int64_t rel = 0;
-    const bool isA = points_into(p, S->A, S->numelA, &rel);
-    const bool isB = !isA && points_into(p, S->B, S->numelB, &rel);
-    if (!isA && !isB) { fail("access to an unknown buffer", off, V); return false; }
-    off += rel;
+    const intptr_t dA = distance(p, S->A, S->numelA * int64_t(sizeof(T)));
+    const intptr_t dB = distance(p, S->B, S->numelB * int64_t(sizeof(T)));
+    const bool isA = dA <= dB;
+    const bool isB = !isA;
+    const intptr_t d = reinterpret_cast<intptr_t>(p) + intptr_t(off) * intptr_t(sizeof(T)) -
+                       reinterpret_cast<intptr_t>(isA ? S->A : S->B);
+    if (d % intptr_t(sizeof(T)) != 0) { fail("access off the element grid", off, V); return false; }
+    off = int64_t(d / intptr_t(sizeof(T)));
     if (isA && isStore) { fail("store into A", off, V); return false; }
     if (isB && !isStore && !S->readsB) { fail("B read although beta == 0", off, V); return false; }
     if (off < 0 || off + V > (isA ? S->numelA : S->numelB)) {
