@@ -62,7 +62,8 @@ typedef enum {
     HPTT_KERNEL_NONE = 1,    /* an extent is 0: execute launches nothing */
     HPTT_KERNEL_AXPBY = 2,   /* the fused permutation is the identity: B <- alpha*A + beta*B */
     HPTT_KERNEL_STREAM = 3,  /* A's stride-1 index is also B's: rows streamed in B order */
-    HPTT_KERNEL_TILE = 4,    /* stride-1 index moves: 2-D tiles staged through LDS */
+    HPTT_KERNEL_TILE = 4,    /* tiles staged through LDS: the stride-1 index moves,
+                                or the runs share indices (a short kept one) */
     HPTT_KERNEL_GENERIC = 5  /* one element per thread in B order; any shape */
 } hptt_kernel_t;
 
@@ -102,6 +103,12 @@ typedef struct {
                               line at or below the chunk); 0 = where they apply
                               and the problem is not small, 1 = wherever they
                               apply, 2 = never */
+    int32_t shared_runs;   /* TILE: runs that share indices (the B run passes
+                              through indices of the A run, e.g. a B stride-1
+                              extent of 2 or a short kept stride-1 index): 0 =
+                              where disjoint runs leave a run shorter than a
+                              128-byte line and shared ones are longer, 1 =
+                              wherever they apply, 2 = never */
 } hptt_options_t;
 
 /* What the plan builder decided; for inspection and tests. */
@@ -138,6 +145,8 @@ typedef struct {
     int32_t depth;                     /* TILE: tiles stacked per workgroup round */
     int32_t shear;                     /* TILE: extra rows staged for sheared B runs
                                           (0: runs not sheared) */
+    int32_t shared_runs;               /* TILE: fused indices shared by the A run and
+                                          the B run (0: disjoint runs) */
 } hptt_plan_info_t;
 
 /*

@@ -108,6 +108,27 @@ struct TileArgs {
     int32_t lineB;
     int32_t misLineB;
     int64_t rowsB;
+    // Shared runs (variant kShared): the A run and the B run share
+    // indices (S).  The tile is the product of the indices of both runs.  Its
+    // load phase stages subRows rows, one per value of the B-run indices
+    // outside the A run (R, B order, digits rExt / rStrideA), each the whole
+    // A run; its store phase writes nColS columns, one per value of the A-run
+    // indices outside the B run (C, A order, digits cExt / cStrideB), each the
+    // whole B run, reading B-run position b of column c from LDS at
+    // ldsRow[b] + ldsCol[c].  ldsCol sums cLds (a C index's position weight
+    // in the A run); ldsRow decodes b over the B-run digits oExt (B order)
+    // with weights oLds (an S index's position weight in the A run, or pitch
+    // times an R index's weight among the rows).  cInnerS / rInnerL: the C
+    // columns / R rows before the chunked A-run / B-run index when that index
+    // is in C / R, else 0 (every column / row of a tile exists).
+    int32_t shared;
+    int32_t nColS;
+    int32_t nO;
+    int32_t cInnerS;
+    int32_t rInnerL;
+    int32_t cLds[kMaxDims];
+    FastDiv oExt[kMaxDims];
+    int32_t oLds[kMaxDims];
     int64_t cInner, cChunk, cLast;  // valid columns = cInner * min(cChunk, cLast - j*cChunk)
     int64_t rInner, rChunk, rLast;  // valid rows    = rInner * min(rChunk, rLast - j*rChunk)
     FastDiv cExt[kMaxDims];         // tile extents of the A-run indices
@@ -141,11 +162,13 @@ struct StreamArgs {
 // kShifted when some do not (runs shifted onto the grid, partial vectors at
 // both ends) or B runs are sheared onto lines, both with 32-bit offsets
 // inside a tile and no stacking; kGeneral otherwise (stacked tiles, 64-bit
-// offsets).
+// offsets).  kShared serves the plans whose runs share indices (32-bit
+// offsets, runs on the vector grid of the launch's widths).
 // g.misA / g.misB must already hold the launch's pointer offsets.
-enum TileVariant : int { kFast = 0, kShifted = 1, kGeneral = 2 };
+enum TileVariant : int { kFast = 0, kShifted = 1, kGeneral = 2, kShared = 3 };
 
 __host__ __device__ inline int tile_variant(const TileArgs& g) {
+    if (g.shared) return kShared;
     if (g.nZ > 1 || !g.offsets32) return kGeneral;
     if (!g.runsOnGridA || !g.runsOnGridB || g.misA != 0 || g.misB != 0 || g.shear > 0)
         return kShifted;

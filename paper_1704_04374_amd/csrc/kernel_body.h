@@ -45,6 +45,11 @@ struct TileBase {
     int64_t validRows;   // rows (B-run elements) inside the tensor
     int64_t validDepth;  // stacked tiles inside the tensor
     int64_t rowBase;     // sheared B runs: run index of the chunk's first row
+    // shared runs: validCols is the valid length of the A run and
+    // validRows the valid load rows; these two are the valid length of the B
+    // run and the valid store columns
+    int64_t validRunB;
+    int64_t validColsS;
 };
 
 // Split the tile number into grid digits (fastest first).  With g.skew = s the
@@ -56,6 +61,7 @@ struct TileBase {
 // With g.xcdSplit the workgroup number is first mapped so that the workgroups
 // one XCD receives (numbers x, x + 8, x + 16, ...) take a contiguous range of
 // tile numbers: tiles that share cache lines then share an L2.
+template <bool OVL = false>
 __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
     if (g.xcdSplit) {
         const uint32_t x = t % kXcds, i = t / kXcds;
@@ -66,9 +72,11 @@ __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
     tb.a = 0;
     tb.b = 0;
     tb.validCols = g.runA;
-    tb.validRows = g.runB;
+    tb.validRows = OVL ? int64_t(g.subRows) : g.runB;
     tb.validDepth = g.nZ;
     tb.rowBase = 0;
+    tb.validRunB = g.runB;
+    tb.validColsS = g.nColS;
     uint32_t j0 = 0;
     for (int k = 0; k < g.nG; ++k) {
         uint32_t q = fast_div(t, g.gExt[k]);
@@ -84,8 +92,19 @@ __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
         const int64_t j = int64_t(jj);
         tb.a += j * g.gStrideA[k];
         tb.b += j * g.gStrideB[k];
-        if (k == g.gChunkC) tb.validCols = g.cInner * imin(g.cChunk, g.cLast - j * g.cChunk);
-        if (k == g.gChunkR) {
+        if (k == g.gChunkC) {
+            const int64_t m = imin(g.cChunk, g.cLast - j * g.cChunk);
+            tb.validCols = g.cInner * m;
+            if (OVL && g.cInnerS) tb.validColsS = g.cInnerS * m;
+        }
+        if (OVL && k == g.gChunkR) {
+            // the chunked B-run index is the last of the B run, and of the
+            // load rows when it is not in the A run
+            const int64_t m = imin(g.rChunk, g.rLast - j * g.rChunk);
+            tb.validRunB = g.rInner * m;
+            if (g.rInnerL) tb.validRows = g.rInnerL * m;
+        }
+        if (!OVL && k == g.gChunkR) {
             // a sheared chunk reaches shear rows back and always has work
             // (its count is that of the rows plus shear), so it takes one
             // full pass; its rows are checked one by one
@@ -128,6 +147,57 @@ __host__ __device__ inline void tile_tables(const TileArgs& g, int tid, int64_t*
             x = q;
         }
         Mem::template lds_st<int64_t>(colOffB, c, off);
+    }
+}
+
+// LDS layout of the shared-run variant, in 64-bit words: rowOffA
+// (subRows), colOffB (nColS), then the 32-bit ldsRow (runB) and ldsCol
+// (nColS), then the subRows rows of the tile.
+__host__ __device__ inline int64_t shared_table_words(const TileArgs& g) {
+    return int64_t(g.subRows) + g.nColS + (g.runB + g.nColS + 1) / 2;
+}
+
+// Tables of the shared-run variant, shared by every tile of the launch:
+// rowOffA[r] = A offset of load row r (the R digits), colOffB[c] = B offset
+// of store column c (the C digits), ldsCol[c] = its position in the A run,
+// and ldsRow[b] = the LDS offset of B-run position b in column 0.
+template <class Mem, int BLOCK = kBlock>
+__host__ __device__ inline void tile_tables_shared(const TileArgs& g, int tid, int64_t* rowOffA,
+                                                    int64_t* colOffB, int32_t* ldsRow,
+                                                    int32_t* ldsCol) {
+    for (int64_t r = tid; r < g.subRows; r += BLOCK) {
+        uint32_t x = uint32_t(r);
+        int64_t off = 0;
+        for (int k = 0; k < g.nR; ++k) {
+            const uint32_t q = fast_div(x, g.rExt[k]);
+            off += int64_t(x - q * g.rExt[k].d) * g.rStrideA[k];
+            x = q;
+        }
+        Mem::template lds_st<int64_t>(rowOffA, r, off);
+    }
+    for (int64_t c = tid; c < g.nColS; c += BLOCK) {
+        uint32_t x = uint32_t(c);
+        int64_t offB = 0;
+        int32_t offL = 0;
+        for (int k = 0; k < g.nC; ++k) {
+            const uint32_t q = fast_div(x, g.cExt[k]);
+            const uint32_t digit = x - q * g.cExt[k].d;
+            offB += int64_t(digit) * g.cStrideB[k];
+            offL += int32_t(digit) * g.cLds[k];
+            x = q;
+        }
+        Mem::template lds_st<int64_t>(colOffB, c, offB);
+        Mem::template lds_st<int32_t>(ldsCol, c, offL);
+    }
+    for (int64_t b = tid; b < g.runB; b += BLOCK) {
+        uint32_t x = uint32_t(b);
+        int32_t off = 0;
+        for (int k = 0; k < g.nO; ++k) {
+            const uint32_t q = fast_div(x, g.oExt[k]);
+            off += int32_t(x - q * g.oExt[k].d) * g.oLds[k];
+            x = q;
+        }
+        Mem::template lds_st<int32_t>(ldsRow, b, off);
     }
 }
 
@@ -302,6 +372,82 @@ __host__ __device__ inline void tile_store_fast(const TileArgs& g, const TileBas
                 } else {
                     for (int e = 0; e < VB; ++e)
                         if (ss + e >= rows0 && ss + e < rows)
+                            Mem::template st1<(HINT & kNtStore) != 0, T>(Bb, off + e, zv.v[e]);
+                }
+            }
+            s += ds;
+            q += dq;
+            if (s >= W) {
+                s -= W;
+                q += 1;
+            }
+        }
+    }
+}
+
+// Store phase of the shared-run variant (its load phase is
+// tile_load_fast's on the vector grid): column q is the contiguous B run
+// colOffB[q] + [0, runB), whose position b sits in LDS at ldsRow[b] +
+// ldsCol[q].  Same thread-to-vector map and batching as tile_store_fast.
+template <class Mem, typename T, int VB, int MODE, int HINT, int BLOCK>
+__host__ __device__ inline void tile_store_shared(const TileArgs& g, const TileBase& tb, int tid,
+                                                   T* B, const T* lds, const int64_t* colOffB,
+                                                   const int32_t* ldsRow, const int32_t* ldsCol,
+                                                   T alpha, T beta) {
+    constexpr int NB = MODE == kAxpby ? kAxpbyStoreBatch : tile_batch(BLOCK);
+    const int W = (int(g.runB) + VB - 1) / VB;  // vectors per column
+    const int vcols = int(tb.validColsS);
+    const int rows = int(tb.validRunB);
+    T* Bb = B + tb.b;
+    int q = tid / W, s = tid % W;
+    const int dq = BLOCK / W, ds = BLOCK % W;
+    while (q < g.nColS) {
+        Vec<T, VB> x[NB], y[NB];
+        const int q0 = q, s0 = s;
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const int ss = s * VB;
+            if (q < vcols) {
+                const int colL = Mem::template lds_ld<int32_t>(ldsCol, q);
+#pragma unroll
+                for (int e = 0; e < VB; ++e)
+                    if (ss + e < rows)
+                        x[u].v[e] =
+                            Mem::template lds_ld<T>(lds, Mem::template lds_ld<int32_t>(ldsRow, ss + e) + colL);
+                if (MODE == kAxpby) {
+                    const int off = int(Mem::template lds_ld<int64_t>(colOffB, q)) + ss;
+                    if (ss + VB <= rows) {
+                        y[u] = Mem::template ld<T, VB, false>(Bb, off);
+                    } else {
+                        for (int e = 0; e < VB; ++e)
+                            if (ss + e < rows) y[u].v[e] = Mem::template ld1<T>(Bb, off + e);
+                    }
+                }
+            }
+            s += ds;
+            q += dq;
+            if (s >= W) {
+                s -= W;
+                q += 1;
+            }
+        }
+        q = q0;
+        s = s0;
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const int ss = s * VB;
+            if (q < vcols && ss < rows) {
+                const int off = int(Mem::template lds_ld<int64_t>(colOffB, q)) + ss;
+                Vec<T, VB> zv;
+#pragma unroll
+                for (int e = 0; e < VB; ++e)
+                    zv.v[e] =
+                        update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
+                if (ss + VB <= rows) {
+                    Mem::template st<(HINT & kNtStore) != 0, T, VB>(Bb, off, zv);
+                } else {
+                    for (int e = 0; e < VB; ++e)
+                        if (ss + e < rows)
                             Mem::template st1<(HINT & kNtStore) != 0, T>(Bb, off + e, zv.v[e]);
                 }
             }
@@ -492,8 +638,13 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
 
 // LDS layout of kernel T: rowOffA[runB + shear], colOffB[runA], then
 // nZ * subRows + shear rows of the tile.  A tile with runB > subRows is
-// staged in passes of subRows rows (never with depth or shear).
+// staged in passes of subRows rows (never with depth or shear).  The
+// shared-run variant: its tables (shared_table_words), then subRows
+// rows.
 __host__ __device__ inline int64_t tile_lds_bytes(const TileArgs& g, int elem) {
+    if (g.shared)
+        return shared_table_words(g) * int64_t(sizeof(int64_t)) +
+               int64_t(g.subRows) * g.pitch * elem;
     return (g.runA + g.runB + g.shear) * int64_t(sizeof(int64_t)) +
            (int64_t(g.nZ) * g.subRows + g.shear) * g.pitch * elem;
 }

@@ -12,6 +12,9 @@
 namespace hptt {
 
 int64_t tile_lds_bytes_host(const TileArgs& t, int elem) {
+    if (t.shared)  // tables: rowOffA, colOffB (64-bit), ldsRow, ldsCol (32-bit)
+        return (int64_t(t.subRows) + t.nColS + (t.runB + t.nColS + 1) / 2) * int64_t(sizeof(int64_t)) +
+               int64_t(t.subRows) * t.pitch * elem;
     return (t.runA + t.runB + t.shear) * int64_t(sizeof(int64_t)) +
            (int64_t(t.nZ) * t.subRows + t.shear) * t.pitch * elem;
 }
@@ -21,6 +24,11 @@ namespace {
 constexpr int64_t kLdsMax = 64 * 1024;     // LDS a kernel-T workgroup may use
 constexpr int64_t kLdsMaxBig = 152 * 1024; // ... with kBigBlock threads (one per CU)
 constexpr int64_t kLdsBudget = 40 * 1024;  // preferred: at least 4 workgroups per CU
+// Shared-run tiles when B is read too (beta != 0): 8 resident workgroups per
+// CU (their position table is as large as the tile's data, fp32).  On the
+// MI355X sweep's 12 shared-run cases: beta = 1 3.87 TB/s against 3.55 with
+// the 40 KiB budget, beta = 0 3.22 against 3.30, so beta = 0 keeps 40 KiB.
+constexpr int64_t kSharedLdsBudgetAxpby = 20 * 1024;
 constexpr int64_t kLine = 128;             // L2 cache line of gfx950
 constexpr int64_t kVecBytes = 16;          // widest global access per lane (dwordx4)
 constexpr int64_t kMinTileBytes = 16 * 1024;  // a workgroup round below this is mostly overhead
@@ -186,6 +194,18 @@ int64_t choose_chunk(int64_t inner, int64_t n, int64_t other, int64_t target, in
 
 void set_div(FastDiv& f, int64_t d) { f = make_fastdiv(uint32_t(d)); }
 
+// Grid order of kernel T (both set-ups): diagonal (the second digit
+// rotated by skew times the first) unless asked otherwise, and optionally
+// contiguous tile ranges per XCD.
+void set_tile_order(TileArgs& t, const hptt_options_t& opt, int g, const int64_t* ext,
+                    hptt_plan_info_t& info) {
+    t.skew = (g >= 2 && opt.tile_order != 1 && opt.tile_order != 4) ? (opt.skew > 0 ? opt.skew : 1)
+                                                                     : 0;
+    if (t.skew > 1 && uint64_t(ext[0]) * uint64_t(t.skew) >= (uint64_t(1) << 32)) t.skew = 1;
+    t.xcdSplit = (opt.tile_order == 3 || opt.tile_order == 4) ? 1 : 0;
+    info.tile_order = t.xcdSplit ? (t.skew ? 3 : 4) : t.skew ? 2 : 1;
+}
+
 // Kernel T set-up for targets tA (A-run) and tB (B-run).  Returns false if the
 // tile does not fit the LDS budget or the grid is too large.
 bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_options_t& opt,
@@ -336,11 +356,7 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     }
     info.depth = t.nZ;
     t.nG = g;
-    t.skew = (g >= 2 && opt.tile_order != 1 && opt.tile_order != 4) ? (opt.skew > 0 ? opt.skew : 1)
-                                                                     : 0;
-    if (t.skew > 1 && uint64_t(ext[0]) * uint64_t(t.skew) >= (uint64_t(1) << 32)) t.skew = 1;
-    t.xcdSplit = (opt.tile_order == 3 || opt.tile_order == 4) ? 1 : 0;
-    info.tile_order = t.xcdSplit ? (t.skew ? 3 : 4) : t.skew ? 2 : 1;
+    set_tile_order(t, opt, g, ext, info);
     for (int j = 0; j < g; ++j) {
         if (ext[j] >= (int64_t(1) << 32)) return false;
         set_div(t.gExt[j], ext[j]);
@@ -380,6 +396,7 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     t.alignedA = (granA == 0 || (granA * elem) % kLine == 0) && (t.runA * elem) % kLine == 0;
     t.alignedB = (granB == 0 || (granB * elem) % kLine == 0) && (t.runB * elem) % kLine == 0;
     info.shear = t.shear;
+    info.shared_runs = 0;
     // Rows staged through LDS per pass: the whole tile by default.  Staging a
     // tile in several passes keeps its run lengths with less LDS, but each
     // pass adds a barrier round trip; on MI355X that cost more than it saved
@@ -410,6 +427,248 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     info.lds_bytes = int32_t(lds);
     info.tiles = t.numTiles;
     return true;
+}
+
+// Kernel T with runs that share indices (variant kShared), for targets tA
+// (A run) and tB (B run), in elements.  The A run is A indices 0..d while
+// they lie back to back in A, the last one chunked towards tA.  The B run
+// walks B positions 0, 1, ... while they lie back to back in B: an index of
+// the A run joins it without enlarging the tile (a shared index, S; the
+// chunked A index only as the B run's last), another index (R) joins while
+// the B run is below tB, the last one chunked towards it.  The tile is
+// C x S x R, C being the A-run indices outside the B run.  Returns false if
+// no index is shared, or the tile does not fit the LDS budget or the offsets.
+bool setup_shared(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_options_t& opt,
+                   int64_t ldsBudget, TileArgs& t, hptt_plan_info_t& info) {
+    memset(&t, 0, sizeof(t));
+    const int M = f.M;
+    if (M < 2 || f.sA[0] != 1 || f.sB[f.p[0]] != 1) return false;
+    int64_t inner = 1;
+    int d = 0;
+    while (d < M - 1 && inner * f.n[d] <= tA && f.sA[d + 1] == f.sA[d] * f.n[d])
+        inner *= f.n[d++];
+    bool inA[kMaxDims] = {false}, inB[kMaxDims] = {false};
+    for (int j = 0; j <= d; ++j) inA[j] = true;
+    int64_t cChunk = f.n[d];
+    if (inner * f.n[d] > tA) {
+        bool outside[kMaxDims];
+        for (int j = 0; j < M; ++j) outside[j] = !inA[j];
+        cChunk = choose_chunk(inner, f.n[d], stride_gcd(f, f.sA, outside), tA, elem, false);
+        if (cChunk == 0) return false;
+    }
+    const bool chunkA = cChunk < f.n[d];
+    // B run
+    int64_t bInner = 1;  // B-run elements before its last position
+    int64_t bRun = 1;    // B-run elements so far
+    int e = 0;           // B positions in the run
+    int64_t rChunk = 0;  // extent taken of the B run's last index
+    for (; e < M; ++e) {
+        const int a = f.p[e];
+        if (e > 0 && f.sB[a] != f.sB[f.p[e - 1]] * f.n[f.p[e - 1]]) break;
+        int64_t x = f.n[a];
+        bool last = false;
+        if (inA[a]) {
+            // shared: free, but the chunked A index ends the B run
+            if (a == d && chunkA) {
+                x = cChunk;
+                last = true;
+            }
+        } else {
+            if (bRun >= tB) break;
+            if (bRun * f.n[a] > tB) {
+                bool outside[kMaxDims];
+                for (int j = 0; j < M; ++j) outside[j] = j != a;
+                x = choose_chunk(bRun, f.n[a], stride_gcd(f, f.sB, outside), tB, elem, false);
+                if (x == 0) return false;
+                last = true;
+            }
+        }
+        inB[a] = true;
+        bInner = bRun;
+        rChunk = x;
+        bRun *= x;
+        if (last) {
+            ++e;
+            break;
+        }
+    }
+    if (e == 0) return false;
+    const int lastB = f.p[e - 1];
+    const bool chunkB = rChunk < f.n[lastB];
+    int shared = 0;
+    for (int j = 0; j < M; ++j) shared += inA[j] && inB[j];
+    if (shared == 0) return false;
+
+    t.shared = 1;
+    t.runA = inner * cChunk;
+    t.runB = bRun;
+    t.cInner = inner;
+    t.cChunk = cChunk;
+    t.cLast = f.n[d];
+    t.rInner = bInner;
+    t.rChunk = rChunk;
+    t.rLast = f.n[lastB];
+    // C: A-run indices outside the B run, A order
+    int nC = 0;
+    int64_t cols = 1;
+    t.cInnerS = 0;
+    for (int j = 0; j <= d; ++j) {
+        if (inB[j]) continue;
+        const int64_t x = j == d ? cChunk : f.n[j];
+        if (j == d && chunkA) t.cInnerS = int32_t(cols);
+        set_div(t.cExt[nC], x);
+        t.cStrideB[nC] = f.sB[j];
+        t.cLds[nC] = int32_t(f.sA[j]);
+        cols *= x;
+        ++nC;
+    }
+    t.nC = nC;
+    t.nColS = int32_t(cols);
+    // R: B-run indices outside the A run, B order (the load rows)
+    int nR = 0;
+    int64_t rows = 1;
+    int64_t rowWeight[kMaxDims];
+    t.rInnerL = 0;
+    for (int k = 0; k < e; ++k) {
+        const int a = f.p[k];
+        if (inA[a]) continue;
+        const int64_t x = k == e - 1 ? rChunk : f.n[a];
+        if (k == e - 1 && chunkB) t.rInnerL = int32_t(rows);
+        set_div(t.rExt[nR], x);
+        t.rStrideA[nR] = f.sA[a];
+        rowWeight[k] = rows;
+        rows *= x;
+        ++nR;
+    }
+    t.nR = nR;
+    if (rows >= (int64_t(1) << 30) || cols >= (int64_t(1) << 30)) return false;
+    t.subRows = int32_t(rows);
+    int64_t pad = t.runA % 2 == 0 ? 1 : 0;
+    if (opt.lds_pad > 0) pad = opt.lds_pad;
+    if (opt.lds_pad < 0) pad = 0;
+    t.pitch = int32_t(t.runA + pad);
+    // B-run digits and their LDS weights
+    t.nO = e;
+    for (int k = 0; k < e; ++k) {
+        const int a = f.p[k];
+        set_div(t.oExt[k], k == e - 1 ? rChunk : f.n[a]);
+        t.oLds[k] = int32_t(inA[a] ? f.sA[a] : rowWeight[k] * t.pitch);
+    }
+    // grid digits: the chunk counters, then the indices outside the tile
+    int g = 0;
+    int64_t ext[kMaxDims];
+    t.gChunkC = t.gChunkR = -1;
+    if (chunkA) {
+        ext[g] = (f.n[d] + cChunk - 1) / cChunk;
+        t.gStrideA[g] = cChunk * f.sA[d];
+        t.gStrideB[g] = cChunk * f.sB[d];
+        t.gChunkC = g;
+        if (lastB == d) t.gChunkR = g;
+        ++g;
+    }
+    if (chunkB && lastB != d) {
+        ext[g] = (f.n[lastB] + rChunk - 1) / rChunk;
+        t.gStrideA[g] = rChunk * f.sA[lastB];
+        t.gStrideB[g] = rChunk * f.sB[lastB];
+        t.gChunkR = g++;
+    }
+    for (int a = 0; a < M; ++a) {
+        if (inA[a] || inB[a]) continue;
+        ext[g] = f.n[a];
+        t.gStrideA[g] = f.sA[a];
+        t.gStrideB[g] = f.sB[a];
+        ++g;
+    }
+    t.nZ = 1;
+    t.gDepth = -1;
+    t.nG = g;
+    set_tile_order(t, opt, g, ext, info);
+    uint64_t tiles = 1;
+    for (int j = 0; j < g; ++j) {
+        if (ext[j] >= (int64_t(1) << 32)) return false;
+        set_div(t.gExt[j], ext[j]);
+        tiles *= uint64_t(ext[j]);
+        if (tiles >= (uint64_t(1) << 32)) return false;
+    }
+    t.numTiles = uint32_t(tiles);
+    // Vector widths: rows start at multiples of granA in A, columns at
+    // multiples of granB in B; every run starts on its vector grid.
+    int64_t granA = 0, granB = 0;
+    for (int j = 0; j < g; ++j)
+        if (ext[j] > 1) {
+            granA = gcd64(granA, t.gStrideA[j]);
+            granB = gcd64(granB, t.gStrideB[j]);
+        }
+    for (int j = 0; j < nR; ++j)
+        if (t.rExt[j].d > 1) granA = gcd64(granA, t.rStrideA[j]);
+    for (int j = 0; j < nC; ++j)
+        if (t.cExt[j].d > 1) granB = gcd64(granB, t.cStrideB[j]);
+    info.vec_a = vec_width(granA, elem, opt.max_vec);
+    info.vec_b = vec_width(granB, elem, opt.max_vec);
+    while (info.vec_a > 1 && info.vec_a > t.runA) info.vec_a /= 2;
+    while (info.vec_b > 1 && info.vec_b > t.runB) info.vec_b /= 2;
+    t.runsOnGridA = t.runsOnGridB = 1;
+    t.alignedA = (granA == 0 || (granA * elem) % kLine == 0) && (t.runA * elem) % kLine == 0;
+    t.alignedB = (granB == 0 || (granB * elem) % kLine == 0) && (t.runB * elem) % kLine == 0;
+    int64_t maxRowA = 0, maxColB = 0;
+    for (int j = 0; j < nR; ++j) maxRowA += (int64_t(t.rExt[j].d) - 1) * t.rStrideA[j];
+    for (int j = 0; j < nC; ++j) maxColB += (int64_t(t.cExt[j].d) - 1) * t.cStrideB[j];
+    if (maxRowA + t.runA >= (int64_t(1) << 31) || maxColB + t.runB >= (int64_t(1) << 31))
+        return false;
+    t.offsets32 = 1;
+    const int64_t lds = tile_lds_bytes_host(t, elem);
+    if (lds > ldsBudget) return false;
+    info.run_a = t.runA;
+    info.run_b = t.runB;
+    info.dims_a = d + 1;
+    info.dims_b = e;
+    info.lds_pitch = t.pitch;
+    info.rows_per_pass = t.subRows;
+    info.lds_bytes = int32_t(lds);
+    info.tiles = t.numTiles;
+    info.depth = 1;
+    info.shear = 0;
+    info.shared_runs = shared;
+    return true;
+}
+
+// Score of a tile shape for the choice between disjoint and shared runs:
+// the bytes of each run up to 512 (a run shorter than a few lines wastes
+// most of each HBM burst), then the tile up to kMinTileBytes, and a penalty
+// for leaving most CUs idle.
+double tile_score(int64_t runA, int64_t runB, int64_t tileElems, uint64_t tiles, int elem) {
+    const double pa = double(runA * elem < 512 ? runA * elem : 512);
+    const double pb = double(runB * elem < 512 ? runB * elem : 512);
+    const double area = double(tileElems * elem < kMinTileBytes ? tileElems * elem : kMinTileBytes);
+    return pa + pb + 64.0 * area / double(kMinTileBytes) - (tiles < 1024 ? 256.0 : 0.0);
+}
+
+// The best shared-run tile over a few pairs of run targets (or the
+// requested ones), by tile_score.
+bool choose_shared(const Fused& f, int elem, const hptt_options_t& opt, TileArgs& best,
+                    hptt_plan_info_t& bestInfo, double& bestScore) {
+    static const int64_t aBytes[] = {512, 1024, 2048, 4096, 8192, 16384};
+    static const int64_t bBytes[] = {128, 512, 2048, 8192};
+    bool found = false;
+    const hptt_plan_info_t base = bestInfo;
+    for (int64_t ab : aBytes)
+        for (int64_t bb : bBytes) {
+            const int64_t tA = opt.run_a > 0 ? opt.run_a : ab / elem;
+            const int64_t tB = opt.run_b > 0 ? opt.run_b : bb / elem;
+            TileArgs t;
+            hptt_plan_info_t in = base;
+            const int64_t budget = base.mode == kAxpby ? kSharedLdsBudgetAxpby : kLdsBudget;
+            if (!setup_shared(f, elem, tA, tB, opt, budget, t, in)) continue;
+            const double sc =
+                tile_score(t.runA, t.runB, t.runA * int64_t(t.subRows), t.numTiles, elem);
+            if (!found || sc > bestScore) {
+                found = true;
+                bestScore = sc;
+                best = t;
+                bestInfo = in;
+            }
+        }
+    return found;
 }
 
 bool setup_stream(const Fused& f, int elem, const hptt_options_t& opt, StreamArgs& s,
@@ -500,7 +759,8 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
         opt.tile_order > 4 || opt.row_passes < 0 || opt.row_passes > 64 || opt.depth < 0 ||
         opt.depth > 4096 || opt.min_tile < 0 || opt.exact_runs < 0 ||
         opt.exact_runs > 1 || (opt.block != 0 && opt.block != kBlock && opt.block != kBigBlock) ||
-        opt.skew < 0 || opt.skew > 1024 || opt.shear < 0 || opt.shear > 2)
+        opt.skew < 0 || opt.skew > 1024 || opt.shear < 0 || opt.shear > 2 || opt.shared_runs < 0 ||
+        opt.shared_runs > 2)
         return HPTT_ERROR_INVALID_ARGUMENT;
 
     const int elem = dtype == HPTT_FLOAT32 ? 4 : 8;
@@ -556,7 +816,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
     hptt_kernel_t k = opt.kernel;
     if (k == HPTT_KERNEL_AXPBY && !(single && unit)) return HPTT_ERROR_UNSUPPORTED;
     if (k == HPTT_KERNEL_STREAM && !kept) return HPTT_ERROR_UNSUPPORTED;
-    if (k == HPTT_KERNEL_TILE && (single || kept)) return HPTT_ERROR_UNSUPPORTED;
+    if (k == HPTT_KERNEL_TILE && single) return HPTT_ERROR_UNSUPPORTED;
     if (k == HPTT_KERNEL_AUTO) {
         if (single) k = unit ? HPTT_KERNEL_AXPBY : HPTT_KERNEL_GENERIC;
         else if (kept) k = f.n[0] * elem >= 64 ? HPTT_KERNEL_STREAM : HPTT_KERNEL_GENERIC;
@@ -564,7 +824,27 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
     }
     const int64_t maxBlocks = opt.max_blocks > 0 ? opt.max_blocks : (int64_t(1) << 31) - 1;
 
-    if (k == HPTT_KERNEL_TILE) {
+    // A kept stride-1 index too short for whole rows (or any, on request)
+    // is shared by the A run and the B run of a tile.
+    bool sharedTile = false;
+    if (kept && opt.shared_runs != 2 &&
+        (opt.kernel == HPTT_KERNEL_TILE ||
+         (opt.kernel == HPTT_KERNEL_AUTO && (k == HPTT_KERNEL_GENERIC || opt.shared_runs == 1)))) {
+        double sc = 0;
+        if (choose_shared(f, elem, opt, plan->tile, info, sc)) {
+            k = HPTT_KERNEL_TILE;
+            sharedTile = true;
+        } else if (k == HPTT_KERNEL_TILE) {
+            return HPTT_ERROR_UNSUPPORTED;
+        }
+    }
+    // disjoint runs need the stride-1 index to move
+    if (k == HPTT_KERNEL_TILE && kept && !sharedTile) return HPTT_ERROR_UNSUPPORTED;
+    if (sharedTile) {
+        const int64_t grid = plan->tile.numTiles;
+        info.grid = grid < maxBlocks ? grid : maxBlocks;
+        info.block = kBlock;
+    } else if (k == HPTT_KERNEL_TILE) {
         // Tile search, in order of preference (each stage halves the longer
         // target until a tile fits): both runs on whole 128-byte lines within
         // the occupancy budget; B runs aligned, A runs cut to length; A runs
@@ -730,13 +1010,45 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
                 break;
             }
         }
+        // Disjoint runs whose B run is shorter than a line give way to runs
+        // that share indices (a B stride-1 extent of 2 whose next B index
+        // is in the A run: 8-byte B runs against runs of several lines on
+        // both sides), unless those take narrower vectors.  Short A runs
+        // stay: their rows usually follow each other in A (the B run's
+        // index comes next in A), so a tile still reads one contiguous
+        // block (MI355X sweep: 14x320 tiles 79 % of axpby, the same data
+        // as one shared-run row per tile 42 %).
+        // (not chosen by itself where a knob asks for what only disjoint
+        // runs have: stacking, row passes, shear, 1024 threads, exact runs)
+        const bool plain = opt.depth == 0 && opt.row_passes <= 1 && opt.shear != 1 &&
+                           opt.block != kBigBlock && opt.exact_runs == 0;
+        if (opt.shared_runs == 1 || (opt.shared_runs == 0 && plain)) {
+            bool consider = opt.shared_runs == 1 || !ok;
+            int32_t classicVec = 0;
+            if (ok) {
+                consider = consider || plan->tile.runB * elem < kLine;
+                classicVec = info.vec_a < info.vec_b ? info.vec_a : info.vec_b;
+            }
+            if (consider) {
+                TileArgs t;
+                hptt_plan_info_t in = info;
+                double sc = 0;
+                if (choose_shared(f, elem, opt, t, in, sc) &&
+                    (opt.shared_runs == 1 || (in.vec_a < in.vec_b ? in.vec_a : in.vec_b) >= classicVec)) {
+                    plan->tile = t;
+                    info = in;
+                    sharedTile = true;
+                    ok = true;
+                }
+            }
+        }
         if (!ok) {
             if (opt.kernel == HPTT_KERNEL_TILE) return HPTT_ERROR_UNSUPPORTED;
             k = HPTT_KERNEL_GENERIC;
         } else {
             const int64_t grid = plan->tile.numTiles;
             info.grid = grid < maxBlocks ? grid : maxBlocks;
-            info.block = opt.block > 0 ? opt.block : kBlock;
+            info.block = sharedTile ? kBlock : opt.block > 0 ? opt.block : kBlock;
         }
     }
     if (k == HPTT_KERNEL_STREAM) {
@@ -794,12 +1106,12 @@ void describe_plan(const hptt_plan_s* p, char* buf, size_t len) {
     snprintf(buf, len,
              "kernel=%s dtype=%s mode=%s fused=(%s) perm=(%s) run_a=%lld run_b=%lld "
              "dims_a=%d dims_b=%d vec=%d/%d pitch=%d rows=%d lds=%d tiles=%lld grid=%lld block=%d "
-             "hints=%d order=%d shear=%d",
+             "hints=%d order=%d shear=%d shared=%d",
              kKernel[in.kernel], p->dtype == HPTT_FLOAT32 ? "f32" : "f64", kMode[in.mode], shape,
              perm, (long long)in.run_a, (long long)in.run_b, in.dims_a, in.dims_b, in.vec_a,
              in.vec_b, in.lds_pitch, in.rows_per_pass, in.lds_bytes, (long long)in.tiles,
              (long long)in.grid,
-             in.block, in.hints, in.tile_order, in.shear);
+             in.block, in.hints, in.tile_order, in.shear, in.shared_runs);
 }
 
 }  // namespace hptt

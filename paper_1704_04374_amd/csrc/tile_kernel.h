@@ -10,8 +10,8 @@
 namespace hptt {
 
 // Address of the tile kernel for (update mode, cache hints, vector widths,
-// workgroup size) in variant kFast (256 or 1024 threads), kShifted or
-// kGeneral (256 threads; see tile_variant), or nullptr for an unsupported
+// workgroup size) in variant kFast (256 or 1024 threads), kShifted, kGeneral
+// or kShared (256 threads; see tile_variant), or nullptr for an unsupported
 // combination.  Defined in tile_f64.hip.
 const void* tile_kernel_f32(int variant, int mode, int hints, int va, int vb, int block);
 const void* tile_kernel_f64(int variant, int mode, int hints, int va, int vb, int block);
@@ -27,6 +27,29 @@ template <typename T, int VA, int VB, int MODE, int HINT, int VAR, int BLOCK>
 __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(BLOCK >= 1024 ? 8 : 1)))
 void tile_kernel(const T* __restrict__ A, T* __restrict__ B, const TileArgs g, T alpha, T beta) {
     extern __shared__ int64_t smem[];
+    if constexpr (VAR == kShared) {
+        // runs that share indices: one pass per tile, the store phase
+        // gathering through the LDS position tables
+        int64_t* rowOffA = smem;
+        int64_t* colOffB = smem + g.subRows;
+        int32_t* ldsRow = reinterpret_cast<int32_t*>(colOffB + g.nColS);
+        int32_t* ldsCol = ldsRow + g.runB;
+        T* lds = reinterpret_cast<T*>(smem + shared_table_words(g));
+        const int tid = int(threadIdx.x);
+        tile_tables_shared<DeviceMem, BLOCK>(g, tid, rowOffA, colOffB, ldsRow, ldsCol);
+        __syncthreads();
+        bool first = true;
+        for (uint32_t t = blockIdx.x; t < g.numTiles; t += gridDim.x) {
+            const TileBase tb = tile_base<true>(g, t);
+            if (!first) __syncthreads();  // the previous tile's LDS reads are done
+            first = false;
+            tile_load<DeviceMem, T, VA, HINT, VAR, BLOCK>(g, tb, 0, tid, A, lds, rowOffA);
+            __syncthreads();
+            tile_store_shared<DeviceMem, T, VB, MODE, HINT, BLOCK>(g, tb, tid, B, lds, colOffB,
+                                                                    ldsRow, ldsCol, alpha, beta);
+        }
+        return;
+    }
     int64_t* rowOffA = smem;
     int64_t* colOffB = smem + g.runB + g.shear;
     T* lds = reinterpret_cast<T*>(colOffB + g.runA);
@@ -92,8 +115,8 @@ const void* tile_mode(int mode, int hints, int va, int vb) {
     }
 }
 
-// Variants kShifted and kGeneral exist for kBlock threads only; kFast for
-// kBlock and kBigBlock.
+// Variants kShifted, kGeneral and kShared exist for kBlock threads only;
+// kFast for kBlock and kBigBlock.
 template <typename T, int VAR>
 const void* tile_kernel_address(int mode, int hints, int va, int vb, int block) {
     if (block == kBlock) return tile_mode<T, VAR, kBlock>(mode, hints, va, vb);

@@ -181,6 +181,46 @@ void emu_tile_variant(const hptt_plan_s* p, const T* A, T* B, int64_t blockStrid
     }
 }
 
+// Mirrors tile_kernel's shared-run variant (kShared).
+template <typename T, int VA, int VB, int MODE, int NT>
+void emu_tile_shared(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
+    using namespace hptt;
+    TileArgs g = p->tile;
+    g.misA = int32_t(S->misA % VA);
+    g.misB = int32_t(S->misB % VB);
+    const T alpha = T(p->alpha), beta = T(p->beta);
+    const int64_t ldsBytes = p->info.lds_bytes;
+    if (tile_lds_bytes(g, int(sizeof(T))) != ldsBytes) {
+        fail("LDS size of the plan differs from the kernel's layout", ldsBytes,
+             tile_lds_bytes(g, int(sizeof(T))));
+        return;
+    }
+    const int64_t tableBytes = shared_table_words(g) * int64_t(sizeof(int64_t));
+    S->lds.assign(size_t(ldsBytes), 0);
+    S->written.assign(size_t(ldsBytes), 0);
+    int64_t* smem = reinterpret_cast<int64_t*>(S->lds.data());
+    int64_t* rowOffA = smem;
+    int64_t* colOffB = smem + g.subRows;
+    int32_t* ldsRow = reinterpret_cast<int32_t*>(colOffB + g.nColS);
+    int32_t* ldsCol = ldsRow + g.runB;
+    T* lds = reinterpret_cast<T*>(smem + shared_table_words(g));
+    const int64_t grid = p->info.grid;
+    for (int64_t blk = 0; blk < grid && S->errors == 0; blk += blockStride) {
+        clear_written(0, ldsBytes);
+        for (int tid = 0; tid < kBlock; ++tid)
+            tile_tables_shared<HostMem, kBlock>(g, tid, rowOffA, colOffB, ldsRow, ldsCol);
+        for (int64_t t = blk; t < g.numTiles && S->errors == 0; t += grid) {
+            const TileBase tb = tile_base<true>(g, uint32_t(t));
+            clear_written(tableBytes, ldsBytes);
+            for (int tid = 0; tid < kBlock; ++tid)
+                tile_load<HostMem, T, VA, NT, kShared, kBlock>(g, tb, 0, tid, A, lds, rowOffA);
+            for (int tid = 0; tid < kBlock; ++tid)
+                tile_store_shared<HostMem, T, VB, MODE, NT, kBlock>(g, tb, tid, B, lds, colOffB,
+                                                                     ldsRow, ldsCol, alpha, beta);
+        }
+    }
+}
+
 // The variant and workgroup size hptt_exec would launch, or a forced variant:
 // kGeneral serves any plan, kShifted any plan kFast serves.
 template <typename T, int VA, int VB, int MODE, int NT>
@@ -190,9 +230,12 @@ void emu_tile(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     g.misA = int32_t(S->misA % VA);
     g.misB = int32_t(S->misB % VB);
     int var = tile_variant(g);
-    if (S->forceVariant == kGeneral || (S->forceVariant == kShifted && var == kFast))
+    if (var != kShared &&
+        (S->forceVariant == kGeneral || (S->forceVariant == kShifted && var == kFast)))
         var = S->forceVariant;
-    if (var == kGeneral)
+    if (var == kShared)
+        emu_tile_shared<T, VA, VB, MODE, NT>(p, A, B, blockStride);
+    else if (var == kGeneral)
         emu_tile_variant<T, VA, VB, MODE, NT, kGeneral, kBlock>(p, A, B, blockStride);
     else if (var == kShifted)
         emu_tile_variant<T, VA, VB, MODE, NT, kShifted, kBlock>(p, A, B, blockStride);
@@ -298,8 +341,9 @@ extern "C" {
 // kernels).  misA/misB: the base pointers' element offsets from the 16-byte
 // grid, which the tile kernel shifts its runs by (vector accesses are checked
 // for alignment relative to that grid).  variant >= 0 runs the tile kernel
-// in that variant (kGeneral on any plan, kShifted on plans kFast serves)
-// instead of the one hptt_exec would launch.
+// in that variant (kGeneral on any plan, kShifted on plans kFast serves;
+// plans whose runs share indices always run kShared) instead of the one
+// hptt_exec would launch.
 // counts (numel
 // bytes, or NULL) is incremented at every B element written.  Only
 // workgroups 0, block_stride, 2*block_stride, ... are run.  Returns the
@@ -323,6 +367,11 @@ int64_t hptt_emulate_exec(hptt_plan_t plan, const void* A, void* B, int32_t va, 
     st.counts = counts;
     if (va <= 0) va = plan->info.vec_a;
     if (vb <= 0) vb = plan->info.vec_b;
+    if (plan->info.kernel == HPTT_KERNEL_TILE && plan->tile.shared) {
+        // as hptt_exec: shared-run tiles narrow to the pointers' alignment
+        while (va > 1 && misA % va != 0) va /= 2;
+        while (vb > 1 && misB % vb != 0) vb /= 2;
+    }
     if (block_stride < 1) block_stride = 1;
     if (plan->info.kernel != HPTT_KERNEL_NONE && plan->info.numel > 0) {
         if (plan->dtype == HPTT_FLOAT32)

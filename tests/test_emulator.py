@@ -312,3 +312,115 @@ def test_small_tiles_grow_or_stack():
         assert i["run_a"] * i["run_b"] * i["depth"] >= 2048, p.describe()
         err, msg, _ = emu.run(emu.plan(perm, size, 1.0, 1.0, "f32"), block_stride=97)
         assert err == 0, msg
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f64"])
+def test_shared_run_tiles_match_oracle(dtype):
+    """Tiles whose A run and B run share indices (kept short stride-1 index,
+    small B stride-1 extents), forced wherever they apply, over every update
+    mode and with base pointers off the vector grid (the launch then narrows
+    the vector widths): bit-exact, each B element written once."""
+    rng = np.random.default_rng(1704 + len(dtype))
+    seen = chunked = 0
+    for it in range(140):
+        size_a, perm = random_problem(rng, max_dims=6, extents=(1, 2, 3, 4, 5, 7, 12, 17, 33, 40),
+                                      max_numel=30000)
+        alpha, beta = CASES[it % len(CASES)]
+        try:
+            p = emu.plan(perm, size_a, alpha, beta, dtype, shared_runs=1)
+        except hptt.HpttError:
+            continue
+        if p.info["kernel"] != "tile" or p.info["shared_runs"] == 0:
+            continue
+        seen += 1
+        chunked += p.info["tiles"] > 1
+        per = 4 if dtype == "f32" else 2
+        _check(p, size_a, perm, alpha, beta, dtype, rng, mis_a=it % per, mis_b=(it // 2) % per)
+    assert seen >= 40 and chunked >= 20, (seen, chunked)
+
+
+@pytest.mark.parametrize("knobs", [dict(run_a=8, run_b=8), dict(run_a=64, run_b=16),
+                                   dict(run_a=3, run_b=200), dict(tile_order=1),
+                                   dict(tile_order=3), dict(tile_order=4), dict(lds_pad=-1),
+                                   dict(lds_pad=4), dict(max_vec=1), dict(max_blocks=7)],
+                         ids=lambda k: "_".join(f"{a}{b}" for a, b in k.items()))
+def test_shared_run_knobs_match_oracle(knobs):
+    """Shared-run tiles under the run targets, tile orders, LDS padding,
+    scalar vectors and a capped grid (workgroups looping over tiles)."""
+    rng = np.random.default_rng(99 + len(knobs))
+    seen = 0
+    shapes = [((12, 3, 2, 23, 13), (2, 1, 4, 3, 0)), ((184, 2, 35), (1, 0, 2)),
+              ((29, 12, 2, 7), (2, 0, 3, 1)), ((2, 601, 41), (0, 2, 1)),
+              ((4, 2, 17, 3, 12), (2, 1, 3, 0, 4)), ((3267, 15), (1, 0)),
+              ((2, 56, 30, 14), (2, 0, 3, 1)), ((4, 2, 82, 5, 7, 3), (0, 4, 2, 1, 5, 3)),
+              ((14, 3582), (1, 0)), ((2, 26, 4, 23), (1, 3, 0, 2))]
+    for it, (size_a, perm) in enumerate(shapes):
+        dtype = ("f32", "f64")[it % 2]
+        alpha, beta = CASES[it % len(CASES)]
+        p = emu.plan(perm, size_a, alpha, beta, dtype, shared_runs=1, **knobs)
+        if p.info["shared_runs"] == 0:
+            continue
+        seen += 1
+        _check(p, size_a, perm, alpha, beta, dtype, rng)
+    assert seen >= 5
+
+
+def test_shared_run_outer_sizes_match_oracle():
+    """Shared-run tiles on sub-tensors (outer sizes break the contiguity the
+    runs rely on at random places)."""
+    rng = np.random.default_rng(77)
+    seen = 0
+    for it in range(80):
+        n = int(rng.integers(2, 6))
+        size_a = tuple(int(x) for x in rng.choice([2, 3, 5, 8, 17, 33], size=n))
+        if np.prod(size_a) > 30000:
+            continue
+        perm = tuple(int(p) for p in rng.permutation(n))
+        size_b = tuple(size_a[p] for p in perm)
+        outer_a = tuple(s + int(rng.choice([0, 0, 0, 1, 3])) for s in size_a)
+        outer_b = tuple(s + int(rng.choice([0, 0, 0, 1, 3])) for s in size_b)
+        dtype = ("f32", "f64")[it % 2]
+        alpha, beta = CASES[it % len(CASES)]
+        try:
+            p = emu.plan(perm, size_a, alpha, beta, dtype, outer_size_a=outer_a,
+                         outer_size_b=outer_b, shared_runs=1)
+        except hptt.HpttError:
+            continue
+        if p.info["kernel"] != "tile" or p.info["shared_runs"] == 0:
+            continue
+        seen += 1
+        npd = np.float32 if dtype == "f32" else np.float64
+        fa, fb = p.info["footprint_a"], p.info["footprint_b"]
+        PA = _rand(rng, int(np.prod(outer_a)), npd)
+        PB = _rand(rng, int(np.prod(outer_b)), npd)
+        want = orc.transpose_outer(PA, size_a, perm, outer_a, outer_b, alpha, beta, PB)
+        A = np.ascontiguousarray(PA[:fa])
+        B = np.ascontiguousarray(PB[:fb])
+        err, msg, cnt = emu.run(p, A, B, counts=True)
+        assert err == 0, f"{p.describe()}: {msg}"
+        assert np.array_equal(B, want[:fb]), p.describe()
+        mask = np.zeros(fb, dtype=bool)
+        idx = np.indices(size_b).reshape(n, -1)
+        strides = np.cumprod((1,) + outer_b[:-1])
+        mask[(idx * np.array(strides)[:, None]).sum(axis=0)] = True
+        assert np.all(cnt[mask] == 1) and np.all(cnt[~mask] == 0), p.describe()
+    assert seen >= 15, seen
+
+
+def test_shared_run_full_size_geometry():
+    """Dry runs of sweep cases planned with shared runs by default (shared
+    chunked index, chunked A-only and B-only indices, kept stride-1 index):
+    every offset in bounds and aligned, every B element written once."""
+    from paper_1704_04374_amd.workloads import sweep57
+    names = ("sweep3d_05", "sweep3d_08", "sweep5d_00", "sweep5d_08", "sweep6d_11")
+    n = 0
+    for w in sweep57():
+        if not w.name.startswith(names):
+            continue
+        p = emu.plan(w.perm, w.size_a, w.alpha, w.beta, "f32")
+        assert p.info["kernel"] == "tile" and p.info["shared_runs"] >= 1, p.describe()
+        n += 1
+        err, msg, cnt = emu.run(p, counts=True)
+        assert err == 0, (w.name, msg)
+        assert cnt.min() == 1 and cnt.max() == 1, w.name
+    assert n == len(names)

@@ -85,7 +85,8 @@ def test_workload_full_size(w):
 
 def test_random_sweep():
     """Seeded sweep of small odd shapes: rank 1..6, extents with tails, both
-    dtypes, several alpha and beta, every kernel class."""
+    dtypes, several alpha and beta, every kernel class the plan builder
+    chooses (the generic kernel only where forced, in test_forced_variants)."""
     rng = np.random.default_rng(4374)
     seen = set()
     alphas, betas = (1.0, 1.5, -0.3), (0.0, 1.0, 0.5, -1.25)
@@ -94,8 +95,8 @@ def test_random_sweep():
         dtype = ("f32", "f64")[it % 2]
         alpha, beta = alphas[it % 3], betas[(it // 3) % 4]
         p = _run_case(size_a, perm, alpha, beta, dtype, rng)
-        seen.add(p.info["kernel"])
-    assert {"tile", "axpby", "generic", "stream"} <= seen
+        seen.add(p.info["kernel"] + ("+shared" if p.info["shared_runs"] else ""))
+    assert {"tile", "tile+shared", "axpby", "stream"} <= seen
 
 
 @pytest.mark.parametrize("knobs", [dict(kernel="generic"), dict(run_a=8, run_b=8),
@@ -173,6 +174,47 @@ def test_sheared_b_runs():
         got = dB.cpu().numpy()
         _assert_parity(got[off:off + n], want, "f64", f"offset {off}: {p.describe()}")
         assert np.all(got[:off] == 0) and np.all(got[off + n:] == 0)
+
+
+def test_shared_runs():
+    """Tiles whose A run and B run share indices (a B stride-1 extent of 2, a
+    short kept stride-1 index, a small block permuted inside itself), forced,
+    over every update mode, both dtypes and ragged chunks, and on tensors
+    that start off the vector grid (the launch then narrows the widths)."""
+    rng = np.random.default_rng(57)
+    shapes = [((12, 3, 2, 23, 13), (2, 1, 4, 3, 0)), ((184, 2, 1350), (1, 0, 2)),
+              ((2925, 12, 2, 7), (2, 0, 3, 1)), ((125, 2, 5, 39), (2, 0, 3, 1)),
+              ((70, 5, 98), (1, 0, 2)), ((4, 2, 17, 3, 122), (2, 1, 3, 0, 4)),
+              ((2, 44, 570), (1, 0, 2)), ((71, 2, 2, 176), (2, 0, 3, 1)),
+              ((2, 2625, 4, 23), (1, 3, 0, 2)), ((22, 6, 2, 82, 8, 3), (4, 1, 5, 3, 0, 2)),
+              ((32678, 15), (1, 0)), ((26, 15, 11, 2, 58), (3, 2, 0, 4, 1)),
+              ((2, 6025, 41), (0, 2, 1)), ((2, 454, 19, 27, 10), (0, 3, 2, 1, 4)),
+              ((4, 2, 82, 15, 7, 7), (0, 4, 2, 1, 5, 3)), ((14, 35820), (1, 0))]
+    modes = [(1.0, 0.0), (1.5, 0.0), (2.0, 0.5), (-0.3, 1.25)]
+    seen = 0
+    for i, (size_a, perm) in enumerate(shapes):
+        dtype = ("f32", "f64")[i % 2]
+        alpha, beta = modes[i % len(modes)]
+        _say(f"[parity] shared runs {size_a} {perm} {dtype} {alpha} {beta}")
+        p = _run_case(size_a, perm, alpha, beta, dtype, rng, shared_runs=1)
+        seen += p.info["shared_runs"] > 0
+    assert seen == len(shapes)
+    for (size_a, perm), dtype, off in itertools.product(
+            [((184, 2, 1350), (1, 0, 2)), ((2, 6025, 41), (0, 2, 1))], ("f32", "f64"), (1, 3)):
+        p = hptt.create_plan(perm, size_a, 1.5, 0.5, dtype, shared_runs=1)
+        n = p.numel
+        A = _rand(rng, n, dtype)
+        B0 = _rand(rng, n, dtype)
+        want = orc.transpose(A, size_a, perm, 1.5, 0.5, B0)
+        bufA = torch.zeros(n + 8, dtype=TORCH[dtype], device="cuda")
+        bufB = torch.zeros(n + 8, dtype=TORCH[dtype], device="cuda")
+        dA, dB = bufA[off:off + n], bufB[off:off + n]
+        dA.copy_(torch.from_numpy(A))
+        dB.copy_(torch.from_numpy(B0))
+        p.exec(dA, dB)
+        torch.cuda.synchronize()
+        _assert_parity(dB.cpu().numpy(), want, dtype, f"offset {off}: {p.describe()}")
+        assert bufB[:off].abs().sum().item() == 0 and bufB[off + n:].abs().sum().item() == 0
 
 
 def test_stream_kernel_variants():

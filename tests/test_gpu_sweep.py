@@ -20,12 +20,14 @@ CASES = sweep57()
 
 def test_sweep_full_size():
     seen = set()
+    shared = 0
     for w in CASES:
         print(f"[sweep] {w.describe()}", flush=True)
         A, B0 = inputs(w)
         dA, dB = A.cuda(), B0.cuda()
         p = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype)
         seen.add(p.info["kernel"])
+        shared += p.info["shared_runs"] > 0
         p.exec(dA, dB)
         torch.cuda.synchronize()
         rng = np.random.default_rng(w.seed_a)
@@ -45,3 +47,4 @@ def test_sweep_full_size():
         assert np.array_equal(got, want), c.describe()
         del dA, dB
     assert {"tile", "stream"} <= seen
+    assert shared >= 10  # tiles whose runs share indices

@@ -60,9 +60,12 @@ def test_fig1_plan():
     rows = {r[0]: r[1:] for r in golden("fig1_plan.txt")}
     size_a = tuple(int(x) for x in rows["sizeA"])
     perm = tuple(int(x) for x in rows["perm"])
-    info = hptt.create_plan(perm, size_a).info
+    info = hptt.create_plan(perm, size_a, shared_runs=2).info
     assert info["size"] == size_a and info["perm"] == perm
     assert info["kernel"] == "tile" and info["dims_a"] == 1 and info["dims_b"] == 1
+    # by default so small a problem is one tile whose runs share both indices
+    info = hptt.create_plan(perm, size_a).info
+    assert info["kernel"] == "tile" and info["shared_runs"] == 2 and info["tiles"] == 1
 
 
 def test_fn4_fusion():
@@ -91,7 +94,10 @@ def test_fusion_cases(perm, size, fsize, fperm):
 def test_kernel_classes():
     assert hptt.create_plan((0, 1), (5, 7)).info["kernel"] == "axpby"
     assert hptt.create_plan((0, 2, 1), (64, 5, 7)).info["kernel"] == "stream"
-    assert hptt.create_plan((0, 2, 1), (3, 5, 7)).info["kernel"] == "generic"   # 12-byte rows
+    # 12-byte kept rows: a tile whose runs share the kept index, else generic
+    info = hptt.create_plan((0, 2, 1), (3, 5, 7)).info
+    assert info["kernel"] == "tile" and info["shared_runs"] >= 1
+    assert hptt.create_plan((0, 2, 1), (3, 5, 7), shared_runs=2).info["kernel"] == "generic"
     assert hptt.create_plan((1, 0), (5, 7)).info["kernel"] == "tile"
     assert hptt.create_plan((1, 0), (0, 7)).info["kernel"] == "none"
 
@@ -198,8 +204,10 @@ def test_invalid_options(field, value):
 
 def test_forced_kernel_that_does_not_apply():
     with pytest.raises(hptt.HpttError) as e:
-        hptt.create_plan((0, 2, 1), (64, 5, 7), kernel="tile")
+        hptt.create_plan((0, 2, 1), (64, 5, 7), kernel="tile", shared_runs=2)
     assert e.value.status == 2
+    # a kept stride-1 index is a shared index of a tile
+    assert hptt.create_plan((0, 2, 1), (64, 5, 7), kernel="tile").info["shared_runs"] >= 1
     with pytest.raises(hptt.HpttError):
         hptt.create_plan((1, 0), (64, 5), kernel="stream")
     with pytest.raises(hptt.HpttError):
