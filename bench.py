@@ -88,21 +88,26 @@ def _events(torch, n):
 
 def time_launches(torch, fn, steps: int, warmup: int):
     """Run fn(i) for i < warmup, then `steps` more back to back between a
-    synchronize on each side, with a HIP event pair around every launch on
-    the launch stream.  Returns (wall seconds of the whole timed region,
-    mean GPU milliseconds of one launch).  The wall time also contains the
-    gaps the GPU leaves between dependent launches in one stream."""
+    synchronize on each side (the timed region: wall seconds, which also
+    contain the gaps the GPU leaves between dependent launches in one
+    stream), then `steps` more with a HIP event pair around every launch on
+    the launch stream (mean GPU milliseconds of one launch; the event records
+    are kept out of the timed region, where they would add gaps of their
+    own).  Returns (wall seconds, mean milliseconds per launch)."""
     for i in range(warmup):
         fn(i)
     torch.cuda.synchronize()
-    starts, ends = _events(torch, steps), _events(torch, steps)
     t0 = time.perf_counter()
     for i in range(steps):
-        starts[i].record()
         fn(warmup + i)
-        ends[i].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    starts, ends = _events(torch, steps), _events(torch, steps)
+    for i in range(steps):
+        starts[i].record()
+        fn(warmup + steps + i)
+        ends[i].record()
+    torch.cuda.synchronize()
     ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
     time_launches.last = sorted(ms)
     return wall, sum(ms) / steps

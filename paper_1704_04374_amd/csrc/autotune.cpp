@@ -102,10 +102,23 @@ int autotune_candidates(const int32_t* perm, int32_t N, const int64_t* sizeA,
                                     (ia != 0) + (ib != 0) + ord + ex + (mt != 0) + (h != 0);
                                 if (changed) var.push_back({changed, v});
                             }
+        // tiles with and without shared runs, whichever the quick path took
+        for (int32_t sr = 1; sr <= 2; ++sr) {
+            hptt_options_t v;
+            memset(&v, 0, sizeof(v));
+            v.shared_runs = sr;
+            var.push_back({1, v});
+        }
         for (int c = 1; c <= 6; ++c)
             for (auto& pv : var)
                 if (pv.first == c) cand.push_back(pv.second);
     } else if (base.info.kernel == HPTT_KERNEL_STREAM || base.info.kernel == HPTT_KERNEL_AXPBY) {
+        if (base.info.kernel == HPTT_KERNEL_STREAM) {  // the kept index as a shared run of tiles
+            hptt_options_t v;
+            memset(&v, 0, sizeof(v));
+            v.shared_runs = 1;
+            cand.push_back(v);
+        }
         for (int h = 1; h < 5; ++h) {
             hptt_options_t v;
             memset(&v, 0, sizeof(v));

@@ -1013,28 +1013,29 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
         // Disjoint runs whose B run is shorter than a line give way to runs
         // that share indices (a B stride-1 extent of 2 whose next B index
         // is in the A run: 8-byte B runs against runs of several lines on
-        // both sides), unless those take narrower vectors.  Short A runs
-        // stay: their rows usually follow each other in A (the B run's
-        // index comes next in A), so a tile still reads one contiguous
-        // block (MI355X sweep: 14x320 tiles 79 % of axpby, the same data
-        // as one shared-run row per tile 42 %).
+        // both sides), unless those take narrower vectors; so do disjoint
+        // runs with narrower vectors than shared ones (2-element A runs
+        // read one element per lane: 2x22x2x11885x48 [1,2,0,3,4] 3.66 ->
+        // 4.31 TB/s).  Short A runs alone stay: their rows usually follow
+        // each other in A (the B run's index comes next in A), so a tile
+        // still reads one contiguous block (MI355X sweep: 14x320 tiles 79 %
+        // of axpby, the same data as one shared-run row per tile 42 %).
         // (not chosen by itself where a knob asks for what only disjoint
         // runs have: stacking, row passes, shear, 1024 threads, exact runs)
         const bool plain = opt.depth == 0 && opt.row_passes <= 1 && opt.shear != 1 &&
                            opt.block != kBigBlock && opt.exact_runs == 0;
         if (opt.shared_runs == 1 || (opt.shared_runs == 0 && plain)) {
-            bool consider = opt.shared_runs == 1 || !ok;
-            int32_t classicVec = 0;
-            if (ok) {
-                consider = consider || plan->tile.runB * elem < kLine;
-                classicVec = info.vec_a < info.vec_b ? info.vec_a : info.vec_b;
-            }
-            if (consider) {
+            const bool shortB = ok && plan->tile.runB * elem < kLine;
+            const int32_t classicVec = ok ? (info.vec_a < info.vec_b ? info.vec_a : info.vec_b) : 0;
+            const int32_t widest = vec_width(0, elem, opt.max_vec);
+            if (opt.shared_runs == 1 || !ok || shortB || classicVec < widest) {
                 TileArgs t;
                 hptt_plan_info_t in = info;
                 double sc = 0;
-                if (choose_shared(f, elem, opt, t, in, sc) &&
-                    (opt.shared_runs == 1 || (in.vec_a < in.vec_b ? in.vec_a : in.vec_b) >= classicVec)) {
+                const bool found = choose_shared(f, elem, opt, t, in, sc);
+                const int32_t sharedVec = in.vec_a < in.vec_b ? in.vec_a : in.vec_b;
+                if (found && (opt.shared_runs == 1 || !ok || sharedVec > classicVec ||
+                              (shortB && sharedVec == classicVec))) {
                     plan->tile = t;
                     info = in;
                     sharedTile = true;
