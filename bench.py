@@ -88,20 +88,25 @@ def _events(torch, n):
 
 def time_launches(torch, fn, steps: int, warmup: int):
     """Run fn(i) for i < warmup, then `steps` more back to back between a
-    synchronize on each side (the timed region: wall seconds, which also
-    contain the gaps the GPU leaves between dependent launches in one
-    stream), then `steps` more with a HIP event pair around every launch on
-    the launch stream (mean GPU milliseconds of one launch; the event records
-    are kept out of the timed region, where they would add gaps of their
-    own).  Returns (wall seconds, mean milliseconds per launch)."""
+    synchronize on each side: the timed region, with one HIP event pair on
+    the launch stream around all of it.  Returns (wall seconds of the
+    region, its GPU milliseconds per launch -- each launch's duration plus
+    the gap the GPU leaves before the next dependent one, which agrees with
+    rocprofv3's kernel trace).  Then `steps` more launches, each between its
+    own event pair, give the distribution (time_launches.last); they stay
+    out of the timed region, where each event record would add a gap."""
     for i in range(warmup):
         fn(i)
     torch.cuda.synchronize()
+    region = _events(torch, 2)
     t0 = time.perf_counter()
+    region[0].record()
     for i in range(steps):
         fn(warmup + i)
+    region[1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    per_launch = region[0].elapsed_time(region[1]) / steps
     starts, ends = _events(torch, steps), _events(torch, steps)
     for i in range(steps):
         starts[i].record()
@@ -110,7 +115,7 @@ def time_launches(torch, fn, steps: int, warmup: int):
     torch.cuda.synchronize()
     ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
     time_launches.last = sorted(ms)
-    return wall, sum(ms) / steps
+    return wall, per_launch
 
 
 def time_cold(torch, hptt, fn, flush_buf, sink, reps: int):
