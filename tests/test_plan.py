@@ -194,7 +194,8 @@ def test_null_arguments():
                                          ("max_blocks", -2), ("tile_order", 5), ("exact_runs", 2),
                                          ("row_passes", -1), ("row_passes", 65), ("block", 512),
                                          ("block", -1), ("skew", -1), ("skew", 1025),
-                                         ("shear", 3), ("shear", -1)])
+                                         ("shear", 3), ("shear", -1), ("shared_runs", 3),
+                                         ("shared_runs", -1)])
 def test_invalid_options(field, value):
     opt = hptt.Options()
     setattr(opt, field, value)
@@ -313,3 +314,31 @@ def test_shear_only_where_b_runs_cannot_be_lines():
     assert p64.info["shear"] == 15
     assert hptt.create_plan((1, 0), (39792, 1257), 1.0, 0.0, "f32", shear=2).info["shear"] == 0
     assert hptt.create_plan((1, 0), (39792, 1280), 1.0, 0.0, "f32").info["shear"] == 0
+
+
+def test_shared_runs_where_disjoint_runs_collapse():
+    """Runs that share indices replace disjoint ones whose B run is shorter
+    than a line (B's stride-1 extent 2 with its next index in the A run), or
+    whose vectors are narrower, and the generic kernel on kept stride-1
+    indices under 64 bytes; never on the named workloads, never with
+    shared_runs = 2."""
+    for w in WORKLOADS:
+        assert hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype).info["shared_runs"] == 0
+    # 12x3x2x2293x303, perm [2,1,4,3,0]: disjoint runs write 8-byte B runs
+    size, perm = (12, 3, 2, 2293, 303), (2, 1, 4, 3, 0)
+    d = hptt.create_plan(perm, size, 1.0, 1.0, "f32", shared_runs=2).info
+    assert d["run_b"] * 4 < 128 and d["shared_runs"] == 0
+    s = hptt.create_plan(perm, size, 1.0, 1.0, "f32").info
+    assert s["kernel"] == "tile" and s["shared_runs"] == 2
+    assert s["run_a"] * 4 >= 512 and s["run_b"] * 4 >= 512 and s["lds_bytes"] <= 20 * 1024
+    # beta = 0 takes the larger budget
+    assert hptt.create_plan(perm, size, 1.0, 0.0, "f32").info["lds_bytes"] <= 40 * 1024
+    # a kept stride-1 index of 8 bytes
+    k = hptt.create_plan((0, 2, 1), (2, 60251, 415), 1.0, 1.0, "f32").info
+    assert k["kernel"] == "tile" and k["shared_runs"] == 1
+    # 2-element A runs read one element per lane; shared runs take 16 bytes
+    n = hptt.create_plan((1, 0, 2), (2, 44, 570480), 1.0, 1.0, "f32").info
+    assert n["shared_runs"] == 3 and n["vec_a"] == 4 and n["vec_b"] == 4
+    # short A runs whose rows follow each other in A stay disjoint
+    assert hptt.create_plan((1, 0), (14, 3582084), 1.0, 1.0, "f32").info["shared_runs"] == 0
+    assert hptt.create_plan(perm, size, 1.0, 1.0, "f32", shared_runs=2).info["shared_runs"] == 0
