@@ -163,7 +163,7 @@ struct StreamArgs {
 // both ends) or B runs are sheared onto lines, both with 32-bit offsets
 // inside a tile and no stacking; kGeneral otherwise (stacked tiles, 64-bit
 // offsets).  kShared serves the plans whose runs share indices (32-bit
-// offsets, runs on the vector grid of the launch's widths).
+// offsets, runs shifted onto the vector grid where they start off it).
 // g.misA / g.misB must already hold the launch's pointer offsets.
 enum TileVariant : int { kFast = 0, kShifted = 1, kGeneral = 2, kShared = 3 };
 

@@ -386,44 +386,54 @@ __host__ __device__ inline void tile_store_fast(const TileArgs& g, const TileBas
 }
 
 // Store phase of the shared-run variant (its load phase is
-// tile_load_fast's on the vector grid): column q is the contiguous B run
+// tile_load_fast's, shifted): column q is the contiguous B run
 // colOffB[q] + [0, runB), whose position b sits in LDS at ldsRow[b] +
-// ldsCol[q].  Same thread-to-vector map and batching as tile_store_fast.
+// ldsCol[q].  A run that starts off the B vector grid is shifted onto it,
+// its first and last vectors partial.  Same thread-to-vector map and
+// batching as tile_store_fast.
 template <class Mem, typename T, int VB, int MODE, int HINT, int BLOCK>
 __host__ __device__ inline void tile_store_shared(const TileArgs& g, const TileBase& tb, int tid,
-                                                   T* B, const T* lds, const int64_t* colOffB,
-                                                   const int32_t* ldsRow, const int32_t* ldsCol,
-                                                   T alpha, T beta) {
+                                                  T* B, const T* lds, const int64_t* colOffB,
+                                                  const int32_t* ldsRow, const int32_t* ldsCol,
+                                                  T alpha, T beta) {
     constexpr int NB = MODE == kAxpby ? kAxpbyStoreBatch : tile_batch(BLOCK);
-    const int W = (int(g.runB) + VB - 1) / VB;  // vectors per column
+    const bool shift = !g.runsOnGridB || g.misB != 0;
+    const int W = (int(g.runB) + (shift ? VB - 1 : 0) + VB - 1) / VB;  // vectors per column
     const int vcols = int(tb.validColsS);
     const int rows = int(tb.validRunB);
     T* Bb = B + tb.b;
+    // element offset of the tile origin from the B vector grid
+    const int tbm = shift ? int((tb.b + g.misB) & (VB - 1)) : 0;
     int q = tid / W, s = tid % W;
     const int dq = BLOCK / W, ds = BLOCK % W;
     while (q < g.nColS) {
         Vec<T, VB> x[NB], y[NB];
+        int sss[NB];
         const int q0 = q, s0 = s;
 #pragma unroll
         for (int u = 0; u < NB; ++u) {
-            const int ss = s * VB;
+            int ss = s * VB;
             if (q < vcols) {
+                int colOff = 0;
+                if (shift || MODE == kAxpby) colOff = int(Mem::template lds_ld<int64_t>(colOffB, q));
+                if (shift) ss -= (tbm + colOff) & (VB - 1);
                 const int colL = Mem::template lds_ld<int32_t>(ldsCol, q);
 #pragma unroll
                 for (int e = 0; e < VB; ++e)
-                    if (ss + e < rows)
+                    if (ss + e >= 0 && ss + e < rows)
                         x[u].v[e] =
                             Mem::template lds_ld<T>(lds, Mem::template lds_ld<int32_t>(ldsRow, ss + e) + colL);
                 if (MODE == kAxpby) {
-                    const int off = int(Mem::template lds_ld<int64_t>(colOffB, q)) + ss;
-                    if (ss + VB <= rows) {
+                    const int off = colOff + ss;
+                    if (ss >= 0 && ss + VB <= rows) {
                         y[u] = Mem::template ld<T, VB, false>(Bb, off);
                     } else {
                         for (int e = 0; e < VB; ++e)
-                            if (ss + e < rows) y[u].v[e] = Mem::template ld1<T>(Bb, off + e);
+                            if (ss + e >= 0 && ss + e < rows) y[u].v[e] = Mem::template ld1<T>(Bb, off + e);
                     }
                 }
             }
+            sss[u] = ss;
             s += ds;
             q += dq;
             if (s >= W) {
@@ -435,19 +445,19 @@ __host__ __device__ inline void tile_store_shared(const TileArgs& g, const TileB
         s = s0;
 #pragma unroll
         for (int u = 0; u < NB; ++u) {
-            const int ss = s * VB;
-            if (q < vcols && ss < rows) {
+            const int ss = sss[u];
+            if (q < vcols && ss + VB > 0 && ss < rows) {
                 const int off = int(Mem::template lds_ld<int64_t>(colOffB, q)) + ss;
                 Vec<T, VB> zv;
 #pragma unroll
                 for (int e = 0; e < VB; ++e)
                     zv.v[e] =
                         update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
-                if (ss + VB <= rows) {
+                if (ss >= 0 && ss + VB <= rows) {
                     Mem::template st<(HINT & kNtStore) != 0, T, VB>(Bb, off, zv);
                 } else {
                     for (int e = 0; e < VB; ++e)
-                        if (ss + e < rows)
+                        if (ss + e >= 0 && ss + e < rows)
                             Mem::template st1<(HINT & kNtStore) != 0, T>(Bb, off + e, zv.v[e]);
                 }
             }
@@ -474,8 +484,8 @@ __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb,
                                           int tid, const T* A, T* lds, const int64_t* rowOffA) {
     static_assert(VAR == kFast || BLOCK == kBlock, "only the kFast variant runs kBigBlock");
     if constexpr (VAR != kGeneral) {
-        tile_load_fast<Mem, T, VA, HINT, BLOCK, VAR == kShifted>(g, tb, int(r0), tid, A, lds,
-                                                                 rowOffA);
+        tile_load_fast<Mem, T, VA, HINT, BLOCK, VAR == kShifted || VAR == kShared>(
+            g, tb, int(r0), tid, A, lds, rowOffA);
         return;
     }
     const bool shift = !g.runsOnGridA || g.misA != 0;

@@ -128,12 +128,10 @@ hptt_status_t launch(const hptt_plan_s* p, const void* A, void* B, hipStream_t s
     const int elem = int(sizeof(T));
     const uintptr_t pa = reinterpret_cast<uintptr_t>(A), pb = reinterpret_cast<uintptr_t>(B);
     // The tile kernel keeps its widths and shifts its runs onto the vector
-    // grid of the actual pointers; the others, and tiles whose runs share
-    // indices, narrow to the pointers' alignment.
+    // grid of the actual pointers; the others narrow to the pointers' alignment.
     const bool tile = in.kernel == HPTT_KERNEL_TILE;
-    const bool keep = tile && !p->tile.shared;
-    const int va = keep ? in.vec_a : aligned_width(in.vec_a, pa, elem);
-    const int vb = keep ? in.vec_b : aligned_width(in.vec_b, pb, elem);
+    const int va = tile ? in.vec_a : aligned_width(in.vec_a, pa, elem);
+    const int vb = tile ? in.vec_b : aligned_width(in.vec_b, pb, elem);
     TileArgs targs;
     if (tile) {
         targs = p->tile;

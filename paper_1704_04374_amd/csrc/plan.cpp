@@ -592,7 +592,7 @@ bool setup_shared(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_o
     }
     t.numTiles = uint32_t(tiles);
     // Vector widths: rows start at multiples of granA in A, columns at
-    // multiples of granB in B; every run starts on its vector grid.
+    // multiples of granB in B; runs off the vector grid are shifted onto it.
     int64_t granA = 0, granB = 0;
     for (int j = 0; j < g; ++j)
         if (ext[j] > 1) {
@@ -603,11 +603,10 @@ bool setup_shared(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_o
         if (t.rExt[j].d > 1) granA = gcd64(granA, t.rStrideA[j]);
     for (int j = 0; j < nC; ++j)
         if (t.cExt[j].d > 1) granB = gcd64(granB, t.cStrideB[j]);
-    info.vec_a = vec_width(granA, elem, opt.max_vec);
-    info.vec_b = vec_width(granB, elem, opt.max_vec);
-    while (info.vec_a > 1 && info.vec_a > t.runA) info.vec_a /= 2;
-    while (info.vec_b > 1 && info.vec_b > t.runB) info.vec_b /= 2;
-    t.runsOnGridA = t.runsOnGridB = 1;
+    info.vec_a = run_vec_width(t.runA, granA, elem, opt.max_vec);
+    info.vec_b = run_vec_width(t.runB, granB, elem, opt.max_vec);
+    t.runsOnGridA = granA % info.vec_a == 0 ? 1 : 0;
+    t.runsOnGridB = granB % info.vec_b == 0 ? 1 : 0;
     t.alignedA = (granA == 0 || (granA * elem) % kLine == 0) && (t.runA * elem) % kLine == 0;
     t.alignedB = (granB == 0 || (granB * elem) % kLine == 0) && (t.runB * elem) % kLine == 0;
     int64_t maxRowA = 0, maxColB = 0;

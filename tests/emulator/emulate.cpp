@@ -367,11 +367,6 @@ int64_t hptt_emulate_exec(hptt_plan_t plan, const void* A, void* B, int32_t va, 
     st.counts = counts;
     if (va <= 0) va = plan->info.vec_a;
     if (vb <= 0) vb = plan->info.vec_b;
-    if (plan->info.kernel == HPTT_KERNEL_TILE && plan->tile.shared) {
-        // as hptt_exec: shared-run tiles narrow to the pointers' alignment
-        while (va > 1 && misA % va != 0) va /= 2;
-        while (vb > 1 && misB % vb != 0) vb /= 2;
-    }
     if (block_stride < 1) block_stride = 1;
     if (plan->info.kernel != HPTT_KERNEL_NONE && plan->info.numel > 0) {
         if (plan->dtype == HPTT_FLOAT32)

@@ -318,8 +318,8 @@ def test_small_tiles_grow_or_stack():
 def test_shared_run_tiles_match_oracle(dtype):
     """Tiles whose A run and B run share indices (kept short stride-1 index,
     small B stride-1 extents), forced wherever they apply, over every update
-    mode and with base pointers off the vector grid (the launch then narrows
-    the vector widths): bit-exact, each B element written once."""
+    mode and with base pointers off the vector grid (runs shifted onto it):
+    bit-exact, each B element written once."""
     rng = np.random.default_rng(1704 + len(dtype))
     seen = chunked = 0
     for it in range(140):

@@ -180,7 +180,7 @@ def test_shared_runs():
     """Tiles whose A run and B run share indices (a B stride-1 extent of 2, a
     short kept stride-1 index, a small block permuted inside itself), forced,
     over every update mode, both dtypes and ragged chunks, and on tensors
-    that start off the vector grid (the launch then narrows the widths)."""
+    that start off the vector grid (runs shifted onto it)."""
     rng = np.random.default_rng(57)
     shapes = [((12, 3, 2, 23, 13), (2, 1, 4, 3, 0)), ((184, 2, 1350), (1, 0, 2)),
               ((2925, 12, 2, 7), (2, 0, 3, 1)), ((125, 2, 5, 39), (2, 0, 3, 1)),
