@@ -109,6 +109,13 @@ typedef struct {
                               where disjoint runs leave a run shorter than a
                               128-byte line and shared ones are longer, 1 =
                               wherever they apply, 2 = never */
+    int32_t flat_runs;     /* TILE: B runs cut from the flattened range of the
+                              B indices they span (back to back in B, none in
+                              the A run) in whole 128-byte lines, instead of
+                              whole multiples of the inner extents: 0 = where
+                              those extents are not whole lines and the usual
+                              B run is not or is long, 1 = wherever they
+                              apply, 2 = never */
 } hptt_options_t;
 
 /* What the plan builder decided; for inspection and tests. */
@@ -147,6 +154,8 @@ typedef struct {
                                           (0: runs not sheared) */
     int32_t shared_runs;               /* TILE: fused indices shared by the A run and
                                           the B run (0: disjoint runs) */
+    int32_t flat_runs;                 /* TILE: fused B indices the flat B run is cut
+                                          from (0: B runs are not flat) */
 } hptt_plan_info_t;
 
 /*

@@ -109,6 +109,13 @@ int autotune_candidates(const int32_t* perm, int32_t N, const int64_t* sizeA,
             v.shared_runs = sr;
             var.push_back({1, v});
         }
+        // flat B runs and runs of whole inner extents, whichever it took
+        for (int32_t fr = 1; fr <= 2; ++fr) {
+            hptt_options_t v;
+            memset(&v, 0, sizeof(v));
+            v.flat_runs = fr;
+            var.push_back({1, v});
+        }
         for (int c = 1; c <= 6; ++c)
             for (auto& pv : var)
                 if (pv.first == c) cand.push_back(pv.second);

@@ -108,6 +108,16 @@ struct TileArgs {
     int32_t lineB;
     int32_t misLineB;
     int64_t rowsB;
+    // Flat B runs (variants kFast, kShifted and kGeneral; no stacking, no
+    // shear).  With flatR = 1 the B run is a chunk of runB consecutive
+    // positions of the flattened range of B positions 0..nR-1 (each whole,
+    // back to back in B, rLast positions in all), not of its last index
+    // alone: a B stride-1 extent that is not a multiple of a 128-byte line
+    // then still gives one-line B runs.  rExt holds the whole extents,
+    // rInner = 1, rChunk = runB; the chunk digit moves B by runB and A by
+    // nothing, and rowOffA is rebuilt for every tile from the chunk's first
+    // flattened position (TileBase::rowBase).
+    int32_t flatR;
     // Shared runs (variant kShared): the A run and the B run share
     // indices (S).  The tile is the product of the indices of both runs.  Its
     // load phase stages subRows rows, one per value of the B-run indices

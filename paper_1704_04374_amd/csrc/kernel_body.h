@@ -124,7 +124,8 @@ __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
 template <class Mem, int BLOCK = kBlock>
 __host__ __device__ inline void tile_tables(const TileArgs& g, int tid, int64_t* rowOffA,
                                             int64_t* colOffB) {
-    for (int64_t r = tid; r < g.runB + g.shear; r += BLOCK) {
+    // flat B runs: the row table belongs to one tile (tile_rows_flat)
+    for (int64_t r = tid; r < (g.flatR ? 0 : g.runB + g.shear); r += BLOCK) {
         int64_t off = 0;
         if (g.shear) {
             off = (r - g.shear) * g.rStrideA[0];
@@ -147,6 +148,25 @@ __host__ __device__ inline void tile_tables(const TileArgs& g, int tid, int64_t*
             x = q;
         }
         Mem::template lds_st<int64_t>(colOffB, c, off);
+    }
+}
+
+// Row table of one tile with flat B runs: rowOffA[r] = A offset of
+// flattened B-run position rowBase + r, split into the B-run digits, for the
+// tile's valid rows.  The caller puts a barrier between the previous tile's
+// load phase and this call, and another before the next load phase.
+template <class Mem, int BLOCK = kBlock>
+__host__ __device__ inline void tile_rows_flat(const TileArgs& g, const TileBase& tb, int tid,
+                                               int64_t* rowOffA) {
+    for (int64_t r = tid; r < tb.validRows; r += BLOCK) {
+        uint32_t x = uint32_t(tb.rowBase + r);
+        int64_t off = 0;
+        for (int k = 0; k < g.nR; ++k) {
+            const uint32_t q = fast_div(x, g.rExt[k]);
+            off += int64_t(x - q * g.rExt[k].d) * g.rStrideA[k];
+            x = q;
+        }
+        Mem::template lds_st<int64_t>(rowOffA, r, off);
     }
 }
 

@@ -210,7 +210,7 @@ void set_tile_order(TileArgs& t, const hptt_options_t& opt, int g, const int64_t
 // tile does not fit the LDS budget or the grid is too large.
 bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_options_t& opt,
                 bool alignA, bool alignB, int64_t ldsBudget, int64_t minTile, TileArgs& t,
-                hptt_plan_info_t& info, bool shear = false) {
+                hptt_plan_info_t& info, bool shear = false, bool flat = false) {
     memset(&t, 0, sizeof(t));
     const int64_t lineB = kLine / elem;
     const int M = f.M;
@@ -249,7 +249,14 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     for (int j = 0; j < M; ++j) outside[j] = true;
     for (int j = 0; j <= k; ++j) outside[f.p[j]] = false;
     int64_t rChunk = f.n[f.p[k]];
-    if (shear) {
+    const int64_t flatLen = inner * f.n[f.p[k]];  // the flattened B-run range
+    if (flat) {
+        // flat B runs: whole lines cut from positions 0..k flattened (two
+        // or more of them, longer than one run)
+        if (k == 0 || shear) return false;
+        rChunk = tB >= lineB ? tB / lineB * lineB : lineB;
+        if (rChunk >= flatLen) return false;
+    } else if (shear) {
         // sheared B runs: one B-run index, chunks of whole lines, and more
         // than one chunk (a run that covers its index needs no shear)
         if (k != 0) return false;
@@ -261,11 +268,12 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     if (rChunk == 0) return false;
     const int nR = k + 1;
     t.nR = nR;
-    t.rInner = inner;
+    t.rInner = flat ? 1 : inner;
     t.rChunk = rChunk;
-    t.rLast = f.n[f.p[k]];
+    t.rLast = flat ? flatLen : f.n[f.p[k]];
+    t.flatR = flat ? 1 : 0;
     for (int j = 0; j < nR; ++j) {
-        set_div(t.rExt[j], j == nR - 1 ? rChunk : f.n[f.p[j]]);
+        set_div(t.rExt[j], j == nR - 1 && !flat ? rChunk : f.n[f.p[j]]);
         t.rStrideA[j] = f.sA[f.p[j]];
     }
     t.runA = t.cInner * t.cChunk;
@@ -289,8 +297,10 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
         // sheared runs start up to lineB - 1 rows early: one chunk more at most
         const int64_t span = t.rLast + (shear ? lineB - 1 : 0);
         ext[g] = (span + t.rChunk - 1) / t.rChunk;
-        t.gStrideA[g] = t.rChunk * f.sA[a];
-        t.gStrideB[g] = t.rChunk * f.sB[a];
+        // a flat chunk moves B by its length; its A offsets are in the
+        // tile's own row table
+        t.gStrideA[g] = flat ? 0 : t.rChunk * f.sA[a];
+        t.gStrideB[g] = flat ? t.rChunk * f.sB[p0] : t.rChunk * f.sB[a];
         t.gChunkR = g++;
     }
     for (int a = 0; a < M; ++a) {
@@ -323,7 +333,7 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
         opt.depth > 0 ? opt.depth : (2 * area >= minTile ? 1 : (minTile + area - 1) / area);
     if (opt.depth == 0 && double(wantZ) > tilesBefore / kMinGrid)
         wantZ = int64_t(tilesBefore / kMinGrid);
-    if (opt.row_passes > 1 || shear) wantZ = 1;
+    if (opt.row_passes > 1 || shear || flat) wantZ = 1;
     if (wantZ > 1) {
         // among the indices long enough for wantZ the one with the smallest
         // strides; if none is, the longest
@@ -397,6 +407,7 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     t.alignedB = (granB == 0 || (granB * elem) % kLine == 0) && (t.runB * elem) % kLine == 0;
     info.shear = t.shear;
     info.shared_runs = 0;
+    info.flat_runs = flat ? nR : 0;
     // Rows staged through LDS per pass: the whole tile by default.  Staging a
     // tile in several passes keeps its run lengths with less LDS, but each
     // pass adds a barrier round trip; on MI355X that cost more than it saved
@@ -759,7 +770,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
         opt.depth > 4096 || opt.min_tile < 0 || opt.exact_runs < 0 ||
         opt.exact_runs > 1 || (opt.block != 0 && opt.block != kBlock && opt.block != kBigBlock) ||
         opt.skew < 0 || opt.skew > 1024 || opt.shear < 0 || opt.shear > 2 || opt.shared_runs < 0 ||
-        opt.shared_runs > 2)
+        opt.shared_runs > 2 || opt.flat_runs < 0 || opt.flat_runs > 2)
         return HPTT_ERROR_INVALID_ARGUMENT;
 
     const int elem = dtype == HPTT_FLOAT32 ? 4 : 8;
@@ -992,6 +1003,39 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
                 tB = sB;
             }
         }
+        // B runs that span two or more B indices whose inner extents are
+        // not whole lines (a B stride-1 extent of 20 fp32) can only start
+        // and end on lines as long runs (160 elements = 5 lines), which
+        // makes the tile large; flat B runs are cut from the flattened range
+        // of those indices in whole lines instead, the A offsets of their
+        // rows tabled per tile.  MI355X: the 6-D fp32 workload 4.86 ->
+        // 5.14 TB/s (96x32 flat tiles against 48x160), two 6-D sweep cases
+        // +4 % and +14 % with beta = 0 and +3 % and +4 % with beta = 1.  The
+        // A-run target stays 512 bytes when B is read: one-line B runs with
+        // 256-byte A runs made tiles of 8 KiB that lost 4 % there.
+        if (ok && opt.flat_runs != 2 && plan->tile.shear == 0 && plan->tile.nZ == 1 &&
+            plan->tile.nR >= 2 && opt.row_passes <= 1 &&
+            (opt.flat_runs == 1 ||
+             (opt.exact_runs == 0 && (plan->tile.rInner * elem) % kLine != 0 &&
+              (!plan->tile.alignedB || plan->tile.runB > 2 * (kLine / elem))))) {
+            TileArgs keep = plan->tile;
+            hptt_plan_info_t keepInfo = info;
+            const int64_t fA = opt.run_a > 0 ? opt.run_a : 512 / elem;
+            const int64_t fB = opt.run_b > 0 ? opt.run_b : kLine / elem;
+            bool flat = false;
+            for (int aligned = opt.exact_runs ? 0 : 1; aligned >= 0 && !flat; --aligned) {
+                flat = setup_tile(f, elem, fA, fB, opt, aligned == 1, true, kLdsBudget, minTile,
+                                  plan->tile, info, false, true) &&
+                       (plan->tile.alignedB || opt.flat_runs == 1);
+            }
+            if (!flat) {
+                plan->tile = keep;
+                info = keepInfo;
+            } else {
+                tA = fA;
+                tB = fB;
+            }
+        }
         // Small problems: shorter runs (down to one 128-byte line) for more
         // tiles, so that more CUs take part.
         while (ok && opt.run_a == 0 && opt.run_b == 0 && plan->tile.numTiles < 512 &&
@@ -1106,12 +1150,12 @@ void describe_plan(const hptt_plan_s* p, char* buf, size_t len) {
     snprintf(buf, len,
              "kernel=%s dtype=%s mode=%s fused=(%s) perm=(%s) run_a=%lld run_b=%lld "
              "dims_a=%d dims_b=%d vec=%d/%d pitch=%d rows=%d lds=%d tiles=%lld grid=%lld block=%d "
-             "hints=%d order=%d shear=%d shared=%d",
+             "hints=%d order=%d shear=%d shared=%d flat=%d",
              kKernel[in.kernel], p->dtype == HPTT_FLOAT32 ? "f32" : "f64", kMode[in.mode], shape,
              perm, (long long)in.run_a, (long long)in.run_b, in.dims_a, in.dims_b, in.vec_a,
              in.vec_b, in.lds_pitch, in.rows_per_pass, in.lds_bytes, (long long)in.tiles,
              (long long)in.grid,
-             in.block, in.hints, in.tile_order, in.shear, in.shared_runs);
+             in.block, in.hints, in.tile_order, in.shear, in.shared_runs, in.flat_runs);
 }
 
 }  // namespace hptt

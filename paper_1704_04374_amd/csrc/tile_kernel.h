@@ -59,6 +59,13 @@ void tile_kernel(const T* __restrict__ A, T* __restrict__ B, const TileArgs g, T
     bool first = true;
     for (uint32_t t = blockIdx.x; t < g.numTiles; t += gridDim.x) {
         const TileBase tb = tile_base(g, t);
+        if (g.flatR) {
+            // every lane is past the previous tile's load phase, the only
+            // reader of the row table; the barrier also ends its store phase
+            tile_rows_flat<DeviceMem, BLOCK>(g, tb, tid, rowOffA);
+            __syncthreads();
+            first = true;
+        }
         for (int64_t r0 = 0; r0 < tb.validRows; r0 += g.subRows) {
             if (!first) __syncthreads();  // the previous pass's LDS reads are done
             first = false;

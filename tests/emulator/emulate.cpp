@@ -169,6 +169,11 @@ void emu_tile_variant(const hptt_plan_s* p, const T* A, T* B, int64_t blockStrid
         for (int tid = 0; tid < BLOCK; ++tid) tile_tables<HostMem, BLOCK>(g, tid, rowOffA, colOffB);
         for (int64_t t = blk; t < g.numTiles && S->errors == 0; t += grid) {
             const TileBase tb = tile_base(g, uint32_t(t));
+            if (g.flatR) {
+                // the row table is the tile's own: a stale entry must not be read
+                clear_written(0, g.runB * int64_t(sizeof(int64_t)));
+                for (int tid = 0; tid < BLOCK; ++tid) tile_rows_flat<HostMem, BLOCK>(g, tb, tid, rowOffA);
+            }
             for (int64_t r0 = 0; r0 < tb.validRows && S->errors == 0; r0 += g.subRows) {
                 clear_written(tableBytes, ldsBytes);
                 for (int tid = 0; tid < BLOCK; ++tid)

@@ -176,6 +176,40 @@ def test_sheared_b_runs():
         assert np.all(got[:off] == 0) and np.all(got[off + n:] == 0)
 
 
+def test_flat_b_runs():
+    """B runs cut in whole lines from the flattened range of two or more B
+    indices (row tables rebuilt per tile): small forced cases with partial
+    last chunks, tensors that start off the vector grid, and the 6-D fp32
+    workload's plan on a smaller grid."""
+    rng = np.random.default_rng(43)
+    flat = 0
+    for size_a, perm in [((24, 6, 16, 20), (3, 2, 0, 1)), ((10, 3, 5, 7), (3, 2, 1, 0)),
+                         ((33, 2, 9, 11), (2, 3, 0, 1)), ((5, 40, 3, 6, 7), (4, 3, 2, 0, 1)),
+                         ((24, 20, 16, 3, 2, 20), (5, 2, 0, 4, 1, 3))]:
+        for knobs in (dict(), dict(run_b=8), dict(run_a=16, run_b=8)):
+            for dtype, (alpha, beta) in (("f32", (1.0, 0.0)), ("f64", (1.5, -0.5)),
+                                         ("f32", (2.0, 0.5))):
+                p = _run_case(size_a, perm, alpha, beta, dtype, rng, flat_runs=1, **knobs)
+                flat += p.info["flat_runs"] > 0
+    assert flat >= 12
+    p = hptt.create_plan((5, 2, 0, 4, 1, 3), (24, 20, 16, 3, 2, 20), 1.5, 0.5, "f32")
+    assert p.info["flat_runs"] == 2, p.describe()
+    for off in (1, 3):
+        n = p.numel
+        A = _rand(rng, n, "f32")
+        B0 = _rand(rng, n, "f32")
+        want = orc.transpose(A, (24, 20, 16, 3, 2, 20), (5, 2, 0, 4, 1, 3), 1.5, 0.5, B0)
+        dA = torch.zeros(n + 8, dtype=torch.float32, device="cuda")
+        dB = torch.zeros(n + 8, dtype=torch.float32, device="cuda")
+        dA[off:off + n] = torch.from_numpy(A).cuda()
+        dB[off:off + n] = torch.from_numpy(B0).cuda()
+        p.exec(dA[off:off + n], dB[off:off + n])
+        torch.cuda.synchronize()
+        got = dB.cpu().numpy()
+        _assert_parity(got[off:off + n], want, "f32", f"offset {off}: {p.describe()}")
+        assert np.all(got[:off] == 0) and np.all(got[off + n:] == 0)
+
+
 def test_shared_runs():
     """Tiles whose A run and B run share indices (a B stride-1 extent of 2, a
     short kept stride-1 index, a small block permuted inside itself), forced,

@@ -108,10 +108,12 @@ EXPECTED = {
                                      run_b=32, tiles=60),
     "transpose2d_8192x8192_f32": dict(kernel="tile", size=(8192, 8192), perm=(1, 0), run_a=128,
                                       run_b=32, tiles=16384, tile_order=2, hints=3),
+    # flat B runs: one line cut from the 20 x 16 = 320 flattened B positions
+    # (10 chunks), A runs of 24 x 4 = 96 elements (3 lines)
     "transpose6d_24x20x16x24x18x20_f32": dict(kernel="tile", size=(24, 20, 16, 24, 18, 20),
-                                              perm=(5, 2, 0, 4, 1, 3), run_a=48, run_b=160,
-                                              dims_a=2, dims_b=2, tiles=8640, hints=1,
-                                              rows_per_pass=160),
+                                              perm=(5, 2, 0, 4, 1, 3), run_a=96, run_b=32,
+                                              dims_a=2, dims_b=2, tiles=21600, hints=3,
+                                              rows_per_pass=32, flat_runs=2),
     "transpose4d_96x96x96x96_keep1_f64": dict(kernel="stream", size=(96, 96, 96, 96),
                                               perm=(0, 3, 2, 1), run_b=96, vec_a=2, vec_b=2),
     # beta != 0: A-run target of 256 bytes, met by 3 x 2 x 16 = 96 elements (384 B)
