@@ -1023,8 +1023,11 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
             const int64_t fA = opt.run_a > 0 ? opt.run_a : 512 / elem;
             const int64_t fB = opt.run_b > 0 ? opt.run_b : kLine / elem;
             bool flat = false;
+            // exact runs take the LDS limit, as the forced stage above does
+            const int64_t fBudget = !opt.exact_runs ? kLdsBudget
+                                    : opt.block == kBigBlock ? kLdsMaxBig : kLdsMax;
             for (int aligned = opt.exact_runs ? 0 : 1; aligned >= 0 && !flat; --aligned) {
-                flat = setup_tile(f, elem, fA, fB, opt, aligned == 1, true, kLdsBudget, minTile,
+                flat = setup_tile(f, elem, fA, fB, opt, aligned == 1, true, fBudget, minTile,
                                   plan->tile, info, false, true) &&
                        (plan->tile.alignedB || opt.flat_runs == 1);
             }
