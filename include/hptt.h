@@ -115,7 +115,11 @@ typedef struct {
                               whole multiples of the inner extents: 0 = where
                               those extents are not whole lines and the usual
                               B run is not or is long, 1 = wherever they
-                              apply, 2 = never */
+                              apply, 2 = never.  STREAM: B (compact) walked as
+                              one flat range of whole vectors, A read element
+                              by element: 0 = where the kept rows would take
+                              narrower vectors, 1 = wherever B is compact,
+                              2 = never */
 } hptt_options_t;
 
 /* What the plan builder decided; for inspection and tests. */
@@ -155,7 +159,8 @@ typedef struct {
     int32_t shared_runs;               /* TILE: fused indices shared by the A run and
                                           the B run (0: disjoint runs) */
     int32_t flat_runs;                 /* TILE: fused B indices the flat B run is cut
-                                          from (0: B runs are not flat) */
+                                          from (0: B runs are not flat); STREAM: 1
+                                          when B is walked flat */
 } hptt_plan_info_t;
 
 /*

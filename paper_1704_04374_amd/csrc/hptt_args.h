@@ -159,7 +159,13 @@ struct TileArgs {
 struct StreamArgs {
     int64_t rowLen;             // extent of the kept stride-1 index
     int64_t numRows;            // numel / rowLen
-    uint32_t numItems[3];       // numRows * W for V = 1, 2, 4
+    uint32_t numItems[3];       // numRows * W for V = 1, 2, 4 (flat: ceil(numel / V))
+    // Flat walk (B compact, numel < 2^32): item i is B's vector i, elements
+    // [i*V, i*V + V) of the flat B range, whatever the row length; its
+    // elements come from at most two rows (rowLen >= V), read from A one by
+    // one.  L divides a flat B offset into (row, column).
+    int32_t flatB;
+    FastDiv L;
     int32_t nO;                 // outer B positions 1..N'-1
     FastDiv W[3];               // vectors per row for V = 1, 2, 4
     FastDiv oExt[kMaxDims];     // extents of B positions 1.. (B order)

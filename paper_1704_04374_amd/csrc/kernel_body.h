@@ -743,6 +743,73 @@ __host__ __device__ inline void stream_items(const StreamArgs& g, uint32_t first
     }
 }
 
+// A offset of row r of the stride-1-kept walk (rows in B order).
+__host__ __device__ inline int64_t stream_row_a(const StreamArgs& g, uint32_t r) {
+    int64_t a = 0;
+    for (int k = 0; k < g.nO; ++k) {
+        const uint32_t q = fast_div(r, g.oExt[k]);
+        a += int64_t(r - q * g.oExt[k].d) * g.oStrideA[k];
+        r = q;
+    }
+    return a;
+}
+
+// Flat walk of kernel S (g.flatB): item i is B's vector i, so every B access
+// is a whole vector even when the row length is not a multiple of the width
+// (rows of 63 fp32 would otherwise move one element per access).  The row
+// split is done once per vector (twice when the vector crosses into the next
+// row); A is read element by element, ordinary loads, since its rows start
+// anywhere.  Same lane map as stream_items.
+template <class Mem, typename T, int V, int MODE, int HINT>
+__host__ __device__ inline void stream_items_flat(const StreamArgs& g, uint32_t first, int tid,
+                                                  const T* A, T* B, T alpha, T beta) {
+    const uint32_t numItems = g.numItems[log2_width(V)];
+    const int64_t numel = g.numRows * g.rowLen;
+    const int rowLen = int(g.L.d);
+    constexpr int NI = items_per_lane(int(sizeof(T)), V);
+    Vec<T, V> x[NI], y[NI];
+    int64_t offB[NI];
+    int n[NI];
+#pragma unroll
+    for (int u = 0; u < NI; ++u) {
+        const uint64_t item = uint64_t(first) + uint64_t(u) * kBlock + uint64_t(tid);
+        n[u] = 0;
+        offB[u] = int64_t(item) * V;
+        if (item < numItems) {
+            n[u] = int(imin(int64_t(V), numel - offB[u]));  // elements of this vector
+            const uint32_t r = fast_div(uint32_t(offB[u]), g.L);
+            const int c0 = int(uint32_t(offB[u]) - r * g.L.d);
+            const int64_t a0 = stream_row_a(g, r);
+            const int64_t a1 = c0 + n[u] > rowLen ? stream_row_a(g, r + 1) - rowLen : a0;
+#pragma unroll
+            for (int e = 0; e < V; ++e)
+                if (e < n[u]) x[u].v[e] = Mem::template ld1<T>(A, (c0 + e < rowLen ? a0 : a1) + c0 + e);
+            if (MODE == kAxpby) {
+                if (n[u] == V) {
+                    y[u] = Mem::template ld<T, V, false>(B, offB[u]);
+                } else {
+                    for (int e = 0; e < V; ++e)
+                        if (e < n[u]) y[u].v[e] = Mem::template ld1<T>(B, offB[u] + e);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < NI; ++u) {
+        if (n[u] == 0) continue;
+        Vec<T, V> z;
+#pragma unroll
+        for (int e = 0; e < V; ++e)
+            z.v[e] = update<MODE>(x[u].v[e], MODE == kAxpby ? y[u].v[e] : T(0), alpha, beta);
+        if (n[u] == V) {
+            Mem::template st<(HINT & kNtStore) != 0, T, V>(B, offB[u], z);
+        } else {
+            for (int e = 0; e < V; ++e)
+                if (e < n[u]) Mem::template st1<(HINT & kNtStore) != 0, T>(B, offB[u] + e, z.v[e]);
+        }
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Identity after fusion: B <- alpha*A + beta*B over a flat range
 // ---------------------------------------------------------------------------

@@ -23,6 +23,12 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(const T* __restrict__ A,
     constexpr uint64_t per = uint64_t(kBlock) * items_per_lane(int(sizeof(T)), V);
     const uint64_t step = uint64_t(gridDim.x) * per;
     const uint64_t items = g.numItems[log2_width(V)];
+    if (g.flatB) {
+        for (uint64_t first = uint64_t(blockIdx.x) * per; first < items; first += step)
+            stream_items_flat<DeviceMem, T, V, MODE, HINT>(g, uint32_t(first), int(threadIdx.x), A,
+                                                           B, alpha, beta);
+        return;
+    }
     for (uint64_t first = uint64_t(blockIdx.x) * per; first < items; first += step)
         stream_items<DeviceMem, T, V, MODE, HINT>(g, uint32_t(first), int(threadIdx.x), A, B, alpha,
                                                   beta);
@@ -89,7 +95,9 @@ const void* generic_fn(bool big) {
 template <typename T, int MODE, int HINT>
 const void* select(const hptt_plan_s* p, int va, int vb) {
     switch (p->info.kernel) {
-        case HPTT_KERNEL_STREAM: return stream_fn<T, MODE, HINT>(va < vb ? va : vb);
+        // the flat walk reads A element by element: only B's width counts
+        case HPTT_KERNEL_STREAM:
+            return stream_fn<T, MODE, HINT>(p->stream.flatB || va >= vb ? vb : va);
         case HPTT_KERNEL_AXPBY: return axpby_fn<T, MODE, HINT>(va < vb ? va : vb);
         case HPTT_KERNEL_GENERIC:
             return generic_fn<T, MODE, HINT>(p->generic.numel >= (int64_t(1) << 32));

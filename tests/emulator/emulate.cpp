@@ -261,8 +261,13 @@ void emu_stream(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     for (uint64_t blk = 0; blk < grid && S->errors == 0; blk += uint64_t(blockStride))
         for (uint64_t first = blk * per;
              first < g.numItems[log2_width(V)] && S->errors == 0; first += step)
-            for (int tid = 0; tid < kBlock; ++tid)
-                stream_items<HostMem, T, V, MODE, NT>(g, uint32_t(first), tid, A, B, alpha, beta);
+            for (int tid = 0; tid < kBlock; ++tid) {
+                if (g.flatB)
+                    stream_items_flat<HostMem, T, V, MODE, NT>(g, uint32_t(first), tid, A, B, alpha,
+                                                               beta);
+                else
+                    stream_items<HostMem, T, V, MODE, NT>(g, uint32_t(first), tid, A, B, alpha, beta);
+            }
 }
 
 // Mirrors axpby_kernel and generic_kernel in kernels.hip.
@@ -296,7 +301,11 @@ template <typename T, int MODE, int NT, int VA, int VB>
 void run_widths(const hptt_plan_s* p, const T* A, T* B, int64_t bs) {
     switch (p->info.kernel) {
         case HPTT_KERNEL_TILE: emu_tile<T, VA, VB, MODE, NT>(p, A, B, bs); break;
-        case HPTT_KERNEL_STREAM: emu_stream<T, (VA < VB ? VA : VB), MODE, NT>(p, A, B, bs); break;
+        case HPTT_KERNEL_STREAM:
+            // the flat walk takes B's width alone, as hptt_exec does
+            if (p->stream.flatB) emu_stream<T, VB, MODE, NT>(p, A, B, bs);
+            else emu_stream<T, (VA < VB ? VA : VB), MODE, NT>(p, A, B, bs);
+            break;
         case HPTT_KERNEL_AXPBY: emu_axpby<T, (VA < VB ? VA : VB), MODE, NT>(p, A, B, bs); break;
         case HPTT_KERNEL_GENERIC: emu_generic<T, MODE, NT>(p, A, B, bs); break;
         default: break;

@@ -465,3 +465,25 @@ def test_flat_b_runs_full_size_geometry():
     err, msg, cnt = emu.run(p, counts=True)
     assert err == 0, msg
     assert cnt.min() == 1 and cnt.max() == 1
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f64"])
+def test_flat_stream_walk_matches_oracle(dtype):
+    """Kernel S walking B flat (rows whose length is not a multiple of the
+    vector width, or any compact B when forced): every element written once
+    and bit-exact, vectors that cross into the next row, a partial last
+    vector, narrower widths for misaligned B pointers."""
+    rng = np.random.default_rng(1705)
+    seen = 0
+    for size_a, perm in [((63, 5, 7), (0, 2, 1)), ((17, 3, 4, 5), (0, 3, 1, 2)),
+                         ((75, 10, 11), (0, 2, 1)), ((33, 7, 3, 2), (0, 2, 3, 1)),
+                         ((64, 5, 6), (0, 2, 1)), ((21, 9), (0, 1)), ((19, 4, 3), (0, 2, 1))]:
+        for knobs in (dict(), dict(flat_runs=1)):
+            for alpha, beta in ((1.0, 0.0), (1.5, 0.0), (-0.3, 1.25)):
+                p = emu.plan(perm, size_a, alpha, beta, dtype, **knobs)
+                if p.info["kernel"] != "stream" or not p.info["flat_runs"]:
+                    continue
+                seen += 1
+                for vb in (0, 2, 1):
+                    _check(p, size_a, perm, alpha, beta, dtype, rng, vb=vb)
+    assert seen >= 12

@@ -260,6 +260,39 @@ def test_stream_kernel_variants():
             _run_case(size_a, perm, 1.0, 0.0, "f32", rng, kernel="stream", **knobs)
 
 
+def test_flat_stream_walk():
+    """Kernel S walking B flat (odd fp32 rows by default, any compact B
+    when forced): vectors that cross rows, a partial last vector, capped
+    grids, and B pointers 1 to 3 elements off the 16-byte grid."""
+    rng = np.random.default_rng(55)
+    flat = 0
+    for size_a, perm in [((63, 5, 7), (0, 2, 1)), ((17, 3, 4, 5), (0, 3, 1, 2)),
+                         ((75, 10, 11), (0, 2, 1)), ((19, 4, 3), (0, 2, 1))]:
+        for knobs in (dict(), dict(flat_runs=1), dict(max_blocks=3)):
+            for dtype, (alpha, beta) in (("f32", (1.0, 0.0)), ("f32", (2.0, 0.5)),
+                                         ("f64", (1.5, -0.5))):
+                p = _run_case(size_a, perm, alpha, beta, dtype, rng, **knobs)
+                flat += p.info["kernel"] == "stream" and p.info["flat_runs"] == 1
+    assert flat >= 20
+    size_a, perm = (63, 5, 7), (0, 2, 1)
+    p = hptt.create_plan(perm, size_a, 1.5, 0.5, "f32")
+    assert p.info["flat_runs"] == 1, p.describe()
+    for off in (1, 2, 3):
+        n = p.numel
+        A = _rand(rng, n, "f32")
+        B0 = _rand(rng, n, "f32")
+        want = orc.transpose(A, size_a, perm, 1.5, 0.5, B0)
+        dA = torch.zeros(n + 8, dtype=torch.float32, device="cuda")
+        dB = torch.zeros(n + 8, dtype=torch.float32, device="cuda")
+        dA[off:off + n] = torch.from_numpy(A).cuda()
+        dB[4 - off:4 - off + n] = torch.from_numpy(B0).cuda()
+        p.exec(dA[off:off + n], dB[4 - off:4 - off + n])
+        torch.cuda.synchronize()
+        got = dB.cpu().numpy()
+        _assert_parity(got[4 - off:4 - off + n], want, "f32", f"offset {off}: {p.describe()}")
+        assert np.all(got[:4 - off] == 0) and np.all(got[4 - off + n:] == 0)
+
+
 def test_misaligned_pointers_fall_back():
     """Tensors starting one element past a 16-byte boundary take narrower
     vector accesses and stay correct."""

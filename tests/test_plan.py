@@ -344,3 +344,22 @@ def test_shared_runs_where_disjoint_runs_collapse():
     # short A runs whose rows follow each other in A stay disjoint
     assert hptt.create_plan((1, 0), (14, 3582084), 1.0, 1.0, "f32").info["shared_runs"] == 0
     assert hptt.create_plan(perm, size, 1.0, 1.0, "f32", shared_runs=2).info["shared_runs"] == 0
+
+
+def test_flat_stream_walk_rule():
+    """Kernel S walks B flat where the kept rows would move one 4-byte
+    element per access (odd fp32 rows), not for fp64 rows or rows that take
+    whole vectors, not where B is a sub-tensor with gaps, and not when
+    switched off."""
+    odd = hptt.create_plan((0, 3, 2, 1), (75, 100, 11, 60), 1.0, 0.0, "f32")
+    assert odd.info["kernel"] == "stream" and odd.info["flat_runs"] == 1
+    assert odd.info["vec_b"] == 4 and odd.info["tiles"] == -(-odd.numel // 4)
+    assert "flat=1" in odd.describe()
+    assert hptt.create_plan((0, 3, 2, 1), (75, 100, 11, 60), 1.0, 0.0, "f32",
+                            flat_runs=2).info["flat_runs"] == 0
+    assert hptt.create_plan((0, 3, 2, 1), (95, 96, 9, 9), 2.0, 0.5, "f64").info["flat_runs"] == 0
+    assert hptt.create_plan((0, 3, 2, 1), (96, 96, 9, 9), 1.0, 0.0, "f32").info["flat_runs"] == 0
+    forced = hptt.create_plan((0, 3, 2, 1), (96, 96, 9, 9), 1.0, 0.0, "f32", flat_runs=1)
+    assert forced.info["flat_runs"] == 1
+    gaps = hptt.create_plan((0, 2, 1), (63, 5, 7), 1.0, 0.0, "f32", outer_size_b=(64, 7, 5))
+    assert gaps.info["kernel"] == "stream" and gaps.info["flat_runs"] == 0
