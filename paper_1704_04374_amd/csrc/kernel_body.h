@@ -234,6 +234,13 @@ constexpr int tile_batch(int block) { return block >= 1024 ? 4 : kBatch; }
 // its B vectors double the registers a batch holds.
 constexpr int kAxpbyStoreBatch = 2;
 
+// Batch of the specialised load phase: 4 in variant kFast when B is read as
+// well, so that it fits 8 waves per SIMD (the attribute in tile_kernel.h)
+// without spilling vector registers; tile_batch otherwise.
+constexpr int tile_load_batch(int mode, int var, int block) {
+    return mode == kAxpby && var == kFast && block < 1024 ? 4 : tile_batch(block);
+}
+
 // Specialised load phase (variant kFast, or kShifted with SHIFT): nZ = 1 and
 // offsets inside a tile fit 32 bits, so the per-vector
 // arithmetic is 32-bit around one 64-bit tile base pointer.  Without SHIFT
@@ -244,11 +251,10 @@ constexpr int kAxpbyStoreBatch = 2;
 // batch's start instead of keeping it (only the shifted column is kept), so
 // little besides the data stays live between the two (fewer registers, more
 // resident waves).  Same thread-to-vector map as tile_load.
-template <class Mem, typename T, int VA, int HINT, int BLOCK, bool SHIFT>
+template <class Mem, typename T, int VA, int HINT, int BLOCK, bool SHIFT, int NB>
 __host__ __device__ inline void tile_load_fast(const TileArgs& g, const TileBase& tb, int r0,
                                                int tid, const T* A, T* lds,
                                                const int64_t* rowOffA) {
-    constexpr int NB = tile_batch(BLOCK);
     const bool shift = SHIFT && (!g.runsOnGridA || g.misA != 0);
     const int W = (int(g.runA) + (shift ? VA - 1 : 0) + VA - 1) / VA;  // vectors per row
     const int rows = int(imin(int64_t(g.subRows), tb.validRows - r0));
@@ -499,12 +505,13 @@ __host__ __device__ inline void tile_store_shared(const TileArgs& g, const TileB
 // the A vector grid: a run that starts off it is covered by one more vector,
 // its first and last ones partial (element loads).  Variants kFast and
 // kShifted (see tile_variant) take tile_load_fast instead.
-template <class Mem, typename T, int VA, int HINT, int VAR, int BLOCK = kBlock>
+template <class Mem, typename T, int VA, int HINT, int VAR, int BLOCK = kBlock,
+          int LB = tile_batch(BLOCK)>
 __host__ __device__ inline void tile_load(const TileArgs& g, const TileBase& tb, int64_t r0,
                                           int tid, const T* A, T* lds, const int64_t* rowOffA) {
     static_assert(VAR == kFast || BLOCK == kBlock, "only the kFast variant runs kBigBlock");
     if constexpr (VAR != kGeneral) {
-        tile_load_fast<Mem, T, VA, HINT, BLOCK, VAR == kShifted || VAR == kShared>(
+        tile_load_fast<Mem, T, VA, HINT, BLOCK, VAR == kShifted || VAR == kShared, LB>(
             g, tb, int(r0), tid, A, lds, rowOffA);
         return;
     }

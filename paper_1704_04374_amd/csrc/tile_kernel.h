@@ -22,10 +22,21 @@ namespace {
 // when the grid is capped): build the offset tables once, then for each pass
 // load A runs into LDS, barrier, and store B runs.  A 1024-thread workgroup
 // asks for 8 waves per SIMD, i.e. two workgroups per CU, which keeps its
-// registers at 64 VGPRs per lane.
+// registers at 64 VGPRs per lane.  So does variant kFast when it reads B
+// (batches of 4 loads and 2 stores): it would otherwise hold 7, limited by
+// its scalar registers (MI355X, the 5-D fp32 beta = 1 workload 5.41 ->
+// 5.57-5.64 TB/s; with beta = 0 the same cap lost 3-15 %, and on the
+// shifted and shared-run variants it lost 3 % of the beta = 1 sweep).
+template <int MODE, int VAR, int BLOCK>
+constexpr int tile_waves_per_eu() {
+    return BLOCK >= 1024 || (MODE == kAxpby && VAR == kFast) ? 8 : 1;
+}
+
 template <typename T, int VA, int VB, int MODE, int HINT, int VAR, int BLOCK>
-__global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(BLOCK >= 1024 ? 8 : 1)))
+__global__ __launch_bounds__(BLOCK)
+__attribute__((amdgpu_waves_per_eu(tile_waves_per_eu<MODE, VAR, BLOCK>())))
 void tile_kernel(const T* __restrict__ A, T* __restrict__ B, const TileArgs g, T alpha, T beta) {
+    constexpr int LB = tile_load_batch(MODE, VAR, BLOCK);
     extern __shared__ int64_t smem[];
     if constexpr (VAR == kShared) {
         // runs that share indices: one pass per tile, the store phase
@@ -43,7 +54,7 @@ void tile_kernel(const T* __restrict__ A, T* __restrict__ B, const TileArgs g, T
             const TileBase tb = tile_base<true>(g, t);
             if (!first) __syncthreads();  // the previous tile's LDS reads are done
             first = false;
-            tile_load<DeviceMem, T, VA, HINT, VAR, BLOCK>(g, tb, 0, tid, A, lds, rowOffA);
+            tile_load<DeviceMem, T, VA, HINT, VAR, BLOCK, LB>(g, tb, 0, tid, A, lds, rowOffA);
             __syncthreads();
             tile_store_shared<DeviceMem, T, VB, MODE, HINT, BLOCK>(g, tb, tid, B, lds, colOffB,
                                                                     ldsRow, ldsCol, alpha, beta);
@@ -69,7 +80,7 @@ void tile_kernel(const T* __restrict__ A, T* __restrict__ B, const TileArgs g, T
         for (int64_t r0 = 0; r0 < tb.validRows; r0 += g.subRows) {
             if (!first) __syncthreads();  // the previous pass's LDS reads are done
             first = false;
-            tile_load<DeviceMem, T, VA, HINT, VAR, BLOCK>(g, tb, r0, tid, A, lds, rowOffA);
+            tile_load<DeviceMem, T, VA, HINT, VAR, BLOCK, LB>(g, tb, r0, tid, A, lds, rowOffA);
             __syncthreads();
             tile_store<DeviceMem, T, VB, MODE, HINT, VAR, BLOCK>(g, tb, r0, tid, B, lds, colOffB,
                                                                  alpha, beta);

@@ -177,7 +177,8 @@ void emu_tile_variant(const hptt_plan_s* p, const T* A, T* B, int64_t blockStrid
             for (int64_t r0 = 0; r0 < tb.validRows && S->errors == 0; r0 += g.subRows) {
                 clear_written(tableBytes, ldsBytes);
                 for (int tid = 0; tid < BLOCK; ++tid)
-                    tile_load<HostMem, T, VA, NT, VAR, BLOCK>(g, tb, r0, tid, A, lds, rowOffA);
+                    tile_load<HostMem, T, VA, NT, VAR, BLOCK, tile_load_batch(MODE, VAR, BLOCK)>(
+                        g, tb, r0, tid, A, lds, rowOffA);
                 for (int tid = 0; tid < BLOCK; ++tid)
                     tile_store<HostMem, T, VB, MODE, NT, VAR, BLOCK>(g, tb, r0, tid, B, lds,
                                                                      colOffB, alpha, beta);
@@ -218,7 +219,8 @@ void emu_tile_shared(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride
             const TileBase tb = tile_base<true>(g, uint32_t(t));
             clear_written(tableBytes, ldsBytes);
             for (int tid = 0; tid < kBlock; ++tid)
-                tile_load<HostMem, T, VA, NT, kShared, kBlock>(g, tb, 0, tid, A, lds, rowOffA);
+                tile_load<HostMem, T, VA, NT, kShared, kBlock, tile_load_batch(MODE, kShared, kBlock)>(
+                    g, tb, 0, tid, A, lds, rowOffA);
             for (int tid = 0; tid < kBlock; ++tid)
                 tile_store_shared<HostMem, T, VB, MODE, NT, kBlock>(g, tb, tid, B, lds, colOffB,
                                                                      ldsRow, ldsCol, alpha, beta);
