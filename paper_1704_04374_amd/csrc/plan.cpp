@@ -254,6 +254,8 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
         // flat B runs: whole lines cut from positions 0..k flattened (two
         // or more of them, longer than one run)
         if (k == 0 || shear) return false;
+        // the kernel splits a flattened position as a 32-bit number
+        if (flatLen >= (int64_t(1) << 32)) return false;
         rChunk = tB >= lineB ? tB / lineB * lineB : lineB;
         if (rChunk >= flatLen) return false;
     } else if (shear) {

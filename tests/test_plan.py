@@ -363,3 +363,24 @@ def test_flat_stream_walk_rule():
     assert forced.info["flat_runs"] == 1
     gaps = hptt.create_plan((0, 2, 1), (63, 5, 7), 1.0, 0.0, "f32", outer_size_b=(64, 7, 5))
     assert gaps.info["kernel"] == "stream" and gaps.info["flat_runs"] == 0
+
+
+def test_flat_b_runs_rule():
+    """Flat B runs where the inner B extents are not whole lines (the 6-D
+    workload), not where they are, not when switched off, and never when the
+    flattened range exceeds 32-bit positions."""
+    p = hptt.create_plan((5, 2, 0, 4, 1, 3), (24, 20, 16, 24, 18, 20), 1.5, 0.0, "f32")
+    assert p.info["flat_runs"] == 2 and p.info["run_b"] == 32
+    assert "flat=2" in p.describe()
+    off = hptt.create_plan((5, 2, 0, 4, 1, 3), (24, 20, 16, 24, 18, 20), 1.5, 0.0, "f32",
+                           flat_runs=2)
+    assert off.info["flat_runs"] == 0 and off.info["run_b"] == 160
+    # inner B extent of 32 fp32 = one line: the usual runs already are lines
+    whole = hptt.create_plan((5, 2, 0, 4, 1, 3), (24, 20, 16, 24, 18, 32), 1.5, 0.0, "f32")
+    assert whole.info["flat_runs"] == 0
+    # 20 x 300,000,000 flattened positions: beyond 32 bits, no flat runs even when asked
+    big = hptt.create_plan((1, 3, 0, 2), (24, 20, 7, 300_000_000), 1.0, 0.0, "f32",
+                           flat_runs=1)
+    assert big.info["flat_runs"] == 0
+    small = hptt.create_plan((1, 3, 0, 2), (24, 20, 7, 3000), 1.0, 0.0, "f32", flat_runs=1)
+    assert small.info["flat_runs"] == 2
