@@ -125,6 +125,12 @@ int autotune_candidates(const int32_t* perm, int32_t N, const int64_t* sizeA,
             memset(&v, 0, sizeof(v));
             v.shared_runs = 1;
             cand.push_back(v);
+            // B walked flat and by rows, whichever the quick path took
+            for (int32_t fr = 1; fr <= 2; ++fr) {
+                memset(&v, 0, sizeof(v));
+                v.flat_runs = fr;
+                cand.push_back(v);
+            }
         }
         for (int h = 1; h < 5; ++h) {
             hptt_options_t v;

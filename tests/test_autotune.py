@@ -25,6 +25,7 @@ SMALL = [
     ((7, 9, 6, 11, 5, 8), (5, 2, 0, 4, 1, 3), 1.5, 0.0, "f32"),
     ((3, 2, 40, 33, 17), (4, 2, 0, 3, 1), 1.0, 1.0, "f32"),
     ((24, 13, 9, 10), (0, 3, 2, 1), 2.0, 0.5, "f64"),
+    ((63, 13, 9), (0, 2, 1), 1.0, 1.0, "f32"),
     ((4100,), (0,), 2.0, 0.5, "f32"),
 ]
 
