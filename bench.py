@@ -12,8 +12,9 @@ Bandwidth follows Eq. (2) of the paper: lambda * S bytes per transposition
 (S = bytes of one tensor, lambda = 2 when beta = 0, 3 otherwise), reported in
 GB/s (1e9 B/s).  Context printed on the same line:
   - roofline: the dominant kernel's achieved GB/s over MI355X's 8 TB/s HBM
-    peak, from HIP events around every timed launch, plus the HBM bytes
-    rocprofv3 counted for it when a matching counter summary is committed;
+    peak, from one HIP event pair around the timed launches (on the launch
+    stream), plus the HBM bytes rocprofv3 counted for it when a matching
+    counter summary is committed;
   - yardsticks: a same-run 16-byte-per-lane copy kernel (2S) and, for
     beta != 0, an axpby kernel (3S) -- the SAXPY yardstick of Table 2 --
     and hipMemcpyAsync device-to-device;
