@@ -13,7 +13,7 @@
  * GPU library: it is a plain, slow, obviously correct CPU definition that the
  * GPU path is compared against.
  *
- * Readings taken where the paper is silent (all restated in the design notes):
+ * Readings taken where the paper is silent:
  *  - perm is 0-based (Fig. 3b passes a zero-based vector) and perm[k] names
  *    the A index that sits at position k of B (Table 1 and the text below it:
  *    the column "6,1,5,4,3,2" is B_{i6 i1 i5 i4 i3 i2}).  Hence
