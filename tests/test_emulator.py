@@ -477,7 +477,8 @@ def test_flat_stream_walk_matches_oracle(dtype):
     seen = 0
     for size_a, perm in [((63, 5, 7), (0, 2, 1)), ((17, 3, 4, 5), (0, 3, 1, 2)),
                          ((75, 10, 11), (0, 2, 1)), ((33, 7, 3, 2), (0, 2, 3, 1)),
-                         ((64, 5, 6), (0, 2, 1)), ((21, 9), (0, 1)), ((19, 4, 3), (0, 2, 1))]:
+                         ((64, 5, 6), (0, 2, 1)), ((21, 9), (0, 1)), ((19, 4, 3), (0, 2, 1)),
+                         ((42, 5, 3, 7), (0, 3, 1, 2))]:
         for knobs in (dict(), dict(flat_runs=1)):
             for alpha, beta in ((1.0, 0.0), (1.5, 0.0), (-0.3, 1.25)):
                 p = emu.plan(perm, size_a, alpha, beta, dtype, **knobs)

@@ -267,7 +267,8 @@ def test_flat_stream_walk():
     rng = np.random.default_rng(55)
     flat = 0
     for size_a, perm in [((63, 5, 7), (0, 2, 1)), ((17, 3, 4, 5), (0, 3, 1, 2)),
-                         ((75, 10, 11), (0, 2, 1)), ((19, 4, 3), (0, 2, 1))]:
+                         ((75, 10, 11), (0, 2, 1)), ((19, 4, 3), (0, 2, 1)),
+                         ((42, 5, 3, 7), (0, 3, 1, 2))]:
         for knobs in (dict(), dict(flat_runs=1), dict(max_blocks=3)):
             for dtype, (alpha, beta) in (("f32", (1.0, 0.0)), ("f32", (2.0, 0.5)),
                                          ("f64", (1.5, -0.5))):

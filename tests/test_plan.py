@@ -359,6 +359,9 @@ def test_flat_stream_walk_rule():
                             flat_runs=2).info["flat_runs"] == 0
     assert hptt.create_plan((0, 3, 2, 1), (95, 96, 9, 9), 2.0, 0.5, "f64").info["flat_runs"] == 0
     assert hptt.create_plan((0, 3, 2, 1), (96, 96, 9, 9), 1.0, 0.0, "f32").info["flat_runs"] == 0
+    # two fp32 elements per access: flat only when B is read as well
+    assert hptt.create_plan((0, 3, 2, 1), (66, 10, 9, 9), 1.0, 0.0, "f32").info["flat_runs"] == 0
+    assert hptt.create_plan((0, 3, 2, 1), (66, 10, 9, 9), 1.0, 1.0, "f32").info["flat_runs"] == 1
     forced = hptt.create_plan((0, 3, 2, 1), (96, 96, 9, 9), 1.0, 0.0, "f32", flat_runs=1)
     assert forced.info["flat_runs"] == 1
     gaps = hptt.create_plan((0, 2, 1), (63, 5, 7), 1.0, 0.0, "f32", outer_size_b=(64, 7, 5))
