@@ -868,7 +868,30 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
         (opt.kernel == HPTT_KERNEL_TILE ||
          (opt.kernel == HPTT_KERNEL_AUTO && (k == HPTT_KERNEL_GENERIC || opt.shared_runs == 1)))) {
         double sc = 0;
-        if (choose_shared(f, elem, opt, plan->tile, info, sc)) {
+        // A short kept index: A runs of 256 bytes and B runs of 512, tiles in
+        // grid-digit order, unless the caller chose them (MI355X, four fp32
+        // cases with kept extents of 2 and 3: +3 to +11 % with beta = 0, +20
+        // to +23 % on three of them with beta = 1, -4 % on the fourth);
+        // the usual search where that tile does not fit or holds less than
+        // 8 KiB (a kept extent of 4 whose next A index is short gave 1.8 KiB
+        // tiles at a third of the usual search's speed).
+        hptt_options_t kopt = opt;
+        bool keptTile = false;
+        if (opt.run_a == 0 && opt.run_b == 0) {
+            kopt.run_a = int32_t(256 / elem);
+            kopt.run_b = int32_t(512 / elem);
+            if (opt.tile_order == 0) kopt.tile_order = 1;
+            TileArgs t;
+            hptt_plan_info_t in = info;
+            double ksc = 0;
+            keptTile = choose_shared(f, elem, kopt, t, in, ksc) &&
+                       t.runA * int64_t(t.subRows) * elem >= 8192;
+            if (keptTile) {
+                plan->tile = t;
+                info = in;
+            }
+        }
+        if (keptTile || choose_shared(f, elem, opt, plan->tile, info, sc)) {
             k = HPTT_KERNEL_TILE;
             sharedTile = true;
         } else if (k == HPTT_KERNEL_TILE) {
