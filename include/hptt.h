@@ -117,9 +117,10 @@ typedef struct {
                               B run is not or is long, 1 = wherever they
                               apply, 2 = never.  STREAM: B (compact) walked as
                               one flat range of whole vectors, A read element
-                              by element: 0 = where the kept rows would take
-                              narrower vectors, 1 = wherever B is compact,
-                              2 = never */
+                              by element: 0 = where the row walk would move
+                              one element per access (odd row lengths), or two
+                              fp32 elements when beta != 0, 1 = wherever B is
+                              compact, 2 = never */
 } hptt_options_t;
 
 /* What the plan builder decided; for inspection and tests. */
