@@ -17,7 +17,8 @@ import torch
 
 from oracle import oracle as orc
 from paper_1704_04374_amd import hptt
-from paper_1704_04374_amd.workloads import WORKLOADS, NUMPY_DTYPE, inputs, random_problem
+from paper_1704_04374_amd.workloads import (NUMPY_DTYPE, SUBTENSOR_WORKLOADS, WORKLOADS, inputs,
+                                            random_problem, uniform)
 
 pytestmark = pytest.mark.gpu
 
@@ -468,22 +469,31 @@ def test_sub_tensors_random(knobs):
         assert {"tile", "generic"} <= kinds
 
 
-def test_large_sub_tensor_compact():
-    """A 4096 x 8192 block of an 8192 x 8192 matrix, transposed and compacted
-    (the shape of the sub-tensor benchmark), against one-by-one samples."""
-    outer_a, size_a, perm = (8192, 8192), (4096, 8192), (1, 0)
-    start_a = (2048, 0)
-    g = torch.Generator(device="cuda").manual_seed(9)
-    PA = torch.rand(8192 * 8192, device="cuda", generator=g)
-    B = torch.full((4096 * 8192,), float("nan"), device="cuda")
-    oa = _fortran_offset(start_a, outer_a)
-    p = hptt.create_plan(perm, size_a, outer_size_a=outer_a)
-    p.exec(PA[oa:], B)
+@pytest.mark.parametrize("w", SUBTENSOR_WORKLOADS, ids=lambda w: w.name)
+def test_sub_tensor_workload_full_size(w):
+    """The transpose-and-compact and transpose-and-scatter workloads the
+    benchmark times (halves of an 8192 x 8192 matrix, Fig. 3), with the plan
+    the benchmark builds, compared whole against the oracle: every element of
+    the enclosing B, including those outside the sub-tensor, which must keep
+    their prior (NaN) bits."""
+    _say(w.describe())
+    PA = uniform(w.parent_numel_a, w.dtype, w.seed_a).numpy()
+    PB = np.full(w.parent_numel_b, np.nan, dtype=NUMPY_DTYPE[w.dtype])
+    oa, ob = w.offset_a, w.offset_b
+    outer_a = w.outer_a or w.size_a
+    outer_b = w.outer_b or w.size_b
+    p = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype, outer_size_a=w.outer_a,
+                         outer_size_b=w.outer_b)
+    want = np.concatenate([PB[:ob], orc.transpose_outer(PA[oa:], w.size_a, w.perm, outer_a,
+                                                        outer_b, w.alpha, w.beta, PB[ob:])])
+    dA = torch.from_numpy(PA).cuda()
+    dB = torch.from_numpy(PB).cuda()
+    p.exec(dA[oa:], dB[ob:])
     torch.cuda.synchronize()
-    got = B.cpu().numpy()
-    assert not np.isnan(got).any()
-    hA = PA.cpu().numpy()
-    rng = np.random.default_rng(1)
-    j = rng.integers(0, 8192, 4000)      # B index 0 (A's index 1)
-    i = rng.integers(0, 4096, 4000)      # B index 1 (A's index 0)
-    assert np.array_equal(got[j + 8192 * i], hA[(start_a[0] + i) + 8192 * j])
+    got = dB.cpu().numpy()
+    assert got.tobytes() == want.tobytes(), p.describe()
+    # the region outside the sub-tensor is untouched, and nothing inside is NaN
+    inside = np.zeros(w.parent_numel_b, dtype=bool)
+    inside[ob:] = ~np.isnan(want[ob:])
+    assert np.isnan(got[~inside]).all() and not np.isnan(got[inside]).any()
+    assert inside.sum() == w.numel

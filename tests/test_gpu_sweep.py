@@ -1,8 +1,9 @@
 """The 57-case sweep (Section 4's benchmark shape) on an MI355X at full size,
-in the launch configuration the benchmark times: beta = 1 results sampled
-against the oracle element by element, and the alpha = 1, beta = 0 copy
-checked whole by a property that holds at any size -- B is a permutation of
-A, so both sort to the same bits."""
+in the launch configuration the benchmark times, each case compared whole,
+element by element and bit for bit, with the CPU oracle: once with beta = 1
+(the paper's default reporting mode, Eq. 2 with lambda = 3) on a seeded prior
+B, and once with alpha = 1, beta = 0 on a NaN-filled B (every element must be
+written, none read)."""
 from __future__ import annotations
 
 import numpy as np
@@ -18,33 +19,32 @@ pytestmark = pytest.mark.gpu
 CASES = sweep57()
 
 
-def test_sweep_full_size():
-    seen = set()
-    shared = 0
-    for w in CASES:
-        print(f"[sweep] {w.describe()}", flush=True)
-        A, B0 = inputs(w)
-        dA, dB = A.cuda(), B0.cuda()
-        p = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype)
-        seen.add(p.info["kernel"])
-        shared += p.info["shared_runs"] > 0
-        p.exec(dA, dB)
-        torch.cuda.synchronize()
-        rng = np.random.default_rng(w.seed_a)
-        offs = np.concatenate([[0, w.numel - 1], rng.integers(0, w.numel, 4000)])
-        got = dB[torch.from_numpy(offs).cuda()].cpu().numpy()
-        want = orc.sample(A.numpy(), w.size_a, w.perm, w.alpha, w.beta, B0.numpy(), offs)
-        assert np.array_equal(got, want), p.describe()
-        # alpha = 1, beta = 0: a pure permutation of A's bits, whole
-        c = hptt.create_plan(w.perm, w.size_a, 1.0, 0.0, w.dtype)
-        dB.fill_(float("nan"))
-        c.exec(dA, dB)
-        torch.cuda.synchronize()
-        ia, ib = dA.view(torch.int32), dB.view(torch.int32)
-        assert torch.equal(torch.sort(ia).values, torch.sort(ib).values), c.describe()
-        got = dB[torch.from_numpy(offs).cuda()].cpu().numpy()
-        want = orc.sample(A.numpy(), w.size_a, w.perm, 1.0, 0.0, None, offs)
-        assert np.array_equal(got, want), c.describe()
-        del dA, dB
-    assert {"tile", "stream"} <= seen
-    assert shared >= 10  # tiles whose runs share indices
+def _check_whole(got: np.ndarray, want: np.ndarray, what: str):
+    if got.view(np.uint32).tobytes() == want.view(np.uint32).tobytes():
+        return
+    bad = np.flatnonzero(got.view(np.uint32) != want.view(np.uint32))
+    raise AssertionError(f"{what}: {bad.size} of {got.size} elements differ, first at B offset "
+                         f"{bad[0]} (got {got[bad[0]]!r}, want {want[bad[0]]!r})")
+
+
+@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+def test_sweep_case_whole(w):
+    print(f"[sweep] {w.describe()}", flush=True)
+    A, B0 = inputs(w)
+    a, b0 = A.numpy(), B0.numpy()
+    dA = A.cuda()
+    # beta = 1 on the seeded prior B
+    p = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype)
+    dB = B0.cuda()
+    p.exec(dA, dB)
+    torch.cuda.synchronize()
+    _check_whole(dB.cpu().numpy(), orc.transpose(a, w.size_a, w.perm, w.alpha, w.beta, b0),
+                 p.describe())
+    # alpha = 1, beta = 0: B is written without being read
+    c = hptt.create_plan(w.perm, w.size_a, 1.0, 0.0, w.dtype)
+    dB.fill_(float("nan"))
+    c.exec(dA, dB)
+    torch.cuda.synchronize()
+    _check_whole(dB.cpu().numpy(), orc.transpose(a, w.size_a, w.perm, 1.0, 0.0, None),
+                 c.describe())
+

@@ -52,3 +52,14 @@ def test_sweep_plans_dry_run(dims):
             knobs = {k: v for k, v in c.items() if v}
             p = emu.plan(w.perm, w.size_a, 0.0, 1.0, w.dtype, **knobs)
             _dry(p, max(1, p.info["grid"] // 31))
+
+
+def test_sweep_covers_kernel_classes():
+    """The sweep reaches both kernel classes and the shared-run tiles."""
+    seen, shared = set(), 0
+    for w in CASES:
+        p = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype)
+        seen.add(p.info["kernel"])
+        shared += p.info["shared_runs"] > 0
+    assert {"tile", "stream"} <= seen
+    assert shared >= 10
