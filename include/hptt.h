@@ -50,7 +50,8 @@ typedef enum {
 typedef enum {
     HPTT_SUCCESS = 0,
     HPTT_ERROR_INVALID_ARGUMENT = 1, /* bad perm, rank, extent, null pointer, misaligned element */
-    HPTT_ERROR_UNSUPPORTED = 2,      /* a forced option the plan cannot honour */
+    HPTT_ERROR_UNSUPPORTED = 2,      /* a forced option the plan cannot honour, or a problem
+                                        beyond an entry point's fixed limit */
     HPTT_ERROR_OVERLAP = 3,          /* A and B share memory */
     HPTT_ERROR_OUT_OF_MEMORY = 4,    /* host allocation of the plan failed */
     HPTT_ERROR_HIP = 5               /* the kernel launch failed */
@@ -218,10 +219,14 @@ typedef struct {
     int32_t timed;           /* plans timed before the timeout */
     int32_t from_cache;      /* 1 when the problem was tuned earlier in this process */
     int32_t flushed;         /* 1 when launches were timed cold, with their write-backs */
-    int32_t own_mode;        /* 1 when beta = 0 plans were timed writing a scratch tensor */
-    float default_ms;        /* the quick path's plan, median of three launches */
-    float best_ms;           /* the chosen plan, median of three launches */
+    int32_t own_mode;        /* 1 when plans were timed writing a scratch tensor in the
+                                caller's own update mode */
+    float default_ms;        /* the quick path's plan, median of three cold launches */
+    float best_ms;           /* the chosen plan, median of three cold launches */
     hptt_options_t options;  /* the chosen plan's knobs (all zero: the quick path's plan) */
+    int32_t finalists;       /* candidates screened at least 1 % faster than the quick
+                                plan and timed again against it (at most 3) */
+    int32_t confirmed;       /* finalists that won again, cold and back to back */
 } hptt_autotune_report_t;
 
 /*
@@ -235,15 +240,21 @@ typedef struct {
  * read has evicted the tensors from the caches; each timed span also holds a
  * second such read, which writes back what the launch left dirty in the
  * caches (its clean time is subtracted), so that plans whose stores stay in
- * the caches are charged for them as in back-to-back use.  The caller's data are not
- * changed: with beta != 0 timing runs, like the paper's, with alpha = 0 and
- * beta = 1, so B is rewritten with its own value and A is read and multiplied
- * by zero (A must then hold no inf or NaN, footnote 5, and a -0.0 in B may
- * come back as +0.0); with beta = 0 the plans write a scratch tensor and B is
- * not touched.  The scratch memory (the flush buffer and, for beta = 0, a
- * tensor of B's footprint) is allocated for the call and freed before it
- * returns; without it, timing falls back to bursts of four back-to-back
- * launches and the paper's alpha = 0, beta = 1 on B.  The chosen plan is cached per problem (perm,
+ * the caches are charged for them as in back-to-back use.  The (at most)
+ * three candidates screened fastest, each at least 1 % ahead of the quick
+ * path's plan, are then timed again against it in five alternating rounds,
+ * cold as above and in bursts of four back-to-back launches; a finalist
+ * replaces the quick plan only if it is at least 1 % faster in both sums
+ * (this confirmation runs after the timeout and adds at most 60 timed
+ * spans).  The caller's data are not changed: the plans write a scratch
+ * tensor of B's footprint (zeroed first when beta != 0) and B is not
+ * touched.  The scratch memory (that tensor and the flush buffer) is
+ * allocated for the call and freed before it returns.  Without memory for
+ * the scratch tensor, timing runs, like the paper's, on B itself with
+ * alpha = 0 and beta = 1, so B is rewritten with its own value and A is read
+ * and multiplied by zero (A must then hold no inf or NaN, footnote 5, and a
+ * -0.0 in B comes back as +0.0); without memory for the flush buffer, timing
+ * falls back to bursts of four back-to-back launches.  The chosen plan is cached per problem (perm,
  * extents, outer sizes, dtype, update mode, device) for the life of the
  * process; a cached problem returns at once without launching anything.
  *

@@ -1,16 +1,20 @@
 // The autotune path of plan creation (Section 3.1): generate candidate plans,
 // rank them with the heuristic plan first, then time them on the caller's own
 // tensors, from good to bad, until a timeout, and keep the fastest (FFTW
-// style).  Timing never changes the caller's data: with beta != 0 it runs with
-// alpha = 0 and beta = 1, so B is rewritten with its own value and A is read
-// and multiplied by zero (Section 3.1; A must not hold inf or NaN, footnote
-// 5); with beta = 0 the plans write a scratch tensor instead, so that they are
-// timed in the mode they will run in.  A 512 MiB read between timed launches
-// evicts the tensors from the last-level cache, as the paper's measurements
-// clear the caches (Section 4).  Winners are cached per problem for the life
+// style).  Timing never changes the caller's data: the plans write a scratch
+// tensor of B's footprint, so that they are timed in the update mode they
+// will run in; without memory for it, timing runs on B itself with alpha = 0
+// and beta = 1, so B is rewritten with its own value and A is read and
+// multiplied by zero (Section 3.1; A must not hold inf or NaN, footnote 5).
+// A 512 MiB read between timed launches evicts the tensors from the
+// last-level cache, as the paper's measurements clear the caches (Section 4).
+// The few fastest candidates are then timed again, alternating with the
+// quick path's plan, cold and in back-to-back bursts; one replaces the quick
+// plan only if it wins in both.  Winners are cached per problem for the life
 // of the process.
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <chrono>
 #include <map>
 #include <mutex>
@@ -168,12 +172,17 @@ constexpr size_t kFlushBytes = size_t(512) << 20;  // two last-level caches (256
 constexpr int kReps = 3;
 constexpr int kBurst = 4;
 constexpr float kMargin = 0.99f;  // leave the quick plan only for a 1 % gain
+// Screening times many candidates three times each, so the fastest of them
+// is partly the luckiest: the finalists are timed again against the quick
+// plan, in alternating order, before one may replace it.
+constexpr int kFinalists = 3;
+constexpr int kConfirmRounds = 5;
 
 // Device memory the tuner borrows for its measurements and returns at the end.
 struct Scratch {
     void* flush = nullptr;  // read between timed launches so they start cold
     void* sink = nullptr;   // checksums of the flush reads
-    void* out = nullptr;    // a stand-in for B when beta = 0
+    void* out = nullptr;    // a stand-in for B, so timing leaves B alone
     ~Scratch() {
         if (flush) (void)hipFree(flush);
         if (sink) (void)hipFree(sink);
@@ -232,14 +241,19 @@ hptt_status_t autotune(hptt_plan_t* planOut, const int32_t* perm, int32_t N, con
                                            cand.data(), kMaxCandidates);
         if (nc < 0) return hptt_status_t(-nc);
         if (!A || !B) return HPTT_ERROR_INVALID_ARGUMENT;
-        // Time in the caller's own update mode.  With beta != 0 that is the
-        // paper's alpha = 0, beta = 1 on B itself (B keeps its value); with
-        // beta = 0 the plan writes a scratch tensor and B is not touched.
-        // Without memory for the scratch tensor, fall back to the paper's way.
+        // Time in the caller's own update mode, writing a scratch tensor so
+        // that B is not touched (with beta != 0 the scratch tensor is zeroed
+        // first and then updated in place by every timed launch: the values
+        // do not change the timing).  Without memory for it, fall back to the
+        // paper's alpha = 0, beta = 1 on B itself, which keeps B's values
+        // (but turns a -0.0 into +0.0 and any inf or NaN of A into NaN).
         Scratch scratch;
         const size_t elem = dtype == HPTT_FLOAT32 ? 4 : 8;
-        const bool ownMode =
-            mode != kAxpby && try_alloc(&scratch.out, size_t(base.info.footprint_b) * elem);
+        const size_t outBytes = (size_t(base.info.footprint_b) * elem + 15) / 16 * 16;
+        bool ownMode = try_alloc(&scratch.out, outBytes);
+        if (ownMode && mode == kAxpby &&
+            hptt_yardstick_fill(scratch.out, outBytes, 0, stream) != HPTT_SUCCESS)
+            return HPTT_ERROR_HIP;
         const double tAlpha = ownMode ? alpha : 0.0, tBeta = ownMode ? beta : 1.0;
         void* const target = ownMode ? scratch.out : B;
         const bool flush = try_alloc(&scratch.flush, kFlushBytes) &&
@@ -277,10 +291,24 @@ hptt_status_t autotune(hptt_plan_t* planOut, const int32_t* perm, int32_t N, con
             *out = median3(ms[0], ms[1], ms[2]);
             return e;
         };
+        // Back-to-back use: [flush] e0 kBurst launches e1, per launch.
+        auto burst = [&](hptt_plan_s* tp, float* ms) -> hptt_status_t {
+            hptt_status_t e = HPTT_SUCCESS;
+            if (flush) e = hptt_yardstick_read(scratch.flush, kFlushBytes, scratch.sink, stream);
+            if (e == HPTT_SUCCESS && hipEventRecord(e0, stream) != hipSuccess) e = HPTT_ERROR_HIP;
+            for (int b = 0; b < kBurst && e == HPTT_SUCCESS; ++b) e = hptt_exec(tp, A, target, stream);
+            if (e == HPTT_SUCCESS && hipEventRecord(e1, stream) != hipSuccess) e = HPTT_ERROR_HIP;
+            if (e == HPTT_SUCCESS && hipEventSynchronize(e1) != hipSuccess) e = HPTT_ERROR_HIP;
+            if (e == HPTT_SUCCESS && hipEventElapsedTime(ms, e0, e1) != hipSuccess)
+                e = HPTT_ERROR_HIP;
+            *ms /= kBurst;
+            return e;
+        };
         const auto t0 = clock::now();
         float bestMs = 0.f, quickMs = 0.f, flushMs = 0.f;
         hptt_status_t err = flush ? measure(nullptr, &flushMs) : HPTT_SUCCESS;
         int timed = 0;
+        std::vector<std::pair<float, int>> ahead;  // screened faster than the quick plan
         for (int c = 0; c < nc && err == HPTT_SUCCESS; ++c) {
             hptt_plan_s tp;
             if (build_plan(perm, N, sizeA, outerA, outerB, tAlpha, tBeta, dtype, &cand[c], &tp) !=
@@ -292,14 +320,50 @@ hptt_status_t autotune(hptt_plan_t* planOut, const int32_t* perm, int32_t N, con
             if (err != HPTT_SUCCESS) break;
             m = flush ? m - flushMs : m / kBurst;
             ++timed;
-            if (c == 0) {
-                quickMs = bestMs = m;
-            } else if (m < bestMs && m < kMargin * quickMs) {
-                bestMs = m;
-                best = cand[c];
-            }
+            if (c == 0) quickMs = bestMs = m;
+            else if (m < kMargin * quickMs) ahead.push_back({m, c});
             const double elapsed = std::chrono::duration<double>(clock::now() - t0).count();
             if (elapsed >= timeoutSeconds) break;
+        }
+        // Confirmation: each finalist against the quick plan, kConfirmRounds
+        // rounds in alternating order, summed cold (as screened) and in
+        // back-to-back bursts; it must beat the quick plan by the margin in
+        // both.  The confirmed finalist with the fastest bursts is chosen.
+        std::sort(ahead.begin(), ahead.end());
+        if (ahead.size() > size_t(kFinalists)) ahead.resize(kFinalists);
+        int confirmed = 0;
+        float bestBurst = 0.f;
+        hptt_plan_s qp;
+        if (err == HPTT_SUCCESS && !ahead.empty() &&
+            build_plan(perm, N, sizeA, outerA, outerB, tAlpha, tBeta, dtype, &cand[0], &qp) !=
+                HPTT_SUCCESS)
+            ahead.clear();
+        for (const auto& fin : ahead) {
+            hptt_plan_s fp;
+            if (build_plan(perm, N, sizeA, outerA, outerB, tAlpha, tBeta, dtype, &cand[fin.second],
+                           &fp) != HPTT_SUCCESS)
+                continue;
+            float qCold = 0.f, fCold = 0.f, qBurst = 0.f, fBurst = 0.f;
+            for (int r = 0; r < kConfirmRounds && err == HPTT_SUCCESS; ++r) {
+                hptt_plan_s* order[2] = {&qp, &fp};
+                if (r & 1) std::swap(order[0], order[1]);
+                for (hptt_plan_s* tp : order) {
+                    float c = 0.f, b = 0.f;
+                    if (flush && err == HPTT_SUCCESS) err = span(tp, &c);
+                    if (err == HPTT_SUCCESS) err = burst(tp, &b);
+                    if (err != HPTT_SUCCESS) break;
+                    (tp == &qp ? qCold : fCold) += flush ? c - flushMs : 0.f;
+                    (tp == &qp ? qBurst : fBurst) += b;
+                }
+            }
+            if (err != HPTT_SUCCESS) break;
+            if (fCold <= kMargin * qCold && fBurst < kMargin * qBurst &&
+                (confirmed == 0 || fBurst < bestBurst)) {
+                bestBurst = fBurst;
+                best = cand[fin.second];
+                bestMs = fin.first;
+            }
+            confirmed += fCold <= kMargin * qCold && fBurst < kMargin * qBurst;
         }
         (void)hipEventDestroy(e0);
         (void)hipEventDestroy(e1);
@@ -311,6 +375,8 @@ hptt_status_t autotune(hptt_plan_t* planOut, const int32_t* perm, int32_t N, con
             report->best_ms = bestMs;
             report->flushed = flush ? 1 : 0;
             report->own_mode = ownMode ? 1 : 0;
+            report->finalists = int32_t(ahead.size());
+            report->confirmed = confirmed;
         }
         std::lock_guard<std::mutex> lock(g_mutex);
         g_wisdom[key] = best;

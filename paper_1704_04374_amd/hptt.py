@@ -52,13 +52,15 @@ class AutotuneReport(ctypes.Structure):
     _fields_ = [("candidates", ctypes.c_int32), ("timed", ctypes.c_int32),
                 ("from_cache", ctypes.c_int32), ("flushed", ctypes.c_int32),
                 ("own_mode", ctypes.c_int32), ("default_ms", ctypes.c_float),
-                ("best_ms", ctypes.c_float), ("options", Options)]
+                ("best_ms", ctypes.c_float), ("options", Options),
+                ("finalists", ctypes.c_int32), ("confirmed", ctypes.c_int32)]
 
     def as_dict(self) -> dict:
         return {"candidates": self.candidates, "timed": self.timed,
                 "from_cache": bool(self.from_cache), "flushed": bool(self.flushed),
                 "own_mode": bool(self.own_mode), "default_ms": self.default_ms,
-                "best_ms": self.best_ms,
+                "best_ms": self.best_ms, "finalists": self.finalists,
+                "confirmed": self.confirmed,
                 "options": {name: getattr(self.options, name) for name, _ in Options._fields_}}
 
 
