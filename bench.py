@@ -5,8 +5,12 @@
 One step is one execution of the plan (all of the hot path: the plan is
 built once, then each step launches the kernel the plan chose) on inputs
 already resident in HBM.  Steps cycle through enough buffer sets that no
-launch finds its tensors in the 256 MB last-level cache.  The headline workload is the 8192 x 8192 fp32
-matrix transpose; the other named workloads are reported in ``per_workload``.
+launch finds its tensors in the 256 MB last-level cache.  The headline workload is the largest
+one: the 5-D fp32 transposition of A(3, 2, 640, 480, 96) with perm [4, 2, 0, 3, 1] and
+alpha = beta = 1 (B read and written, the paper's default reporting mode, Eq. 2
+with lambda = 3); the other named workloads are reported in ``per_workload``,
+each with its own roofline block, and the 57-case sweep's distribution in
+``per_sweep``.
 
 Bandwidth follows Eq. (2) of the paper: lambda * S bytes per transposition
 (S = bytes of one tensor, lambda = 2 when beta = 0, 3 otherwise), reported in
@@ -20,7 +24,8 @@ GB/s (1e9 B/s).  Context printed on the same line:
     and hipMemcpyAsync device-to-device;
   - cold: the paper's protocol (Section 4), best and median of single
     launches with the caches cleared in between;
-  - cpu_baseline: the CPU oracle on this machine's host, single-threaded.
+  - cpu_baseline: the CPU oracle on this machine's host, single-threaded, with
+    the host's logical CPU count and CPU model.
 """
 from __future__ import annotations
 
@@ -37,7 +42,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD published peak
-HEADLINE = "transpose2d_8192x8192_f32"
+HEADLINE = "transpose5d_3x2x640x480x96_f32"
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 FLUSH_BYTES = 1 << 30           # > 256 MB last-level cache + 8 x 4 MB L2
 ROTATE_BYTES = 2 << 30          # traffic between two uses of one buffer set
@@ -83,11 +88,23 @@ def load_traffic(kernel_class: str, workload: str):
         return None
 
 
+def roofline_block(achieved_gbs: float, kernel_class: str, w) -> dict:
+    """Roofline of one workload's transposition kernel: achieved GB/s (Eq. 2
+    bytes over the kernel's average launch time) against the HBM peak, and the
+    HBM bytes per launch that a committed counter summary gives, if any."""
+    traffic = load_traffic(kernel_class, w.name)
+    return {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+            "algorithmic_bytes": w.moved_bytes,
+            "traffic_over_algorithmic": (None if traffic is None
+                                         else round(traffic / w.moved_bytes, 4))}
+
+
 def _events(torch, n):
     return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
 
 
-def time_launches(torch, fn, steps: int, warmup: int):
+def time_launches(torch, fn, steps: int, warmup: int, dist: bool = True):
     """Run fn(i) for i < warmup, then `steps` more back to back between a
     synchronize on each side: the timed region, with one HIP event pair on
     the launch stream around all of it.  Returns (wall seconds of the
@@ -95,7 +112,8 @@ def time_launches(torch, fn, steps: int, warmup: int):
     the gap the GPU leaves before the next dependent one, which agrees with
     rocprofv3's kernel trace).  Then `steps` more launches, each between its
     own event pair, give the distribution (time_launches.last); they stay
-    out of the timed region, where each event record would add a gap."""
+    out of the timed region, where each event record would add a gap; with
+    dist=False they are skipped."""
     for i in range(warmup):
         fn(i)
     torch.cuda.synchronize()
@@ -108,6 +126,8 @@ def time_launches(torch, fn, steps: int, warmup: int):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     per_launch = region[0].elapsed_time(region[1]) / steps
+    if not dist:
+        return wall, per_launch
     starts, ends = _events(torch, steps), _events(torch, steps)
     for i in range(steps):
         starts[i].record()
@@ -245,23 +265,59 @@ def measure_workload(torch, hptt, w, steps, warmup, reps, flush_buf, sink, full:
                                         w.dtype, timeout=tune_s, outer_size_a=w.outer_a,
                                         outer_size_b=w.outer_b)
         tune_wall = time.perf_counter() - t0
-        truns = [tuned.launcher(As[j].data_ptr(), Bs[j].data_ptr(), stream) for j in range(k)]
-        tms = time_launches(torch, lambda i: truns[i % k](), steps, warmup)[1]
+        same = tuned.describe() == plan.describe()
+        if same:
+            # the quick path's own plan: nothing to compare but noise
+            qms = tms = ms
+        else:
+            # both plans in alternating rounds, so that clock drift between
+            # two separate timings does not pass for a speedup
+            truns = [tuned.launcher(As[j].data_ptr(), Bs[j].data_ptr(), stream)
+                     for j in range(k)]
+            qs, ts = [], []
+            for r in range(5):
+                pair = [(runs, qs), (truns, ts)]
+                for rs, acc in (pair if r % 2 == 0 else pair[::-1]):
+                    acc.append(time_launches(torch, lambda i, rs=rs: rs[i % k](), steps, warmup,
+                                             dist=False)[1])
+            qms, tms = statistics.median(qs), statistics.median(ts)
         out["autotune"] = {
             "seconds": round(tune_wall, 2), "candidates": rep["candidates"],
-            "timed": rep["timed"], "plan": tuned.describe(),
+            "timed": rep["timed"], "finalists": rep["finalists"], "confirmed": rep["confirmed"],
+            "plan": tuned.describe(), "same_plan_as_quick": same,
             "knobs": {n: v for n, v in rep["options"].items() if v},
             "kernel_gbs": round(gbs(moved, tms), 1),
-            "speedup_vs_quick": round(ms / tms, 3),
+            "speedup_vs_quick": round(qms / tms, 3),
         }
     del As, Bs, PA, PB
     torch.cuda.empty_cache()
     return out
 
 
+def host_description() -> dict:
+    """The host the CPU baseline ran on: logical CPUs, the CPUs this process
+    may use, and the CPU model."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = os.cpu_count()
+    return {"host_logical_cpus": os.cpu_count(), "host_usable_cpus": usable,
+            "host_cpu_model": model}
+
+
 def cpu_baseline(w, budget_s: float = 12.0):
     """The oracle, as it stands, on this host: repeated whole transpositions
-    of the headline workload until about budget_s seconds have passed."""
+    of the headline workload until about budget_s seconds have passed, on one
+    thread (the oracle is a single-threaded loop)."""
     from oracle import oracle
     from paper_1704_04374_amd.workloads import inputs
     A, B0 = inputs(w)
@@ -274,10 +330,12 @@ def cpu_baseline(w, budget_s: float = 12.0):
         el = time.perf_counter() - t0
         if el >= budget_s or runs >= 50:
             break
-    return {"value": round(w.moved_bytes * runs / el / 1e9, 3), "unit": "GB/s",
-            "cores": 1, "kind": "oracle",
-            "sample": f"{runs} whole transpositions of {w.name} "
-                      f"({w.numel} elements each, {el:.1f} s, single thread)"}
+    out = {"value": round(w.moved_bytes * runs / el / 1e9, 3), "unit": "GB/s",
+           "cores": 1, "kind": "oracle",
+           "sample": f"{runs} whole transpositions of {w.name} "
+                     f"({w.numel} elements each, {el:.1f} s, single thread)"}
+    out.update(host_description())
+    return out
 
 
 def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, command: str, out_path: str):
@@ -383,6 +441,59 @@ def summarize_trace(trace_dir: str, workload: str, command: str, out_path: str):
     print("\n".join(lines))
 
 
+def sweep_summary(torch, hptt, steps: int, warmup: int) -> dict:
+    """The 57-case sweep (Section 4's benchmark shape, Figs. 6 and 7) on the
+    quick path, timed like the named workloads but lean: per case one
+    rotation of device buffers, then back-to-back launches of the beta = 1
+    plan, the same-run axpby yardstick (the paper's SAXPY), the alpha = 1,
+    beta = 0 plan and the same-run copy yardstick.  Returns the distribution
+    of % of axpby (beta = 1) and % of copy (beta = 0) with one row per case."""
+    from paper_1704_04374_amd.workloads import sweep57
+    rows = []
+    t_start = time.perf_counter()
+    for w in sweep57(beta=1.0):
+        k = rotation(w)
+        gen = torch.Generator(device="cuda").manual_seed(w.seed_a)
+        As = [torch.rand(w.numel, device="cuda", generator=gen) * 2 - 1 for _ in range(k)]
+        Bs = [torch.rand(w.numel, device="cuda", generator=gen) * 2 - 1 for _ in range(k)]
+        stream = torch.cuda.current_stream().cuda_stream
+        p1 = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype)
+        p0 = hptt.create_plan(w.perm, w.size_a, 1.0, 0.0, w.dtype)
+        r1 = [p1.launcher(As[j].data_ptr(), Bs[j].data_ptr(), stream) for j in range(k)]
+        r0 = [p0.launcher(As[j].data_ptr(), Bs[j].data_ptr(), stream) for j in range(k)]
+        S = w.tensor_bytes
+        S16 = S // 16 * 16
+        ms1 = time_launches(torch, lambda i: r1[i % k](), steps, warmup, dist=False)[1]
+        msx = time_launches(torch, lambda i: hptt.yardstick_axpby(
+            w.dtype, w.alpha, As[i % k], w.beta, Bs[i % k], S16 // 4), steps, warmup,
+            dist=False)[1]
+        ms0 = time_launches(torch, lambda i: r0[i % k](), steps, warmup, dist=False)[1]
+        msc = time_launches(torch, lambda i: hptt.yardstick_copy(As[i % k], Bs[i % k], S16),
+                            steps, warmup, dist=False)[1]
+        g1, g0 = 3 * S / ms1 / 1e6, 2 * S / ms0 / 1e6
+        row = {"case": w.name, "kernel": p1.info["kernel"], "gbs": round(g1, 1),
+               "pct_of_axpby": round(100 * g1 / (3 * S16 / msx / 1e6), 1),
+               "beta0_gbs": round(g0, 1),
+               "beta0_pct_of_copy": round(100 * g0 / (2 * S16 / msc / 1e6), 1)}
+        rows.append(row)
+        print(f"[sweep] {w.name}: {row['kernel']} {row['gbs']:.0f} GB/s = "
+              f"{row['pct_of_axpby']:.1f}% of axpby; beta=0 {row['beta0_gbs']:.0f} GB/s = "
+              f"{row['beta0_pct_of_copy']:.1f}% of copy", file=sys.stderr, flush=True)
+        del As, Bs, r1, r0, p1, p0
+        torch.cuda.empty_cache()
+
+    def stats(key):
+        v = [r[key] for r in rows]
+        return {"mean": round(statistics.mean(v), 2), "median": round(statistics.median(v), 2),
+                "min": round(min(v), 2), "max": round(max(v), 2)}
+    return {"sweep": "57 seeded fp32 transpositions, 2-D to 6-D, 200 MB per tensor, quick path",
+            "steps": steps, "warmup": warmup, "seconds": round(time.perf_counter() - t_start, 1),
+            "pct_of_axpby": stats("pct_of_axpby"), "gbs": stats("gbs"),
+            "beta0_pct_of_copy": stats("beta0_pct_of_copy"), "beta0_gbs": stats("beta0_gbs"),
+            "cases_below_60_pct_of_axpby": sum(r["pct_of_axpby"] < 60 for r in rows),
+            "cases": rows}
+
+
 def run_sweep(torch, hptt, args, flush_buf, sink) -> dict:
     """The 57-case sweep (Section 4, Figs. 6 and 7): every case with beta != 0
     against the same-run axpby yardstick (the paper's SAXPY), with and
@@ -483,6 +594,8 @@ def main():
     ap.add_argument("--only-headline", action="store_true",
                     help="time only the headline workload (for profiler runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep-summary", action="store_true",
+                    help="skip the 57-case sweep summary of the default run")
     ap.add_argument("--autotune", type=float, default=2.0, metavar="SECONDS",
                     help="also tune each named workload for this long (0: skip)")
     ap.add_argument("--sweep", action="store_true",
@@ -548,6 +661,7 @@ def main():
                 torch, hptt, w, args.steps, args.warmup, args.reps, flush_buf, sink, full=True,
                 tune_s=args.autotune)
             per[w.name] = {k: (round(v, 2) if isinstance(v, float) else v) for k, v in r.items()}
+            per[w.name]["roofline"] = roofline_block(r["kernel_gbs"], r["kernel_class"], w)
             tuned = r.get("autotune")
             print(f"[bench] {w.name}: kernel {r['kernel_gbs']:.0f} GB/s, "
                   f"{r['pct_of_copy']:.1f}% of copy, {r['pct_of_hbm_peak']:.1f}% of peak"
@@ -555,8 +669,14 @@ def main():
                      f"{tuned['candidates']} plans timed)" if tuned else ""),
                   file=sys.stderr, flush=True)
 
-    traffic = load_traffic(headline["kernel_class"], head.name)
-    achieved = headline["kernel_gbs"]
+    roof = roofline_block(headline["kernel_gbs"], headline["kernel_class"], head)
+    per_sweep = None
+    if not args.only_headline and not args.no_sweep_summary:
+        per_sweep = sweep_summary(torch, hptt, min(args.steps, 20), min(args.warmup, 5))
+        print(f"[bench] sweep: {per_sweep['pct_of_axpby']['mean']:.1f}% of axpby on average "
+              f"(min {per_sweep['pct_of_axpby']['min']:.1f}), beta=0 "
+              f"{per_sweep['beta0_pct_of_copy']['mean']:.1f}% of copy, "
+              f"{per_sweep['seconds']:.0f} s", file=sys.stderr, flush=True)
     line = {
         "metric": "effective GB/s per transpose (Eq. 2 bytes) and % of HBM peak / same-run copy",
         "value": round(headline["gbs"], 2),
@@ -573,9 +693,7 @@ def main():
         "config": {"workload": head.name, "dtype": head.dtype, "size_a": list(head.size_a),
                    "perm": list(head.perm), "alpha": head.alpha, "beta": head.beta,
                    "bytes_per_step": head.moved_bytes},
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic},
+        "roofline": roof,
         "pct_of_copy": round(headline["pct_of_copy"], 2),
         "copy_gbs": round(headline["copy_gbs"], 1),
         "hipmemcpy_d2d_gbs": round(headline["hipmemcpy_d2d_gbs"], 1),
@@ -586,6 +704,7 @@ def main():
         "plan_create_us": headline["plan_create_us"],
         "kernel_source_hash": kernel_source_hash(),
         "per_workload": per or None,
+        "per_sweep": per_sweep,
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
