@@ -102,6 +102,46 @@ hptt_status_t hptt_contraction_exec(hptt_contraction_t plan, const void *A, cons
                                     void *C, void *workspace, size_t workspace_bytes,
                                     hipStream_t stream);
 
+/*
+ * Size of the device array hptt_contraction_exec_no_alloc works in (64 MiB,
+ * held by every device the library runs on until the process ends): its last
+ * HPTT_CONTRACTION_STATIC_BLAS_BYTES are rocBLAS's workspace, the rest holds
+ * the transposed operands and product (a plan's workspace_bytes).
+ */
+#define HPTT_CONTRACTION_STATIC_BYTES (64u << 20)
+#define HPTT_CONTRACTION_STATIC_BLAS_BYTES (16u << 20)
+
+/*
+ * For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc: the same
+ * contraction as hptt_contraction_exec, on the same kernels, with the
+ * workspace taken from a file-scope device array instead of the caller.
+ * Allocates nothing: no hipMalloc, hipFree or allocating library call.
+ *
+ * The first call on a device sets that device up (once, with it current):
+ * it looks up the array's device address and creates a rocBLAS handle whose
+ * workspace is the array's rocBLAS share, so that rocBLAS never allocates;
+ * rocBLAS also loads a GEMM kernel's code the first time that kernel runs.
+ * A caller that must never allocate therefore runs each plan once (on
+ * tensors of its shape) before, e.g., capturing a graph.
+ *
+ * Every call on one device works in that device's one array, which keeps the
+ * last call's contents (nothing in it needs to start at zero): calls that
+ * overlap on one device -- from several host threads, or queued on streams
+ * that run concurrently -- race and give wrong results.  Order them on one
+ * stream, or use hptt_contraction_exec with a workspace per stream.
+ *
+ * Returns HPTT_ERROR_INVALID_ARGUMENT for a NULL plan or tensor;
+ * HPTT_ERROR_UNSUPPORTED when the plan's workspace_bytes exceed
+ * HPTT_CONTRACTION_STATIC_BYTES - HPTT_CONTRACTION_STATIC_BLAS_BYTES (48 MiB),
+ * when rocBLAS would need more than HPTT_CONTRACTION_STATIC_BLAS_BYTES for
+ * the GEMM, or for a device ordinal of 64 or more; HPTT_ERROR_HIP when the
+ * set-up, a launch or the GEMM fails (hptt_contraction_last_blas_status
+ * gives rocBLAS's status).  Nothing is queued when the plan does not fit.
+ */
+hptt_status_t hptt_contraction_exec_no_alloc(hptt_contraction_t plan, const void *A,
+                                             const void *B, void *C, hipStream_t stream);
+
 /* The rocBLAS status of this thread's last failed GEMM (0 if none). */
 int32_t hptt_contraction_last_blas_status(void);
 

@@ -22,7 +22,7 @@ LIB = os.path.join(PKG, "libhptt.so")
 # Contractions (transposition - GEMM - transposition) link rocBLAS, so they
 # live in a library of their own on top of libhptt.so.
 CONTRACT_LIB = os.path.join(PKG, "libhptt_contract.so")
-CONTRACT_SOURCES = ["contract.cpp"]
+CONTRACT_SOURCES = ["contract.hip"]
 
 ARCH = "gfx950"
 # the tile kernel instantiations are split over five files so they compile in parallel

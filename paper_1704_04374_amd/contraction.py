@@ -13,7 +13,11 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhptt_con
 
 EXPORTS = ("hptt_contraction_create", "hptt_contraction_destroy", "hptt_contraction_info",
            "hptt_contraction_describe", "hptt_contraction_exec",
-           "hptt_contraction_last_blas_status")
+           "hptt_contraction_exec_no_alloc", "hptt_contraction_last_blas_status")
+
+# the device array hptt_contraction_exec_no_alloc works in, and rocBLAS's share of it
+STATIC_BYTES = 64 << 20
+STATIC_BLAS_BYTES = 16 << 20
 
 
 class ContractionInfo(ctypes.Structure):
@@ -53,9 +57,11 @@ def library() -> ctypes.CDLL:
         lib.hptt_contraction_info.argtypes = [vp, ctypes.POINTER(ContractionInfo)]
         lib.hptt_contraction_describe.argtypes = [vp, ctypes.c_char_p, ctypes.c_size_t]
         lib.hptt_contraction_exec.argtypes = [vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        lib.hptt_contraction_exec_no_alloc.argtypes = [vp, vp, vp, vp, vp]
         lib.hptt_contraction_last_blas_status.restype = ctypes.c_int32
         for f in ("hptt_contraction_create", "hptt_contraction_destroy", "hptt_contraction_info",
-                  "hptt_contraction_describe", "hptt_contraction_exec"):
+                  "hptt_contraction_describe", "hptt_contraction_exec",
+                  "hptt_contraction_exec_no_alloc"):
             getattr(lib, f).restype = st
         _lib = lib
     return _lib
@@ -110,8 +116,7 @@ class Contraction:
             self._workspace = torch.empty(need, dtype=torch.uint8, device="cuda")
         return self._workspace
 
-    def exec(self, A, B, C, stream=None):
-        """Queue the contraction on `stream` (default: torch's current one)."""
+    def _check_tensors(self, A, B, C):
         for t, name, n in ((A, "A", self.size_a), (B, "B", self.size_b), (C, "C", self.size_c)):
             numel = 1
             for s in n:
@@ -120,16 +125,33 @@ class Contraction:
                 raise ValueError(f"{name} must be a contiguous device tensor of {numel} elements")
             if hptt._dtype_id(t.dtype) != hptt.DTYPES[self.dtype]:
                 raise ValueError(f"{name} has dtype {t.dtype}, plan is {self.dtype}")
+
+    def _raise(self, st, what):
+        if st == hptt.HIP_ERROR:
+            raise hptt.HpttError(st, f"{what} (hipError {hptt.library().hptt_last_hip_error()}, "
+                                     f"rocBLAS status "
+                                     f"{self._lib.hptt_contraction_last_blas_status()})")
+        hptt._check(st, what)
+
+    def exec(self, A, B, C, stream=None):
+        """Queue the contraction on `stream` (default: torch's current one)."""
+        self._check_tensors(A, B, C)
         ws = self.workspace()
         st = self._lib.hptt_contraction_exec(
             self._handle, ctypes.c_void_p(A.data_ptr()), ctypes.c_void_p(B.data_ptr()),
             ctypes.c_void_p(C.data_ptr()), ctypes.c_void_p(0 if ws is None else ws.data_ptr()),
             0 if ws is None else ws.numel(), ctypes.c_void_p(hptt._stream(stream)))
-        if st == hptt.HIP_ERROR:
-            raise hptt.HpttError(st, f"hptt_contraction_exec (hipError "
-                                     f"{hptt.library().hptt_last_hip_error()}, rocBLAS status "
-                                     f"{self._lib.hptt_contraction_last_blas_status()})")
-        hptt._check(st, "hptt_contraction_exec")
+        self._raise(st, "hptt_contraction_exec")
+
+    def exec_no_alloc(self, A, B, C, stream=None):
+        """Queue the contraction on `stream` with the library's own device
+        array as the workspace (hptt_contraction_exec_no_alloc): nothing is
+        allocated; calls that overlap on one device race."""
+        self._check_tensors(A, B, C)
+        st = self._lib.hptt_contraction_exec_no_alloc(
+            self._handle, ctypes.c_void_p(A.data_ptr()), ctypes.c_void_p(B.data_ptr()),
+            ctypes.c_void_p(C.data_ptr()), ctypes.c_void_p(hptt._stream(stream)))
+        self._raise(st, "hptt_contraction_exec_no_alloc")
 
     def __del__(self):
         if getattr(self, "_handle", None) is not None and self._handle.value:

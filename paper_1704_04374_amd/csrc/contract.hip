@@ -8,6 +8,7 @@
 #include <rocblas/rocblas.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 #include <stdio.h>
 #include <string.h>
@@ -280,6 +281,68 @@ hptt_status_t hptt_contraction_describe(hptt_contraction_t plan, char* buf, size
 
 int32_t hptt_contraction_last_blas_status(void) { return t_blasStatus; }
 
+}  // extern "C"
+
+namespace {
+
+// The GEMM of a plan on `handle`, queued on the handle's stream (inside a
+// rocBLAS device-memory size query nothing runs: the call only reports the
+// workspace the GEMM would need).
+rocblas_status gemm(const hptt_contraction_s* p, rocblas_handle handle, const void* P,
+                    const void* Q, void* out) {
+    const Choice& c = p->ch;
+    const hptt_contraction_info_t& in = p->info;
+    const int64_t m = in.gemm_m, n = in.gemm_n, k = in.gemm_k;
+    const rocblas_operation oP = c.opP ? rocblas_operation_transpose : rocblas_operation_none;
+    const rocblas_operation oQ = c.opQ ? rocblas_operation_transpose : rocblas_operation_none;
+    if (p->dtype == HPTT_FLOAT32) {
+        const float al = float(p->alpha), be = c.tC ? 0.f : float(p->beta);
+        return rocblas_sgemm_strided_batched_64(
+            handle, oP, oQ, m, n, k, &al, static_cast<const float*>(P), in.ld_p, in.stride_p,
+            static_cast<const float*>(Q), in.ld_q, in.stride_q, &be, static_cast<float*>(out),
+            in.ld_c, in.stride_c, in.batch);
+    }
+    const double al = p->alpha, be = c.tC ? 0.0 : p->beta;
+    return rocblas_dgemm_strided_batched_64(
+        handle, oP, oQ, m, n, k, &al, static_cast<const double*>(P), in.ld_p, in.stride_p,
+        static_cast<const double*>(Q), in.ld_q, in.stride_q, &be, static_cast<double*>(out),
+        in.ld_c, in.stride_c, in.batch);
+}
+
+// Queue a plan with the given workspace (wsBytes of it at least) and rocBLAS
+// handle: the transpositions of A and B into the workspace where needed, the
+// GEMM, the transposition of the product into C where needed.
+hptt_status_t run(const hptt_contraction_s* p, const void* A, const void* B, void* C,
+                  void* workspace, rocblas_handle handle, hipStream_t stream) {
+    const Choice& c = p->ch;
+    char* ws = static_cast<char*>(workspace);
+    const void* P = c.swap ? B : A;
+    const void* Q = c.swap ? A : B;
+    hptt_status_t st = HPTT_SUCCESS;
+    if (c.tP) {
+        st = hptt_exec(p->planP, P, ws + p->offP, stream);
+        P = ws + p->offP;
+    }
+    if (st == HPTT_SUCCESS && c.tQ) {
+        st = hptt_exec(p->planQ, Q, ws + p->offQ, stream);
+        Q = ws + p->offQ;
+    }
+    if (st != HPTT_SUCCESS) return st;
+    void* out = c.tC ? static_cast<void*>(ws + p->offC) : C;
+    rocblas_status bs = rocblas_set_stream(handle, stream);
+    if (bs == rocblas_status_success) bs = gemm(p, handle, P, Q, out);
+    if (bs != rocblas_status_success) {
+        t_blasStatus = int32_t(bs);
+        return HPTT_ERROR_HIP;
+    }
+    if (c.tC) st = hptt_exec(p->planC, out, C, stream);
+    return st;
+}
+
+}  // namespace
+
+extern "C" {
+
 hptt_status_t hptt_contraction_exec(hptt_contraction_t p, const void* A, const void* B, void* C,
                                     void* workspace, size_t workspaceBytes, hipStream_t stream) {
     if (!p || !A || !B || !C) return HPTT_ERROR_INVALID_ARGUMENT;
@@ -299,47 +362,88 @@ hptt_status_t hptt_contraction_exec(hptt_contraction_t p, const void* A, const v
         }
         p->handleDevice = device;
     }
-    const Choice& c = p->ch;
-    char* ws = static_cast<char*>(workspace);
-    const void* P = c.swap ? B : A;
-    const void* Q = c.swap ? A : B;
-    hptt_status_t st = HPTT_SUCCESS;
-    if (c.tP) {
-        st = hptt_exec(p->planP, P, ws + p->offP, stream);
-        P = ws + p->offP;
-    }
-    if (st == HPTT_SUCCESS && c.tQ) {
-        st = hptt_exec(p->planQ, Q, ws + p->offQ, stream);
-        Q = ws + p->offQ;
-    }
-    if (st != HPTT_SUCCESS) return st;
-    void* out = c.tC ? static_cast<void*>(ws + p->offC) : C;
-    const hptt_contraction_info_t& in = p->info;
-    const int64_t m = in.gemm_m, n = in.gemm_n, k = in.gemm_k;
-    const rocblas_operation oP = c.opP ? rocblas_operation_transpose : rocblas_operation_none;
-    const rocblas_operation oQ = c.opQ ? rocblas_operation_transpose : rocblas_operation_none;
-    rocblas_status bs = rocblas_set_stream(p->handle, stream);
-    if (bs == rocblas_status_success) {
-        if (p->dtype == HPTT_FLOAT32) {
-            const float al = float(p->alpha), be = c.tC ? 0.f : float(p->beta);
-            bs = rocblas_sgemm_strided_batched_64(
-                p->handle, oP, oQ, m, n, k, &al, static_cast<const float*>(P), in.ld_p, in.stride_p,
-                static_cast<const float*>(Q), in.ld_q, in.stride_q, &be, static_cast<float*>(out),
-                in.ld_c, in.stride_c, in.batch);
-        } else {
-            const double al = p->alpha, be = c.tC ? 0.0 : p->beta;
-            bs = rocblas_dgemm_strided_batched_64(
-                p->handle, oP, oQ, m, n, k, &al, static_cast<const double*>(P), in.ld_p,
-                in.stride_p, static_cast<const double*>(Q), in.ld_q, in.stride_q, &be,
-                static_cast<double*>(out), in.ld_c, in.stride_c, in.batch);
+    return run(p, A, B, C, workspace, p->handle, stream);
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Execution without allocation: the workspace is a file-scope device array,
+// HPTT_CONTRACTION_STATIC_BYTES long; rocBLAS gets its last
+// HPTT_CONTRACTION_STATIC_BLAS_BYTES as a user-owned workspace, the
+// transposed operands and products the rest.
+
+static __device__ __align__(256) unsigned char scratch[HPTT_CONTRACTION_STATIC_BYTES];
+
+namespace {
+
+constexpr size_t kStaticWorkspace =
+    size_t(HPTT_CONTRACTION_STATIC_BYTES) - size_t(HPTT_CONTRACTION_STATIC_BLAS_BYTES);
+constexpr int kMaxDevices = 64;
+
+// Per device, set up by the first call on it: the array's device address
+// (each device holds its own copy of the array) and a rocBLAS handle whose
+// workspace is the array's rocBLAS share, so that no GEMM allocates.
+struct StaticDevice {
+    char* base = nullptr;
+    rocblas_handle handle = nullptr;
+};
+std::mutex g_staticMutex;
+StaticDevice g_static[kMaxDevices];
+
+}  // namespace
+
+extern "C" {
+
+hptt_status_t hptt_contraction_exec_no_alloc(hptt_contraction_t p, const void* A, const void* B,
+                                             void* C, hipStream_t stream) {
+    if (!p || !A || !B || !C) return HPTT_ERROR_INVALID_ARGUMENT;
+    if (size_t(p->wsBytes) > kStaticWorkspace) return HPTT_ERROR_UNSUPPORTED;
+    int device = 0;
+    if (hipGetDevice(&device) != hipSuccess) return HPTT_ERROR_HIP;
+    if (device < 0 || device >= kMaxDevices) return HPTT_ERROR_UNSUPPORTED;
+    StaticDevice dev;
+    {
+        std::lock_guard<std::mutex> lock(g_staticMutex);
+        StaticDevice& d = g_static[device];
+        if (!d.base) {  // set-up, once per device, with that device current
+            void* ptr = nullptr;
+            if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+                (void)hipGetLastError();
+                return HPTT_ERROR_HIP;
+            }
+            rocblas_handle h = nullptr;
+            rocblas_status bs = rocblas_create_handle(&h);
+            if (bs == rocblas_status_success)
+                bs = rocblas_set_workspace(h, static_cast<char*>(ptr) + kStaticWorkspace,
+                                           size_t(HPTT_CONTRACTION_STATIC_BLAS_BYTES));
+            if (bs != rocblas_status_success) {
+                if (h) (void)rocblas_destroy_handle(h);
+                t_blasStatus = int32_t(bs);
+                return HPTT_ERROR_HIP;
+            }
+            d.handle = h;
+            d.base = static_cast<char*>(ptr);
         }
+        dev = d;
+    }
+    // The GEMM must fit rocBLAS's share of the array: ask rocBLAS (a size
+    // query runs nothing; the tensors stand in for the operands).
+    size_t need = 0;
+    rocblas_status bs = rocblas_start_device_memory_size_query(dev.handle);
+    if (bs == rocblas_status_success) {
+        const rocblas_status q = gemm(p, dev.handle, A, B, C);
+        bs = rocblas_stop_device_memory_size_query(dev.handle, &need);
+        if (q != rocblas_status_success && q != rocblas_status_size_increased &&
+            q != rocblas_status_size_unchanged)
+            bs = q;
     }
     if (bs != rocblas_status_success) {
         t_blasStatus = int32_t(bs);
         return HPTT_ERROR_HIP;
     }
-    if (c.tC) st = hptt_exec(p->planC, out, C, stream);
-    return st;
+    if (need > size_t(HPTT_CONTRACTION_STATIC_BLAS_BYTES)) return HPTT_ERROR_UNSUPPORTED;
+    return run(p, A, B, C, dev.base, dev.handle, stream);
 }
 
 }  // extern "C"
