@@ -122,6 +122,10 @@ typedef struct {
                               one element per access (odd row lengths), or two
                               fp32 elements when beta != 0, 1 = wherever B is
                               compact, 2 = never */
+    int32_t grid_order;    /* TILE: order of the grid digits of the indices outside
+                              the tile (after the chunk counters): 1 = A order, 2 =
+                              by the sum of their strides in A and B, 3 = B
+                              order; 0 = choose */
 } hptt_options_t;
 
 /* What the plan builder decided; for inspection and tests. */
@@ -163,6 +167,9 @@ typedef struct {
     int32_t flat_runs;                 /* TILE: fused B indices the flat B run is cut
                                           from (0: B runs are not flat); STREAM: 1
                                           when B is walked flat */
+    int32_t grid_order;                /* TILE: order of the grid digits outside the tile:
+                                          1 A order, 2 by the sum of their strides, 3 B
+                                          order (0: not a tile plan) */
 } hptt_plan_info_t;
 
 /*

@@ -120,6 +120,13 @@ int autotune_candidates(const int32_t* perm, int32_t N, const int64_t* sizeA,
             v.flat_runs = fr;
             var.push_back({1, v});
         }
+        // the outer grid digits in each order the quick path did not take
+        for (int32_t go = 1; go <= 3; ++go) {
+            hptt_options_t v;
+            memset(&v, 0, sizeof(v));
+            v.grid_order = go;
+            var.push_back({1, v});
+        }
         for (int c = 1; c <= 6; ++c)
             for (auto& pv : var)
                 if (pv.first == c) cand.push_back(pv.second);

@@ -7,6 +7,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
+
 #include "plan.h"
 
 namespace hptt {
@@ -194,6 +196,9 @@ int64_t choose_chunk(int64_t inner, int64_t n, int64_t other, int64_t target, in
 
 void set_div(FastDiv& f, int64_t d) { f = make_fastdiv(uint32_t(d)); }
 
+// Order of the grid digits outside the tile (outer_indices); 0 = A order.
+int32_t grid_order(const hptt_options_t& opt) { return opt.grid_order ? opt.grid_order : 1; }
+
 // Grid order of kernel T (both set-ups): diagonal (the second digit
 // rotated by skew times the first) unless asked otherwise, and optionally
 // contiguous tile ranges per XCD.
@@ -204,10 +209,96 @@ void set_tile_order(TileArgs& t, const hptt_options_t& opt, int g, const int64_t
     if (t.skew > 1 && uint64_t(ext[0]) * uint64_t(t.skew) >= (uint64_t(1) << 32)) t.skew = 1;
     t.xcdSplit = (opt.tile_order == 3 || opt.tile_order == 4) ? 1 : 0;
     info.tile_order = t.xcdSplit ? (t.skew ? 3 : 4) : t.skew ? 2 : 1;
+    info.grid_order = grid_order(opt);
 }
 
 // Kernel T set-up for targets tA (A-run) and tB (B-run).  Returns false if the
 // tile does not fit the LDS budget or the grid is too large.
+// The fused indices outside a tile, in the order they become grid digits
+// (after the chunk counters): 1 = A order, 2 = by the sum of their strides
+// in A and B (the index closest to contiguous in both tensors first, ties in
+// A order), 3 = B order.
+int outer_indices(const Fused& f, const bool* skip, int32_t order, int* out) {
+    int n = 0;
+    if (order == 3) {
+        for (int k = 0; k < f.M; ++k)
+            if (!skip[f.p[k]]) out[n++] = f.p[k];
+        return n;
+    }
+    for (int a = 0; a < f.M; ++a)
+        if (!skip[a]) out[n++] = a;
+    if (order == 2)
+        std::stable_sort(out, out + n, [&](int x, int y) {
+            return f.sA[x] + f.sB[x] < f.sA[y] + f.sB[y];
+        });
+    return n;
+}
+
+// Contiguous regions of A plus those of B that a window of kResident
+// consecutive tiles touches, for one order of the outer grid digits: a model
+// of how scattered the traffic of the workgroups resident at one time is.
+// covered[d] = how many values of fused index d the window spans (the tile's
+// own run, times the window's count of the digit that chunks it; a digit
+// after the window's first partial one contributes one value); a side's
+// contiguous block grows over its indices in memory order while each is
+// spanned whole (and back to back), and its regions are the window's
+// elements over that block.  Flat B runs (flatR) span the flattened B-run
+// range: its window count is spread over the B-run indices in B order.
+constexpr double kResident = 2048;  // workgroups resident at one time, about 8 per CU
+
+double window_regions(const Fused& f, const TileArgs& t, const int* outer, int no) {
+    const int M = f.M;
+    double covered[kMaxDims];
+    for (int d = 0; d < M; ++d) covered[d] = 1;
+    // the window's count of each digit, in digit order
+    double P = 1;
+    auto take = [&](double e) {
+        double c = P >= kResident ? 1 : (P * e <= kResident ? e : kResident / P);
+        P *= c;
+        return c;
+    };
+    double cCount = 1, rCount = 1;
+    if (t.cChunk < t.cLast) cCount = take(double((t.cLast + t.cChunk - 1) / t.cChunk));
+    if (t.rChunk < t.rLast) rCount = take(double((t.rLast + t.rChunk - 1) / t.rChunk));
+    for (int i = 0; i < no; ++i) covered[outer[i]] = take(double(f.n[outer[i]]));
+    for (int d = 0; d < t.nC; ++d)
+        covered[d] = d < t.nC - 1 ? double(f.n[d])
+                                  : std::min(double(f.n[d]), double(t.cChunk) * cCount);
+    if (t.flatR) {
+        double left = std::min(double(t.rLast), double(t.rChunk) * rCount);
+        for (int j = 0; j < t.nR; ++j) {
+            const double n = double(f.n[f.p[j]]);
+            covered[f.p[j]] = left >= n ? n : std::max(1.0, left);
+            left = left >= n ? left / n : 1;
+        }
+    } else {
+        for (int j = 0; j < t.nR; ++j)
+            covered[f.p[j]] = j < t.nR - 1 ? double(f.n[f.p[j]])
+                                           : std::min(double(f.n[f.p[j]]),
+                                                      double(t.rChunk) * rCount);
+    }
+    double total = 1;
+    for (int d = 0; d < M; ++d) total *= covered[d];
+    auto block = [&](const int64_t* stride, const int* order) {
+        double blk = 1;
+        int64_t span = 1;  // elements of the contiguous prefix when every index is whole
+        for (int i = 0; i < M; ++i) {
+            const int d = order[i];
+            if (stride[d] != span) break;
+            blk *= covered[d];
+            span *= f.n[d];
+            if (covered[d] < double(f.n[d])) break;
+        }
+        return blk;
+    };
+    int orderA[kMaxDims], orderB[kMaxDims];
+    for (int d = 0; d < M; ++d) orderA[d] = d;
+    for (int k = 0; k < M; ++k) orderB[k] = f.p[k];
+    std::stable_sort(orderA, orderA + M, [&](int x, int y) { return f.sA[x] < f.sA[y]; });
+    std::stable_sort(orderB, orderB + M, [&](int x, int y) { return f.sB[x] < f.sB[y]; });
+    return total / block(f.sA, orderA) + total / block(f.sB, orderB);
+}
+
 bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_options_t& opt,
                 bool alignA, bool alignB, int64_t ldsBudget, int64_t minTile, TileArgs& t,
                 hptt_plan_info_t& info, bool shear = false, bool flat = false) {
@@ -305,12 +396,35 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
         t.gStrideB[g] = flat ? t.rChunk * f.sB[p0] : t.rChunk * f.sB[a];
         t.gChunkR = g++;
     }
-    for (int a = 0; a < M; ++a) {
-        if (inRun[a]) continue;
-        ext[g] = f.n[a];
-        t.gStrideA[g] = f.sA[a];
-        t.gStrideB[g] = f.sB[a];
-        ++g;
+    // Outer digit order: the one whose resident window touches the fewest
+    // regions of A and B (window_regions), A order unless another has at
+    // most 0.8 times as many.
+    int32_t gorder = opt.grid_order;
+    if (gorder == 0) {
+        gorder = 1;
+        int outer[kMaxDims];
+        const int no = outer_indices(f, inRun, 1, outer);
+        const double base = window_regions(f, t, outer, no);
+        double best = base;
+        for (int32_t o = 2; o <= 3; ++o) {
+            outer_indices(f, inRun, o, outer);
+            const double r = window_regions(f, t, outer, no);
+            if (r <= 0.8 * base && r < best) {
+                best = r;
+                gorder = o;
+            }
+        }
+    }
+    {
+        int outer[kMaxDims];
+        const int no = outer_indices(f, inRun, gorder, outer);
+        for (int i = 0; i < no; ++i) {
+            const int a = outer[i];
+            ext[g] = f.n[a];
+            t.gStrideA[g] = f.sA[a];
+            t.gStrideB[g] = f.sB[a];
+            ++g;
+        }
     }
     // LDS pitch: an odd number of elements by default, so the column-wise
     // reads of the store phase spread over the LDS banks.
@@ -369,6 +483,7 @@ bool setup_tile(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_opt
     info.depth = t.nZ;
     t.nG = g;
     set_tile_order(t, opt, g, ext, info);
+    info.grid_order = gorder;
     for (int j = 0; j < g; ++j) {
         if (ext[j] >= (int64_t(1) << 32)) return false;
         set_div(t.gExt[j], ext[j]);
@@ -585,12 +700,18 @@ bool setup_shared(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_o
         t.gStrideB[g] = rChunk * f.sB[lastB];
         t.gChunkR = g++;
     }
-    for (int a = 0; a < M; ++a) {
-        if (inA[a] || inB[a]) continue;
-        ext[g] = f.n[a];
-        t.gStrideA[g] = f.sA[a];
-        t.gStrideB[g] = f.sB[a];
-        ++g;
+    {
+        bool skip[kMaxDims];
+        for (int a = 0; a < M; ++a) skip[a] = inA[a] || inB[a];
+        int outer[kMaxDims];
+        const int no = outer_indices(f, skip, grid_order(opt), outer);
+        for (int i = 0; i < no; ++i) {
+            const int a = outer[i];
+            ext[g] = f.n[a];
+            t.gStrideA[g] = f.sA[a];
+            t.gStrideB[g] = f.sB[a];
+            ++g;
+        }
     }
     t.nZ = 1;
     t.gDepth = -1;
@@ -798,7 +919,8 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
         opt.depth > 4096 || opt.min_tile < 0 || opt.exact_runs < 0 ||
         opt.exact_runs > 1 || (opt.block != 0 && opt.block != kBlock && opt.block != kBigBlock) ||
         opt.skew < 0 || opt.skew > 1024 || opt.shear < 0 || opt.shear > 2 || opt.shared_runs < 0 ||
-        opt.shared_runs > 2 || opt.flat_runs < 0 || opt.flat_runs > 2)
+        opt.shared_runs > 2 || opt.flat_runs < 0 || opt.flat_runs > 2 || opt.grid_order < 0 ||
+        opt.grid_order > 3)
         return HPTT_ERROR_INVALID_ARGUMENT;
 
     const int elem = dtype == HPTT_FLOAT32 ? 4 : 8;
@@ -1213,12 +1335,13 @@ void describe_plan(const hptt_plan_s* p, char* buf, size_t len) {
     snprintf(buf, len,
              "kernel=%s dtype=%s mode=%s fused=(%s) perm=(%s) run_a=%lld run_b=%lld "
              "dims_a=%d dims_b=%d vec=%d/%d pitch=%d rows=%d lds=%d tiles=%lld grid=%lld block=%d "
-             "hints=%d order=%d shear=%d shared=%d flat=%d",
+             "hints=%d order=%d shear=%d shared=%d flat=%d gorder=%d",
              kKernel[in.kernel], p->dtype == HPTT_FLOAT32 ? "f32" : "f64", kMode[in.mode], shape,
              perm, (long long)in.run_a, (long long)in.run_b, in.dims_a, in.dims_b, in.vec_a,
              in.vec_b, in.lds_pitch, in.rows_per_pass, in.lds_bytes, (long long)in.tiles,
              (long long)in.grid,
-             in.block, in.hints, in.tile_order, in.shear, in.shared_runs, in.flat_runs);
+             in.block, in.hints, in.tile_order, in.shear, in.shared_runs, in.flat_runs,
+             in.grid_order);
 }
 
 }  // namespace hptt

@@ -44,7 +44,8 @@ class Options(ctypes.Structure):
                 ("exact_runs", ctypes.c_int32), ("row_passes", ctypes.c_int32),
                 ("depth", ctypes.c_int32), ("min_tile", ctypes.c_int32),
                 ("block", ctypes.c_int32), ("skew", ctypes.c_int32), ("shear", ctypes.c_int32),
-                ("shared_runs", ctypes.c_int32), ("flat_runs", ctypes.c_int32)]
+                ("shared_runs", ctypes.c_int32), ("flat_runs", ctypes.c_int32),
+                ("grid_order", ctypes.c_int32)]
 
 
 class AutotuneReport(ctypes.Structure):
@@ -79,7 +80,7 @@ class PlanInfo(ctypes.Structure):
                 ("hints", ctypes.c_int32), ("mode", ctypes.c_int32),
                 ("tile_order", ctypes.c_int32), ("depth", ctypes.c_int32),
                 ("shear", ctypes.c_int32), ("shared_runs", ctypes.c_int32),
-                ("flat_runs", ctypes.c_int32)]
+                ("flat_runs", ctypes.c_int32), ("grid_order", ctypes.c_int32)]
 
     def as_dict(self) -> dict:
         n = self.ndim
@@ -93,7 +94,8 @@ class PlanInfo(ctypes.Structure):
                 "tiles": self.tiles, "grid": self.grid, "block": self.block,
                 "hints": self.hints, "mode": MODES[self.mode],
                 "tile_order": self.tile_order, "depth": self.depth, "shear": self.shear,
-                "shared_runs": self.shared_runs, "flat_runs": self.flat_runs}
+                "shared_runs": self.shared_runs, "flat_runs": self.flat_runs,
+                "grid_order": self.grid_order}
 
 
 # Every entry point declared in include/hptt.h and include/hptt_yardstick.h.

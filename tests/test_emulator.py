@@ -149,6 +149,10 @@ def test_general_tile_variant_on_every_plan():
     dict(block=1024, tile_order=3),
     dict(skew=3),
     dict(skew=7, tile_order=3),
+    dict(grid_order=1),
+    dict(grid_order=2),
+    dict(grid_order=3),
+    dict(grid_order=3, tile_order=3, max_blocks=11),
 ])
 def test_knobs_match_oracle(knobs):
     rng = np.random.default_rng(11)
@@ -189,10 +193,10 @@ def test_small_workload_matches_oracle(w):
 
 
 @pytest.mark.parametrize("knobs", [dict(), dict(tile_order=1), dict(tile_order=3),
-                                   dict(tile_order=4), dict(block=1024), dict(row_passes=3)],
+                                   dict(tile_order=4), dict(block=1024), dict(row_passes=3),
+                                   dict(grid_order=1), dict(grid_order=3)],
                          ids=["default", "digit_order", "xcd_order", "xcd_digit_order",
-                              "block1024",
-                              "three_passes"])
+                              "block1024", "three_passes", "outer_a_order", "outer_b_order"])
 @pytest.mark.parametrize("w", WORKLOADS, ids=lambda w: w.name)
 def test_full_size_geometry(w, knobs):
     """Dry run of every workgroup of each full-size workload: every offset in

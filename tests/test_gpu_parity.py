@@ -109,7 +109,8 @@ def test_random_sweep():
                                    dict(exact_runs=1, run_a=6, run_b=10),
                                    dict(block=1024), dict(block=1024, run_a=64, run_b=64),
                                    dict(block=1024, max_blocks=5), dict(tile_order=4),
-                                   dict(skew=3), dict(store_hint=2, load_hint=2)],
+                                   dict(skew=3), dict(store_hint=2, load_hint=2),
+                                   dict(grid_order=2), dict(grid_order=3)],
                          ids=lambda k: ",".join(f"{a}={b}" for a, b in k.items()))
 def test_forced_variants(knobs):
     rng = np.random.default_rng(99)

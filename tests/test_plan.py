@@ -107,19 +107,24 @@ EXPECTED = {
     "transpose3d_48x40x32_f32": dict(kernel="tile", size=(1920, 32), perm=(1, 0), run_a=32,
                                      run_b=32, tiles=60),
     "transpose2d_8192x8192_f32": dict(kernel="tile", size=(8192, 8192), perm=(1, 0), run_a=128,
-                                      run_b=32, tiles=16384, tile_order=2, hints=3),
+                                      run_b=32, tiles=16384, tile_order=2, hints=3,
+                                      grid_order=1),
     # flat B runs: one line cut from the 20 x 16 = 320 flattened B positions
     # (10 chunks), A runs of 24 x 4 = 96 elements (3 lines)
     "transpose6d_24x20x16x24x18x20_f32": dict(kernel="tile", size=(24, 20, 16, 24, 18, 20),
                                               perm=(5, 2, 0, 4, 1, 3), run_a=96, run_b=32,
                                               dims_a=2, dims_b=2, tiles=21600, hints=3,
-                                              rows_per_pass=32, flat_runs=2),
+                                              rows_per_pass=32, flat_runs=2,
+                                              # outer digits by the sum of their strides: A4
+                                              # (B-adjacent) before A3 (A-adjacent)
+                                              grid_order=2),
     "transpose4d_96x96x96x96_keep1_f64": dict(kernel="stream", size=(96, 96, 96, 96),
                                               perm=(0, 3, 2, 1), run_b=96, vec_a=2, vec_b=2),
     # beta != 0: A-run target of 256 bytes, met by 3 x 2 x 16 = 96 elements (384 B)
     "transpose5d_3x2x640x480x96_f32": dict(kernel="tile", size=(3, 2, 640, 480, 96),
                                            perm=(4, 2, 0, 3, 1), run_a=96, run_b=32, dims_a=3,
-                                           dims_b=1, tiles=57600, hints=3, depth=1),
+                                           dims_b=1, tiles=57600, hints=3, depth=1,
+                                           grid_order=1),
 }
 
 
@@ -388,3 +393,24 @@ def test_flat_b_runs_rule():
     assert big.info["flat_runs"] == 0
     small = hptt.create_plan((1, 3, 0, 2), (24, 20, 7, 3000), 1.0, 0.0, "f32", flat_runs=1)
     assert small.info["flat_runs"] == 2
+
+
+@pytest.mark.parametrize("size_a,perm,want", [
+    # the window of resident tiles touches far fewer B regions with A4 first
+    ((24, 20, 16, 24, 18, 20), (5, 2, 0, 4, 1, 3), 2),
+    # B order: A0 (outer, B-adjacent) before A2
+    ((427, 110, 3, 355), (3, 2, 1, 0), 3),
+    # 10-element A runs: A order keeps A3 (A-adjacent) first
+    ((2, 5, 9, 15, 220, 168), (2, 4, 1, 0, 5, 3), 1),
+    ((6, 5126, 2, 3, 7, 39), (5, 1, 2, 4, 0, 3), 1),
+    ((8192, 8192), (1, 0), 1),
+])
+def test_grid_order_choice(size_a, perm, want):
+    """The quick path orders the outer grid digits by the regions of A and B
+    a window of resident tiles touches (A order unless another order has at
+    most 0.8 times as many); forced orders are kept."""
+    assert hptt.create_plan(perm, size_a).info["grid_order"] == want
+    for forced in (1, 2, 3):
+        assert hptt.create_plan(perm, size_a, grid_order=forced).info["grid_order"] == forced
+    with pytest.raises(hptt.HpttError):
+        hptt.create_plan(perm, size_a, grid_order=4)
