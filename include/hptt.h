@@ -187,6 +187,9 @@ typedef struct {
  *          bit-exact copy; alpha == 0 is not short-cut (A is still read).
  *   dtype  element type of A and B.
  * Makes no HIP call.  Errors: HPTT_ERROR_INVALID_ARGUMENT, HPTT_ERROR_OUT_OF_MEMORY.
+ * With the environment variable HPTT_LOG set to anything but "" or "0", every
+ * plan this or any other plan call creates prints one line to stderr,
+ * "[hptt] plan: " followed by hptt_describe_plan's text.
  */
 hptt_status_t hptt_create_plan(hptt_plan_t *plan, const int32_t *perm, int32_t N,
                                const int64_t *sizeA, double alpha, double beta,

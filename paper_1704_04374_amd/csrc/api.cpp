@@ -1,6 +1,10 @@
 // Host half of the C ABI: plan creation, inspection and destruction.  None of
-// these functions makes a HIP call; hptt_exec lives in kernels.hip.
+// these functions makes a HIP call; hptt_exec lives in kernels.hip.  With the
+// environment variable HPTT_LOG set (and not "0"), every plan created prints
+// its description to stderr.
 #include <new>
+#include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include "plan.h"
@@ -22,6 +26,13 @@ hptt_status_t hptt_create_plan_outer(hptt_plan_t* plan, const int32_t* perm, int
         return st;
     }
     *plan = p;
+    // HPTT_LOG=1: one line per new plan on stderr (fused shape, kernel, tile, grid)
+    const char* log = getenv("HPTT_LOG");
+    if (log && log[0] && strcmp(log, "0") != 0) {
+        char desc[512];
+        hptt::describe_plan(p, desc, sizeof(desc));
+        fprintf(stderr, "[hptt] plan: %s\n", desc);
+    }
     return HPTT_SUCCESS;
 }
 

@@ -414,3 +414,24 @@ def test_grid_order_choice(size_a, perm, want):
         assert hptt.create_plan(perm, size_a, grid_order=forced).info["grid_order"] == forced
     with pytest.raises(hptt.HpttError):
         hptt.create_plan(perm, size_a, grid_order=4)
+
+
+def test_hptt_log_prints_each_plan():
+    """HPTT_LOG=1 prints every new plan (fused shape, kernel, tile, grid) to
+    stderr; unset or "0" prints nothing."""
+    import subprocess
+    import sys
+    code = ("from paper_1704_04374_amd import hptt; "
+            "hptt.create_plan((1, 0), (64, 32)); hptt.create_plan((2, 0, 1), (48, 40, 32))")
+    for val, lines in (("1", 2), ("0", 0), (None, 0)):
+        env = {k: v for k, v in os.environ.items() if k != "HPTT_LOG"}
+        if val is not None:
+            env["HPTT_LOG"] = val
+        r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True,
+                           text=True, timeout=120)
+        assert r.returncode == 0, r.stderr
+        got = [ln for ln in r.stderr.splitlines() if ln.startswith("[hptt] plan: ")]
+        assert len(got) == lines, r.stderr
+        if lines:
+            assert "fused=(64,32) perm=(1,0)" in got[0] and "kernel=tile" in got[0]
+            assert "fused=(1920,32) perm=(1,0)" in got[1]
