@@ -498,3 +498,53 @@ def test_sub_tensor_workload_full_size(w):
     inside[ob:] = ~np.isnan(want[ob:])
     assert np.isnan(got[~inside]).all() and not np.isnan(got[inside]).any()
     assert inside.sum() == w.numel
+
+
+# --------------------------------------------------------------------------
+# Beyond 32-bit element counts, and ranks up to 16
+# --------------------------------------------------------------------------
+
+def test_above_2_31_elements():
+    """A 46341 x 46341 fp32 transposition (2,147,488,281 elements, 8.6 GB per
+    tensor): the tile kernel's 64-bit offset variant.  With alpha = 1.5,
+    beta = -0.5 on a random prior B, then alpha = 1, beta = 0 on a NaN-filled
+    B: sampled elements (the first and last included) against the oracle
+    computed one by one, and no NaN left anywhere in B."""
+    size, perm = (46341, 46341), (1, 0)
+    n = size[0] * size[1]
+    _say(f"[parity] {size} perm {perm}: {n} elements")
+    g = torch.Generator(device="cuda").manual_seed(31)
+    dA = torch.rand(n, device="cuda", generator=g) * 2 - 1
+    dB = torch.rand(n, device="cuda", generator=g) * 2 - 1
+    hA, hB0 = dA.cpu().numpy(), dB.cpu().numpy()
+    rng = np.random.default_rng(31)
+    offs = np.concatenate([[0, 1, n - 2, n - 1, 2 ** 31 - 1, 2 ** 31, 2 ** 31 + 1],
+                           rng.integers(0, n, 6000)])
+    toffs = torch.from_numpy(offs).cuda()
+    for alpha, beta in ((1.5, -0.5), (1.0, 0.0)):
+        p = hptt.create_plan(perm, size, alpha, beta, "f32")
+        if beta == 0:
+            dB.fill_(float("nan"))
+        p.exec(dA, dB)
+        torch.cuda.synchronize()
+        got = dB[toffs].cpu().numpy()
+        want = orc.sample(hA, size, perm, alpha, beta, hB0 if beta != 0 else None, offs)
+        assert got.tobytes() == want.tobytes(), p.describe()
+        assert not bool(torch.isnan(dB).any()), p.describe()
+    del dA, dB
+
+
+def test_high_ranks():
+    """Ranks 7 to 16 (extents 2 and 3, fusion and dropped extent-1 indices
+    included), both dtypes, whole results against the oracle."""
+    rng = np.random.default_rng(16)
+    for n in range(7, 17):
+        for it in range(3):
+            size = [int(x) for x in rng.choice([1, 2, 2, 3], size=n)]
+            while int(np.prod(size)) > (1 << 17):
+                size[int(rng.integers(0, n))] = 2
+            perm = tuple(int(x) for x in rng.permutation(n))
+            dtype = ("f32", "f64")[it % 2]
+            alpha, beta = ((1.0, 0.0), (-0.375, 1.25), (2.0, 0.5))[it]
+            p = _run_case(tuple(size), perm, alpha, beta, dtype, rng)
+            assert p.info["numel"] == int(np.prod(size))
