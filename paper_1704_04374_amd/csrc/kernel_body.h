@@ -750,6 +750,67 @@ __host__ __device__ inline void stream_items(const StreamArgs& g, uint32_t first
     }
 }
 
+// Kernel S over more than 2^32 items at width V (StreamArgs::numItems[log2 V]
+// is 0): the rows are cut into slabs, launched one by one.  A slab holds the
+// rows of the outer B positions 0..m-1 whole and a chunk of `chunk` values of
+// position m (the most rows whose items the kernel can still count); the
+// slowest positions m+1.. and the chunk number give the slab's base offsets.
+// The launch sees nO = m + 1 positions; position m's local value stays below
+// its extent, so its split leaves it whole.
+struct StreamSlabs {
+    int m;           // first outer position not whole in a slab (nO: none)
+    int64_t chunk;   // values of position m per slab
+    int64_t rows;    // rows of a full slab
+    int64_t count;   // slabs
+};
+
+inline StreamSlabs stream_slabs_of(const StreamArgs& g, int V) {
+    const int64_t limit = (int64_t(1) << 32) - int64_t(kBlock) * kMaxItems;
+    const int64_t W = g.W[log2_width(V)].d;
+    StreamSlabs s;
+    s.m = 0;
+    s.rows = 1;
+    while (s.m < g.nO && s.rows * int64_t(g.oExt[s.m].d) * W < limit) s.rows *= g.oExt[s.m++].d;
+    s.chunk = 1;
+    s.count = 1;
+    if (s.m < g.nO) {
+        const int64_t e = g.oExt[s.m].d;
+        s.chunk = (limit - 1) / (s.rows * W);  // >= 1: a row's vectors fit (plan builder)
+        if (s.chunk > e) s.chunk = e;
+        s.count = (e + s.chunk - 1) / s.chunk;
+        for (int k = s.m + 1; k < g.nO; ++k) s.count *= g.oExt[k].d;
+        s.rows *= s.chunk;
+    }
+    return s;
+}
+
+// Arguments and base offsets of slab `sl` (0 <= sl < s.count).
+inline StreamArgs stream_slab_args(const StreamArgs& g, const StreamSlabs& s, int64_t sl, int V,
+                                   int64_t* offA, int64_t* offB) {
+    StreamArgs a = g;
+    *offA = *offB = 0;
+    int64_t rows = s.rows;
+    if (s.m < g.nO) {
+        const int64_t e = g.oExt[s.m].d, nChunks = (e + s.chunk - 1) / s.chunk;
+        const int64_t c = sl % nChunks;
+        int64_t x = sl / nChunks;
+        *offA += c * s.chunk * g.oStrideA[s.m];
+        *offB += c * s.chunk * g.oStrideB[s.m];
+        const int64_t here = imin(s.chunk, e - c * s.chunk);
+        rows = rows / s.chunk * here;
+        for (int k = s.m + 1; k < g.nO; ++k) {
+            const int64_t ek = g.oExt[k].d, j = x % ek;
+            x /= ek;
+            *offA += j * g.oStrideA[k];
+            *offB += j * g.oStrideB[k];
+        }
+        a.nO = s.m + 1;
+    }
+    a.numRows = rows;
+    a.numItems[log2_width(V)] = uint32_t(rows * int64_t(g.W[log2_width(V)].d));
+    return a;
+}
+
 // A offset of row r of the stride-1-kept walk (rows in B order).
 __host__ __device__ inline int64_t stream_row_a(const StreamArgs& g, uint32_t r) {
     int64_t a = 0;

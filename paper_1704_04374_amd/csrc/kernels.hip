@@ -130,6 +130,31 @@ int aligned_width(int v, uintptr_t ptr, int elem) {
     return v;
 }
 
+// Kernel S over more than 2^32 items at width v: one launch per slab
+// (stream_slabs_of), each with the slab's base pointers and arguments.
+template <typename T>
+hptt_status_t stream_slabs(const hptt_plan_s* p, const void* fn, const T* A, T* B, int v,
+                           T alpha, T beta, hipStream_t stream) {
+    const StreamSlabs s = stream_slabs_of(p->stream, v);
+    const int64_t per = int64_t(kBlock) * items_per_lane(int(sizeof(T)), v);
+    for (int64_t sl = 0; sl < s.count; ++sl) {
+        int64_t offA = 0, offB = 0;
+        StreamArgs sa = stream_slab_args(p->stream, s, sl, v, &offA, &offB);
+        int64_t grid = (int64_t(sa.numItems[log2_width(v)]) + per - 1) / per;
+        if (grid > p->info.grid) grid = p->info.grid;
+        const T* a = A + offA;
+        T* b = B + offB;
+        void* args[5] = {&a, &b, &sa, &alpha, &beta};
+        const hipError_t err =
+            hipLaunchKernel(fn, dim3(uint32_t(grid)), dim3(kBlock), args, 0, stream);
+        if (err != hipSuccess) {
+            g_last_hip_error = int32_t(err);
+            return HPTT_ERROR_HIP;
+        }
+    }
+    return HPTT_SUCCESS;
+}
+
 template <typename T>
 hptt_status_t launch(const hptt_plan_s* p, const void* A, void* B, hipStream_t stream) {
     const hptt_plan_info_t& in = p->info;
@@ -178,6 +203,12 @@ hptt_status_t launch(const hptt_plan_s* p, const void* A, void* B, hipStream_t s
             lds = size_t(in.lds_bytes);
             break;
         case HPTT_KERNEL_STREAM:
+            if (!p->stream.flatB) {
+                // the width the row walk launches with (as select() picks it)
+                const int v = va >= vb ? vb : va;
+                if (p->stream.numItems[log2_width(v)] == 0)
+                    return stream_slabs<T>(p, fn, a, b, v, alpha, beta, stream);
+            }
             args[2] = const_cast<StreamArgs*>(&p->stream);
             lds = size_t(in.lds_bytes);
             break;

@@ -847,16 +847,23 @@ bool setup_stream(const Fused& f, int elem, const hptt_options_t& opt, StreamArg
         info.flat_runs = 1;
         return true;
     }
+    // The kernel splits item and row numbers as 32-bit numbers.  Every outer
+    // extent, and a row's vectors, must fit; a width whose items do not fit
+    // in all keeps numItems 0, and hptt_exec launches it per slab of the
+    // slowest B positions (stream_slabs), each slab's items below the limit.
+    for (int k = 1; k < f.M; ++k)
+        if (f.n[f.p[k]] >= (int64_t(1) << 32)) return false;
+    const int64_t limit = (int64_t(1) << 32) - int64_t(kBlock) * kMaxItems;
     for (int w = 0; w < 3; ++w) {  // every width hptt_exec may launch with
         const int64_t W = (s.rowLen + (1 << w) - 1) >> w;
+        if (W >= limit) return false;
         const int64_t items = rows * W;
-        if (items >= (int64_t(1) << 32) - int64_t(kBlock) * kMaxItems) return false;
         set_div(s.W[w], W);
-        s.numItems[w] = uint32_t(items);
+        s.numItems[w] = items < limit ? uint32_t(items) : 0;
     }
     info.vec_a = info.vec_b = v;
     info.run_b = s.rowLen;
-    info.tiles = s.numItems[v >= 4 ? 2 : v >= 2 ? 1 : 0];
+    info.tiles = rows * ((s.rowLen + v - 1) / v);
     return true;
 }
 
@@ -1277,7 +1284,8 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
             k = HPTT_KERNEL_GENERIC;
         } else {
             const int64_t per = int64_t(kBlock) * items_per_lane(elem, info.vec_a);
-            const int64_t grid = (info.tiles + per - 1) / per;
+            int64_t grid = (info.tiles + per - 1) / per;
+            if (grid > (int64_t(1) << 30)) grid = int64_t(1) << 30;
             info.grid = grid < maxBlocks ? grid : maxBlocks;
         }
     }

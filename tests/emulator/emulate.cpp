@@ -254,12 +254,11 @@ void emu_tile(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
 
 // Mirrors stream_kernel in kernels.hip.
 template <typename T, int V, int MODE, int NT>
-void emu_stream(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
+void emu_stream_launch(const hptt::StreamArgs& g, uint64_t grid, const T* A, T* B, T alpha,
+                       T beta, int64_t blockStride) {
     using namespace hptt;
-    const StreamArgs& g = p->stream;
-    const T alpha = T(p->alpha), beta = T(p->beta);
     const uint64_t per = uint64_t(kBlock) * items_per_lane(int(sizeof(T)), V);
-    const uint64_t grid = uint64_t(p->info.grid), step = grid * per;
+    const uint64_t step = grid * per;
     for (uint64_t blk = 0; blk < grid && S->errors == 0; blk += uint64_t(blockStride))
         for (uint64_t first = blk * per;
              first < g.numItems[log2_width(V)] && S->errors == 0; first += step)
@@ -270,6 +269,30 @@ void emu_stream(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
                 else
                     stream_items<HostMem, T, V, MODE, NT>(g, uint32_t(first), tid, A, B, alpha, beta);
             }
+}
+
+// Mirrors stream_kernel in kernels.hip, launched once, or once per slab
+// (stream_slabs in kernels.hip) when its items exceed 32 bits.
+template <typename T, int V, int MODE, int NT>
+void emu_stream(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
+    using namespace hptt;
+    const StreamArgs& g = p->stream;
+    const T alpha = T(p->alpha), beta = T(p->beta);
+    if (g.flatB || g.numItems[log2_width(V)] != 0) {
+        emu_stream_launch<T, V, MODE, NT>(g, uint64_t(p->info.grid), A, B, alpha, beta,
+                                          blockStride);
+        return;
+    }
+    const StreamSlabs s = stream_slabs_of(g, V);
+    const int64_t per = int64_t(kBlock) * items_per_lane(int(sizeof(T)), V);
+    for (int64_t sl = 0; sl < s.count && S->errors == 0; ++sl) {
+        int64_t offA = 0, offB = 0;
+        const StreamArgs sa = stream_slab_args(g, s, sl, V, &offA, &offB);
+        int64_t grid = (int64_t(sa.numItems[log2_width(V)]) + per - 1) / per;
+        if (grid > p->info.grid) grid = p->info.grid;
+        emu_stream_launch<T, V, MODE, NT>(sa, uint64_t(grid), A + offA, B + offB, alpha, beta,
+                                          blockStride);
+    }
 }
 
 // Mirrors axpby_kernel and generic_kernel in kernels.hip.

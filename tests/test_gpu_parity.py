@@ -548,3 +548,38 @@ def test_high_ranks():
             alpha, beta = ((1.0, 0.0), (-0.375, 1.25), (2.0, 0.5))[it]
             p = _run_case(tuple(size), perm, alpha, beta, dtype, rng)
             assert p.info["numel"] == int(np.prod(size))
+
+
+def test_stream_slabs_above_2_32_items():
+    """The stride-1-kept walk with more than 2^32 vectors: 64 x 4096 x 16385
+    fp32 (2^32 + 2^18 elements, 17 GB per tensor) on pointers one element off
+    the 16-byte grid, so hptt_exec narrows to 1-element vectors and launches
+    per slab of the slowest B index.  alpha = -0.5, beta = 1 on a random prior
+    B, then alpha = 1, beta = 0 on a NaN-filled B: sampled elements (slab
+    edges included) against the oracle computed one by one, no NaN left."""
+    size, perm = (64, 4096, 16385), (0, 2, 1)
+    n = size[0] * size[1] * size[2]
+    _say(f"[parity] {size} perm {perm}: {n} elements, pointers off the vector grid")
+    g = torch.Generator(device="cuda").manual_seed(32)
+    PA = torch.rand(n + 1, device="cuda", generator=g) * 2 - 1
+    PB = torch.rand(n + 1, device="cuda", generator=g) * 2 - 1
+    dA, dB = PA[1:], PB[1:]
+    hA, hB0 = dA.cpu().numpy(), dB.cpu().numpy()
+    rng = np.random.default_rng(32)
+    rowsB = size[2] * 64                          # B elements per value of the slowest index
+    edges = [0, n - 1, 2 ** 32 - 1, 2 ** 32, 4095 * rowsB - 1, 4095 * rowsB]
+    offs = np.concatenate([edges, rng.integers(0, n, 6000)])
+    toffs = torch.from_numpy(offs).cuda()
+    for alpha, beta in ((-0.5, 1.0), (1.0, 0.0)):
+        p = hptt.create_plan(perm, size, alpha, beta, "f32")
+        assert p.info["kernel"] == "stream"
+        if beta == 0:
+            dB.fill_(float("nan"))
+        p.exec(dA, dB)
+        torch.cuda.synchronize()
+        got = dB[toffs].cpu().numpy()
+        want = orc.sample(hA, size, perm, alpha, beta, hB0 if beta != 0 else None, offs)
+        assert got.tobytes() == want.tobytes(), p.describe()
+        assert not bool(torch.isnan(dB).any()), p.describe()
+    assert float(PB[0]) == float(PB[0])           # the element before B is untouched (not NaN)
+    del PA, PB, dA, dB

@@ -34,7 +34,7 @@ def test_tile_just_above_2_31_elements_covers_b_once():
     ((65537, 65537), (1, 0), "f32", "tile"),
     ((3, 65537, 21846), (0, 2, 1), "f32", "tile"),
     ((2, 2147483649), (1, 0), "f32", "tile"),
-    ((64, 1024, 256, 257), (0, 2, 1, 3), "f32", None),
+    ((64, 1024, 256, 257), (0, 2, 1, 3), "f32", "stream"),
     ((4294971392,), (0,), "f32", "axpby"),
     ((32768, 65537, 2), (1, 0, 2), "f64", None),
 ], ids=lambda x: "x".join(map(str, x)) if isinstance(x, tuple) else str(x))
@@ -50,3 +50,23 @@ def test_above_2_32_elements_in_bounds(size, perm, dtype, kernel, beta):
     for stride in (max(1, grid // 1500), max(1, grid - 1)):
         err, msg, _ = emu.run(p, block_stride=stride)
         assert err == 0, f"{p.describe()} (workgroup stride {stride}): {msg}"
+
+
+@pytest.mark.parametrize("va", [1, 2])
+def test_stream_slabs_beyond_2_32_items(va):
+    """The stride-1-kept walk at a width whose items exceed 32 bits (here the
+    widths a misaligned pointer narrows to) launches once per slab of the
+    slowest B positions: a 64 x 4096 x 16385 fp32 problem (2^32 + 2^18
+    elements) at 1-element vectors covered whole, every B element written
+    exactly once; at 2-element vectors on a stride of workgroups."""
+    size, perm = (64, 4096, 16385), (0, 2, 1)
+    p = emu.plan(perm, size, 1.0, 0.0, "f32")
+    assert p.info["kernel"] == "stream" and p.info["vec_a"] == 4
+    if va == 1:
+        err, msg, cnt = emu.run(p, va=1, vb=1, counts=True, mis_a=1, mis_b=1)
+        assert err == 0, msg
+        assert cnt.min() == 1 and cnt.max() == 1
+    else:
+        for stride in (997, max(1, p.info["grid"] - 1)):
+            err, msg, _ = emu.run(p, va=2, vb=2, block_stride=stride, mis_a=2, mis_b=2)
+            assert err == 0, msg

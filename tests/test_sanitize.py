@@ -40,7 +40,7 @@ def _build() -> str:
     os.makedirs(BUILD, exist_ok=True)
     # host code only: -Xarch_host applies each sanitizer flag to the host pass
     san = ["-Xarch_host", "-fsanitize=address,undefined",
-           "-Xarch_host", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer", "-g", "-O1"]
+           "-Xarch_host", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer", "-g1", "-O0"]
     oracle_src = os.path.join(ROOT, "oracle", "oracle.c")
     jobs = [(oracle_src, [CLANG, "-x", "c", "-std=c99", "-ffp-contract=off", *san])]
     for src in (os.path.join(TESTS, "sanitize", "host_check.cpp"),
