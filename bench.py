@@ -215,7 +215,7 @@ def measure_workload(torch, hptt, w, steps, warmup, reps, flush_buf, sink, full:
     Bs = [x[w.offset_b:] for x in PB]
     t0 = time.perf_counter()
     plan = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype, outer_size_a=w.outer_a,
-                            outer_size_b=w.outer_b)
+                            outer_size_b=w.outer_b, **dict(w.knobs))
     plan_us = (time.perf_counter() - t0) * 1e6
     moved = w.moved_bytes
     S = w.tensor_bytes
@@ -390,7 +390,8 @@ def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, command: str, o
         return names[0], statistics.median(vals)
 
     from paper_1704_04374_amd import hptt
-    cls = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype).info["kernel"]
+    cls = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype,
+                           **dict(w.knobs)).info["kernel"]
     tk, tf = pick(fetch, kernel_label(cls))
     _, tw = pick(write, tk.split("(")[0])
     _, cf = pick(fetch, "copy_kernel")
@@ -422,6 +423,40 @@ def summarize_pmc(fetch_dir: str, write_dir: str, workload: str, command: str, o
         f"traffic_over_algorithmic: {(fetch_b + write_b) / w.moved_bytes:.4f}",
         f"kernel_source_hash: {kernel_source_hash()}",
     ]
+    with open(out_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def summarize_counters(dirs, workload: str, command: str, out_path: str):
+    """Turn rocprofv3 --pmc runs (one per counter group) into a committed
+    summary: the median per dispatch of every counter collected, for the
+    workload's transposition kernel and for the same-run copy yardstick."""
+    import csv
+
+    from paper_1704_04374_amd.workloads import BY_NAME
+    w = BY_NAME[workload]
+    acc = {}
+    for d in dirs:
+        for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(path) as f:
+                for r in csv.DictReader(f):
+                    name = r["Kernel_Name"]
+                    kind = ("transposition" if ("tile_kernel" in name or "stream_kernel" in name
+                                                or "axpby_kernel<" in name)
+                            else "copy" if "copy_kernel" in name else None)
+                    if kind:
+                        acc.setdefault((kind, r["Counter_Name"]), []).append(
+                            float(r["Counter_Value"]))
+    if not acc:
+        raise SystemExit("no transposition or copy dispatches in the counter files")
+    lines = [f"# rocprofv3 counters, workload {w.describe()}",
+             f"# command (one run per counter group): {command}",
+             f"# algorithmic bytes per transposition (Eq. 2, lambda*S): {w.moved_bytes}",
+             "# kernel | counter | median per dispatch | dispatches"]
+    for (kind, counter), vals in sorted(acc.items()):
+        lines.append(f"{kind} | {counter} | {statistics.median(vals):.1f} | {len(vals)}")
+    lines.append(f"kernel_source_hash: {kernel_source_hash()}")
     with open(out_path, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
@@ -628,16 +663,18 @@ def main():
                     help="time the contraction workloads against torch.einsum instead")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     ap.add_argument("--summarize-trace", metavar="TRACE_DIR")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="PMC_DIR")
     ap.add_argument("--pmc-command", default="")
     ap.add_argument("--pmc-out", default="")
     args = ap.parse_args()
 
-    if args.summarize_pmc or args.summarize_trace:
+    if args.summarize_pmc or args.summarize_trace or args.summarize_counters:
         from paper_1704_04374_amd.workloads import BY_NAME as _W
         _w = _W[args.workload]
         import ctypes  # noqa: F401  (plan creation needs only the host half of the library)
         from paper_1704_04374_amd import hptt as _h
-        _cls = _h.create_plan(_w.perm, _w.size_a, _w.alpha, _w.beta, _w.dtype).info["kernel"]
+        _cls = _h.create_plan(_w.perm, _w.size_a, _w.alpha, _w.beta, _w.dtype,
+                              **dict(_w.knobs)).info["kernel"]
     if args.summarize_pmc:
         out = args.pmc_out or profile_path(_cls, args.workload, "pmc")
         summarize_pmc(*args.summarize_pmc, args.workload, args.pmc_command, out)
@@ -645,6 +682,10 @@ def main():
     if args.summarize_trace:
         out = args.pmc_out or profile_path(_cls, args.workload, "trace")
         summarize_trace(args.summarize_trace, args.workload, args.pmc_command, out)
+        return 0
+    if args.summarize_counters:
+        out = args.pmc_out or profile_path(_cls, args.workload, "counters")
+        summarize_counters(args.summarize_counters, args.workload, args.pmc_command, out)
         return 0
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this transposition library has no multi-GPU "

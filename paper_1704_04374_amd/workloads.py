@@ -36,6 +36,9 @@ class Workload:
     outer_b: tuple | None = None
     start_a: tuple | None = None
     start_b: tuple | None = None
+    # plan options ((name, value), ...) the benchmark builds the plan with;
+    # () = the quick path's own choices (every benchmark workload)
+    knobs: tuple = ()
 
     @property
     def numel(self) -> int:
@@ -111,7 +114,17 @@ SUBTENSOR_WORKLOADS = [
              None, outer_b=(8192, 8192), start_b=(0, 2048)),
 ]
 
-BY_NAME = {w.name: w for w in WORKLOADS + SUBTENSOR_WORKLOADS}
+# Diagnostic workload for profiling, not a benchmark line: the 6-D fp32
+# workload with its A2 and A5 indices merged into one, so that the 32 rows of
+# each 96 x 32 flat tile lie in one plane of A instead of up to 20 planes 13 MB
+# apart (same extents, tile shape, bytes and kernel; A(24, 20, 320, 24, 18),
+# perm [2, 0, 4, 1, 3]).
+DIAGNOSTIC_WORKLOADS = [
+    Workload("oneplane6d_24x20x320x24x18_f32", "f32", (24, 20, 320, 24, 18), (2, 0, 4, 1, 3),
+             1.5, 0.0, 2, None, knobs=(("run_a", 96), ("run_b", 32))),
+]
+
+BY_NAME = {w.name: w for w in WORKLOADS + SUBTENSOR_WORKLOADS + DIAGNOSTIC_WORKLOADS}
 
 
 def _fortran_offset(index, outer) -> int:
