@@ -125,13 +125,17 @@ struct TileArgs {
     // A run; its store phase writes nColS columns, one per value of the A-run
     // indices outside the B run (C, A order, digits cExt / cStrideB), each the
     // whole B run, reading B-run position b of column c from LDS at
-    // ldsRow[b] + ldsCol[c].  ldsCol sums cLds (a C index's position weight
-    // in the A run); ldsRow decodes b over the B-run digits oExt (B order)
-    // with weights oLds (an S index's position weight in the A run, or pitch
-    // times an R index's weight among the rows).  cInnerS / rInnerL: the C
+    // pos(b) + ldsCol[c].  ldsCol sums cLds (a C index's position weight in
+    // the A run); pos decodes b over the B-run digits oExt (B order) with
+    // weights oLds (an S index's position weight in the A run, or pitch times
+    // an R index's weight among the rows): from an LDS table ldsRow built
+    // once per workgroup when posTable = 1 (many columns share it), else
+    // computed per vector (a table as long as the B run would take as much
+    // LDS as the tile's own data).  cInnerS / rInnerL: the C
     // columns / R rows before the chunked A-run / B-run index when that index
     // is in C / R, else 0 (every column / row of a tile exists).
     int32_t shared;
+    int32_t posTable;
     int32_t nColS;
     int32_t nO;
     int32_t cInnerS;

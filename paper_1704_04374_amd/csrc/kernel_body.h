@@ -171,20 +171,53 @@ __host__ __device__ inline void tile_rows_flat(const TileArgs& g, const TileBase
 }
 
 // LDS layout of the shared-run variant, in 64-bit words: rowOffA
-// (subRows), colOffB (nColS), then the 32-bit ldsRow (runB) and ldsCol
-// (nColS), then the subRows rows of the tile.
+// (subRows), colOffB (nColS), then the 32-bit ldsCol (nColS) and, with
+// posTable, ldsRow (runB), then the subRows rows of the tile.
 __host__ __device__ inline int64_t shared_table_words(const TileArgs& g) {
-    return int64_t(g.subRows) + g.nColS + (g.runB + g.nColS + 1) / 2;
+    return int64_t(g.subRows) + g.nColS + (g.nColS + (g.posTable ? g.runB : 0) + 1) / 2;
+}
+
+// LDS offset, in column 0, of B-run position b of a shared-run tile: b split
+// over the B-run digits oExt (B order), each digit weighted by oLds.  d0
+// returns b's first digit.
+__host__ __device__ inline int32_t shared_pos(const TileArgs& g, uint32_t b, uint32_t& d0) {
+    int32_t off = 0;
+    d0 = 0;
+    for (int k = 0; k < g.nO; ++k) {
+        const uint32_t q = fast_div(b, g.oExt[k]);
+        const uint32_t d = b - q * g.oExt[k].d;
+        if (k == 0) d0 = d;
+        off += int32_t(d) * g.oLds[k];
+        b = q;
+    }
+    return off;
+}
+
+// LDS offsets (column 0) of B-run positions ss .. ss + V - 1 that lie in
+// [0, rows): from the table ldsRow, or each split on its own (a step of the
+// first digit with a split only where it wraps measured no better: the wrap
+// branch diverges across lanes).
+template <class Mem, int V>
+__host__ __device__ inline void shared_positions(const TileArgs& g, const int32_t* ldsRow, int ss,
+                                                 int rows, int32_t* pos) {
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+        if (ss + e < 0 || ss + e >= rows) continue;
+        uint32_t d0;
+        pos[e] = g.posTable ? Mem::template lds_ld<int32_t>(ldsRow, ss + e)
+                            : shared_pos(g, uint32_t(ss + e), d0);
+    }
 }
 
 // Tables of the shared-run variant, shared by every tile of the launch:
 // rowOffA[r] = A offset of load row r (the R digits), colOffB[c] = B offset
 // of store column c (the C digits), ldsCol[c] = its position in the A run,
-// and ldsRow[b] = the LDS offset of B-run position b in column 0.
+// and with posTable ldsRow[b] = the LDS offset of B-run position b in
+// column 0.
 template <class Mem, int BLOCK = kBlock>
 __host__ __device__ inline void tile_tables_shared(const TileArgs& g, int tid, int64_t* rowOffA,
-                                                    int64_t* colOffB, int32_t* ldsRow,
-                                                    int32_t* ldsCol) {
+                                                    int64_t* colOffB, int32_t* ldsCol,
+                                                    int32_t* ldsRow) {
     for (int64_t r = tid; r < g.subRows; r += BLOCK) {
         uint32_t x = uint32_t(r);
         int64_t off = 0;
@@ -209,16 +242,11 @@ __host__ __device__ inline void tile_tables_shared(const TileArgs& g, int tid, i
         Mem::template lds_st<int64_t>(colOffB, c, offB);
         Mem::template lds_st<int32_t>(ldsCol, c, offL);
     }
-    for (int64_t b = tid; b < g.runB; b += BLOCK) {
-        uint32_t x = uint32_t(b);
-        int32_t off = 0;
-        for (int k = 0; k < g.nO; ++k) {
-            const uint32_t q = fast_div(x, g.oExt[k]);
-            off += int32_t(x - q * g.oExt[k].d) * g.oLds[k];
-            x = q;
+    if (g.posTable)
+        for (int64_t b = tid; b < g.runB; b += BLOCK) {
+            uint32_t d0;
+            Mem::template lds_st<int32_t>(ldsRow, b, shared_pos(g, uint32_t(b), d0));
         }
-        Mem::template lds_st<int32_t>(ldsRow, b, off);
-    }
 }
 
 // Vectors a lane loads before the first of them is written to LDS (4, 8 and
@@ -413,14 +441,14 @@ __host__ __device__ inline void tile_store_fast(const TileArgs& g, const TileBas
 
 // Store phase of the shared-run variant (its load phase is
 // tile_load_fast's, shifted): column q is the contiguous B run
-// colOffB[q] + [0, runB), whose position b sits in LDS at ldsRow[b] +
-// ldsCol[q].  A run that starts off the B vector grid is shifted onto it,
+// colOffB[q] + [0, runB), whose position b sits in LDS at pos(b) + ldsCol[q]
+// (shared_positions).  A run that starts off the B vector grid is shifted onto it,
 // its first and last vectors partial.  Same thread-to-vector map and
 // batching as tile_store_fast.
 template <class Mem, typename T, int VB, int MODE, int HINT, int BLOCK>
 __host__ __device__ inline void tile_store_shared(const TileArgs& g, const TileBase& tb, int tid,
                                                   T* B, const T* lds, const int64_t* colOffB,
-                                                  const int32_t* ldsRow, const int32_t* ldsCol,
+                                                  const int32_t* ldsCol, const int32_t* ldsRow,
                                                   T alpha, T beta) {
     constexpr int NB = MODE == kAxpby ? kAxpbyStoreBatch : tile_batch(BLOCK);
     const bool shift = !g.runsOnGridB || g.misB != 0;
@@ -444,11 +472,12 @@ __host__ __device__ inline void tile_store_shared(const TileArgs& g, const TileB
                 if (shift || MODE == kAxpby) colOff = int(Mem::template lds_ld<int64_t>(colOffB, q));
                 if (shift) ss -= (tbm + colOff) & (VB - 1);
                 const int colL = Mem::template lds_ld<int32_t>(ldsCol, q);
+                int32_t pos[VB];
+                shared_positions<Mem, VB>(g, ldsRow, ss, rows, pos);
 #pragma unroll
                 for (int e = 0; e < VB; ++e)
                     if (ss + e >= 0 && ss + e < rows)
-                        x[u].v[e] =
-                            Mem::template lds_ld<T>(lds, Mem::template lds_ld<int32_t>(ldsRow, ss + e) + colL);
+                        x[u].v[e] = Mem::template lds_ld<T>(lds, pos[e] + colL);
                 if (MODE == kAxpby) {
                     const int off = colOff + ss;
                     if (ss >= 0 && ss + VB <= rows) {

@@ -14,8 +14,9 @@
 namespace hptt {
 
 int64_t tile_lds_bytes_host(const TileArgs& t, int elem) {
-    if (t.shared)  // tables: rowOffA, colOffB (64-bit), ldsRow, ldsCol (32-bit)
-        return (int64_t(t.subRows) + t.nColS + (t.runB + t.nColS + 1) / 2) * int64_t(sizeof(int64_t)) +
+    if (t.shared)  // tables: rowOffA, colOffB (64-bit), ldsCol, ldsRow with posTable (32-bit)
+        return (int64_t(t.subRows) + t.nColS + (t.nColS + (t.posTable ? t.runB : 0) + 1) / 2) *
+                   int64_t(sizeof(int64_t)) +
                int64_t(t.subRows) * t.pitch * elem;
     return (t.runA + t.runB + t.shear) * int64_t(sizeof(int64_t)) +
            (int64_t(t.nZ) * t.subRows + t.shear) * t.pitch * elem;
@@ -749,6 +750,13 @@ bool setup_shared(const Fused& f, int elem, int64_t tA, int64_t tB, const hptt_o
     if (maxRowA + t.runA >= (int64_t(1) << 31) || maxColB + t.runB >= (int64_t(1) << 31))
         return false;
     t.offsets32 = 1;
+    // B-run positions from an LDS table when two or more columns share it;
+    // computed for single-column tiles, where the table would take as much
+    // LDS as fp32 data (MI355X, 57-case sweep: single-column tiles +12 to
+    // +52 % from the LDS the table no longer takes, on the same tile or a
+    // larger one it allows; tiles of 2 and 5-63 columns lost 3 to 21 %
+    // without the table).
+    t.posTable = t.nColS >= 2 ? 1 : 0;
     const int64_t lds = tile_lds_bytes_host(t, elem);
     if (lds > ldsBudget) return false;
     info.run_a = t.runA;

@@ -40,14 +40,14 @@ void tile_kernel(const T* __restrict__ A, T* __restrict__ B, const TileArgs g, T
     extern __shared__ int64_t smem[];
     if constexpr (VAR == kShared) {
         // runs that share indices: one pass per tile, the store phase
-        // gathering through the LDS position tables
+        // gathering from LDS at positions from a table or computed
         int64_t* rowOffA = smem;
         int64_t* colOffB = smem + g.subRows;
-        int32_t* ldsRow = reinterpret_cast<int32_t*>(colOffB + g.nColS);
-        int32_t* ldsCol = ldsRow + g.runB;
+        int32_t* ldsCol = reinterpret_cast<int32_t*>(colOffB + g.nColS);
+        int32_t* ldsRow = ldsCol + g.nColS;
         T* lds = reinterpret_cast<T*>(smem + shared_table_words(g));
         const int tid = int(threadIdx.x);
-        tile_tables_shared<DeviceMem, BLOCK>(g, tid, rowOffA, colOffB, ldsRow, ldsCol);
+        tile_tables_shared<DeviceMem, BLOCK>(g, tid, rowOffA, colOffB, ldsCol, ldsRow);
         __syncthreads();
         bool first = true;
         for (uint32_t t = blockIdx.x; t < g.numTiles; t += gridDim.x) {
@@ -57,7 +57,7 @@ void tile_kernel(const T* __restrict__ A, T* __restrict__ B, const TileArgs g, T
             tile_load<DeviceMem, T, VA, HINT, VAR, BLOCK, LB>(g, tb, 0, tid, A, lds, rowOffA);
             __syncthreads();
             tile_store_shared<DeviceMem, T, VB, MODE, HINT, BLOCK>(g, tb, tid, B, lds, colOffB,
-                                                                    ldsRow, ldsCol, alpha, beta);
+                                                                    ldsCol, ldsRow, alpha, beta);
         }
         return;
     }

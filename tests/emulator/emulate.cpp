@@ -207,14 +207,14 @@ void emu_tile_shared(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride
     int64_t* smem = reinterpret_cast<int64_t*>(S->lds.data());
     int64_t* rowOffA = smem;
     int64_t* colOffB = smem + g.subRows;
-    int32_t* ldsRow = reinterpret_cast<int32_t*>(colOffB + g.nColS);
-    int32_t* ldsCol = ldsRow + g.runB;
+    int32_t* ldsCol = reinterpret_cast<int32_t*>(colOffB + g.nColS);
+    int32_t* ldsRow = ldsCol + g.nColS;
     T* lds = reinterpret_cast<T*>(smem + shared_table_words(g));
     const int64_t grid = p->info.grid;
     for (int64_t blk = 0; blk < grid && S->errors == 0; blk += blockStride) {
         clear_written(0, ldsBytes);
         for (int tid = 0; tid < kBlock; ++tid)
-            tile_tables_shared<HostMem, kBlock>(g, tid, rowOffA, colOffB, ldsRow, ldsCol);
+            tile_tables_shared<HostMem, kBlock>(g, tid, rowOffA, colOffB, ldsCol, ldsRow);
         for (int64_t t = blk; t < g.numTiles && S->errors == 0; t += grid) {
             const TileBase tb = tile_base<true>(g, uint32_t(t));
             clear_written(tableBytes, ldsBytes);
@@ -223,7 +223,7 @@ void emu_tile_shared(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride
                     g, tb, 0, tid, A, lds, rowOffA);
             for (int tid = 0; tid < kBlock; ++tid)
                 tile_store_shared<HostMem, T, VB, MODE, NT, kBlock>(g, tb, tid, B, lds, colOffB,
-                                                                     ldsRow, ldsCol, alpha, beta);
+                                                                     ldsCol, ldsRow, alpha, beta);
         }
     }
 }
