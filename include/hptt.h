@@ -253,13 +253,15 @@ typedef struct {
  * the caches are charged for them as in back-to-back use.  The (at most)
  * three candidates screened fastest, each at least 1 % ahead of the quick
  * path's plan, are then timed again against it in five alternating rounds,
- * cold as above and in bursts of four back-to-back launches; a finalist
- * replaces the quick plan only if it is at least 1 % faster in both sums
- * (this confirmation runs after the timeout and adds at most 60 timed
- * spans).  The caller's data are not changed: the plans write a scratch
+ * cold as above and in bursts of back-to-back launches that rotate over
+ * scratch copies of A's and B's footprints (up to 8 sets, 2 GiB of traffic
+ * between two uses of one set, as fits in memory), so that no launch finds
+ * its tensors in the caches; a finalist replaces the quick plan only if it is
+ * at least 1 % faster in both sums (this confirmation runs after the timeout
+ * and adds at most 60 timed spans).  The caller's data are not changed: the plans write a scratch
  * tensor of B's footprint (zeroed first when beta != 0) and B is not
- * touched.  The scratch memory (that tensor and the flush buffer) is
- * allocated for the call and freed before it returns.  Without memory for
+ * touched.  The scratch memory (that tensor, the rotation copies and the
+ * flush buffer) is allocated for the call and freed before it returns.  Without memory for
  * the scratch tensor, timing runs, like the paper's, on B itself with
  * alpha = 0 and beta = 1, so B is rewritten with its own value and A is read
  * and multiplied by zero (A must then hold no inf or NaN, footnote 5, and a

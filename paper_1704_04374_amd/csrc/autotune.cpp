@@ -190,12 +190,20 @@ struct Scratch {
     void* flush = nullptr;  // read between timed launches so they start cold
     void* sink = nullptr;   // checksums of the flush reads
     void* out = nullptr;    // a stand-in for B, so timing leaves B alone
+    // more (A, B) stand-ins, so back-to-back confirmation launches rotate
+    // over enough memory that none finds its tensors in the caches
+    std::vector<void*> rotA, rotB;
     ~Scratch() {
         if (flush) (void)hipFree(flush);
         if (sink) (void)hipFree(sink);
         if (out) (void)hipFree(out);
+        for (void* p : rotA) (void)hipFree(p);
+        for (void* p : rotB) (void)hipFree(p);
     }
 };
+
+constexpr size_t kRotateBytes = size_t(2) << 30;  // traffic between two uses of one set
+constexpr int kMaxSets = 8;
 
 bool try_alloc(void** p, size_t bytes) {
     if (hipMalloc(p, bytes) == hipSuccess) return true;
@@ -265,6 +273,35 @@ hptt_status_t autotune(hptt_plan_t* planOut, const int32_t* perm, int32_t N, con
         void* const target = ownMode ? scratch.out : B;
         const bool flush = try_alloc(&scratch.flush, kFlushBytes) &&
                            try_alloc(&scratch.sink, 4096 * sizeof(uint32_t));
+        // Buffer sets the confirmation bursts rotate over: set 0 is the
+        // caller's A with the timing target, the others scratch copies of
+        // their footprints (zeroed: the values do not change the timing).
+        // Fewer sets when memory is short (then bursts partly reuse the
+        // caches, as a caller reusing its tensors would).
+        const size_t inBytes = (size_t(base.info.footprint_a) * elem + 15) / 16 * 16;
+        std::vector<const void*> setA{A};
+        std::vector<void*> setB{target};
+        {
+            const size_t perSet = inBytes + outBytes;
+            const size_t want = std::min<size_t>(kMaxSets, std::max<size_t>(
+                                                               2, (kRotateBytes + perSet - 1) / perSet));
+            // each copy sits as far from a 256-byte boundary as the original,
+            // so that every set launches the same kernel variant and hints
+            const size_t offA = reinterpret_cast<uintptr_t>(A) % 256;
+            const size_t offB = reinterpret_cast<uintptr_t>(target) % 256;
+            while (setA.size() < want) {
+                void *a = nullptr, *b = nullptr;
+                if (!try_alloc(&a, inBytes + 256)) break;
+                scratch.rotA.push_back(a);
+                if (!try_alloc(&b, outBytes + 256)) break;
+                scratch.rotB.push_back(b);
+                if (hptt_yardstick_fill(a, inBytes + 256, 0, stream) != HPTT_SUCCESS ||
+                    hptt_yardstick_fill(b, outBytes + 256, 0, stream) != HPTT_SUCCESS)
+                    return HPTT_ERROR_HIP;
+                setA.push_back(static_cast<const char*>(a) + offA);
+                setB.push_back(static_cast<char*>(b) + offB);
+            }
+        }
         hipEvent_t e0, e1;
         if (hipEventCreate(&e0) != hipSuccess) return HPTT_ERROR_HIP;
         if (hipEventCreate(&e1) != hipSuccess) {
@@ -298,17 +335,20 @@ hptt_status_t autotune(hptt_plan_t* planOut, const int32_t* perm, int32_t N, con
             *out = median3(ms[0], ms[1], ms[2]);
             return e;
         };
-        // Back-to-back use: [flush] e0 kBurst launches e1, per launch.
+        // Back-to-back use: [flush] e0 n launches over the rotating sets e1,
+        // per launch (n = two rounds of the sets, at least kBurst).
+        const int burstLaunches = std::max<int>(kBurst, 2 * int(setA.size()));
         auto burst = [&](hptt_plan_s* tp, float* ms) -> hptt_status_t {
             hptt_status_t e = HPTT_SUCCESS;
             if (flush) e = hptt_yardstick_read(scratch.flush, kFlushBytes, scratch.sink, stream);
             if (e == HPTT_SUCCESS && hipEventRecord(e0, stream) != hipSuccess) e = HPTT_ERROR_HIP;
-            for (int b = 0; b < kBurst && e == HPTT_SUCCESS; ++b) e = hptt_exec(tp, A, target, stream);
+            for (int b = 0; b < burstLaunches && e == HPTT_SUCCESS; ++b)
+                e = hptt_exec(tp, setA[b % setA.size()], setB[b % setB.size()], stream);
             if (e == HPTT_SUCCESS && hipEventRecord(e1, stream) != hipSuccess) e = HPTT_ERROR_HIP;
             if (e == HPTT_SUCCESS && hipEventSynchronize(e1) != hipSuccess) e = HPTT_ERROR_HIP;
             if (e == HPTT_SUCCESS && hipEventElapsedTime(ms, e0, e1) != hipSuccess)
                 e = HPTT_ERROR_HIP;
-            *ms /= kBurst;
+            *ms /= burstLaunches;
             return e;
         };
         const auto t0 = clock::now();
