@@ -259,8 +259,11 @@ constexpr int kBatch = 8;
 constexpr int tile_batch(int block) { return block >= 1024 ? 4 : kBatch; }
 
 // Batch of the specialised store phase when it also reads B (beta != 0):
-// its B vectors double the registers a batch holds.
-constexpr int kAxpbyStoreBatch = 2;
+// its B vectors double the registers a batch holds.  2 in variant kFast (its
+// 8 waves per SIMD; 3 or 4 lost 2-3 % on the 5-D and 6-D fp32 workloads),
+// 4 in kShifted and kShared, which run 7 waves either way (MI355X, beta = 1
+// sweep cases: sheared runs +1 % on average, shared runs +3 to +6 %).
+constexpr int axpby_store_batch(int var) { return var == kShifted || var == kShared ? 4 : 2; }
 
 // Batch of the specialised load phase: 4 in variant kFast when B is read as
 // well, so that it fits 8 waves per SIMD (the attribute in tile_kernel.h)
@@ -352,7 +355,8 @@ template <class Mem, typename T, int VB, int MODE, int HINT, int BLOCK, bool SHI
 __host__ __device__ inline void tile_store_fast(const TileArgs& g, const TileBase& tb, int r0,
                                                 int tid, T* B, const T* lds,
                                                 const int64_t* colOffB, T alpha, T beta) {
-    constexpr int NB = MODE == kAxpby ? kAxpbyStoreBatch : tile_batch(BLOCK);
+    constexpr int NB = MODE == kAxpby ? axpby_store_batch(SHIFT ? kShifted : kFast)
+                                      : tile_batch(BLOCK);
     // B runs sheared onto lines (each column's run starts on the line at or
     // below the chunk's first row), or else shifted onto the vector grid
     const bool sheared = SHIFT && g.shear > 0;
@@ -450,7 +454,7 @@ __host__ __device__ inline void tile_store_shared(const TileArgs& g, const TileB
                                                   T* B, const T* lds, const int64_t* colOffB,
                                                   const int32_t* ldsCol, const int32_t* ldsRow,
                                                   T alpha, T beta) {
-    constexpr int NB = MODE == kAxpby ? kAxpbyStoreBatch : tile_batch(BLOCK);
+    constexpr int NB = MODE == kAxpby ? axpby_store_batch(kShared) : tile_batch(BLOCK);
     const bool shift = !g.runsOnGridB || g.misB != 0;
     const int W = (int(g.runB) + (shift ? VB - 1 : 0) + VB - 1) / VB;  // vectors per column
     const int vcols = int(tb.validColsS);
@@ -621,7 +625,7 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
                                                                         colOffB, alpha, beta);
         return;
     }
-    constexpr int NB = MODE == kAxpby ? kAxpbyStoreBatch : kBatch;
+    constexpr int NB = MODE == kAxpby ? axpby_store_batch(kGeneral) : kBatch;
     // B side: with shear, each column's run starts on the line at or below
     // the chunk's first row (d = the column's offset from that line); else,
     // without the vector grid, vectors are shifted onto it (d < VB).
