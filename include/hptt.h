@@ -77,7 +77,8 @@ typedef struct {
                               A run of a tile (its columns) */
     int32_t run_b;         /* TILE: target length of the contiguous B run (rows) */
     int32_t max_vec;       /* cap on the vector width in elements (1 = scalar) */
-    int32_t store_hint;    /* 1: non-temporal stores of B; 2: ordinary stores */
+    int32_t store_hint;    /* 1: non-temporal stores of B (and, when beta != 0,
+                              non-temporal loads of B); 2: ordinary ones */
     int32_t load_hint;     /* 1: non-temporal loads of A; 2: ordinary loads */
     int32_t lds_pad;       /* TILE: LDS row padding in elements, 0 = default, -1 = none */
     int32_t max_blocks;    /* cap on the grid; workgroups loop over tiles beyond it */
@@ -153,8 +154,9 @@ typedef struct {
     int64_t grid;                      /* workgroups launched */
     int32_t block;                     /* threads per workgroup (TILE: of the specialised
                                           variant; the general one runs 256) */
-    int32_t hints;                     /* bit 0: non-temporal B stores; bit 1:
-                                          non-temporal A loads */
+    int32_t hints;                     /* bit 0: non-temporal B stores (and B loads
+                                          when beta != 0); bit 1: non-temporal A
+                                          loads */
     int32_t mode;                      /* 0 raw copy, 1 scale (beta = 0), 2 alpha*A + beta*B */
     int32_t tile_order;                /* TILE: 1 grid-digit order, 2 diagonal, 3 diagonal
                                           with contiguous tile ranges per XCD, 4

@@ -396,7 +396,7 @@ __host__ __device__ inline void tile_store_fast(const TileArgs& g, const TileBas
                 if (MODE == kAxpby) {
                     const int off = colOff + ss;
                     if (ss >= rows0 && ss + VB <= rows) {
-                        y[u] = Mem::template ld<T, VB, false>(Bb, off);
+                        y[u] = Mem::template ld<T, VB, (HINT & kNtStore) != 0>(Bb, off);
                     } else {
                         for (int e = 0; e < VB; ++e)
                             if (ss + e >= rows0 && ss + e < rows)
@@ -485,7 +485,7 @@ __host__ __device__ inline void tile_store_shared(const TileArgs& g, const TileB
                 if (MODE == kAxpby) {
                     const int off = colOff + ss;
                     if (ss >= 0 && ss + VB <= rows) {
-                        y[u] = Mem::template ld<T, VB, false>(Bb, off);
+                        y[u] = Mem::template ld<T, VB, (HINT & kNtStore) != 0>(Bb, off);
                     } else {
                         for (int e = 0; e < VB; ++e)
                             if (ss + e >= 0 && ss + e < rows) y[u].v[e] = Mem::template ld1<T>(Bb, off + e);
@@ -671,7 +671,7 @@ __host__ __device__ inline void tile_store(const TileArgs& g, const TileBase& tb
                             x[u].v[e] = Mem::template lds_ld<T>(lds, base + e * g.pitch);
                     if (MODE == kAxpby) {
                         if (ss[u] >= lo && ss[u] + VB <= hi) {
-                            y[u] = Mem::template ld<T, VB, false>(B, off[u]);
+                            y[u] = Mem::template ld<T, VB, (HINT & kNtStore) != 0>(B, off[u]);
                         } else {
                             for (int e = 0; e < VB; ++e)
                                 if (ss[u] + e >= lo && ss[u] + e < hi)
@@ -757,7 +757,7 @@ __host__ __device__ inline void stream_items(const StreamArgs& g, uint32_t first
             offB[u] = b + col[u];
             if (col[u] + V <= g.rowLen) {
                 x[u] = Mem::template ld<T, V, (HINT & kNtLoad) != 0>(A, offA[u]);
-                if (MODE == kAxpby) y[u] = Mem::template ld<T, V, false>(B, offB[u]);
+                if (MODE == kAxpby) y[u] = Mem::template ld<T, V, (HINT & kNtStore) != 0>(B, offB[u]);
             } else {
                 for (int e = 0; e < V; ++e)
                     if (col[u] + e < g.rowLen) {
@@ -887,7 +887,7 @@ __host__ __device__ inline void stream_items_flat(const StreamArgs& g, uint32_t 
                 if (e < n[u]) x[u].v[e] = Mem::template ld1<T>(A, (c0 + e < rowLen ? a0 : a1) + c0 + e);
             if (MODE == kAxpby) {
                 if (n[u] == V) {
-                    y[u] = Mem::template ld<T, V, false>(B, offB[u]);
+                    y[u] = Mem::template ld<T, V, (HINT & kNtStore) != 0>(B, offB[u]);
                 } else {
                     for (int e = 0; e < V; ++e)
                         if (e < n[u]) y[u].v[e] = Mem::template ld1<T>(B, offB[u] + e);
@@ -928,7 +928,7 @@ __host__ __device__ inline void axpby_items(int64_t numel, int64_t first, int ti
         const int64_t off = (first + int64_t(u) * kBlock + tid) * V;
         if (off + V <= numel) {
             x[u] = Mem::template ld<T, V, (HINT & kNtLoad) != 0>(A, off);
-            if (MODE == kAxpby) y[u] = Mem::template ld<T, V, false>(B, off);
+            if (MODE == kAxpby) y[u] = Mem::template ld<T, V, (HINT & kNtStore) != 0>(B, off);
         }
     }
 #pragma unroll

@@ -59,8 +59,9 @@ struct alignas(16) VT {
     T v[16 / sizeof(T)];
 };
 
-// y <- alpha*x + beta*y, one 16-byte vector per lane, x read and y written
-// with non-temporal hints (y is read with an ordinary load).
+// y <- alpha*x + beta*y, one 16-byte vector per lane, every access with a
+// non-temporal hint (each line is touched once: y's read line is written
+// back by the same lane).
 template <typename T>
 __global__ __launch_bounds__(kThreads) void axpby_kernel(T alpha, const VT<T>* __restrict__ x,
                                                          T beta, VT<T>* __restrict__ y, size_t n) {
@@ -70,7 +71,7 @@ __global__ __launch_bounds__(kThreads) void axpby_kernel(T alpha, const VT<T>* _
     const size_t i = size_t(blockIdx.x) * kThreads + threadIdx.x;
     if (i < n) {
         const vt a = __builtin_nontemporal_load(reinterpret_cast<const vt*>(x) + i);
-        const vt b = reinterpret_cast<const vt*>(y)[i];
+        const vt b = __builtin_nontemporal_load(reinterpret_cast<const vt*>(y) + i);
         vt c;
 #pragma unroll
         for (int e = 0; e < V; ++e) {
