@@ -707,6 +707,10 @@ def main():
     print(f"[bench] device {torch.cuda.get_device_name(0)}; headline {head.describe()}",
           file=sys.stderr, flush=True)
 
+    # load every kernel's code object now: the first dispatch from a code
+    # object not yet loaded leaves the next few milliseconds of kernels
+    # several percent slower, which would land on the first workload timed
+    hptt.load_kernels()
     preheat(torch, hptt)
     if args.sweep:
         print(json.dumps(run_sweep(torch, hptt, args, flush_buf, sink)), flush=True)

@@ -335,6 +335,14 @@ const char *hptt_status_string(hptt_status_t status);
 /* The hipError_t of the last failed launch on this thread (hipSuccess if none). */
 int32_t hptt_last_hip_error(void);
 
+/* Load the library's GPU code onto the current device now instead of at the
+ * first hptt_exec that needs it.  Optional: a process whose first launches
+ * are timed calls it once per device beforehand (the first dispatch of a
+ * kernel from a not yet loaded code object leaves the next few milliseconds
+ * of kernels several percent slower).  Blocks the calling thread; launches
+ * nothing.  Errors: HPTT_ERROR_HIP (see hptt_last_hip_error). */
+hptt_status_t hptt_load_kernels(void);
+
 #ifdef __cplusplus
 }
 #endif

@@ -250,4 +250,25 @@ hptt_status_t hptt_exec(hptt_plan_t plan, const void* A, void* B, hipStream_t st
 
 int32_t hptt_last_hip_error(void) { return hptt::g_last_hip_error; }
 
+hptt_status_t hptt_load_kernels(void) {
+    using namespace hptt;
+    // one kernel of each source file: each file's kernels are one code object
+    const void* fns[] = {tile_kernel_f32(kFast, kCopy, 0, 1, 1, kBlock),
+                         tile_kernel_f32(kShifted, kCopy, 0, 1, 1, kBlock),
+                         tile_kernel_f32(kGeneral, kCopy, 0, 1, 1, kBlock),
+                         tile_kernel_f32(kShared, kCopy, 0, 1, 1, kBlock),
+                         tile_kernel_f64(kFast, kCopy, 0, 1, 1, kBlock),
+                         stream_fn<float, kCopy, 0>(1)};
+    for (const void* f : fns) {
+        if (!f) continue;
+        hipFuncAttributes attr;
+        const hipError_t err = hipFuncGetAttributes(&attr, f);
+        if (err != hipSuccess) {
+            g_last_hip_error = int32_t(err);
+            return HPTT_ERROR_HIP;
+        }
+    }
+    return HPTT_SUCCESS;
+}
+
 }  // extern "C"

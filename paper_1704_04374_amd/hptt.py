@@ -103,7 +103,8 @@ EXPORTS = ("hptt_create_plan", "hptt_create_plan_ex", "hptt_create_plan_outer",
            "hptt_create_plan_autotune", "hptt_autotune_candidates", "hptt_forget_wisdom",
            "hptt_exec", "hptt_destroy_plan",
            "hptt_plan_info", "hptt_describe_plan", "hptt_status_string",
-           "hptt_last_hip_error", "hptt_yardstick_copy", "hptt_yardstick_axpby",
+           "hptt_last_hip_error", "hptt_load_kernels", "hptt_yardstick_copy",
+           "hptt_yardstick_axpby",
            "hptt_yardstick_fill", "hptt_yardstick_read")
 
 
@@ -140,6 +141,7 @@ def _declare(lib: ctypes.CDLL, gpu: bool) -> ctypes.CDLL:
         lib.hptt_exec.argtypes = [vp, vp, vp, vp]
         lib.hptt_exec.restype = st
         lib.hptt_last_hip_error.restype = ctypes.c_int32
+        lib.hptt_load_kernels.restype = st
         lib.hptt_yardstick_copy.argtypes = [vp, vp, ctypes.c_size_t, vp]
         lib.hptt_yardstick_axpby.argtypes = [ctypes.c_int, ctypes.c_double, vp, ctypes.c_double,
                                              vp, ctypes.c_size_t, vp]
@@ -162,6 +164,14 @@ def library() -> ctypes.CDLL:
             raise HpttError(-1, f"{LIB_PATH} is missing; run paper_1704_04374_amd.build")
         _lib = _declare(ctypes.CDLL(LIB_PATH), gpu=True)
     return _lib
+
+
+def load_kernels() -> None:
+    """hptt_load_kernels: load the library's GPU code onto the current device."""
+    st = library().hptt_load_kernels()
+    if st == HIP_ERROR:
+        raise HpttError(st, f"hptt_load_kernels (hipError {library().hptt_last_hip_error()})")
+    _check(st, "hptt_load_kernels")
 
 
 def load_plan_api(path: str) -> ctypes.CDLL:

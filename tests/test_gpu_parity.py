@@ -329,6 +329,18 @@ def test_overlap_rejected_and_nothing_written():
     assert buf.abs().sum().item() == 0
 
 
+def test_load_kernels_then_exec():
+    """hptt_load_kernels loads every code object without launching anything
+    (twice: a second call is a no-op) and leaves every kernel class usable."""
+    hptt.load_kernels()
+    hptt.load_kernels()
+    rng = np.random.default_rng(11)
+    for size_a, perm, beta, dtype in [((64, 48, 5), (1, 0, 2), 0.0, "f32"),
+                                      ((65, 33, 17), (2, 0, 1), 0.5, "f64"),
+                                      ((33, 7, 5), (0, 2, 1), 1.0, "f32")]:
+        _run_case(size_a, perm, 1.5, beta, dtype, rng)
+
+
 def test_zero_size_is_noop():
     p = hptt.create_plan((2, 1, 0), (4, 0, 3))
     assert p.info["kernel"] == "none"
