@@ -257,7 +257,8 @@ typedef struct {
  * path's plan, are then timed again against it in five alternating rounds,
  * cold as above and in bursts of back-to-back launches that rotate over
  * scratch copies of A's and B's footprints (up to 8 sets, 2 GiB of traffic
- * between two uses of one set, as fits in memory), so that no launch finds
+ * between two uses of one set, as fits in memory; none beyond the caller's
+ * own when A's and B's footprints alone exceed 2 GiB), so that no launch finds
  * its tensors in the caches; a finalist replaces the quick plan only if it is
  * at least 1 % faster in both sums (this confirmation runs after the timeout
  * and adds at most 60 timed spans).  The caller's data are not changed: the plans write a scratch

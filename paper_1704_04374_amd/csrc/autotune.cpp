@@ -282,9 +282,9 @@ hptt_status_t autotune(hptt_plan_t* planOut, const int32_t* perm, int32_t N, con
         std::vector<const void*> setA{A};
         std::vector<void*> setB{target};
         {
+            // (one set when a launch alone moves kRotateBytes: it evicts itself)
             const size_t perSet = inBytes + outBytes;
-            const size_t want = std::min<size_t>(kMaxSets, std::max<size_t>(
-                                                               2, (kRotateBytes + perSet - 1) / perSet));
+            const size_t want = std::min<size_t>(kMaxSets, (kRotateBytes + perSet - 1) / perSet);
             // each copy sits as far from a 256-byte boundary as the original,
             // so that every set launches the same kernel variant and hints
             const size_t offA = reinterpret_cast<uintptr_t>(A) % 256;

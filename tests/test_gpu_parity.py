@@ -383,6 +383,41 @@ def test_streams_and_plan_reuse():
         _assert_parity(b.cpu().numpy(), w, "f32", p.describe())
 
 
+def test_graph_capture_replays():
+    """hptt_exec captured into a HIP graph and replayed four times, with eager
+    work and synchronisations between the replays: every replay matches the
+    oracle (tile, shared-run, sheared, stream and generic plans; with beta !=
+    0, B is reset eagerly before each replay, outside the graph)."""
+    rng = np.random.default_rng(41)
+    cases = [((256, 96, 8), (1, 2, 0), 1.5, 0.0, "f32", {}),
+             ((12, 3, 2, 93, 33), (2, 1, 4, 3, 0), 1.5, 0.0, "f32", {}),
+             ((66, 7576), (1, 0), 1.0, 1.0, "f32", dict(shear=1)),
+             ((96, 40, 6), (0, 2, 1), 2.0, 0.5, "f64", {}),
+             ((17, 5, 33), (2, 0, 1), 1.0, 1.0, "f32", dict(kernel="generic"))]
+    for size_a, perm, alpha, beta, dtype, knobs in cases:
+        p = hptt.create_plan(perm, size_a, alpha, beta, dtype, **knobs)
+        _say(f"graph: {p.describe()}")
+        n = p.numel
+        A = _rand(rng, n, dtype)
+        B0 = _rand(rng, n, dtype) if beta != 0 else np.full(n, np.nan, NUMPY_DTYPE[dtype])
+        want = orc.transpose(A, size_a, perm, alpha, beta, B0 if beta != 0 else None)
+        dA = torch.from_numpy(A).cuda()
+        dB0 = torch.from_numpy(B0).cuda()
+        dB = dB0.clone()
+        p.exec(dA, dB)  # eager run first: the kernel is loaded before capture
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            p.exec(dA, dB)
+        for rep in range(4):
+            dB.copy_(dB0)
+            junk = torch.empty(1 << 20, device="cuda").uniform_()  # eager work between replays
+            g.replay()
+            torch.cuda.synchronize()
+            _assert_parity(dB.cpu().numpy(), want, dtype, f"replay {rep}: {p.describe()}")
+            del junk
+
+
 def test_inverse_round_trip_on_gpu():
     """Pi then Pi^-1 returns A bit for bit on the device."""
     rng = np.random.default_rng(31)
