@@ -492,3 +492,21 @@ def test_flat_stream_walk_matches_oracle(dtype):
                 for vb in (0, 2, 1):
                     _check(p, size_a, perm, alpha, beta, dtype, rng, vb=vb)
     assert seen >= 12
+
+
+def test_sheared_whole_short_index_matches_oracle():
+    """Sheared tiles holding a short stride-1 A index whole (B runs of two
+    lines), with ragged B-run chunks, in both update modes."""
+    rng = np.random.default_rng(66)
+    for size_a, perm, dtype in [((66, 3000), (1, 0), "f32"), ((69, 90, 70), (1, 2, 0), "f32")]:
+        p = emu.plan(perm, size_a, 1.0, 0.0, dtype)
+        assert p.info["shear"] > 0 and p.info["run_a"] == size_a[0], p.describe()
+        _check(p, size_a, perm, 1.0, 0.0, dtype, rng)
+        q = emu.plan(perm, size_a, -0.3, 1.25, dtype, shear=1)
+        _check(q, size_a, perm, -0.3, 1.25, dtype, rng)
+    # fp64 takes it at full size only: a dry run of every workgroup
+    p = emu.plan((1, 2, 3, 0), (30, 2762, 85, 7), 1.0, 1.0, "f64")
+    assert p.info["shear"] > 0 and p.info["run_a"] == 30, p.describe()
+    err, msg, cnt = emu.run(p, counts=True)
+    assert err == 0, msg
+    assert cnt.min() == 1 and cnt.max() == 1

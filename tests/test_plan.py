@@ -395,6 +395,26 @@ def test_flat_b_runs_rule():
     assert small.info["flat_runs"] == 2
 
 
+@pytest.mark.parametrize("size_a,perm,dtype,whole", [
+    ((66, 757576), (1, 0), "f32", 66),       # one-line target would cut 66 into 33 + 33
+    ((69, 988, 733), (1, 2, 0), "f32", 69),
+    ((30, 2762, 85, 7), (1, 2, 3, 0), "f64", 30),
+])
+def test_sheared_tiles_keep_a_short_stride1_index_whole(size_a, perm, dtype, whole):
+    """Sheared tiles take a stride-1 A index that the one-line A-run target
+    would cut in two whole, with B runs of two lines (the next A index is the
+    B run's, so a tile's A rows are one contiguous block); an index cut in
+    three keeps the cut."""
+    for beta in (0.0, 1.0):
+        i = hptt.create_plan(perm, size_a, 1.0, beta, dtype).info
+        assert i["shear"] > 0 and i["run_a"] == whole, i
+        assert i["run_b"] >= 128 // i["elem_bytes"] * 2
+    # a B-run target given by the caller is kept
+    assert hptt.create_plan(perm, size_a, 1.0, 0.0, dtype, run_b=256).info["run_b"] > 64
+    i = hptt.create_plan((1, 0), (87, 30000), 1.0, 0.0, "f32").info
+    assert i["shear"] > 0 and i["run_a"] == 29
+
+
 @pytest.mark.parametrize("size_a,perm,want", [
     # the window of resident tiles touches far fewer B regions with A4 first
     ((24, 20, 16, 24, 18, 20), (5, 2, 0, 4, 1, 3), 2),
