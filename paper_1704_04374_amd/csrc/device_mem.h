@@ -1,6 +1,7 @@
 // Memory policy of the device kernels: plain global and LDS accesses.  A
 // vector of V elements is one global_load/store of V*sizeof(T) bytes; the
-// plan only asks for widths that keep every such access aligned.
+// plan only asks for widths that keep every such access aligned, except
+// ldu, whose loads need only element alignment.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -28,6 +29,15 @@ struct DeviceMem {
     template <typename T>
     __device__ __forceinline__ static T ld1(const T* p, int64_t off) {
         return p[off];
+    }
+    // V consecutive elements from any element boundary: one global_load of
+    // V*sizeof(T) bytes at a dword-aligned address (gfx950 serves those
+    // in both of its alignment modes).
+    template <typename T, int V>
+    __device__ __forceinline__ static Vec<T, V> ldu(const T* p, int64_t off) {
+        Vec<T, V> r;
+        __builtin_memcpy(&r, p + off, sizeof(r));
+        return r;
     }
     template <bool NT, typename T>
     __device__ __forceinline__ static void st1(T* p, int64_t off, T v) {

@@ -859,8 +859,12 @@ __host__ __device__ inline int64_t stream_row_a(const StreamArgs& g, uint32_t r)
 // is a whole vector even when the row length is not a multiple of the width
 // (rows of 63 fp32 would otherwise move one element per access).  The row
 // split is done once per vector (twice when the vector crosses into the next
-// row); A is read element by element, ordinary loads, since its rows start
-// anywhere.  Same lane map as stream_items.
+// row); A is read with ordinary loads, since its rows start anywhere: fp32
+// with B only written takes one element-aligned vector load where the
+// vector's elements lie in one row (MI355X, rows of 55-213 elements +27 to
+// +35 %); elsewhere, and where a vector crosses into the next row, element by
+// element (the vector load lost 2-6 % when B is read, and with fp64).  Same
+// lane map as stream_items.
 template <class Mem, typename T, int V, int MODE, int HINT>
 __host__ __device__ inline void stream_items_flat(const StreamArgs& g, uint32_t first, int tid,
                                                   const T* A, T* B, T alpha, T beta) {
@@ -881,10 +885,16 @@ __host__ __device__ inline void stream_items_flat(const StreamArgs& g, uint32_t 
             const uint32_t r = fast_div(uint32_t(offB[u]), g.L);
             const int c0 = int(uint32_t(offB[u]) - r * g.L.d);
             const int64_t a0 = stream_row_a(g, r);
-            const int64_t a1 = c0 + n[u] > rowLen ? stream_row_a(g, r + 1) - rowLen : a0;
+            if (sizeof(T) == 4 && MODE != kAxpby && n[u] == V && c0 + V <= rowLen) {
+                // inside one row: one load from wherever the row puts it
+                x[u] = Mem::template ldu<T, V>(A, a0 + c0);
+            } else {
+                const int64_t a1 = c0 + n[u] > rowLen ? stream_row_a(g, r + 1) - rowLen : a0;
 #pragma unroll
-            for (int e = 0; e < V; ++e)
-                if (e < n[u]) x[u].v[e] = Mem::template ld1<T>(A, (c0 + e < rowLen ? a0 : a1) + c0 + e);
+                for (int e = 0; e < V; ++e)
+                    if (e < n[u])
+                        x[u].v[e] = Mem::template ld1<T>(A, (c0 + e < rowLen ? a0 : a1) + c0 + e);
+            }
             if (MODE == kAxpby) {
                 if (n[u] == V) {
                     y[u] = Mem::template ld<T, V, (HINT & kNtStore) != 0>(B, offB[u]);

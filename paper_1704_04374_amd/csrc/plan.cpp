@@ -830,13 +830,15 @@ bool setup_stream(const Fused& f, int elem, const hptt_options_t& opt, StreamArg
     }
     const int32_t v = vec_width(gran, elem, opt.max_vec);
     // Flat walk: B compact (its rows back to back), and rows that would move
-    // one element per access (odd row lengths), or two fp32 elements when B
-    // is read as well; every B access is then a whole vector.  MI355X, fp32
-    // rows of 55-213 elements: +13 to +24 % (e.g. 63-element rows 3.11 ->
-    // 3.65 TB/s with beta = 0, 4.25 -> 5.27 with beta = 1); fp32 rows of 42
-    // and 66 (two elements per access) +12 % and +9 % with beta = 1 but -9 %
-    // with beta = 0; fp64 rows of 33-211 elements +5 to +19 % with beta = 0,
-    // +2 to +14 % on three of four with beta = 0.5 (-3 % on rows of 95).
+    // one element per access (odd row lengths), or two fp32 elements; every
+    // B access is then a whole vector.  MI355X, fp32 rows of 55-213
+    // elements: +13 to +24 % (e.g. 63-element rows 3.11 -> 3.65 TB/s with
+    // beta = 0, 4.25 -> 5.27 with beta = 1), and +27 to +35 % more with beta
+    // = 0 since A is read a vector at a time there; fp32 rows of 42 and 66
+    // (two elements per access) +12 % and +9 % with beta = 1, and with beta =
+    // 0 rows of 42 and 498 +11 % and +14 % (they lost 7-9 % while A was read
+    // element by element); fp64 rows of 33-211 elements +5 to +19 % with beta
+    // = 0, +2 to +14 % on three of four with beta = 0.5 (-3 % on rows of 95).
     const int32_t vWide = vec_width(0, elem, opt.max_vec);
     bool compactB = f.M < 2 || f.sB[f.p[1]] == s.rowLen;
     for (int k = 1; k + 1 < f.M; ++k)
@@ -845,7 +847,7 @@ bool setup_stream(const Fused& f, int elem, const hptt_options_t& opt, StreamArg
     if (opt.flat_runs != 2 && compactB && numel < (int64_t(1) << 32) - int64_t(kBlock) * kMaxItems &&
         s.rowLen >= vWide &&
         (opt.flat_runs == 1 ||
-         (v < vWide && (v == 1 || (elem == 4 && v == 2 && info.mode == kAxpby))))) {
+         (v < vWide && (v == 1 || (elem == 4 && v == 2))))) {
         s.flatB = 1;
         set_div(s.L, s.rowLen);
         for (int w = 0; w < 3; ++w) s.numItems[w] = uint32_t((numel + (1 << w) - 1) >> w);

@@ -66,7 +66,7 @@ intptr_t distance(const void* p, const void* base, int64_t bytes) {
 // element accessed must lie inside it.  off is turned into an offset from
 // that tensor's first element before every check.
 template <typename T>
-bool check_global(const T* p, int64_t& off, int V, bool isStore) {
+bool check_global(const T* p, int64_t& off, int V, bool isStore, bool aligned = true) {
     const intptr_t dA = distance(p, S->A, S->numelA * int64_t(sizeof(T)));
     const intptr_t dB = distance(p, S->B, S->numelB * int64_t(sizeof(T)));
     const bool isA = dA <= dB;
@@ -81,7 +81,7 @@ bool check_global(const T* p, int64_t& off, int V, bool isStore) {
         fail(isA ? "A offset out of bounds" : "B offset out of bounds", off, V);
         return false;
     }
-    if ((off + (isA ? S->misA : S->misB)) % V != 0) {
+    if (aligned && (off + (isA ? S->misA : S->misB)) % V != 0) {
         fail("misaligned vector access", off, V);
         return false;
     }
@@ -104,6 +104,14 @@ struct HostMem {
         memset(&r, 0, sizeof(r));
         int64_t at = off;  // offset from the tensor's first element
         if (check_global(p, at, V, false) && !S->dry) memcpy(&r, p + off, sizeof(r));
+        return r;
+    }
+    template <typename T, int V>
+    static hptt::Vec<T, V> ldu(const T* p, int64_t off) {
+        hptt::Vec<T, V> r;
+        memset(&r, 0, sizeof(r));
+        int64_t at = off;
+        if (check_global(p, at, V, false, false) && !S->dry) memcpy(&r, p + off, sizeof(r));
         return r;
     }
     template <typename T>

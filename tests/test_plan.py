@@ -353,9 +353,9 @@ def test_shared_runs_where_disjoint_runs_collapse():
 
 def test_flat_stream_walk_rule():
     """Kernel S walks B flat where the kept rows would move one element per
-    access (odd rows), or two fp32 elements with beta != 0; not for rows
-    that take whole vectors, not where B is a sub-tensor with gaps, and not
-    when switched off."""
+    access (odd rows), or two fp32 elements; not for rows that take whole
+    vectors, not where B is a sub-tensor with gaps, and not when switched
+    off."""
     odd = hptt.create_plan((0, 3, 2, 1), (75, 100, 11, 60), 1.0, 0.0, "f32")
     assert odd.info["kernel"] == "stream" and odd.info["flat_runs"] == 1
     assert odd.info["vec_b"] == 4 and odd.info["tiles"] == -(-odd.numel // 4)
@@ -365,9 +365,11 @@ def test_flat_stream_walk_rule():
     assert hptt.create_plan((0, 3, 2, 1), (95, 96, 9, 9), 2.0, 0.5, "f64").info["flat_runs"] == 1
     assert hptt.create_plan((0, 3, 2, 1), (96, 96, 9, 9), 2.0, 0.5, "f64").info["flat_runs"] == 0
     assert hptt.create_plan((0, 3, 2, 1), (96, 96, 9, 9), 1.0, 0.0, "f32").info["flat_runs"] == 0
-    # two fp32 elements per access: flat only when B is read as well
-    assert hptt.create_plan((0, 3, 2, 1), (66, 10, 9, 9), 1.0, 0.0, "f32").info["flat_runs"] == 0
+    # two fp32 elements per access: flat in both update modes; two fp64
+    # elements (whole vectors) keep the row walk
+    assert hptt.create_plan((0, 3, 2, 1), (66, 10, 9, 9), 1.0, 0.0, "f32").info["flat_runs"] == 1
     assert hptt.create_plan((0, 3, 2, 1), (66, 10, 9, 9), 1.0, 1.0, "f32").info["flat_runs"] == 1
+    assert hptt.create_plan((0, 3, 2, 1), (66, 10, 9, 9), 1.0, 0.0, "f64").info["flat_runs"] == 0
     forced = hptt.create_plan((0, 3, 2, 1), (96, 96, 9, 9), 1.0, 0.0, "f32", flat_runs=1)
     assert forced.info["flat_runs"] == 1
     gaps = hptt.create_plan((0, 2, 1), (63, 5, 7), 1.0, 0.0, "f32", outer_size_b=(64, 7, 5))
