@@ -55,7 +55,7 @@ def kernel_source_hash() -> str:
     h = hashlib.sha256()
     for f in ("kernel_body.h", "kernels.hip", "plan.cpp", "hptt_args.h", "device_mem.h",
               "tile_kernel.h", "tile_f32_fast.hip", "tile_f32_shifted.hip", "tile_f32_general.hip",
-              "tile_shared.hip", "tile_f64.hip"):
+              "tile_shared.hip", "tile_direct.hip", "tile_f64.hip"):
         with open(os.path.join(ROOT, "paper_1704_04374_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

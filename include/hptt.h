@@ -127,6 +127,12 @@ typedef struct {
                               the tile (after the chunk counters): 1 = A order, 2 =
                               by the sum of their strides in A and B, 3 = B
                               order; 0 = choose */
+    int32_t direct_lds;    /* TILE, beta == 0: A fetched straight into LDS
+                              (global_load_lds_dwordx4) by the variant whose runs
+                              all start on the 16-byte grid, where A's vectors are
+                              16 bytes, the tile is staged in one pass and its
+                              column count is whole vectors: 0 = where it
+                              applies, 2 = never */
 } hptt_options_t;
 
 /* What the plan builder decided; for inspection and tests. */
@@ -172,6 +178,9 @@ typedef struct {
     int32_t grid_order;                /* TILE: order of the grid digits outside the tile:
                                           1 A order, 2 by the sum of their strides, 3 B
                                           order (0: not a tile plan) */
+    int32_t direct_lds;                /* TILE: 1 when tiles are fetched straight into
+                                          LDS (by launches that take the variant
+                                          with every run on the 16-byte grid) */
 } hptt_plan_info_t;
 
 /*

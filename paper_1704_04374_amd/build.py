@@ -25,9 +25,9 @@ CONTRACT_LIB = os.path.join(PKG, "libhptt_contract.so")
 CONTRACT_SOURCES = ["contract.hip"]
 
 ARCH = "gfx950"
-# the tile kernel instantiations are split over five files so they compile in parallel
+# the tile kernel instantiations are split over six files so they compile in parallel
 SOURCES = ["tile_f32_fast.hip", "tile_f32_shifted.hip", "tile_f32_general.hip", "tile_shared.hip",
-           "tile_f64.hip", "kernels.hip",
+           "tile_direct.hip", "tile_f64.hip", "kernels.hip",
            "yardstick.hip", "api.cpp", "plan.cpp", "autotune.cpp"]
 
 # -ffp-contract=off: alpha*a + beta*b is two roundings and an add, never an

@@ -127,6 +127,13 @@ int autotune_candidates(const int32_t* perm, int32_t N, const int64_t* sizeA,
             v.grid_order = go;
             var.push_back({1, v});
         }
+        // tiles staged through registers instead of fetched straight into LDS
+        {
+            hptt_options_t v;
+            memset(&v, 0, sizeof(v));
+            v.direct_lds = 2;
+            var.push_back({1, v});
+        }
         for (int c = 1; c <= 6; ++c)
             for (auto& pv : var)
                 if (pv.first == c) cand.push_back(pv.second);

@@ -57,6 +57,30 @@ struct DeviceMem {
             else *reinterpret_cast<vt*>(p + off) = x;
         }
     }
+    // V elements (16 bytes) from p + off straight into LDS: the wave's 64
+    // lanes write the 64 consecutive 16-byte slots from ldsWave on (lane is
+    // implied by the hardware; ldsWave must be the same for every lane).
+    template <typename T, int V, bool NT>
+    __device__ __forceinline__ static void ld_lds(const T* p, int64_t off, T* ldsWave, int) {
+        static_assert(V * sizeof(T) == 16, "direct LDS loads move 16 bytes per lane");
+#if defined(__HIP_DEVICE_COMPILE__)
+        __builtin_amdgcn_global_load_lds(p + off, ldsWave, 16, 0, NT ? 2 : 0);
+#endif
+    }
+    // Wait until this lane's direct LDS loads have landed (before a barrier).
+    __device__ __forceinline__ static void wait_ld_lds() {
+#if defined(__HIP_DEVICE_COMPILE__)
+        __builtin_amdgcn_s_waitcnt(0);
+#endif
+    }
+    // A value the whole wave holds, kept in a scalar register.
+    __device__ __forceinline__ static int wave_uniform(int x) {
+#if defined(__HIP_DEVICE_COMPILE__)
+        return __builtin_amdgcn_readfirstlane(x);
+#else
+        return x;
+#endif
+    }
     template <typename T>
     __device__ __forceinline__ static T lds_ld(const T* l, int64_t i) {
         return l[i];

@@ -121,6 +121,13 @@ struct TileArgs {
     // nothing, and rowOffA is rebuilt for every tile from the chunk's first
     // flattened position (TileBase::rowBase).
     int32_t flatR;
+    // Direct LDS loads (variant kDirect: B only written, 16-byte A vectors,
+    // one pass, no stacking or shear, every tile's columns whole vectors):
+    // with directLds = 1 tiles are fetched with global_load_lds_dwordx4,
+    // straight from A into an unpadded LDS tile (tile_load_direct), and
+    // written out by tile_store_rotated, wherever the launch would take
+    // variant kFast.
+    int32_t directLds;
     // Shared runs (variant kShared): the A run and the B run share
     // indices (S).  The tile is the product of the indices of both runs.  Its
     // load phase stages subRows rows, one per value of the B-run indices
@@ -187,15 +194,17 @@ struct StreamArgs {
 // inside a tile and no stacking; kGeneral otherwise (stacked tiles, 64-bit
 // offsets).  kShared serves the plans whose runs share indices (32-bit
 // offsets, runs shifted onto the vector grid where they start off it).
-// g.misA / g.misB must already hold the launch's pointer offsets.
-enum TileVariant : int { kFast = 0, kShifted = 1, kGeneral = 2, kShared = 3 };
+// kDirect serves what kFast serves when the plan asks for direct LDS loads
+// (TileArgs::directLds).  g.misA / g.misB must already hold the launch's
+// pointer offsets.
+enum TileVariant : int { kFast = 0, kShifted = 1, kGeneral = 2, kShared = 3, kDirect = 4 };
 
 __host__ __device__ inline int tile_variant(const TileArgs& g) {
     if (g.shared) return kShared;
     if (g.nZ > 1 || !g.offsets32) return kGeneral;
     if (!g.runsOnGridA || !g.runsOnGridB || g.misA != 0 || g.misB != 0 || g.shear > 0)
         return kShifted;
-    return kFast;
+    return g.directLds ? kDirect : kFast;
 }
 
 constexpr int log2_width(int v) { return v >= 4 ? 2 : v >= 2 ? 1 : 0; }

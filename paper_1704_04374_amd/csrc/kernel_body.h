@@ -443,6 +443,109 @@ __host__ __device__ inline void tile_store_fast(const TileArgs& g, const TileBas
     }
 }
 
+// Direct LDS loads (TileArgs::directLds): whether this tile takes them with
+// A vectors of VA elements.  Its columns must be whole vectors, and the
+// rotation of its rows (row / 4, below) must stay below the vectors per row.
+__host__ __device__ inline bool tile_direct_lds(const TileArgs& g, const TileBase& tb, int va) {
+    return g.directLds && g.subRows >= g.runB && g.runA % va == 0 && tb.validCols % va == 0 &&
+           ((g.subRows - 1) >> 2) < g.runA / va;
+}
+
+// Load phase with direct LDS loads: the tile is staged without padding,
+// row R (one A run, W = runA / VA vectors) in 16-byte slots R*W .. R*W+W-1.
+// Each wave fetches 64 consecutive slots per instruction, one per lane, and
+// slot cs of row R holds A vector (cs + R/4) mod W: rotating each group of
+// four rows spreads the store phase's column reads (four rows of one column
+// per lane) over the LDS banks.  Only the vectors of valid rows and columns
+// are fetched; the others' slots are never read.
+template <class Mem, typename T, int VA, int HINT, int BLOCK>
+__host__ __device__ inline void tile_load_direct(const TileArgs& g, const TileBase& tb, int tid,
+                                                 const T* A, T* lds, const int64_t* rowOffA) {
+    const int W = int(g.runA) / VA;
+    const int rows = int(imin(int64_t(g.subRows), tb.validRows));
+    const int vcols = int(tb.validCols);
+    const int total = g.subRows * W;
+    const int wave = Mem::wave_uniform(tid >> 6), lane = tid & 63;
+    const T* Ab = A + tb.a;
+    for (int k0 = wave * 64; k0 < total; k0 += BLOCK) {
+        const int k = k0 + lane;
+        const int R = k / W, cs = k - R * W;
+        int c = cs + (R >> 2);
+        if (c >= W) c -= W;
+        if (k < total && R < rows && c * VA < vcols) {
+            const int off = int(Mem::template lds_ld<int64_t>(rowOffA, R)) + c * VA;
+            Mem::template ld_lds<T, VA, (HINT & kNtLoad) != 0>(Ab, off, lds + k0 * VA, lane);
+        }
+    }
+    Mem::wait_ld_lds();
+}
+
+// Store phase after tile_load_direct (B only written): tile_store_fast's
+// thread-to-vector map, element (R, q) read from slot
+// R*W + (q/VA - R/4) mod W.  The rows of one B vector share R/4, since a
+// vector starts at a multiple of VB <= 4.
+template <class Mem, typename T, int VA, int VB, int MODE, int HINT, int BLOCK>
+__host__ __device__ inline void tile_store_rotated(const TileArgs& g, const TileBase& tb, int tid,
+                                                   T* B, const T* lds, const int64_t* colOffB,
+                                                   T alpha, T beta) {
+    static_assert(MODE != kAxpby, "direct LDS loads serve tiles whose B is only written");
+    constexpr int NB = 4;
+    const int WA = int(g.runA) / VA;
+    const int W = (g.subRows + VB - 1) / VB;  // vectors per column
+    const int vcols = int(tb.validCols);
+    const int rows = int(imin(int64_t(g.subRows), tb.validRows));
+    T* Bb = B + tb.b;
+    int q = tid / W, s = tid % W;
+    const int dq = BLOCK / W, ds = BLOCK % W;
+    while (q < int(g.runA)) {
+        Vec<T, VB> x[NB];
+        const int q0 = q, s0 = s;
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const int ss = s * VB;
+            if (q < vcols) {
+                int cs = q / VA - (ss >> 2);
+                if (cs < 0) cs += WA;
+                const int base = (ss * WA + cs) * VA + (q & (VA - 1));
+#pragma unroll
+                for (int e = 0; e < VB; ++e)
+                    if (ss + e < rows) x[u].v[e] = Mem::template lds_ld<T>(lds, base + e * WA * VA);
+            }
+            s += ds;
+            q += dq;
+            if (s >= W) {
+                s -= W;
+                q += 1;
+            }
+        }
+        q = q0;
+        s = s0;
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const int ss = s * VB;
+            if (q < vcols && ss < rows) {
+                const int off = int(Mem::template lds_ld<int64_t>(colOffB, q)) + ss;
+                Vec<T, VB> zv;
+#pragma unroll
+                for (int e = 0; e < VB; ++e) zv.v[e] = update<MODE>(x[u].v[e], T(0), alpha, beta);
+                if (ss + VB <= rows) {
+                    Mem::template st<(HINT & kNtStore) != 0, T, VB>(Bb, off, zv);
+                } else {
+                    for (int e = 0; e < VB; ++e)
+                        if (ss + e < rows)
+                            Mem::template st1<(HINT & kNtStore) != 0, T>(Bb, off + e, zv.v[e]);
+                }
+            }
+            s += ds;
+            q += dq;
+            if (s >= W) {
+                s -= W;
+                q += 1;
+            }
+        }
+    }
+}
+
 // Store phase of the shared-run variant (its load phase is
 // tile_load_fast's, shifted): column q is the contiguous B run
 // colOffB[q] + [0, runB), whose position b sits in LDS at pos(b) + ldsCol[q]

@@ -200,6 +200,27 @@ void set_div(FastDiv& f, int64_t d) { f = make_fastdiv(uint32_t(d)); }
 // Order of the grid digits outside the tile (outer_indices); 0 = A order.
 int32_t grid_order(const hptt_options_t& opt) { return opt.grid_order ? opt.grid_order : 1; }
 
+// Direct LDS loads (TileArgs::directLds): tiles whose B is only written, with
+// 16-byte A vectors, staged in one pass without stacking or shear, whose LDS
+// data starts on 16 bytes (the tables before it hold an even number of
+// 64-bit words) and whose row rotation (row / 4) stays below the vectors per
+// row.  MI355X, same process, against the register-staged load phase: the
+// 6-D fp32 workload 1.05x, 8192x4096 fp64 1.06x, the 2-D fp32 workload
+// 1.01x, its transpose-and-compact half 1.02x; with beta != 0 it lost 5 %
+// (the 5-D workload), so B read and written keeps the register path.
+void set_direct_lds(const hptt_options_t& opt, int elem, hptt_plan_info_t& info, TileArgs& t) {
+    const int64_t va = info.vec_a;
+    // every tile's columns whole vectors, the last chunk's too
+    const bool wholeCols = t.runA % va == 0 && (t.cChunk >= t.cLast || t.cLast % t.cChunk == 0 ||
+                                                (t.cInner * (t.cLast % t.cChunk)) % va == 0);
+    t.directLds = opt.direct_lds != 2 && info.mode != kAxpby && !t.shared && t.nZ == 1 &&
+                          t.shear == 0 && t.subRows >= t.runB && elem * va == 16 && wholeCols &&
+                          (t.runA + t.runB + t.shear) % 2 == 0 && ((t.subRows - 1) >> 2) < t.runA / va
+                      ? 1
+                      : 0;
+    info.direct_lds = t.directLds;
+}
+
 // Grid order of kernel T (both set-ups): diagonal (the second digit
 // rotated by skew times the first) unless asked otherwise, and optionally
 // contiguous tile ranges per XCD.
@@ -937,7 +958,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
         opt.exact_runs > 1 || (opt.block != 0 && opt.block != kBlock && opt.block != kBigBlock) ||
         opt.skew < 0 || opt.skew > 1024 || opt.shear < 0 || opt.shear > 2 || opt.shared_runs < 0 ||
         opt.shared_runs > 2 || opt.flat_runs < 0 || opt.flat_runs > 2 || opt.grid_order < 0 ||
-        opt.grid_order > 3)
+        opt.grid_order > 3 || opt.direct_lds < 0 || opt.direct_lds > 2)
         return HPTT_ERROR_INVALID_ARGUMENT;
 
     const int elem = dtype == HPTT_FLOAT32 ? 4 : 8;
@@ -1307,6 +1328,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
             const int64_t grid = plan->tile.numTiles;
             info.grid = grid < maxBlocks ? grid : maxBlocks;
             info.block = sharedTile ? kBlock : opt.block > 0 ? opt.block : kBlock;
+            set_direct_lds(opt, elem, info, plan->tile);
         }
     }
     if (k == HPTT_KERNEL_STREAM) {
@@ -1374,13 +1396,13 @@ void describe_plan(const hptt_plan_s* p, char* buf, size_t len) {
     snprintf(buf, len,
              "kernel=%s dtype=%s mode=%s fused=(%s) perm=(%s) run_a=%lld run_b=%lld "
              "dims_a=%d dims_b=%d vec=%d/%d pitch=%d rows=%d lds=%d tiles=%lld grid=%lld block=%d "
-             "hints=%d order=%d shear=%d shared=%d flat=%d gorder=%d",
+             "hints=%d order=%d shear=%d shared=%d flat=%d gorder=%d dlds=%d",
              kKernel[in.kernel], p->dtype == HPTT_FLOAT32 ? "f32" : "f64", kMode[in.mode], shape,
              perm, (long long)in.run_a, (long long)in.run_b, in.dims_a, in.dims_b, in.vec_a,
              in.vec_b, in.lds_pitch, in.rows_per_pass, in.lds_bytes, (long long)in.tiles,
              (long long)in.grid,
              in.block, in.hints, in.tile_order, in.shear, in.shared_runs, in.flat_runs,
-             in.grid_order);
+             in.grid_order, in.direct_lds);
 }
 
 }  // namespace hptt

@@ -36,54 +36,82 @@ template <typename T, int VA, int VB, int MODE, int HINT, int VAR, int BLOCK>
 __global__ __launch_bounds__(BLOCK)
 __attribute__((amdgpu_waves_per_eu(tile_waves_per_eu<MODE, VAR, BLOCK>())))
 void tile_kernel(const T* __restrict__ A, T* __restrict__ B, const TileArgs g, T alpha, T beta) {
-    constexpr int LB = tile_load_batch(MODE, VAR, BLOCK);
+    constexpr int LB = VAR == kDirect ? 0 : tile_load_batch(MODE, VAR, BLOCK);
     extern __shared__ int64_t smem[];
-    if constexpr (VAR == kShared) {
-        // runs that share indices: one pass per tile, the store phase
-        // gathering from LDS at positions from a table or computed
+    if constexpr (VAR == kDirect) {
+        // A fetched straight into LDS, one pass per tile (tile_load_direct)
         int64_t* rowOffA = smem;
-        int64_t* colOffB = smem + g.subRows;
-        int32_t* ldsCol = reinterpret_cast<int32_t*>(colOffB + g.nColS);
-        int32_t* ldsRow = ldsCol + g.nColS;
-        T* lds = reinterpret_cast<T*>(smem + shared_table_words(g));
+        int64_t* colOffB = smem + g.runB;
+        T* lds = reinterpret_cast<T*>(colOffB + g.runA);
         const int tid = int(threadIdx.x);
-        tile_tables_shared<DeviceMem, BLOCK>(g, tid, rowOffA, colOffB, ldsCol, ldsRow);
+        tile_tables<DeviceMem, BLOCK>(g, tid, rowOffA, colOffB);
         __syncthreads();
         bool first = true;
         for (uint32_t t = blockIdx.x; t < g.numTiles; t += gridDim.x) {
-            const TileBase tb = tile_base<true>(g, t);
-            if (!first) __syncthreads();  // the previous tile's LDS reads are done
+            const TileBase tb = tile_base(g, t);
+            if (g.flatR) {
+                // past the previous tile's load phase, the only reader of the
+                // row table; the barrier also ends its store phase
+                tile_rows_flat<DeviceMem, BLOCK>(g, tb, tid, rowOffA);
+                __syncthreads();
+            } else if (!first) {
+                __syncthreads();  // the previous tile's LDS reads are done
+            }
             first = false;
-            tile_load<DeviceMem, T, VA, HINT, VAR, BLOCK, LB>(g, tb, 0, tid, A, lds, rowOffA);
+            tile_load_direct<DeviceMem, T, VA, HINT, BLOCK>(g, tb, tid, A, lds, rowOffA);
             __syncthreads();
-            tile_store_shared<DeviceMem, T, VB, MODE, HINT, BLOCK>(g, tb, tid, B, lds, colOffB,
-                                                                    ldsCol, ldsRow, alpha, beta);
+            tile_store_rotated<DeviceMem, T, VA, VB, MODE, HINT, BLOCK>(g, tb, tid, B, lds, colOffB,
+                                                                        alpha, beta);
         }
-        return;
-    }
-    int64_t* rowOffA = smem;
-    int64_t* colOffB = smem + g.runB + g.shear;
-    T* lds = reinterpret_cast<T*>(colOffB + g.runA);
-    const int tid = int(threadIdx.x);
-    tile_tables<DeviceMem, BLOCK>(g, tid, rowOffA, colOffB);
-    __syncthreads();
-    bool first = true;
-    for (uint32_t t = blockIdx.x; t < g.numTiles; t += gridDim.x) {
-        const TileBase tb = tile_base(g, t);
-        if (g.flatR) {
-            // every lane is past the previous tile's load phase, the only
-            // reader of the row table; the barrier also ends its store phase
-            tile_rows_flat<DeviceMem, BLOCK>(g, tb, tid, rowOffA);
+    } else {
+        // the variants that stage A through registers
+        if constexpr (VAR == kShared) {
+            // runs that share indices: one pass per tile, the store phase
+            // gathering from LDS at positions from a table or computed
+            int64_t* rowOffA = smem;
+            int64_t* colOffB = smem + g.subRows;
+            int32_t* ldsCol = reinterpret_cast<int32_t*>(colOffB + g.nColS);
+            int32_t* ldsRow = ldsCol + g.nColS;
+            T* lds = reinterpret_cast<T*>(smem + shared_table_words(g));
+            const int tid = int(threadIdx.x);
+            tile_tables_shared<DeviceMem, BLOCK>(g, tid, rowOffA, colOffB, ldsCol, ldsRow);
             __syncthreads();
-            first = true;
+            bool first = true;
+            for (uint32_t t = blockIdx.x; t < g.numTiles; t += gridDim.x) {
+                const TileBase tb = tile_base<true>(g, t);
+                if (!first) __syncthreads();  // the previous tile's LDS reads are done
+                first = false;
+                tile_load<DeviceMem, T, VA, HINT, VAR, BLOCK, LB>(g, tb, 0, tid, A, lds, rowOffA);
+                __syncthreads();
+                tile_store_shared<DeviceMem, T, VB, MODE, HINT, BLOCK>(g, tb, tid, B, lds, colOffB,
+                                                                        ldsCol, ldsRow, alpha, beta);
+            }
+            return;
         }
-        for (int64_t r0 = 0; r0 < tb.validRows; r0 += g.subRows) {
-            if (!first) __syncthreads();  // the previous pass's LDS reads are done
-            first = false;
-            tile_load<DeviceMem, T, VA, HINT, VAR, BLOCK, LB>(g, tb, r0, tid, A, lds, rowOffA);
-            __syncthreads();
-            tile_store<DeviceMem, T, VB, MODE, HINT, VAR, BLOCK>(g, tb, r0, tid, B, lds, colOffB,
-                                                                 alpha, beta);
+        int64_t* rowOffA = smem;
+        int64_t* colOffB = smem + g.runB + g.shear;
+        T* lds = reinterpret_cast<T*>(colOffB + g.runA);
+        const int tid = int(threadIdx.x);
+        tile_tables<DeviceMem, BLOCK>(g, tid, rowOffA, colOffB);
+        __syncthreads();
+        bool first = true;
+        for (uint32_t t = blockIdx.x; t < g.numTiles; t += gridDim.x) {
+            const TileBase tb = tile_base(g, t);
+            if (g.flatR) {
+                // every lane is past the previous tile's load phase, the only
+                // reader of the row table; the barrier also ends its store phase
+                tile_rows_flat<DeviceMem, BLOCK>(g, tb, tid, rowOffA);
+                __syncthreads();
+                first = true;
+            }
+            for (int64_t r0 = 0; r0 < tb.validRows; r0 += g.subRows) {
+                if (!first) __syncthreads();  // the previous pass's LDS reads are done
+                first = false;
+                tile_load<DeviceMem, T, VA, HINT, VAR, BLOCK, LB>(g, tb, r0, tid, A, lds, rowOffA);
+                __syncthreads();
+                tile_store<DeviceMem, T, VB, MODE, HINT, VAR, BLOCK>(g, tb, r0, tid, B, lds, colOffB,
+                                                                     alpha, beta);
+            }
         }
     }
 }
@@ -104,14 +132,18 @@ const void* tile_vb(int vb) {
 
 template <typename T, int MODE, int HINT, int VAR, int BLOCK>
 const void* tile_va(int va, int vb) {
-    switch (va) {
-        case 1: return tile_vb<T, 1, MODE, HINT, VAR, BLOCK>(vb);
-        case 2: return tile_vb<T, 2, MODE, HINT, VAR, BLOCK>(vb);
-        case 4:
-            if constexpr (kMaxVec<T> >= 4) return tile_vb<T, 4, MODE, HINT, VAR, BLOCK>(vb);
-            return nullptr;
+    if constexpr (VAR == kDirect) {  // A vectors of 16 bytes only
+        return va == kMaxVec<T> ? tile_vb<T, kMaxVec<T>, MODE, HINT, VAR, BLOCK>(vb) : nullptr;
+    } else {
+        switch (va) {
+            case 1: return tile_vb<T, 1, MODE, HINT, VAR, BLOCK>(vb);
+            case 2: return tile_vb<T, 2, MODE, HINT, VAR, BLOCK>(vb);
+            case 4:
+                if constexpr (kMaxVec<T> >= 4) return tile_vb<T, 4, MODE, HINT, VAR, BLOCK>(vb);
+                return nullptr;
+        }
+        return nullptr;
     }
-    return nullptr;
 }
 
 template <typename T, int MODE, int VAR, int BLOCK>
@@ -126,19 +158,25 @@ const void* tile_hint(int hints, int va, int vb) {
 
 template <typename T, int VAR, int BLOCK>
 const void* tile_mode(int mode, int hints, int va, int vb) {
-    switch (mode) {
-        case kCopy: return tile_hint<T, kCopy, VAR, BLOCK>(hints, va, vb);
-        case kScale: return tile_hint<T, kScale, VAR, BLOCK>(hints, va, vb);
-        default: return tile_hint<T, kAxpby, VAR, BLOCK>(hints, va, vb);
+    if constexpr (VAR == kDirect) {  // B only written, 16-byte A vectors
+        if (mode == kAxpby || va != kMaxVec<T>) return nullptr;
+        if (mode == kCopy) return tile_hint<T, kCopy, VAR, BLOCK>(hints, va, vb);
+        return tile_hint<T, kScale, VAR, BLOCK>(hints, va, vb);
+    } else {
+        switch (mode) {
+            case kCopy: return tile_hint<T, kCopy, VAR, BLOCK>(hints, va, vb);
+            case kScale: return tile_hint<T, kScale, VAR, BLOCK>(hints, va, vb);
+            default: return tile_hint<T, kAxpby, VAR, BLOCK>(hints, va, vb);
+        }
     }
 }
 
 // Variants kShifted, kGeneral and kShared exist for kBlock threads only;
-// kFast for kBlock and kBigBlock.
+// kFast and kDirect for kBlock and kBigBlock.
 template <typename T, int VAR>
 const void* tile_kernel_address(int mode, int hints, int va, int vb, int block) {
     if (block == kBlock) return tile_mode<T, VAR, kBlock>(mode, hints, va, vb);
-    if constexpr (VAR == kFast)
+    if constexpr (VAR == kFast || VAR == kDirect)
         if (block == kBigBlock) return tile_mode<T, VAR, kBigBlock>(mode, hints, va, vb);
     return nullptr;
 }

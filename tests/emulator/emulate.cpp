@@ -106,6 +106,20 @@ struct HostMem {
         if (check_global(p, at, V, false) && !S->dry) memcpy(&r, p + off, sizeof(r));
         return r;
     }
+    // the lane's 16-byte slot is ldsWave + lane * V elements
+    template <typename T, int V, bool NT>
+    static void ld_lds(const T* p, int64_t off, T* ldsWave, int lane) {
+        static_assert(V * sizeof(T) == 16, "direct LDS loads move 16 bytes per lane");
+        int64_t at = off;
+        hptt::Vec<T, V> r;
+        memset(&r, 0, sizeof(r));
+        if (check_global(p, at, V, false) && !S->dry) memcpy(&r, p + off, sizeof(r));
+        T* slot = ldsWave + int64_t(lane) * V;
+        check_lds(slot, sizeof(r), true);
+        if (S->errors == 0) memcpy(slot, &r, sizeof(r));
+    }
+    static void wait_ld_lds() {}
+    static int wave_uniform(int x) { return x; }
     template <typename T, int V>
     static hptt::Vec<T, V> ldu(const T* p, int64_t off) {
         hptt::Vec<T, V> r;
@@ -182,14 +196,28 @@ void emu_tile_variant(const hptt_plan_s* p, const T* A, T* B, int64_t blockStrid
                 clear_written(0, g.runB * int64_t(sizeof(int64_t)));
                 for (int tid = 0; tid < BLOCK; ++tid) tile_rows_flat<HostMem, BLOCK>(g, tb, tid, rowOffA);
             }
-            for (int64_t r0 = 0; r0 < tb.validRows && S->errors == 0; r0 += g.subRows) {
+            if constexpr (VAR == kDirect) {
+                if (!tile_direct_lds(g, tb, VA)) {
+                    fail("tile of a direct-load plan that direct loads cannot serve", int64_t(t),
+                         tb.validCols);
+                    return;
+                }
                 clear_written(tableBytes, ldsBytes);
                 for (int tid = 0; tid < BLOCK; ++tid)
-                    tile_load<HostMem, T, VA, NT, VAR, BLOCK, tile_load_batch(MODE, VAR, BLOCK)>(
-                        g, tb, r0, tid, A, lds, rowOffA);
+                    tile_load_direct<HostMem, T, VA, NT, BLOCK>(g, tb, tid, A, lds, rowOffA);
                 for (int tid = 0; tid < BLOCK; ++tid)
-                    tile_store<HostMem, T, VB, MODE, NT, VAR, BLOCK>(g, tb, r0, tid, B, lds,
-                                                                     colOffB, alpha, beta);
+                    tile_store_rotated<HostMem, T, VA, VB, MODE, NT, BLOCK>(g, tb, tid, B, lds,
+                                                                            colOffB, alpha, beta);
+            } else {
+                for (int64_t r0 = 0; r0 < tb.validRows && S->errors == 0; r0 += g.subRows) {
+                    clear_written(tableBytes, ldsBytes);
+                    for (int tid = 0; tid < BLOCK; ++tid)
+                        tile_load<HostMem, T, VA, NT, VAR, BLOCK, tile_load_batch(MODE, VAR, BLOCK)>(
+                            g, tb, r0, tid, A, lds, rowOffA);
+                    for (int tid = 0; tid < BLOCK; ++tid)
+                        tile_store<HostMem, T, VB, MODE, NT, VAR, BLOCK>(g, tb, r0, tid, B, lds,
+                                                                         colOffB, alpha, beta);
+                }
             }
         }
     }
@@ -237,7 +265,8 @@ void emu_tile_shared(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride
 }
 
 // The variant and workgroup size hptt_exec would launch, or a forced variant:
-// kGeneral serves any plan, kShifted any plan kFast serves.
+// kGeneral serves any plan, kShifted and kFast any plan kDirect serves,
+// kShifted any plan kFast serves.
 template <typename T, int VA, int VB, int MODE, int NT>
 void emu_tile(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     using namespace hptt;
@@ -246,8 +275,23 @@ void emu_tile(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride) {
     g.misB = int32_t(S->misB % VB);
     int var = tile_variant(g);
     if (var != kShared &&
-        (S->forceVariant == kGeneral || (S->forceVariant == kShifted && var == kFast)))
+        (S->forceVariant == kGeneral ||
+         (S->forceVariant == kShifted && (var == kFast || var == kDirect)) ||
+         (S->forceVariant == kFast && var == kDirect)))
         var = S->forceVariant;
+    if constexpr (MODE != kAxpby && sizeof(T) * VA == 16) {
+        if (var == kDirect) {
+            if (p->info.block == kBigBlock)
+                emu_tile_variant<T, VA, VB, MODE, NT, kDirect, kBigBlock>(p, A, B, blockStride);
+            else
+                emu_tile_variant<T, VA, VB, MODE, NT, kDirect, kBlock>(p, A, B, blockStride);
+            return;
+        }
+    }
+    if (var == kDirect) {
+        fail("direct-load plan with B read or A vectors narrower than 16 bytes", VA, MODE);
+        return;
+    }
     if (var == kShared)
         emu_tile_shared<T, VA, VB, MODE, NT>(p, A, B, blockStride);
     else if (var == kGeneral)
@@ -388,9 +432,9 @@ extern "C" {
 // kernels).  misA/misB: the base pointers' element offsets from the 16-byte
 // grid, which the tile kernel shifts its runs by (vector accesses are checked
 // for alignment relative to that grid).  variant >= 0 runs the tile kernel
-// in that variant (kGeneral on any plan, kShifted on plans kFast serves;
-// plans whose runs share indices always run kShared) instead of the one
-// hptt_exec would launch.
+// in that variant (kGeneral on any plan, kShifted on plans kFast or kDirect
+// serves, kFast on plans kDirect serves; plans whose runs share indices
+// always run kShared) instead of the one hptt_exec would launch.
 // counts (numel
 // bytes, or NULL) is incremented at every B element written.  Only
 // workgroups 0, block_stride, 2*block_stride, ... are run.  Returns the

@@ -510,3 +510,35 @@ def test_sheared_whole_short_index_matches_oracle():
     err, msg, cnt = emu.run(p, counts=True)
     assert err == 0, msg
     assert cnt.min() == 1 and cnt.max() == 1
+
+
+def test_direct_lds_tiles_match_oracle():
+    """Tiles fetched straight into LDS (variant kDirect: B only written,
+    16-byte A vectors): random shapes with ragged row tails and ragged last
+    column chunks, fp32 and fp64, against the oracle, the same plans in the
+    register-staged variants, and plans with direct loads switched off."""
+    rng = np.random.default_rng(1950)
+    seen = 0
+    for it in range(800):
+        size_a, perm = random_problem(rng, max_dims=5, max_numel=60000,
+                                      extents=(2, 3, 4, 8, 12, 16, 17, 32, 33, 64, 65, 96))
+        dtype = "f32" if it % 3 else "f64"
+        alpha = (1.0, 1.5)[it % 2]
+        p = emu.plan(perm, size_a, alpha, 0.0, dtype)
+        if not p.info["direct_lds"]:
+            continue
+        seen += 1
+        _check(p, size_a, perm, alpha, 0.0, dtype, rng)
+        if it % 3 == 0:
+            q = emu.plan(perm, size_a, alpha, 0.0, dtype, direct_lds=2)
+            assert not q.info["direct_lds"]
+            _check(q, size_a, perm, alpha, 0.0, dtype, rng)
+        if it % 3 == 1:  # the register-staged variants on the same plan
+            _check(p, size_a, perm, alpha, 0.0, dtype, rng, variant="fast")
+            _check(p, size_a, perm, alpha, 0.0, dtype, rng, variant="shifted")
+    for size_a, knobs in (((128, 36), dict(run_a=32, run_b=16)), ((128, 64), dict(block=1024)),
+                          ((256, 32), dict(max_blocks=7)), ((64, 100), dict(run_a=128, run_b=32))):
+        p = emu.plan((1, 0), size_a, 1.5, 0.0, "f32", **knobs)
+        assert p.info["direct_lds"], p.describe()
+        _check(p, size_a, (1, 0), 1.5, 0.0, "f32", rng)
+    assert seen >= 30, seen
