@@ -443,9 +443,10 @@ __host__ __device__ inline void tile_store_fast(const TileArgs& g, const TileBas
     }
 }
 
-// Direct LDS loads (TileArgs::directLds): whether this tile takes them with
-// A vectors of VA elements.  Its columns must be whole vectors, and the
-// rotation of its rows (row / 4, below) must stay below the vectors per row.
+// Direct LDS loads (TileArgs::directLds): whether this tile can take them
+// with A vectors of VA elements: its columns whole vectors, and the rotation
+// of its rows (row / 4, below) below the vectors per row.  The plan builder
+// sets directLds only where every tile can; the host emulator checks it.
 __host__ __device__ inline bool tile_direct_lds(const TileArgs& g, const TileBase& tb, int va) {
     return g.directLds && g.subRows >= g.runB && g.runA % va == 0 && tb.validCols % va == 0 &&
            ((g.subRows - 1) >> 2) < g.runA / va;
