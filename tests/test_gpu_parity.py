@@ -100,6 +100,22 @@ def test_random_sweep():
     assert {"tile", "tile+shared", "axpby", "stream"} <= seen
 
 
+@pytest.mark.parametrize("w", [w for w in WORKLOADS if w.beta == 0], ids=lambda w: w.name)
+def test_workload_full_size_register_staged(w):
+    """The named workloads whose tiles are fetched straight into LDS, at full
+    size with the register-staged load phase instead (direct_lds = 2)."""
+    _say(f"[parity] {w.describe()} direct_lds=2")
+    A, _ = inputs(w)
+    B = torch.full_like(A, float("nan"))
+    want = orc.transpose(A.numpy(), w.size_a, w.perm, w.alpha, w.beta, None)
+    p = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype, direct_lds=2)
+    assert not p.info["direct_lds"]
+    dA, dB = A.cuda(), B.cuda()
+    p.exec(dA, dB)
+    torch.cuda.synchronize()
+    _assert_parity(dB.cpu().numpy(), want, w.dtype, p.describe())
+
+
 @pytest.mark.parametrize("knobs", [dict(kernel="generic"), dict(run_a=8, run_b=8),
                                    dict(run_a=3, run_b=5), dict(max_blocks=7),
                                    dict(max_vec=1), dict(store_hint=1, load_hint=1), dict(lds_pad=-1),
@@ -110,7 +126,8 @@ def test_random_sweep():
                                    dict(block=1024), dict(block=1024, run_a=64, run_b=64),
                                    dict(block=1024, max_blocks=5), dict(tile_order=4),
                                    dict(skew=3), dict(store_hint=2, load_hint=2),
-                                   dict(grid_order=2), dict(grid_order=3)],
+                                   dict(grid_order=2), dict(grid_order=3), dict(direct_lds=2),
+                                   dict(block=1024, run_a=128, run_b=32)],
                          ids=lambda k: ",".join(f"{a}={b}" for a, b in k.items()))
 def test_forced_variants(knobs):
     rng = np.random.default_rng(99)
@@ -124,10 +141,12 @@ def test_forced_variants(knobs):
     ("transpose6d_24x20x16x24x18x20_f32", dict(exact_runs=1, run_a=96, run_b=160, block=1024)),
     ("transpose6d_24x20x16x24x18x20_f32", dict(exact_runs=1, run_a=96, run_b=320, block=1024)),
     ("transpose5d_3x2x640x480x96_f32", dict(exact_runs=1, run_a=192, run_b=96, block=1024)),
-    ("transpose2d_8192x8192_f32", dict(block=1024, tile_order=4))],
+    ("transpose2d_8192x8192_f32", dict(block=1024, tile_order=4)),
+    ("transpose2d_8192x8192_f32", dict(block=1024, run_a=128, run_b=32))],
     ids=lambda x: x if isinstance(x, str) else ",".join(f"{a}={b}" for a, b in x.items()))
 def test_large_tiles_full_size(name, knobs):
-    """1024-thread workgroups and tiles above 64 KiB of LDS, at full size,
+    """1024-thread workgroups and tiles above 64 KiB of LDS (register-staged
+    and, for the 2-D 128x32 tile, fetched straight into LDS), at full size,
     against the whole oracle result."""
     from paper_1704_04374_amd.workloads import BY_NAME
     w = BY_NAME[name]
