@@ -811,25 +811,46 @@ bool choose_shared(const Fused& f, int elem, const hptt_options_t& opt, TileArgs
                     hptt_plan_info_t& bestInfo, double& bestScore) {
     static const int64_t aBytes[] = {512, 1024, 2048, 4096, 8192, 16384};
     static const int64_t bBytes[] = {128, 512, 2048, 8192};
-    bool found = false;
     const hptt_plan_info_t base = bestInfo;
-    for (int64_t ab : aBytes)
-        for (int64_t bb : bBytes) {
-            const int64_t tA = opt.run_a > 0 ? opt.run_a : ab / elem;
-            const int64_t tB = opt.run_b > 0 ? opt.run_b : bb / elem;
-            TileArgs t;
-            hptt_plan_info_t in = base;
-            const int64_t budget = base.mode == kAxpby ? kSharedLdsBudgetAxpby : kLdsBudget;
-            if (!setup_shared(f, elem, tA, tB, opt, budget, t, in)) continue;
-            const double sc =
-                tile_score(t.runA, t.runB, t.runA * int64_t(t.subRows), t.numTiles, elem);
-            if (!found || sc > bestScore) {
-                found = true;
-                bestScore = sc;
-                best = t;
-                bestInfo = in;
+    // best tile within an LDS budget (and at most maxRows rows, if > 0)
+    auto search = [&](int64_t budget, int32_t maxRows, TileArgs& bt, hptt_plan_info_t& bi,
+                      double& bs) {
+        bool fnd = false;
+        for (int64_t ab : aBytes)
+            for (int64_t bb : bBytes) {
+                const int64_t tA = opt.run_a > 0 ? opt.run_a : ab / elem;
+                const int64_t tB = opt.run_b > 0 ? opt.run_b : bb / elem;
+                TileArgs t;
+                hptt_plan_info_t in = base;
+                if (!setup_shared(f, elem, tA, tB, opt, budget, t, in)) continue;
+                if (maxRows > 0 && t.subRows > maxRows) continue;
+                const double sc =
+                    tile_score(t.runA, t.runB, t.runA * int64_t(t.subRows), t.numTiles, elem);
+                if (!fnd || sc > bs) {
+                    fnd = true;
+                    bs = sc;
+                    bt = t;
+                    bi = in;
+                }
             }
+        return fnd;
+    };
+    const bool readsB = base.mode == kAxpby;
+    bool found = search(readsB ? kSharedLdsBudgetAxpby : kLdsBudget, 0, best, bestInfo, bestScore);
+    // With B read, fp32 tiles of one or two rows take the larger budget too
+    // (MI355X, 40 against 20 KiB: 2x26250x4x238 [1,3,0,2] 1.26x, single-row
+    // tiles of 2100 -> 4040 elements; 2925x1207x2x7 [2,0,3,1] 1.13x; taller
+    // tiles split from 1.10x to 0.93x, and an fp64 two-row tile lost 5 %).
+    if (found && readsB && elem == 4 && best.subRows <= 2) {
+        TileArgs t2;
+        hptt_plan_info_t i2 = base;
+        double s2 = 0;
+        if (search(kLdsBudget, 2, t2, i2, s2)) {
+            best = t2;
+            bestInfo = i2;
+            bestScore = s2;
         }
+    }
     return found;
 }
 

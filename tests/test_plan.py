@@ -417,6 +417,19 @@ def test_sheared_tiles_keep_a_short_stride1_index_whole(size_a, perm, dtype, who
     assert i["shear"] > 0 and i["run_a"] == 29
 
 
+def test_shared_runs_budget_with_b_read():
+    """fp32 shared-run tiles of one or two rows take 40 KiB of LDS when B is
+    read (the usual budget then is 20 KiB); taller tiles and fp64 do not."""
+    one = hptt.create_plan((1, 3, 0, 2), (2, 26250, 4, 238), 1.0, 1.0, "f32").info
+    assert one["shared_runs"] and one["rows_per_pass"] == 1 and one["lds_bytes"] > 20 * 1024
+    assert hptt.create_plan((1, 3, 0, 2), (2, 26250, 4, 238), 1.0, 0.0,
+                            "f32").info["lds_bytes"] <= 40 * 1024
+    tall = hptt.create_plan((2, 1, 4, 3, 0), (12, 3, 2, 2293, 303), 1.0, 1.0, "f32").info
+    assert tall["shared_runs"] and tall["rows_per_pass"] > 2 and tall["lds_bytes"] <= 20 * 1024
+    f64 = hptt.create_plan((3, 0, 1, 4, 2), (10, 71, 2, 2, 17606), 1.0, 1.0, "f64").info
+    assert f64["shared_runs"] and f64["rows_per_pass"] <= 2 and f64["lds_bytes"] <= 20 * 1024
+
+
 @pytest.mark.parametrize("size_a,perm,want", [
     # the window of resident tiles touches far fewer B regions with A4 first
     ((24, 20, 16, 24, 18, 20), (5, 2, 0, 4, 1, 3), 2),
