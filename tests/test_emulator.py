@@ -328,7 +328,7 @@ def test_shared_run_tiles_match_oracle(dtype):
     bit-exact, each B element written once."""
     rng = np.random.default_rng(1704 + len(dtype))
     seen = chunked = 0
-    for it in range(140):
+    for it in range(200):
         size_a, perm = random_problem(rng, max_dims=6, extents=(1, 2, 3, 4, 5, 7, 12, 17, 33, 40),
                                       max_numel=30000)
         alpha, beta = CASES[it % len(CASES)]
