@@ -127,6 +127,15 @@ int autotune_candidates(const int32_t* perm, int32_t N, const int64_t* sizeA,
             v.grid_order = go;
             var.push_back({1, v});
         }
+        // tiles dealt to the XCDs in groups of 16 (grid-digit order) or one
+        // by one, whichever the quick path did not take
+        for (int32_t xg = 1; xg <= 16; xg += 15) {
+            hptt_options_t v;
+            memset(&v, 0, sizeof(v));
+            v.xcd_group = xg;
+            if (xg > 1) v.tile_order = 1;
+            var.push_back({1, v});
+        }
         // tiles staged through registers instead of fetched straight into LDS
         {
             hptt_options_t v;

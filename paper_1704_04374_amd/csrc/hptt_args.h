@@ -76,6 +76,7 @@ struct TileArgs {
     int32_t gChunkR;     // grid digit that counts chunks of the last B-run index, or -1
     int32_t skew;        // s > 0: grid digit 1 is shifted by s times digit 0 (diagonal order)
     int32_t xcdSplit;    // 1: tile numbers dealt so that each XCD gets a contiguous range
+    int32_t xcdGroupLog; // L > 0 (without xcdSplit): each XCD takes 2^L consecutive tiles at a time
     int32_t alignedA;    // 1 when every A run is whole 128-byte lines (set by the plan builder)
     int32_t alignedB;    // 1 when every B run is whole 128-byte lines
     int32_t subRows;     // rows staged through LDS per pass (runB, or runB / passes)

@@ -60,13 +60,25 @@ struct TileBase {
 //
 // With g.xcdSplit the workgroup number is first mapped so that the workgroups
 // one XCD receives (numbers x, x + 8, x + 16, ...) take a contiguous range of
-// tile numbers: tiles that share cache lines then share an L2.
+// tile numbers: tiles that share cache lines then share an L2.  With
+// g.xcdGroupLog = L instead, XCD x takes 2^L consecutive tile numbers at a
+// time: round n of 8 * 2^L workgroups gives XCD x the tiles from
+// (8n + x) * 2^L on, so neighbouring tiles share an L2 while the tiles in
+// flight remain a near-contiguous range; the last, incomplete round keeps
+// the plain numbering (a bijection either way).
 template <bool OVL = false>
 __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
     if (g.xcdSplit) {
         const uint32_t x = t % kXcds, i = t / kXcds;
         const uint32_t q = g.numTiles / kXcds, r = g.numTiles % kXcds;
         t = x * q + (x < r ? x : r) + i;
+    } else if (g.xcdGroupLog) {
+        const uint32_t L = uint32_t(g.xcdGroupLog);
+        const uint32_t span = uint32_t(kXcds) << L;
+        if (t < g.numTiles / span * span) {
+            const uint32_t x = t % kXcds, i = t / kXcds;
+            t = (i >> L) * span + (x << L) + (i & ((1u << L) - 1u));
+        }
     }
     TileBase tb;
     tb.a = 0;
@@ -84,7 +96,9 @@ __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
         t = q;
         if (k == 0) j0 = jj;
         if (k == 1 && g.skew) {
-            const uint32_t js = j0 * uint32_t(g.skew);  // below 2^32: checked by the plan
+            // with XCD groups the rotation advances once per group, so that
+            // a group's tiles are neighbours along digit 0
+            const uint32_t js = (j0 >> g.xcdGroupLog) * uint32_t(g.skew);  // below 2^32 (plan)
             const uint32_t r = js - fast_div(js, g.gExt[1]) * g.gExt[1].d;  // (s*j0) mod n1
             jj += r;
             if (jj >= g.gExt[1].d) jj -= g.gExt[1].d;

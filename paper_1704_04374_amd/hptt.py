@@ -45,7 +45,8 @@ class Options(ctypes.Structure):
                 ("depth", ctypes.c_int32), ("min_tile", ctypes.c_int32),
                 ("block", ctypes.c_int32), ("skew", ctypes.c_int32), ("shear", ctypes.c_int32),
                 ("shared_runs", ctypes.c_int32), ("flat_runs", ctypes.c_int32),
-                ("grid_order", ctypes.c_int32), ("direct_lds", ctypes.c_int32)]
+                ("grid_order", ctypes.c_int32), ("direct_lds", ctypes.c_int32),
+                ("xcd_group", ctypes.c_int32)]
 
 
 class AutotuneReport(ctypes.Structure):
@@ -81,7 +82,7 @@ class PlanInfo(ctypes.Structure):
                 ("tile_order", ctypes.c_int32), ("depth", ctypes.c_int32),
                 ("shear", ctypes.c_int32), ("shared_runs", ctypes.c_int32),
                 ("flat_runs", ctypes.c_int32), ("grid_order", ctypes.c_int32),
-                ("direct_lds", ctypes.c_int32)]
+                ("direct_lds", ctypes.c_int32), ("xcd_group", ctypes.c_int32)]
 
     def as_dict(self) -> dict:
         n = self.ndim
@@ -96,7 +97,8 @@ class PlanInfo(ctypes.Structure):
                 "hints": self.hints, "mode": MODES[self.mode],
                 "tile_order": self.tile_order, "depth": self.depth, "shear": self.shear,
                 "shared_runs": self.shared_runs, "flat_runs": self.flat_runs,
-                "grid_order": self.grid_order, "direct_lds": self.direct_lds}
+                "grid_order": self.grid_order, "direct_lds": self.direct_lds,
+                "xcd_group": self.xcd_group}
 
 
 # Every entry point declared in include/hptt.h and include/hptt_yardstick.h.

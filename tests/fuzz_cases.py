@@ -34,7 +34,7 @@ def case(seed: int, i: int) -> dict:
     knobs = {}
     if rng.random() >= 0.45:
         for k in rng.choice(["run", "shear", "flat", "shared", "gorder", "order", "block", "depth",
-                             "hints", "vec", "kernel", "passes", "maxblocks"],
+                             "hints", "vec", "kernel", "passes", "maxblocks", "xcd"],
                             size=int(rng.integers(1, 3)), replace=False):
             if k == "run":
                 knobs["run_a"] = int(rng.choice([4, 8, 16, 32, 64, 128, 256]))
@@ -64,6 +64,8 @@ def case(seed: int, i: int) -> dict:
                 knobs["row_passes"] = int(rng.integers(2, 4))
             elif k == "maxblocks":
                 knobs["max_blocks"] = int(rng.choice([1, 7, 64, 300]))
+            elif k == "xcd":
+                knobs["xcd_group"] = int(rng.choice([2, 16, 1024]))
     outer = None
     if rng.random() < 0.2:
         size_b = [size[p] for p in perm]

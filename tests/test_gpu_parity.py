@@ -127,7 +127,9 @@ def test_workload_full_size_register_staged(w):
                                    dict(block=1024, max_blocks=5), dict(tile_order=4),
                                    dict(skew=3), dict(store_hint=2, load_hint=2),
                                    dict(grid_order=2), dict(grid_order=3), dict(direct_lds=2),
-                                   dict(block=1024, run_a=128, run_b=32)],
+                                   dict(block=1024, run_a=128, run_b=32), dict(xcd_group=16),
+                                   dict(xcd_group=2, max_blocks=5),
+                                   dict(xcd_group=1024, tile_order=1)],
                          ids=lambda k: ",".join(f"{a}={b}" for a, b in k.items()))
 def test_forced_variants(knobs):
     rng = np.random.default_rng(99)
@@ -142,12 +144,14 @@ def test_forced_variants(knobs):
     ("transpose6d_24x20x16x24x18x20_f32", dict(exact_runs=1, run_a=96, run_b=320, block=1024)),
     ("transpose5d_3x2x640x480x96_f32", dict(exact_runs=1, run_a=192, run_b=96, block=1024)),
     ("transpose2d_8192x8192_f32", dict(block=1024, tile_order=4)),
-    ("transpose2d_8192x8192_f32", dict(block=1024, run_a=128, run_b=32))],
+    ("transpose2d_8192x8192_f32", dict(block=1024, run_a=128, run_b=32)),
+    ("transpose2d_8192x8192_f32", dict(xcd_group=16)),
+    ("transpose5d_3x2x640x480x96_f32", dict(xcd_group=8, tile_order=1))],
     ids=lambda x: x if isinstance(x, str) else ",".join(f"{a}={b}" for a, b in x.items()))
 def test_large_tiles_full_size(name, knobs):
     """1024-thread workgroups and tiles above 64 KiB of LDS (register-staged
-    and, for the 2-D 128x32 tile, fetched straight into LDS), at full size,
-    against the whole oracle result."""
+    and, for the 2-D 128x32 tile, fetched straight into LDS), and tiles dealt
+    to the XCDs in groups, at full size, against the whole oracle result."""
     from paper_1704_04374_amd.workloads import BY_NAME
     w = BY_NAME[name]
     _say(f"[parity] {w.describe()} {knobs}")
@@ -157,7 +161,10 @@ def test_large_tiles_full_size(name, knobs):
     want = orc.transpose(A.numpy(), w.size_a, w.perm, w.alpha, w.beta,
                          B0.numpy() if w.beta != 0 else None)
     p = hptt.create_plan(w.perm, w.size_a, w.alpha, w.beta, w.dtype, **knobs)
-    assert p.info["block"] == 1024
+    if "block" in knobs:
+        assert p.info["block"] == 1024
+    if "xcd_group" in knobs:
+        assert p.info["xcd_group"] == knobs["xcd_group"]
     dA, dB = A.cuda(), B0.cuda()
     p.exec(dA, dB)
     torch.cuda.synchronize()

@@ -470,3 +470,30 @@ def test_hptt_log_prints_each_plan():
         if lines:
             assert "fused=(64,32) perm=(1,0)" in got[0] and "kernel=tile" in got[0]
             assert "fused=(1920,32) perm=(1,0)" in got[1]
+
+
+def test_xcd_group_rule():
+    """Tiles whose A runs are at most 256 bytes and do not start on 128-byte
+    lines are dealt to the XCDs 16 at a time in grid-digit order; aligned
+    runs, longer runs and shared-run tiles keep the diagonal round robin;
+    forced values are kept, and the contiguous XCD ranges of tile orders 3
+    and 4 replace the groups."""
+    for beta in (0.0, 1.0):
+        short = hptt.create_plan((1, 0), (2193, 22800), 1.0, beta).info
+        assert short["xcd_group"] == 16 and short["tile_order"] == 1, short
+        assert short["run_a"] * 4 <= 256
+    assert hptt.create_plan((1, 0), (8192, 8192)).info["xcd_group"] == 1       # whole lines
+    long_run = hptt.create_plan((1, 0), (3001, 16384)).info                     # 131 elements
+    assert long_run["run_a"] * 4 > 256 and long_run["xcd_group"] == 1
+    assert long_run["tile_order"] == 2
+    shared = hptt.create_plan((1, 3, 0, 2), (2, 26250, 4, 238)).info
+    assert shared["shared_runs"] and shared["xcd_group"] == 1
+    forced = hptt.create_plan((1, 0), (2193, 22800), xcd_group=1).info
+    assert forced["xcd_group"] == 1 and forced["tile_order"] == 2
+    forced = hptt.create_plan((1, 0), (8192, 8192), xcd_group=64).info
+    assert forced["xcd_group"] == 64 and forced["tile_order"] == 2
+    ranges = hptt.create_plan((1, 0), (2193, 22800), tile_order=3, xcd_group=16).info
+    assert ranges["xcd_group"] == 0 and ranges["tile_order"] == 3
+    for bad in (3, 12, 2048, -1):
+        with pytest.raises(hptt.HpttError):
+            hptt.create_plan((1, 0), (64, 32), xcd_group=bad)
