@@ -30,6 +30,14 @@ struct DeviceMem {
     __device__ __forceinline__ static T ld1(const T* p, int64_t off) {
         return p[off];
     }
+    // The aligned vector of V elements at p + off when only some of them
+    // belong to the tensor (the caller keeps those and drops the rest): an
+    // aligned access of at most 16 bytes lies inside one page, which holds a
+    // valid element and so is mapped.  One load instead of one per element.
+    template <typename T, int V, bool NT>
+    __device__ __forceinline__ static Vec<T, V> ld_part(const T* p, int64_t off) {
+        return ld<T, V, NT>(p, off);
+    }
     // V consecutive elements from any element boundary: one global_load of
     // V*sizeof(T) bytes at a dword-aligned address (gfx950 serves those
     // in both of its alignment modes).

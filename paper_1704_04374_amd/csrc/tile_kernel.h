@@ -81,7 +81,8 @@ void tile_kernel(const T* __restrict__ A, T* __restrict__ B, const TileArgs g, T
                 const TileBase tb = tile_base<true>(g, t);
                 if (!first) __syncthreads();  // the previous tile's LDS reads are done
                 first = false;
-                tile_load<DeviceMem, T, VA, HINT, VAR, BLOCK, LB>(g, tb, 0, tid, A, lds, rowOffA);
+                tile_load<DeviceMem, T, VA, HINT, VAR, BLOCK, LB, tile_part_loads(MODE, VAR)>(
+                    g, tb, 0, tid, A, lds, rowOffA);
                 __syncthreads();
                 tile_store_shared<DeviceMem, T, VB, MODE, HINT, BLOCK>(g, tb, tid, B, lds, colOffB,
                                                                         ldsCol, ldsRow, alpha, beta);
@@ -107,7 +108,8 @@ void tile_kernel(const T* __restrict__ A, T* __restrict__ B, const TileArgs g, T
             for (int64_t r0 = 0; r0 < tb.validRows; r0 += g.subRows) {
                 if (!first) __syncthreads();  // the previous pass's LDS reads are done
                 first = false;
-                tile_load<DeviceMem, T, VA, HINT, VAR, BLOCK, LB>(g, tb, r0, tid, A, lds, rowOffA);
+                tile_load<DeviceMem, T, VA, HINT, VAR, BLOCK, LB, tile_part_loads(MODE, VAR)>(
+                    g, tb, r0, tid, A, lds, rowOffA);
                 __syncthreads();
                 tile_store<DeviceMem, T, VB, MODE, HINT, VAR, BLOCK>(g, tb, r0, tid, B, lds, colOffB,
                                                                      alpha, beta);

@@ -88,6 +88,20 @@ bool check_global(const T* p, int64_t& off, int V, bool isStore, bool aligned = 
     return true;
 }
 
+// whether p + off lies inside the tensor p points into (A or B)
+template <typename T>
+bool is_a(const T* p) {
+    return distance(p, S->A, S->numelA * int64_t(sizeof(T))) <=
+           distance(p, S->B, S->numelB * int64_t(sizeof(T)));
+}
+template <typename T>
+bool in_tensor(const T* p, int64_t off) {
+    const bool isA = is_a(p);
+    const intptr_t d = reinterpret_cast<intptr_t>(p) + intptr_t(off) * intptr_t(sizeof(T)) -
+                       reinterpret_cast<intptr_t>(isA ? S->A : S->B);
+    return d >= 0 && d / intptr_t(sizeof(T)) < (isA ? S->numelA : S->numelB);
+}
+
 void check_lds(const void* p, int64_t bytes, bool isStore) {
     const int64_t at = static_cast<const uint8_t*>(p) - S->lds.data();
     if (at < 0 || at + bytes > int64_t(S->lds.size())) { fail("LDS access out of bounds", at, bytes); return; }
@@ -126,6 +140,34 @@ struct HostMem {
         memset(&r, 0, sizeof(r));
         int64_t at = off;
         if (check_global(p, at, V, false, false) && !S->dry) memcpy(&r, p + off, sizeof(r));
+        return r;
+    }
+    // an aligned vector of which at least one element is inside the tensor;
+    // only those are copied (the device reads the rest from the same page)
+    template <typename T, int V, bool NT>
+    static hptt::Vec<T, V> ld_part(const T* p, int64_t off) {
+        hptt::Vec<T, V> r;
+        memset(&r, 0, sizeof(r));
+        int first = -1;
+        for (int e = 0; e < V && first < 0; ++e) {
+            int64_t at = off + e;
+            if (in_tensor(p, at)) first = e;
+        }
+        if (first < 0) {
+            fail("partial vector without an element inside the tensor", off, V);
+            return r;
+        }
+        int64_t at = off + first;
+        check_global(p, at, 1, false);  // the tensor, the direction, B read only when beta != 0
+        const int64_t start = at - first;
+        if ((start + (is_a(p) ? S->misA : S->misB)) % V != 0) {
+            fail("misaligned partial vector", start, V);
+            return r;
+        }
+        for (int e = 0; e < V; ++e) {
+            int64_t x = off + e;
+            if (in_tensor(p, x) && !S->dry) r.v[e] = p[off + e];
+        }
         return r;
     }
     template <typename T>
@@ -212,7 +254,8 @@ void emu_tile_variant(const hptt_plan_s* p, const T* A, T* B, int64_t blockStrid
                 for (int64_t r0 = 0; r0 < tb.validRows && S->errors == 0; r0 += g.subRows) {
                     clear_written(tableBytes, ldsBytes);
                     for (int tid = 0; tid < BLOCK; ++tid)
-                        tile_load<HostMem, T, VA, NT, VAR, BLOCK, tile_load_batch(MODE, VAR, BLOCK)>(
+                        tile_load<HostMem, T, VA, NT, VAR, BLOCK, tile_load_batch(MODE, VAR, BLOCK),
+                                  tile_part_loads(MODE, VAR)>(
                             g, tb, r0, tid, A, lds, rowOffA);
                     for (int tid = 0; tid < BLOCK; ++tid)
                         tile_store<HostMem, T, VB, MODE, NT, VAR, BLOCK>(g, tb, r0, tid, B, lds,
@@ -255,7 +298,8 @@ void emu_tile_shared(const hptt_plan_s* p, const T* A, T* B, int64_t blockStride
             const TileBase tb = tile_base<true>(g, uint32_t(t));
             clear_written(tableBytes, ldsBytes);
             for (int tid = 0; tid < kBlock; ++tid)
-                tile_load<HostMem, T, VA, NT, kShared, kBlock, tile_load_batch(MODE, kShared, kBlock)>(
+                tile_load<HostMem, T, VA, NT, kShared, kBlock, tile_load_batch(MODE, kShared, kBlock),
+                          tile_part_loads(MODE, kShared)>(
                     g, tb, 0, tid, A, lds, rowOffA);
             for (int tid = 0; tid < kBlock; ++tid)
                 tile_store_shared<HostMem, T, VB, MODE, NT, kBlock>(g, tb, tid, B, lds, colOffB,
