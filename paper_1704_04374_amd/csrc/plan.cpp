@@ -227,15 +227,16 @@ void set_direct_lds(const hptt_options_t& opt, int elem, hptt_plan_info_t& info,
 // L2s (rocprofv3 on MI355X: 2193x22800 [1,0] fetched 2.46x A's bytes,
 // 112582x444 2.35x).  Groups of 16 tiles per XCD, in grid-digit order (the
 // diagonal rotation would part the neighbours), fetch each line once.  Runs
-// of up to 256 bytes only, where the boundary line is a third of the run or
-// more: MI355X, the 25 cases of the 57-case sweep this picks, -0.4 to +29 %
-// (mean +9.5 %) with beta = 0 and -1.5 to +14 % (mean +3.8 %) with beta = 1;
-// longer runs (512 bytes over a power-of-two B stride) lost up to 6 % with
-// beta = 1 to the diagonal order's spread over the HBM channels, and
-// shared-run tiles 1-3 %.
+// of up to 320 bytes only, where the boundary lines are a large share of the
+// run: MI355X, the cases of the 57-case sweep with runs up to 256 bytes,
+// -0.4 to +29 % (mean +9.5 %) with beta = 0 and -1.5 to +14 % (mean +3.8 %)
+// with beta = 1; runs of 257-320 bytes (fp32 and fp64) -1.6 to +13 %, mean
+// +2.6 %; runs of 500 bytes and more over a power-of-two B stride lost up to
+// 6 % with beta = 1 to the diagonal order's spread over the HBM channels,
+// and shared-run tiles 1-3 %.
 void set_xcd_groups(const hptt_options_t& opt, int elem, hptt_plan_info_t& info, TileArgs& t) {
     if (opt.xcd_group != 0 || opt.tile_order != 0 || t.shared || t.alignedA ||
-        t.runA * elem > 2 * kLine)
+        t.runA * elem > 320)
         return;
     t.skew = 0;
     t.xcdGroupLog = 4;

@@ -473,7 +473,7 @@ def test_hptt_log_prints_each_plan():
 
 
 def test_xcd_group_rule():
-    """Tiles whose A runs are at most 256 bytes and do not start on 128-byte
+    """Tiles whose A runs are at most 320 bytes and do not start on 128-byte
     lines are dealt to the XCDs 16 at a time in grid-digit order; aligned
     runs, longer runs and shared-run tiles keep the diagonal round robin;
     forced values are kept, and the contiguous XCD ranges of tile orders 3
@@ -482,6 +482,10 @@ def test_xcd_group_rule():
         short = hptt.create_plan((1, 0), (2193, 22800), 1.0, beta).info
         assert short["xcd_group"] == 16 and short["tile_order"] == 1, short
         assert short["run_a"] * 4 <= 256
+        mid = hptt.create_plan((1, 0), (66, 757576), 1.0, beta).info    # 264-byte runs
+        assert mid["xcd_group"] == 16 and 256 < mid["run_a"] * 4 <= 320, mid
+        f64 = hptt.create_plan((3, 1, 0, 2), (77, 1651, 2, 99), 1.0, beta, "f64").info
+        assert f64["xcd_group"] == 16 and f64["run_a"] * 8 <= 320, f64
     assert hptt.create_plan((1, 0), (8192, 8192)).info["xcd_group"] == 1       # whole lines
     long_run = hptt.create_plan((1, 0), (3001, 16384)).info                     # 131 elements
     assert long_run["run_a"] * 4 > 256 and long_run["xcd_group"] == 1
