@@ -133,15 +133,16 @@ typedef struct {
                               16 bytes, the tile is staged in one pass and its
                               column count is whole vectors: 0 = where it
                               applies, 2 = never */
-    int32_t xcd_group;     /* TILE: workgroups are dealt to MI355X's 8 XCDs
-                              (each with its own L2) round robin; with k > 1
-                              each XCD takes tile numbers k consecutive at a
-                              time, so tiles that share 128-byte lines of A
-                              (runs that do not start on lines) share an L2
-                              while the tiles in flight stay a near-contiguous
-                              range: 0 = choose, 1 = no grouping, k = a power
-                              of two up to 1024.  Ignored with tile_order 3
-                              and 4, which give each XCD one contiguous range */
+    int32_t xcd_group;     /* TILE, STREAM: workgroups are dealt to MI355X's
+                              8 XCDs (each with its own L2) round robin; with
+                              k > 1 each XCD takes tile (block) numbers k
+                              consecutive at a time, so tiles that share
+                              128-byte lines of A (runs that do not start on
+                              lines) share an L2 while the tiles in flight
+                              stay a near-contiguous range: 0 = choose (STREAM:
+                              no grouping), 1 = no grouping, k = a power of two
+                              up to 1024.  Ignored with tile_order 3 and 4,
+                              which give each XCD one contiguous range */
 } hptt_options_t;
 
 /* What the plan builder decided; for inspection and tests. */
@@ -190,10 +191,11 @@ typedef struct {
     int32_t direct_lds;                /* TILE: 1 when tiles are fetched straight into
                                           LDS (by launches that take the variant
                                           with every run on the 16-byte grid) */
-    int32_t xcd_group;                 /* TILE: consecutive tile numbers each XCD takes
-                                          at a time (1 = plain round robin; 0 with
-                                          the contiguous XCD ranges of tile_order 3
-                                          and 4) */
+    int32_t xcd_group;                 /* TILE, STREAM: consecutive tile (block) numbers
+                                          each XCD takes at a time (1 = plain round
+                                          robin; 0 with the contiguous XCD ranges of
+                                          tile_order 3 and 4, and for the other
+                                          kernels) */
 } hptt_plan_info_t;
 
 /*

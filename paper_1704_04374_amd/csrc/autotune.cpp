@@ -49,9 +49,13 @@ std::mutex g_mutex;
 std::map<std::string, hptt_options_t> g_wisdom;
 
 bool same_plan(const hptt_plan_s& a, const hptt_plan_s& b) {
-    if (a.info.kernel != b.info.kernel || a.info.hints != b.info.hints) return false;
+    if (a.info.kernel != b.info.kernel || a.info.hints != b.info.hints ||
+        a.info.vec_a != b.info.vec_a || a.info.vec_b != b.info.vec_b)
+        return false;
     if (a.info.kernel == HPTT_KERNEL_TILE)
         return memcmp(&a.tile, &b.tile, sizeof(a.tile)) == 0;
+    if (a.info.kernel == HPTT_KERNEL_STREAM)  // row or flat walk, XCD groups
+        return memcmp(&a.stream, &b.stream, sizeof(a.stream)) == 0;
     return true;
 }
 
@@ -156,6 +160,12 @@ int autotune_candidates(const int32_t* perm, int32_t N, const int64_t* sizeA,
             for (int32_t fr = 1; fr <= 2; ++fr) {
                 memset(&v, 0, sizeof(v));
                 v.flat_runs = fr;
+                cand.push_back(v);
+            }
+            // blocks dealt to the XCDs 16 or 64 at a time
+            for (int32_t xg = 16; xg <= 64; xg *= 4) {
+                memset(&v, 0, sizeof(v));
+                v.xcd_group = xg;
                 cand.push_back(v);
             }
         }

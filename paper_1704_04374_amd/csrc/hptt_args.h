@@ -180,6 +180,10 @@ struct StreamArgs {
     // elements come from at most two rows (rowLen >= V), read from A one by
     // one.  L divides a flat B offset into (row, column).
     int32_t flatB;
+    // L > 0: the workgroups one XCD receives take block numbers 2^L
+    // consecutive at a time (xcd_group_map), so that blocks reading
+    // neighbouring rows of A share an L2
+    int32_t xcdGroupLog;
     FastDiv L;
     int32_t nO;                 // outer B positions 1..N'-1
     FastDiv W[3];               // vectors per row for V = 1, 2, 4

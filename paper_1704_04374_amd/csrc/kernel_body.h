@@ -66,6 +66,15 @@ struct TileBase {
 // (8n + x) * 2^L on, so neighbouring tiles share an L2 while the tiles in
 // flight remain a near-contiguous range; the last, incomplete round keeps
 // the plain numbering (a bijection either way).
+__host__ __device__ inline uint32_t xcd_group_map(uint32_t t, uint32_t n, uint32_t L) {
+    const uint32_t span = uint32_t(kXcds) << L;
+    if (t < n / span * span) {
+        const uint32_t x = t % kXcds, i = t / kXcds;
+        t = (i >> L) * span + (x << L) + (i & ((1u << L) - 1u));
+    }
+    return t;
+}
+
 template <bool OVL = false>
 __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
     if (g.xcdSplit) {
@@ -73,12 +82,7 @@ __host__ __device__ inline TileBase tile_base(const TileArgs& g, uint32_t t) {
         const uint32_t q = g.numTiles / kXcds, r = g.numTiles % kXcds;
         t = x * q + (x < r ? x : r) + i;
     } else if (g.xcdGroupLog) {
-        const uint32_t L = uint32_t(g.xcdGroupLog);
-        const uint32_t span = uint32_t(kXcds) << L;
-        if (t < g.numTiles / span * span) {
-            const uint32_t x = t % kXcds, i = t / kXcds;
-            t = (i >> L) * span + (x << L) + (i & ((1u << L) - 1u));
-        }
+        t = xcd_group_map(t, g.numTiles, uint32_t(g.xcdGroupLog));
     }
     TileBase tb;
     tb.a = 0;

@@ -23,13 +23,15 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(const T* __restrict__ A,
     constexpr uint64_t per = uint64_t(kBlock) * items_per_lane(int(sizeof(T)), V);
     const uint64_t step = uint64_t(gridDim.x) * per;
     const uint64_t items = g.numItems[log2_width(V)];
+    const uint32_t blk = g.xcdGroupLog ? xcd_group_map(blockIdx.x, gridDim.x, uint32_t(g.xcdGroupLog))
+                                       : blockIdx.x;
     if (g.flatB) {
-        for (uint64_t first = uint64_t(blockIdx.x) * per; first < items; first += step)
+        for (uint64_t first = uint64_t(blk) * per; first < items; first += step)
             stream_items_flat<DeviceMem, T, V, MODE, HINT>(g, uint32_t(first), int(threadIdx.x), A,
                                                            B, alpha, beta);
         return;
     }
-    for (uint64_t first = uint64_t(blockIdx.x) * per; first < items; first += step)
+    for (uint64_t first = uint64_t(blk) * per; first < items; first += step)
         stream_items<DeviceMem, T, V, MODE, HINT>(g, uint32_t(first), int(threadIdx.x), A, B, alpha,
                                                   beta);
 }

@@ -885,6 +885,10 @@ bool setup_stream(const Fused& f, int elem, const hptt_options_t& opt, StreamArg
                   hptt_plan_info_t& info) {
     memset(&s, 0, sizeof(s));
     if (f.sA[0] != 1 || f.sB[0] != 1) return false;
+    int log = 0;
+    while ((int64_t(1) << (log + 1)) <= opt.xcd_group) ++log;
+    s.xcdGroupLog = log;
+    info.xcd_group = 1 << log;
     s.rowLen = f.n[0];
     int64_t rows = 1;
     for (int d = 1; d < f.M; ++d) rows *= f.n[d];

@@ -355,7 +355,10 @@ void emu_stream_launch(const hptt::StreamArgs& g, uint64_t grid, const T* A, T* 
     using namespace hptt;
     const uint64_t per = uint64_t(kBlock) * items_per_lane(int(sizeof(T)), V);
     const uint64_t step = grid * per;
-    for (uint64_t blk = 0; blk < grid && S->errors == 0; blk += uint64_t(blockStride))
+    for (uint64_t blk0 = 0; blk0 < grid && S->errors == 0; blk0 += uint64_t(blockStride)) {
+        const uint64_t blk =
+            g.xcdGroupLog ? xcd_group_map(uint32_t(blk0), uint32_t(grid), uint32_t(g.xcdGroupLog))
+                          : blk0;
         for (uint64_t first = blk * per;
              first < g.numItems[log2_width(V)] && S->errors == 0; first += step)
             for (int tid = 0; tid < kBlock; ++tid) {
@@ -365,6 +368,7 @@ void emu_stream_launch(const hptt::StreamArgs& g, uint64_t grid, const T* A, T* 
                 else
                     stream_items<HostMem, T, V, MODE, NT>(g, uint32_t(first), tid, A, B, alpha, beta);
             }
+    }
 }
 
 // Mirrors stream_kernel in kernels.hip, launched once, or once per slab

@@ -501,3 +501,17 @@ def test_xcd_group_rule():
     for bad in (3, 12, 2048, -1):
         with pytest.raises(hptt.HpttError):
             hptt.create_plan((1, 0), (64, 32), xcd_group=bad)
+
+
+def test_stream_xcd_groups_are_an_option():
+    """Kernel S deals its blocks to the XCDs in groups only when asked (the
+    quick path keeps plain round robin), and the autotuner lists the groups
+    and the flat and row walks as distinct candidates."""
+    perm, size = (0, 4, 3, 1, 2), (42, 4, 13, 1067, 21)
+    assert hptt.create_plan(perm, size).info["xcd_group"] == 1
+    p = hptt.create_plan(perm, size, xcd_group=64).info
+    assert p["kernel"] == "stream" and p["xcd_group"] == 64
+    cands = hptt.autotune_candidates(perm, size, 1.0, 0.0, "f32")
+    got = [c for c in cands if c.get("xcd_group") in (16, 64)]
+    assert len(got) == 2, cands
+    assert any(c.get("flat_runs") == 2 for c in cands), cands
