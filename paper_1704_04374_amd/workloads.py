@@ -119,9 +119,18 @@ SUBTENSOR_WORKLOADS = [
 # each 96 x 32 flat tile lie in one plane of A instead of up to 20 planes 13 MB
 # apart (same extents, tile shape, bytes and kernel; A(24, 20, 320, 24, 18),
 # perm [2, 0, 4, 1, 3]).
+#
+# And a 2-D fp32 transposition whose 32-element A runs start off the 128-byte
+# lines (A rows of 2193 elements), once with the quick plan (tiles dealt to
+# the XCDs 16 at a time) and once with the same tiles dealt one by one, round
+# robin: neighbouring tiles, which share A's boundary lines, then sit in
+# different XCDs' L2s.
 DIAGNOSTIC_WORKLOADS = [
     Workload("oneplane6d_24x20x320x24x18_f32", "f32", (24, 20, 320, 24, 18), (2, 0, 4, 1, 3),
              1.5, 0.0, 2, None, knobs=(("run_a", 96), ("run_b", 32))),
+    Workload("xcdgroups2d_2193x22800_f32", "f32", (2193, 22800), (1, 0), 1.0, 0.0, 9, None),
+    Workload("roundrobin2d_2193x22800_f32", "f32", (2193, 22800), (1, 0), 1.0, 0.0, 9, None,
+             knobs=(("xcd_group", 1), ("tile_order", 2))),
 ]
 
 BY_NAME = {w.name: w for w in WORKLOADS + SUBTENSOR_WORKLOADS + DIAGNOSTIC_WORKLOADS}
