@@ -108,7 +108,7 @@ EXPECTED = {
                                      run_b=32, tiles=60),
     "transpose2d_8192x8192_f32": dict(kernel="tile", size=(8192, 8192), perm=(1, 0), run_a=128,
                                       run_b=32, tiles=16384, tile_order=2, hints=3,
-                                      grid_order=1),
+                                      grid_order=1, xcd_group=1),
     # flat B runs: one line cut from the 20 x 16 = 320 flattened B positions
     # (10 chunks), A runs of 24 x 4 = 96 elements (3 lines)
     "transpose6d_24x20x16x24x18x20_f32": dict(kernel="tile", size=(24, 20, 16, 24, 18, 20),
@@ -117,14 +117,18 @@ EXPECTED = {
                                               rows_per_pass=32, flat_runs=2,
                                               # outer digits by the sum of their strides: A4
                                               # (B-adjacent) before A3 (A-adjacent)
-                                              grid_order=2),
+                                              grid_order=2, xcd_group=1),
     "transpose4d_96x96x96x96_keep1_f64": dict(kernel="stream", size=(96, 96, 96, 96),
                                               perm=(0, 3, 2, 1), run_b=96, vec_a=2, vec_b=2),
     # beta != 0: A-run target of 256 bytes, met by 3 x 2 x 16 = 96 elements (384 B)
     "transpose5d_3x2x640x480x96_f32": dict(kernel="tile", size=(3, 2, 640, 480, 96),
                                            perm=(4, 2, 0, 3, 1), run_a=96, run_b=32, dims_a=3,
                                            dims_b=1, tiles=57600, hints=3, depth=1,
-                                           grid_order=1),
+                                           grid_order=1, xcd_group=1),
+    # 32-element A runs off the line grid: sheared tiles dealt to the XCDs in
+    # groups of 16, grid-digit order
+    "xcdgroups2d_2193x22800_f32": dict(kernel="tile", size=(2193, 22800), perm=(1, 0), run_a=32,
+                                       run_b=128, shear=31, tile_order=1, xcd_group=16),
 }
 
 
