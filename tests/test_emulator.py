@@ -549,21 +549,24 @@ def test_xcd_groups_match_oracle(k):
     """Tile numbers dealt to the XCDs in groups of k (with and without the
     diagonal rotation, which then advances once per group) still cover every
     tile once: disjoint, sheared, flat, stacked and shared-run tiles, grids
-    with and without an incomplete last round of 8k tiles, against the
-    oracle."""
+    with and without an incomplete last round of 8k tiles, and kernel S's
+    blocks (row and flat walks), against the oracle."""
     rng = np.random.default_rng(77 + k)
     cases = [((1759, 444), (1, 0), {}), ((274, 2280), (1, 0), {}),
              ((427, 110, 3, 35), (3, 2, 1, 0), {}), ((77, 165, 2, 197), (3, 1, 0, 2), {}),
              ((96, 96, 9, 7), (2, 0, 3, 1), {}), ((4, 2, 17, 3, 1225), (2, 1, 3, 0, 4), {}),
              ((24, 20, 16, 24, 18, 5), (5, 2, 0, 4, 1, 3), {}),
-             ((33, 17, 65), (2, 0, 1), dict(depth=3)), ((600, 130), (1, 0), dict(max_blocks=7))]
+             ((33, 17, 65), (2, 0, 1), dict(depth=3)), ((600, 130), (1, 0), dict(max_blocks=7)),
+             ((42, 4, 13, 107, 21), (0, 4, 3, 1, 2), {}), ((96, 12, 13, 17), (0, 3, 2, 1), {}),
+             ((97, 12, 13, 17), (0, 3, 2, 1), dict(flat_runs=2))]
     for size_a, perm, knobs in cases:
         for beta, order in ((0.0, 0), (1.0, 1), (0.5, 2)):
             kw = dict(knobs, xcd_group=k)
-            if order:
+            p0 = emu.plan(perm, size_a, 1.5, beta, "f32", **kw)
+            if order and p0.info["kernel"] == "tile":
                 kw["tile_order"] = order
             p = emu.plan(perm, size_a, 1.5, beta, "f32", **kw)
-            if p.info["kernel"] != "tile":
+            if p.info["kernel"] not in ("tile", "stream"):
                 continue
             assert p.info["xcd_group"] == k, p.describe()
             _check(p, size_a, perm, 1.5, beta, "f32", rng)
