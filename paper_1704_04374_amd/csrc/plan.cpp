@@ -231,13 +231,20 @@ void set_direct_lds(const hptt_options_t& opt, int elem, hptt_plan_info_t& info,
 // run: MI355X, the cases of the 57-case sweep with runs up to 256 bytes,
 // -0.4 to +29 % (mean +9.5 %) with beta = 0 and -1.5 to +14 % (mean +3.8 %)
 // with beta = 1; runs of 257-320 bytes (fp32 and fp64) -1.6 to +13 %, mean
-// +2.6 %; runs of 500 bytes and more over a power-of-two B stride lost up to
-// 6 % with beta = 1 to the diagonal order's spread over the HBM channels,
-// and shared-run tiles 1-3 %.
+// +2.6 %; tiles whose columns lie a multiple of 4 KiB apart in B lost up to
+// 7 % to the diagonal order's spread over the HBM channels (below), and
+// shared-run tiles 1-3 %.
 void set_xcd_groups(const hptt_options_t& opt, int elem, hptt_plan_info_t& info, TileArgs& t) {
     if (opt.xcd_group != 0 || opt.tile_order != 0 || t.shared || t.alignedA ||
         t.runA * elem > 320)
         return;
+    // A B stride of the A run's first index that is a multiple of 4 KiB
+    // (every column of the tile, and of its neighbours, the same distance
+    // from a channel boundary) keeps the diagonal order, which spreads the
+    // tiles in flight over the HBM channels (MI355X, beta = 1, 64-element
+    // runs: 3001x16384 [1,0], columns 64 KiB apart in B, -7 % in groups;
+    // 999x4x12288 [2,0,1], 48 KiB, -6 %).
+    if (t.nC > 0 && (t.cStrideB[0] * elem) % 4096 == 0) return;
     t.skew = 0;
     t.xcdGroupLog = 4;
     info.tile_order = 1;

@@ -491,9 +491,14 @@ def test_xcd_group_rule():
         f64 = hptt.create_plan((3, 1, 0, 2), (77, 1651, 2, 99), 1.0, beta, "f64").info
         assert f64["xcd_group"] == 16 and f64["run_a"] * 8 <= 320, f64
     assert hptt.create_plan((1, 0), (8192, 8192)).info["xcd_group"] == 1       # whole lines
-    long_run = hptt.create_plan((1, 0), (3001, 16384)).info                     # 131 elements
-    assert long_run["run_a"] * 4 > 256 and long_run["xcd_group"] == 1
+    long_run = hptt.create_plan((3, 2, 1, 4, 0, 5), (6, 55, 48, 6, 7, 75)).info  # 672 bytes
+    assert long_run["run_a"] * 4 > 320 and long_run["xcd_group"] == 1, long_run
     assert long_run["tile_order"] == 2
+    # columns a multiple of 4 KiB apart in B (64 KiB here) keep the diagonal
+    for beta in (0.0, 1.0):
+        pow2 = hptt.create_plan((1, 0), (3001, 16384), 1.0, beta).info
+        assert pow2["xcd_group"] == 1 and pow2["tile_order"] == 2, pow2
+    assert hptt.create_plan((1, 0), (3001, 16384), 1.0, 1.0).info["run_a"] * 4 <= 320
     shared = hptt.create_plan((1, 3, 0, 2), (2, 26250, 4, 238)).info
     assert shared["shared_runs"] and shared["xcd_group"] == 1
     forced = hptt.create_plan((1, 0), (2193, 22800), xcd_group=1).info
