@@ -232,11 +232,13 @@ void set_direct_lds(const hptt_options_t& opt, int elem, hptt_plan_info_t& info,
 // -0.4 to +29 % (mean +9.5 %) with beta = 0 and -1.5 to +14 % (mean +3.8 %)
 // with beta = 1; runs of 257-320 bytes (fp32 and fp64) -1.6 to +13 %, mean
 // +2.6 %; tiles whose columns lie a multiple of 4 KiB apart in B lost up to
-// 7 % to the diagonal order's spread over the HBM channels (below), and
-// shared-run tiles 1-3 %.
+// 7 % to the diagonal order's spread over the HBM channels (below).
+// Shared-run tiles take the same rule: the five such plans measured (A runs
+// of 63-70 elements off the line grid, three of them kept-index tiles)
+// gained -0.1 to +5 % (mean +2.6 %) with beta = 0 and -0.7 to +2.8 % (mean
+// +1.1 %) with beta = 1, while the long single-row ones lost 1-3 %.
 void set_xcd_groups(const hptt_options_t& opt, int elem, hptt_plan_info_t& info, TileArgs& t) {
-    if (opt.xcd_group != 0 || opt.tile_order != 0 || t.shared || t.alignedA ||
-        t.runA * elem > 320)
+    if (opt.xcd_group != 0 || opt.tile_order != 0 || t.alignedA || t.runA * elem > 320)
         return;
     // A B stride of the A run's first index that is a multiple of 4 KiB
     // (every column of the tile, and of its neighbours, the same distance
@@ -1125,6 +1127,7 @@ hptt_status_t build_plan(const int32_t* perm, int32_t N, const int64_t* sizeA,
         const int64_t grid = plan->tile.numTiles;
         info.grid = grid < maxBlocks ? grid : maxBlocks;
         info.block = kBlock;
+        set_xcd_groups(opt, elem, info, plan->tile);
     } else if (k == HPTT_KERNEL_TILE) {
         // Tile search, in order of preference (each stage halves the longer
         // target until a tile fits): both runs on whole 128-byte lines within

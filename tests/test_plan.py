@@ -499,8 +499,11 @@ def test_xcd_group_rule():
         pow2 = hptt.create_plan((1, 0), (3001, 16384), 1.0, beta).info
         assert pow2["xcd_group"] == 1 and pow2["tile_order"] == 2, pow2
     assert hptt.create_plan((1, 0), (3001, 16384), 1.0, 1.0).info["run_a"] * 4 <= 320
-    shared = hptt.create_plan((1, 3, 0, 2), (2, 26250, 4, 238)).info
+    shared = hptt.create_plan((1, 3, 0, 2), (2, 26250, 4, 238)).info        # long runs
     assert shared["shared_runs"] and shared["xcd_group"] == 1
+    for beta in (0.0, 1.0):  # kept-index shared-run tiles with 256-byte runs off the lines
+        kept = hptt.create_plan((0, 2, 1), (2, 60251, 415), 1.0, beta).info
+        assert kept["shared_runs"] and kept["run_a"] * 4 <= 320 and kept["xcd_group"] == 16, kept
     forced = hptt.create_plan((1, 0), (2193, 22800), xcd_group=1).info
     assert forced["xcd_group"] == 1 and forced["tile_order"] == 2
     forced = hptt.create_plan((1, 0), (8192, 8192), xcd_group=64).info
